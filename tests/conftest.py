@@ -1,0 +1,20 @@
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+    config.addinivalue_line("markers", "slow: long-running CPU oracle test")
+
+
+def read_fixture(name):
+    """Non-comment, non-empty lines of tests/golden/<name>, split on whitespace."""
+    path = os.path.join(ROOT, "tests", "golden", name)
+    with open(path) as f:
+        return [ln.split() for ln in f if ln.strip() and not ln.lstrip().startswith("#")]
