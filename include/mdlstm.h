@@ -1,0 +1,206 @@
+/*
+ * mdlstm.h — C ABI of the packed four-direction MDLSTM layer for MI355X (gfx950).
+ *
+ * What is computed (Maillette de Buy Wenniger, Schomaker, Way, "No Padding
+ * Please: Efficient Neural Handwriting Recognition"):
+ *
+ *   - Example packing (Section V-A; Algorithm 1 in Appendix B): variable-size
+ *     examples are bucketed by height, rows are filled greedily with the widest
+ *     example that still fits, and examples are tiled within and across rows
+ *     with one separating pixel; a binary mask marks example pixels.
+ *   - The four-direction 2D MDLSTM layer (Section III, Section IV-B): per scan
+ *     direction d and cell, with left/top predecessors L and T in d's frame,
+ *         a   = Wx_d x + b_d + U_d [h_L ; h_T]       5H rows, gates in the order
+ *                                                    (i, f_L, f_T, o, g)
+ *         c   = sig(a_i) tanh(a_g) + sig(a_fL) c_L + sig(a_fT) c_T
+ *         h   = sig(a_o) tanh(c)
+ *     Direction 0 scans from the top-left, 1 from the top-right, 2 from the
+ *     bottom-left, 3 from the bottom-right. State handed over by a predecessor
+ *     outside the cell's rectangle or with mask 0 is zero (Section V, binary
+ *     masking), so a packed canvas gives every example exactly the result it
+ *     has alone.
+ *
+ * Conventions shared by every entry point:
+ *   - Canvas tensors are row-major [canvas_h][canvas_w][channels] ("HWC"),
+ *     unskewed; the input-skewing of Section IV-A is index arithmetic inside
+ *     the kernels.
+ *   - Pointers named d_* are DEVICE memory of the current HIP device; all
+ *     other pointers are HOST memory. The caller owns every buffer; the library
+ *     allocates no memory of its own and keeps no pointer after returning.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream). Work
+ *     is enqueued on it asynchronously unless stated otherwise.
+ *   - Every argument is validated on the host before any HIP call; on error
+ *     nothing is enqueued and mdlstm_last_error() describes the problem.
+ *   - Calls are reentrant given distinct workspaces.
+ */
+#ifndef MDLSTM_H
+#define MDLSTM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MDLSTM_OK = 0,
+    MDLSTM_ERR_INVALID_ARG = 1, /* NULL pointer, negative size, bad descriptor   */
+    MDLSTM_ERR_TOO_WIDE = 2,    /* an example is wider than the canvas          */
+    MDLSTM_ERR_BAD_LAYOUT = 3,  /* rectangles overlap or leave the canvas       */
+    MDLSTM_ERR_WORKSPACE = 4,   /* workspace or output buffer too small         */
+    MDLSTM_ERR_UNSUPPORTED = 5, /* hidden size / dtype / rectangle height not built */
+    MDLSTM_ERR_DEVICE = 6       /* a HIP call failed; message has the HIP string */
+} mdlstm_status;
+
+/* Storage type of x, y, weights, dx and the saved gates. Accumulation and the
+ * saved cell state are always fp32; weight gradients are always fp32. */
+typedef enum { MDLSTM_F32 = 0, MDLSTM_BF16 = 1 } mdlstm_dtype;
+
+/* A rectangle of the canvas: top-left corner (y0, x0), height h, width w. */
+typedef struct {
+    int32_t y0, x0, h, w;
+} mdlstm_rect;
+
+/* One MDLSTM layer. Supported: F32 with hidden in {4, 8, 16, 32, 64};
+ * BF16 with hidden in {32, 64, 128}; c_in a multiple of 4 (F32) or 8 (BF16),
+ * 4 <= c_in <= 256. */
+typedef struct {
+    int32_t c_in;
+    int32_t hidden;
+    int32_t dtype; /* mdlstm_dtype */
+} mdlstm_layer_desc;
+
+/* Largest rectangle height the wavefront kernels accept. */
+#define MDLSTM_MAX_RECT_H 64
+
+/* Device workspace needed by mdlstm_pack_layout / mdlstm_pack_data /
+ * mdlstm_unpack_data for n examples. */
+size_t mdlstm_pack_workspace_bytes(int32_t n);
+
+/*
+ * Example packing, placement and mask (Section V-A steps 1-3; Algorithm 1).
+ *
+ * heights[n], widths[n] (host): example sizes, all >= 1.
+ * canvas_w: width of the canvas; every example must fit (else TOO_WIDE).
+ * rects[n] (host, out): rects[k] is the placement of ORIGINAL example k.
+ * canvas_h (host, out): height of the packed canvas (0 when n == 0).
+ * d_mask (device, out, may be NULL): uint8 [canvas_h][canvas_w], 1 on example
+ *   pixels and 0 on separators and slack; needs mask_bytes >= canvas_h*canvas_w
+ *   (else WORKSPACE, with rects and canvas_h still written). With NULL only the
+ *   placement is computed, so a caller can learn canvas_h, allocate, and call again.
+ * d_workspace: mdlstm_pack_workspace_bytes(n) bytes of device memory.
+ *
+ * Placement runs as a kernel on `stream`, and the call waits for it because
+ * rects and canvas_h are host outputs. The mask is written asynchronously; the
+ * workspace must stay untouched until the stream has passed the mask kernel.
+ * Readings of the paper this follows: buckets in ascending height; ties in
+ * width broken by original index; the fit test counts a separator only between
+ * two examples; a partial row is flushed when its bucket runs empty.
+ */
+mdlstm_status mdlstm_pack_layout(int32_t n, const int32_t* heights, const int32_t* widths,
+                                 int32_t canvas_w, mdlstm_rect* rects, int32_t* canvas_h,
+                                 uint8_t* d_mask, size_t mask_bytes,
+                                 void* d_workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Last-minute batch padding layout (Section VI-B): every example padded to the
+ * batch maximum height and width; tiles stacked vertically with no separators.
+ * tiles[n] (host, out) are the scheduling rectangles, place[n] (host, out) the
+ * example extents (top-left of each tile). canvas_h/canvas_w (host, out).
+ * d_mask (device, out, may be NULL): 1 on example pixels, 0 on padding.
+ * Host-only computation plus an asynchronous mask kernel.
+ */
+mdlstm_status mdlstm_pad_layout(int32_t n, const int32_t* heights, const int32_t* widths,
+                                mdlstm_rect* tiles, mdlstm_rect* place,
+                                int32_t* canvas_h, int32_t* canvas_w,
+                                uint8_t* d_mask, size_t mask_bytes,
+                                void* d_workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Scatter (Section V-A step 3) / gather (unpacking, Section V-A last paragraph).
+ * d_examples[k] (host array of device pointers): example k, HWC [h][w][c]
+ *   with (h, w) = (rects[k].h, rects[k].w), storage dtype `dt`.
+ * rects[n] (host): where example k sits on the canvas (disjoint, inside).
+ * d_canvas: [canvas_h][canvas_w][c]. pack_data overwrites the whole canvas,
+ *   zero outside the rectangles; unpack_data reads it and overwrites each example.
+ */
+mdlstm_status mdlstm_pack_data(int32_t n, const void* const* d_examples, const mdlstm_rect* rects,
+                               int32_t canvas_h, int32_t canvas_w, int32_t c, int32_t dt,
+                               void* d_canvas, void* d_workspace, size_t workspace_bytes,
+                               void* stream);
+mdlstm_status mdlstm_unpack_data(int32_t n, void* const* d_examples, const mdlstm_rect* rects,
+                                 int32_t canvas_h, int32_t canvas_w, int32_t c, int32_t dt,
+                                 const void* d_canvas, void* d_workspace, size_t workspace_bytes,
+                                 void* stream);
+
+/* Device workspace needed by mdlstm_forward followed by mdlstm_backward. */
+size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
+                              int32_t n_rects);
+
+/*
+ * Forward pass of the four-direction layer over a canvas.
+ *
+ * d_x: [canvas_h][canvas_w][c_in], storage dtype.
+ * d_mask: uint8 [canvas_h][canvas_w]; a cell is valid iff its mask byte is
+ *   nonzero AND it lies inside one of the rectangles.
+ * rects[n_rects] (host): scheduling rectangles; the recurrence of every
+ *   direction restarts at each rectangle edge. Must be inside the canvas,
+ *   pairwise disjoint, with h <= MDLSTM_MAX_RECT_H (else BAD_LAYOUT /
+ *   UNSUPPORTED). Packed canvases pass the example placements; padded canvases
+ *   pass the tiles and carry the true extents in the mask.
+ * d_wx: [4][5H][c_in], d_u: [4][5H][2H] (columns 0..H-1 multiply h_L,
+ *   H..2H-1 multiply h_T), d_b: [4][5H]; storage dtype; gate order (i, f_L,
+ *   f_T, o, g) along 5H.
+ * d_y (out): [canvas_h][canvas_w][4H], channel d*H + j; 0 at invalid cells.
+ * d_workspace: mdlstm_workspace_bytes(...) bytes; keeps the gates and the cell
+ *   state for mdlstm_backward, so it must not be modified in between.
+ * Asynchronous on `stream`.
+ */
+mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
+                             const void* d_x, const uint8_t* d_mask,
+                             int32_t n_rects, const mdlstm_rect* rects,
+                             const void* d_wx, const void* d_u, const void* d_b,
+                             void* d_y, void* d_workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Backward pass: gradients of L = sum(Y * dY) after an mdlstm_forward with the
+ * same arguments and workspace (reverse anti-diagonal sweep, then weight and
+ * input gradient reductions).
+ * d_y: the forward output; d_dy: [canvas_h][canvas_w][4H], ignored at invalid cells.
+ * d_dx (out): [canvas_h][canvas_w][c_in] storage dtype, 0 at invalid cells.
+ * d_dwx [4][5H][c_in], d_du [4][5H][2H], d_db [4][5H] (out, fp32): sums over
+ *   all valid cells, OVERWRITTEN (not accumulated); fixed reduction order, so
+ *   repeated calls give bitwise-identical results.
+ * The gates saved in the workspace are overwritten by their gradients.
+ * Asynchronous on `stream`.
+ */
+mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
+                              const void* d_x, const uint8_t* d_mask,
+                              int32_t n_rects, const mdlstm_rect* rects,
+                              const void* d_wx, const void* d_u, const void* d_b,
+                              const void* d_y, const void* d_dy,
+                              void* d_dx, float* d_dwx, float* d_du, float* d_db,
+                              void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* Message for the last non-OK status returned on the calling thread. */
+const char* mdlstm_last_error(void);
+
+/*
+ * Optional kernel-boundary timing (profiling hook, off by default).
+ * events[n] (host array of hipEvent_t handles owned by the caller). While set,
+ * mdlstm_forward and mdlstm_backward called on this thread record them on
+ * their stream at kernel boundaries:
+ *   [0] before the projection   [1] after the projection   [2] after zeroing
+ *   invalid output rows         [3] after the forward wavefront
+ *   [4] before the backward wavefront  [5] after it  [6] after the input
+ *   gradient  [7] after the weight gradients.
+ * n must be 0 (disable) or 8. The handles must stay valid while set.
+ */
+mdlstm_status mdlstm_set_phase_events(int32_t n, void* const* events);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MDLSTM_H */

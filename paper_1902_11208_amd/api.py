@@ -1,0 +1,221 @@
+"""Python binding of the C ABI: argument marshalling only.
+
+torch provides device memory and the current stream; every step of the
+computation runs in libmdlstm.so's HIP kernels.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import torch
+
+from ._lib import LayerDesc, Rect, P_VOIDP, check, lib
+
+F32, BF16 = 0, 1
+TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
+
+
+def dtype_code(t: torch.dtype) -> int:
+    if t == torch.float32:
+        return F32
+    if t == torch.bfloat16:
+        return BF16
+    raise TypeError(f"storage dtype {t} is not float32 or bfloat16")
+
+
+def _stream(stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _rect_array(rects) -> ctypes.Array:
+    r = np.ascontiguousarray(np.asarray(rects, dtype=np.int32).reshape(-1, 4))
+    arr = (Rect * max(1, r.shape[0]))()
+    ctypes.memmove(arr, r.ctypes.data, r.nbytes)
+    return arr
+
+
+def _rects_from(arr, n) -> np.ndarray:
+    out = np.zeros((n, 4), np.int32)
+    if n:
+        ctypes.memmove(out.ctypes.data, arr, n * 16)
+    return out
+
+
+def _i32_array(v) -> ctypes.Array:
+    a = np.ascontiguousarray(np.asarray(v, dtype=np.int32).reshape(-1))
+    arr = (ctypes.c_int32 * max(1, a.size))()
+    ctypes.memmove(arr, a.ctypes.data, a.nbytes)
+    return arr
+
+
+def _check_dev(t: torch.Tensor, name: str):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+# ---------------------------------------------------------------------------
+# Packing
+# ---------------------------------------------------------------------------
+def pack_workspace_bytes(n: int) -> int:
+    return int(lib().mdlstm_pack_workspace_bytes(int(n)))
+
+
+def pack_layout(heights, widths, canvas_w: int, device="cuda", stream=None):
+    """Example packing (placement kernel + mask kernel).
+    Returns (rects int32 [n, 4] by original index, canvas_h, mask uint8 [canvas_h, canvas_w])."""
+    hs, ws = _i32_array(heights), _i32_array(widths)
+    n = len(np.asarray(heights).reshape(-1))
+    work = torch.empty(pack_workspace_bytes(n), dtype=torch.uint8, device=device)
+    rects = (Rect * max(1, n))()
+    ch = ctypes.c_int32(0)
+    st = _stream(stream)
+    check(lib().mdlstm_pack_layout(n, hs, ws, int(canvas_w), rects, ctypes.byref(ch), None, 0, _ptr(work),
+                                   work.numel(), st))
+    mask = torch.empty((ch.value, int(canvas_w)), dtype=torch.uint8, device=device)
+    check(lib().mdlstm_pack_layout(n, hs, ws, int(canvas_w), rects, ctypes.byref(ch), _ptr(mask), mask.numel(),
+                                   _ptr(work), work.numel(), st))
+    torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+    return _rects_from(rects, n), ch.value, mask
+
+
+def pad_layout(heights, widths, device="cuda", stream=None):
+    """Last-minute batch padding layout. Returns (tiles, place, canvas_h, canvas_w, mask)."""
+    n = len(np.asarray(heights).reshape(-1))
+    hs, ws = _i32_array(heights), _i32_array(widths)
+    tiles, place = (Rect * max(1, n))(), (Rect * max(1, n))()
+    ch, cw = ctypes.c_int32(0), ctypes.c_int32(0)
+    check(lib().mdlstm_pad_layout(n, hs, ws, tiles, place, ctypes.byref(ch), ctypes.byref(cw), None, 0, None, 0, 0))
+    mask = torch.empty((ch.value, cw.value), dtype=torch.uint8, device=device)
+    work = torch.empty(pack_workspace_bytes(n), dtype=torch.uint8, device=device)
+    s = stream if stream is not None else torch.cuda.current_stream()
+    check(lib().mdlstm_pad_layout(n, hs, ws, tiles, place, ctypes.byref(ch), ctypes.byref(cw), _ptr(mask),
+                                  mask.numel(), _ptr(work), work.numel(), _stream(s)))
+    s.synchronize()
+    return _rects_from(tiles, n), _rects_from(place, n), ch.value, cw.value, mask
+
+
+def pack_data(examples, rects, canvas_h: int, canvas_w: int, stream=None, out=None):
+    """Scatter HWC example tensors into a zeroed [canvas_h, canvas_w, c] canvas."""
+    n = len(examples)
+    if n == 0:
+        raise ValueError("pack_data needs at least one example to know channels and dtype")
+    c = examples[0].shape[2]
+    dt = examples[0].dtype
+    dev = examples[0].device
+    r = np.asarray(rects, np.int32).reshape(-1, 4)
+    for k, e in enumerate(examples):
+        _check_dev(e, f"example {k}")
+        if e.dtype != dt or e.shape != (r[k, 2], r[k, 3], c):
+            raise ValueError(f"example {k} has shape {tuple(e.shape)}, rect says {tuple(r[k, 2:])}x{c}")
+    canvas = out if out is not None else torch.empty((canvas_h, canvas_w, c), dtype=dt, device=dev)
+    ptrs = (ctypes.c_void_p * n)(*[e.data_ptr() for e in examples])
+    work = torch.empty(pack_workspace_bytes(n), dtype=torch.uint8, device=dev)
+    s = stream if stream is not None else torch.cuda.current_stream()
+    check(lib().mdlstm_pack_data(n, ctypes.cast(ptrs, P_VOIDP), _rect_array(r), canvas_h, canvas_w, c,
+                                 dtype_code(dt), _ptr(canvas), _ptr(work), work.numel(), _stream(s)))
+    s.synchronize()  # the workspace (pointer table) is released on return
+    return canvas
+
+
+def unpack_data(canvas: torch.Tensor, rects, stream=None):
+    """Gather per-example HWC tensors out of a canvas."""
+    _check_dev(canvas, "canvas")
+    r = np.asarray(rects, np.int32).reshape(-1, 4)
+    n = r.shape[0]
+    ch, cw, c = canvas.shape
+    outs = [torch.empty((int(h), int(w), c), dtype=canvas.dtype, device=canvas.device) for _, _, h, w in r]
+    if n == 0:
+        return outs
+    ptrs = (ctypes.c_void_p * n)(*[o.data_ptr() for o in outs])
+    work = torch.empty(pack_workspace_bytes(n), dtype=torch.uint8, device=canvas.device)
+    s = stream if stream is not None else torch.cuda.current_stream()
+    check(lib().mdlstm_unpack_data(n, ctypes.cast(ptrs, P_VOIDP), _rect_array(r), ch, cw, c, dtype_code(canvas.dtype),
+                                   _ptr(canvas), _ptr(work), work.numel(), _stream(s)))
+    s.synchronize()
+    return outs
+
+
+# ---------------------------------------------------------------------------
+# Layer
+# ---------------------------------------------------------------------------
+def layer_desc(c_in: int, hidden: int, dtype: int) -> LayerDesc:
+    return LayerDesc(int(c_in), int(hidden), int(dtype))
+
+
+def workspace_bytes(c_in: int, hidden: int, dtype: int, canvas_h: int, canvas_w: int, n_rects: int) -> int:
+    d = layer_desc(c_in, hidden, dtype)
+    return int(lib().mdlstm_workspace_bytes(ctypes.byref(d), canvas_h, canvas_w, n_rects))
+
+
+class Prepared:
+    """Host-side argument bundle for one canvas layout, reused across calls."""
+
+    def __init__(self, c_in: int, hidden: int, dtype: int, canvas_h: int, canvas_w: int, rects):
+        self.desc = layer_desc(c_in, hidden, dtype)
+        self.canvas_h, self.canvas_w = int(canvas_h), int(canvas_w)
+        self.rects_np = np.asarray(rects, np.int32).reshape(-1, 4)
+        self.n_rects = int(self.rects_np.shape[0])
+        self.rects = _rect_array(self.rects_np)
+        self.ws_bytes = int(lib().mdlstm_workspace_bytes(ctypes.byref(self.desc), self.canvas_h, self.canvas_w,
+                                                         self.n_rects))
+
+
+def forward(prep: Prepared, x, mask, wx, u, b, y, workspace, stream=None):
+    """Enqueue the forward pass; y and workspace are caller-allocated."""
+    check(lib().mdlstm_forward(ctypes.byref(prep.desc), prep.canvas_h, prep.canvas_w, _ptr(x), _ptr(mask),
+                               prep.n_rects, prep.rects, _ptr(wx), _ptr(u), _ptr(b), _ptr(y), _ptr(workspace),
+                               prep.ws_bytes if workspace is not None else 0, _stream(stream)))
+
+
+def backward(prep: Prepared, x, mask, wx, u, b, y, dy, dx, dwx, du, db, workspace, stream=None):
+    """Enqueue the backward pass; all outputs caller-allocated, overwritten."""
+    check(lib().mdlstm_backward(ctypes.byref(prep.desc), prep.canvas_h, prep.canvas_w, _ptr(x), _ptr(mask),
+                                prep.n_rects, prep.rects, _ptr(wx), _ptr(u), _ptr(b), _ptr(y), _ptr(dy), _ptr(dx),
+                                _ptr(dwx), _ptr(du), _ptr(db), _ptr(workspace),
+                                prep.ws_bytes if workspace is not None else 0, _stream(stream)))
+
+
+class MDLSTMLayer:
+    """Four-direction MDLSTM layer over a canvas with a fixed layout.
+
+    Owns the workspace and the output/gradient buffers for that layout.
+    """
+
+    def __init__(self, wx: torch.Tensor, u: torch.Tensor, b: torch.Tensor, canvas_h: int, canvas_w: int, rects,
+                 mask: torch.Tensor):
+        for t, nm in ((wx, "wx"), (u, "u"), (b, "b"), (mask, "mask")):
+            _check_dev(t, nm)
+        self.dtype = dtype_code(wx.dtype)
+        self.hidden = int(u.shape[2]) // 2
+        self.c_in = int(wx.shape[2])
+        self.wx, self.u, self.b, self.mask = wx, u, b, mask
+        dev = wx.device
+        self.prep = Prepared(self.c_in, self.hidden, self.dtype, canvas_h, canvas_w, rects)
+        self.workspace = torch.empty(max(1, self.prep.ws_bytes), dtype=torch.uint8, device=dev)
+        td = wx.dtype
+        H = self.hidden
+        self.y = torch.empty((canvas_h, canvas_w, 4 * H), dtype=td, device=dev)
+        self.dx = torch.empty((canvas_h, canvas_w, self.c_in), dtype=td, device=dev)
+        self.dwx = torch.empty((4, 5 * H, self.c_in), dtype=torch.float32, device=dev)
+        self.du = torch.empty((4, 5 * H, 2 * H), dtype=torch.float32, device=dev)
+        self.db = torch.empty((4, 5 * H), dtype=torch.float32, device=dev)
+
+    def forward(self, x: torch.Tensor, stream=None) -> torch.Tensor:
+        _check_dev(x, "x")
+        self.x = x
+        forward(self.prep, x, self.mask, self.wx, self.u, self.b, self.y, self.workspace, stream)
+        return self.y
+
+    def backward(self, dy: torch.Tensor, stream=None):
+        _check_dev(dy, "dy")
+        backward(self.prep, self.x, self.mask, self.wx, self.u, self.b, self.y, dy, self.dx, self.dwx, self.du,
+                 self.db, self.workspace, stream)
+        return self.dx, self.dwx, self.du, self.db

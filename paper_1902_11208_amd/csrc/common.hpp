@@ -1,0 +1,107 @@
+// Shared device helpers for the MDLSTM kernels (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t bf16_t;  // bfloat16 storage (upper half of an fp32)
+
+// ---------------------------------------------------------------------------
+// bfloat16 <-> fp32
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf2f(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
+
+__device__ __forceinline__ bf16_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (bf16_t)((u >> 16) | 0x40);  // NaN
+    u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest, ties to even
+    return (bf16_t)(u >> 16);
+}
+
+// Storage traits: loads/stores of 4 consecutive elements as fp32.
+template <typename T>
+struct St;
+
+template <>
+struct St<float> {
+    static __device__ __forceinline__ floatx4 ld4(const float* p) {
+        float4 v = *reinterpret_cast<const float4*>(p);
+        return floatx4{v.x, v.y, v.z, v.w};
+    }
+    static __device__ __forceinline__ void st4(float* p, floatx4 v) {
+        *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+    static __device__ __forceinline__ float ld1(const float* p) { return *p; }
+    static __device__ __forceinline__ void st1(float* p, float v) { *p = v; }
+};
+
+template <>
+struct St<bf16_t> {
+    static __device__ __forceinline__ floatx4 ld4(const bf16_t* p) {
+        uint2 v = *reinterpret_cast<const uint2*>(p);
+        return floatx4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                       __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u)};
+    }
+    static __device__ __forceinline__ void st4(bf16_t* p, floatx4 v) {
+        uint2 o;
+        o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+        o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+        *reinterpret_cast<uint2*>(p) = o;
+    }
+    static __device__ __forceinline__ float ld1(const bf16_t* p) { return bf2f(*p); }
+    static __device__ __forceinline__ void st1(bf16_t* p, float v) { *p = f2bf(v); }
+};
+
+// ---------------------------------------------------------------------------
+// Gate nonlinearities (fp32).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float sigm(float z) { return 1.0f / (1.0f + expf(-z)); }
+
+__device__ __forceinline__ float tanh_acc(float z) {
+    float a = fabsf(z);
+    float r;
+    if (a < 0.125f) {
+        // odd Taylor series, error below 2e-10 relative on |z| < 1/8
+        float p = z * z;
+        r = z * (1.0f + p * (-1.0f / 3.0f + p * (2.0f / 15.0f + p * (-17.0f / 315.0f))));
+    } else {
+        float e = expf(-2.0f * a);
+        r = copysignf((1.0f - e) / (1.0f + e), z);
+    }
+    return r;
+}
+
+// ---------------------------------------------------------------------------
+// MFMA 16x16 tiles. For both instructions used here the output tile D[16][16]
+// lives in lane l = 16*q + n as D[4*q + r][n], r = 0..3; the A operand row is
+// l % 16 and the B operand column is l % 16, with the reduction slot l / 16.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ floatx4 mfma_f32(float a, float b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ floatx4 mfma_bf16(bf16x8 a, bf16x8 b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
+    bf16x8 r;
+    __builtin_memcpy(&r, &v, sizeof(r));
+    return r;
+}
+
+// ---------------------------------------------------------------------------
+// Device-side rectangle and unit decoding.
+// ---------------------------------------------------------------------------
+struct RectD {
+    int32_t y0, x0, h, w;
+};
+
+// Canvas index of a unit's local cell (y, x) in scan direction d's frame:
+// direction bit 0 mirrors x (scan from the right), bit 1 mirrors y (from the bottom).
+__device__ __forceinline__ int64_t canvas_index(const RectD& R, int d, int y, int x, int canvas_w) {
+    int cy = R.y0 + ((d & 2) ? (R.h - 1 - y) : y);
+    int cx = R.x0 + ((d & 1) ? (R.w - 1 - x) : x);
+    return (int64_t)cy * canvas_w + cx;
+}

@@ -1,0 +1,60 @@
+// Internal launcher interface between the C-ABI host layer and the HIP kernels.
+// All launchers enqueue on `stream` and return the hipError_t of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace mdl {
+
+struct LayerGeom {
+    int c_in, hidden, dtype;  // dtype: 0 fp32, 1 bf16
+    int canvas_h, canvas_w;
+    int64_t n_cells;          // canvas_h * canvas_w
+};
+
+// --- packing -------------------------------------------------------------
+// Placement of n examples; sizes in d_hw[2n] (heights then widths), result
+// d_rects[4n] (y0,x0,h,w by original index) and d_rects[4n] = canvas_h.
+hipError_t launch_pack_place(int n, int canvas_w, const int32_t* d_hw, int32_t* d_out,
+                             int32_t* d_scratch, hipStream_t s);
+// mask[canvas] = 1 inside any of the rects, else 0.
+hipError_t launch_mask(int n, const int32_t* d_rects, int canvas_h, int canvas_w, uint8_t* d_mask,
+                       hipStream_t s);
+// rect id per cell (-1 outside every rect).
+hipError_t launch_rect_ids(int n, const int32_t* d_rects, int canvas_h, int canvas_w, int32_t* d_rid,
+                           hipStream_t s);
+// scatter/gather of n HWC examples of c channels, element size esize (2 or 4).
+hipError_t launch_scatter(int n, const void* const* d_ptrs, const int32_t* d_rects, int canvas_h,
+                          int canvas_w, int c, int esize, void* d_canvas, int max_h, hipStream_t s);
+hipError_t launch_gather(int n, void* const* d_ptrs, const int32_t* d_rects, int canvas_w, int c,
+                         int esize, const void* d_canvas, int max_h, hipStream_t s);
+
+// --- forward ---------------------------------------------------------------
+// Z[p][20H] = Wx_all[20H][C] x[p] + b_all.
+hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_wx, const void* d_b,
+                             void* d_z, hipStream_t s);
+// Zero the rows of a [n_cells][width] tensor (storage dtype) whose cell is invalid.
+hipError_t launch_zero_invalid(const LayerGeom& g, int width, const uint8_t* d_mask,
+                               const int32_t* d_rid, void* d_t, hipStream_t s);
+// Forward anti-diagonal wavefront, one workgroup per unit.
+hipError_t launch_wavefront_fwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
+                                const int32_t* d_rects, const uint8_t* d_mask, const void* d_u,
+                                void* d_z, float* d_c, void* d_y, hipStream_t s);
+
+// --- backward --------------------------------------------------------------
+hipError_t launch_wavefront_bwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
+                                const int32_t* d_rects, const uint8_t* d_mask, const void* d_u,
+                                const void* d_dy, void* d_z, const float* d_c, hipStream_t s);
+// dX = valid * (dZ Wx_all).
+hipError_t launch_dx(const LayerGeom& g, const void* d_dz, const void* d_wx, const uint8_t* d_mask,
+                     const int32_t* d_rid, void* d_dx, hipStream_t s);
+// Number of cell chunks used by the weight-gradient reduction, and its scratch size.
+int dw_chunks(const LayerGeom& g);
+size_t dw_partial_bytes(const LayerGeom& g);
+hipError_t launch_dw(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y,
+                     const uint8_t* d_mask, const int32_t* d_rid, float* d_part, float* d_dwx,
+                     float* d_du, float* d_db, hipStream_t s);
+
+}  // namespace mdl

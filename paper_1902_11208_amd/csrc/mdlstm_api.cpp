@@ -1,0 +1,444 @@
+// Host side of the C ABI declared in include/mdlstm.h: argument and layout
+// validation (always before the first HIP call), workspace planning, unit
+// ordering and kernel dispatch.
+#include "mdlstm.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+thread_local hipEvent_t g_phase_events[8];
+thread_local bool g_phase_on = false;
+
+hipError_t mark(int i, hipStream_t s) { return g_phase_on ? hipEventRecord(g_phase_events[i], s) : hipSuccess; }
+
+mdlstm_status fail(mdlstm_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+mdlstm_status device_fail(hipError_t e, const char* where) {
+    return fail(MDLSTM_ERR_DEVICE, "%s: %s", where, hipGetErrorString(e));
+}
+
+#define HIP_OR_FAIL(expr)                                     \
+    do {                                                      \
+        hipError_t _e = (expr);                               \
+        if (_e != hipSuccess) return device_fail(_e, #expr);  \
+    } while (0)
+
+constexpr int32_t kMaxDim = (1 << 21) - 1;  // largest canvas side / example side
+constexpr int32_t kMaxPackN = 4096;         // placement keys + skip list fit 48 KB of LDS
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ---------------------------------------------------------------------------
+// Layer descriptor and workspace plan.
+// ---------------------------------------------------------------------------
+mdlstm_status check_desc(const mdlstm_layer_desc* d) {
+    if (!d) return fail(MDLSTM_ERR_INVALID_ARG, "desc is NULL");
+    if (d->dtype != MDLSTM_F32 && d->dtype != MDLSTM_BF16)
+        return fail(MDLSTM_ERR_INVALID_ARG, "dtype %d is not MDLSTM_F32 or MDLSTM_BF16", d->dtype);
+    if (d->c_in < 1 || d->hidden < 1) return fail(MDLSTM_ERR_INVALID_ARG, "c_in and hidden must be positive");
+    if (d->dtype == MDLSTM_F32) {
+        const int h = d->hidden;
+        if (!(h == 4 || h == 8 || h == 16 || h == 32 || h == 64))
+            return fail(MDLSTM_ERR_UNSUPPORTED, "fp32 hidden size %d not built (4, 8, 16, 32, 64)", h);
+        if (d->c_in % 4 || d->c_in < 4 || d->c_in > 256)
+            return fail(MDLSTM_ERR_UNSUPPORTED, "fp32 c_in %d must be a multiple of 4 in [4, 256]", d->c_in);
+    } else {
+        const int h = d->hidden;
+        if (!(h == 32 || h == 64 || h == 128))
+            return fail(MDLSTM_ERR_UNSUPPORTED, "bf16 hidden size %d not built (32, 64, 128)", h);
+        if (d->c_in % 8 || d->c_in < 8 || d->c_in > 256)
+            return fail(MDLSTM_ERR_UNSUPPORTED, "bf16 c_in %d must be a multiple of 8 in [8, 256]", d->c_in);
+    }
+    return MDLSTM_OK;
+}
+
+struct Plan {
+    size_t z, c, rid, rects, units, part, total;
+};
+
+mdl::LayerGeom geom(const mdlstm_layer_desc* d, int32_t ch, int32_t cw) {
+    mdl::LayerGeom g;
+    g.c_in = d->c_in;
+    g.hidden = d->hidden;
+    g.dtype = d->dtype;
+    g.canvas_h = ch;
+    g.canvas_w = cw;
+    g.n_cells = (int64_t)ch * cw;
+    return g;
+}
+
+Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
+    const mdl::LayerGeom g = geom(d, ch, cw);
+    const size_t es = d->dtype == MDLSTM_BF16 ? 2 : 4;
+    const size_t H = (size_t)d->hidden;
+    Plan p;
+    size_t off = 0;
+    p.z = off;
+    off += align_up((size_t)g.n_cells * 20 * H * es);
+    p.c = off;
+    off += align_up((size_t)g.n_cells * 4 * H * 4);
+    p.rid = off;
+    off += align_up((size_t)g.n_cells * 4);
+    p.rects = off;
+    off += align_up((size_t)(nr > 0 ? nr : 1) * 16);
+    p.units = off;
+    off += align_up((size_t)(nr > 0 ? nr : 1) * 16);
+    p.part = off;
+    off += align_up(mdl::dw_partial_bytes(g));
+    p.total = off;
+    return p;
+}
+
+// ---------------------------------------------------------------------------
+// Rectangle validation: inside the canvas, height within the kernel limit,
+// pairwise disjoint. Sorted by y0, a rectangle can only overlap those that
+// start fewer than MDLSTM_MAX_RECT_H rows before it.
+// ---------------------------------------------------------------------------
+mdlstm_status check_rects(int32_t n, const mdlstm_rect* r, int32_t ch, int32_t cw, int32_t* max_h) {
+    if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n_rects is negative");
+    if (n > 0 && !r) return fail(MDLSTM_ERR_INVALID_ARG, "rects is NULL");
+    int32_t mh = 0;
+    for (int32_t k = 0; k < n; ++k) {
+        const mdlstm_rect& a = r[k];
+        if (a.h < 1 || a.w < 1) return fail(MDLSTM_ERR_BAD_LAYOUT, "rect %d has size %dx%d", k, a.h, a.w);
+        if (a.y0 < 0 || a.x0 < 0 || (int64_t)a.y0 + a.h > ch || (int64_t)a.x0 + a.w > cw)
+            return fail(MDLSTM_ERR_BAD_LAYOUT, "rect %d (%d,%d,%d,%d) leaves the %dx%d canvas", k, a.y0, a.x0, a.h,
+                        a.w, ch, cw);
+        if (a.h > MDLSTM_MAX_RECT_H)
+            return fail(MDLSTM_ERR_UNSUPPORTED, "rect %d is %d high; at most %d is supported", k, a.h,
+                        MDLSTM_MAX_RECT_H);
+        mh = std::max(mh, a.h);
+    }
+    std::vector<int32_t> order(n);
+    for (int32_t k = 0; k < n; ++k) order[k] = k;
+    std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+        return r[a].y0 != r[b].y0 ? r[a].y0 < r[b].y0 : a < b;
+    });
+    for (int32_t i = 0; i < n; ++i) {
+        const mdlstm_rect& a = r[order[i]];
+        for (int32_t j = i + 1; j < n; ++j) {
+            const mdlstm_rect& b = r[order[j]];
+            if (b.y0 >= a.y0 + a.h) break;
+            if (b.x0 < a.x0 + a.w && a.x0 < b.x0 + b.w)
+                return fail(MDLSTM_ERR_BAD_LAYOUT, "rects %d and %d overlap", order[i], order[j]);
+        }
+    }
+    *max_h = mh;
+    return MDLSTM_OK;
+}
+
+// Units (rect, direction) ordered longest first (h + w - 1 steps), so the
+// in-order workgroup dispatcher starts the critical-path units first.
+std::vector<int32_t> unit_order(int32_t n, const mdlstm_rect* r) {
+    std::vector<int32_t> u(4 * (size_t)n);
+    for (int32_t k = 0; k < n; ++k)
+        for (int d = 0; d < 4; ++d) u[4 * (size_t)k + d] = 4 * k + d;
+    std::stable_sort(u.begin(), u.end(), [&](int32_t a, int32_t b) {
+        return r[a >> 2].h + r[a >> 2].w > r[b >> 2].h + r[b >> 2].w;
+    });
+    return u;
+}
+
+struct Common {
+    mdl::LayerGeom g;
+    Plan p;
+    int nt;
+    char* ws;
+};
+
+mdlstm_status prepare(const mdlstm_layer_desc* desc, int32_t ch, int32_t cw, const void* d_x, const uint8_t* d_mask,
+                      int32_t n_rects, const mdlstm_rect* rects, const void* d_wx, const void* d_u,
+                      const void* d_b, void* d_workspace, size_t ws_bytes, Common* out) {
+    mdlstm_status st = check_desc(desc);
+    if (st != MDLSTM_OK) return st;
+    if (ch < 0 || cw < 0 || ch > kMaxDim || cw > kMaxDim)
+        return fail(MDLSTM_ERR_INVALID_ARG, "canvas %dx%d out of range", ch, cw);
+    int32_t max_h = 0;
+    st = check_rects(n_rects, rects, ch, cw, &max_h);
+    if (st != MDLSTM_OK) return st;
+    const int64_t cells = (int64_t)ch * cw;
+    if (cells > 0 && (!d_x || !d_mask)) return fail(MDLSTM_ERR_INVALID_ARG, "x or mask is NULL");
+    if (!d_wx || !d_u || !d_b) return fail(MDLSTM_ERR_INVALID_ARG, "a weight pointer is NULL");
+    Plan p = plan(desc, ch, cw, n_rects);
+    if (!d_workspace) return fail(MDLSTM_ERR_INVALID_ARG, "workspace is NULL");
+    if (ws_bytes < p.total)
+        return fail(MDLSTM_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, p.total);
+    out->g = geom(desc, ch, cw);
+    out->p = p;
+    out->nt = (max_h + 15) / 16;
+    if (out->nt < 1) out->nt = 1;
+    out->ws = static_cast<char*>(d_workspace);
+    return MDLSTM_OK;
+}
+
+mdlstm_status stage_layout(const Common& c, int32_t n_rects, const mdlstm_rect* rects, const uint8_t*,
+                           hipStream_t s) {
+    if (n_rects > 0) {
+        std::vector<int32_t> units = unit_order(n_rects, rects);
+        HIP_OR_FAIL(hipMemcpyAsync(c.ws + c.p.rects, rects, (size_t)n_rects * 16, hipMemcpyHostToDevice, s));
+        HIP_OR_FAIL(hipMemcpyAsync(c.ws + c.p.units, units.data(), units.size() * 4, hipMemcpyHostToDevice, s));
+    }
+    HIP_OR_FAIL(mdl::launch_rect_ids(n_rects, reinterpret_cast<const int32_t*>(c.ws + c.p.rects), c.g.canvas_h,
+                                     c.g.canvas_w, reinterpret_cast<int32_t*>(c.ws + c.p.rid), s));
+    return MDLSTM_OK;
+}
+
+size_t pack_ws_bytes(int32_t n) {
+    size_t nn = (size_t)(n > 0 ? n : 1);
+    return align_up(nn * 8) + align_up(nn * 16) + align_up((6 * nn + 1) * 4);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mdlstm_last_error(void) { return g_last_error.c_str(); }
+
+mdlstm_status mdlstm_set_phase_events(int32_t n, void* const* events) {
+    if (n == 0) {
+        g_phase_on = false;
+        return MDLSTM_OK;
+    }
+    if (n != 8 || !events) return fail(MDLSTM_ERR_INVALID_ARG, "phase events: n must be 0 or 8");
+    for (int i = 0; i < 8; ++i) {
+        if (!events[i]) return fail(MDLSTM_ERR_INVALID_ARG, "phase event %d is NULL", i);
+        g_phase_events[i] = reinterpret_cast<hipEvent_t>(events[i]);
+    }
+    g_phase_on = true;
+    return MDLSTM_OK;
+}
+
+size_t mdlstm_pack_workspace_bytes(int32_t n) { return pack_ws_bytes(n); }
+
+mdlstm_status mdlstm_pack_layout(int32_t n, const int32_t* heights, const int32_t* widths, int32_t canvas_w,
+                                 mdlstm_rect* rects, int32_t* canvas_h, uint8_t* d_mask, size_t mask_bytes,
+                                 void* d_workspace, size_t workspace_bytes, void* stream) {
+    if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n is negative");
+    if (n > kMaxPackN) return fail(MDLSTM_ERR_UNSUPPORTED, "at most %d examples per packing call", kMaxPackN);
+    if (!canvas_h) return fail(MDLSTM_ERR_INVALID_ARG, "canvas_h is NULL");
+    if (n > 0 && (!heights || !widths || !rects)) return fail(MDLSTM_ERR_INVALID_ARG, "size or rect array is NULL");
+    if (canvas_w < 1 || canvas_w > kMaxDim) return fail(MDLSTM_ERR_INVALID_ARG, "canvas width %d out of range", canvas_w);
+    for (int32_t k = 0; k < n; ++k) {
+        if (heights[k] < 1 || widths[k] < 1 || heights[k] > kMaxDim || widths[k] > kMaxDim)
+            return fail(MDLSTM_ERR_INVALID_ARG, "example %d has size %dx%d", k, heights[k], widths[k]);
+        if (widths[k] > canvas_w)
+            return fail(MDLSTM_ERR_TOO_WIDE, "example %d is %d wide; the canvas is %d", k, widths[k], canvas_w);
+    }
+    if (n == 0) {
+        *canvas_h = 0;
+        return MDLSTM_OK;
+    }
+    if (!d_workspace || workspace_bytes < pack_ws_bytes(n))
+        return fail(MDLSTM_ERR_WORKSPACE, "packing workspace of %zu bytes, %zu needed", workspace_bytes,
+                    pack_ws_bytes(n));
+    // total canvas height must stay addressable
+    int64_t hsum = 0;
+    for (int32_t k = 0; k < n; ++k) hsum += (int64_t)heights[k] + 1;
+    if (hsum > kMaxDim) return fail(MDLSTM_ERR_UNSUPPORTED, "packed canvas could exceed %d rows", kMaxDim);
+
+    hipStream_t s = as_stream(stream);
+    char* ws = static_cast<char*>(d_workspace);
+    const size_t nn = (size_t)n;
+    int32_t* d_hw = reinterpret_cast<int32_t*>(ws + align_up(nn * 8) + align_up(nn * 16));
+    int32_t* d_out = d_hw + 2 * nn;
+    std::vector<int32_t> hw(2 * nn);
+    std::copy(heights, heights + n, hw.begin());
+    std::copy(widths, widths + n, hw.begin() + n);
+    HIP_OR_FAIL(hipMemcpyAsync(d_hw, hw.data(), 2 * nn * 4, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(mdl::launch_pack_place(n, canvas_w, d_hw, d_out, nullptr, s));
+    std::vector<int32_t> res(4 * nn + 1);
+    HIP_OR_FAIL(hipMemcpyAsync(res.data(), d_out, (4 * nn + 1) * 4, hipMemcpyDeviceToHost, s));
+    HIP_OR_FAIL(hipStreamSynchronize(s));
+    for (size_t k = 0; k < nn; ++k) {
+        rects[k].y0 = res[4 * k];
+        rects[k].x0 = res[4 * k + 1];
+        rects[k].h = res[4 * k + 2];
+        rects[k].w = res[4 * k + 3];
+    }
+    *canvas_h = res[4 * nn];
+    if (d_mask) {
+        const size_t need = (size_t)(*canvas_h) * (size_t)canvas_w;
+        if (mask_bytes < need)
+            return fail(MDLSTM_ERR_WORKSPACE, "mask of %zu bytes, %zu needed", mask_bytes, need);
+        HIP_OR_FAIL(mdl::launch_mask(n, d_out, *canvas_h, canvas_w, d_mask, s));
+    }
+    return MDLSTM_OK;
+}
+
+mdlstm_status mdlstm_pad_layout(int32_t n, const int32_t* heights, const int32_t* widths, mdlstm_rect* tiles,
+                                mdlstm_rect* place, int32_t* canvas_h, int32_t* canvas_w, uint8_t* d_mask,
+                                size_t mask_bytes, void* d_workspace, size_t workspace_bytes, void* stream) {
+    if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n is negative");
+    if (!canvas_h || !canvas_w) return fail(MDLSTM_ERR_INVALID_ARG, "canvas_h or canvas_w is NULL");
+    if (n > 0 && (!heights || !widths || !tiles || !place))
+        return fail(MDLSTM_ERR_INVALID_ARG, "size or rect array is NULL");
+    int32_t hm = 0, wm = 0;
+    for (int32_t k = 0; k < n; ++k) {
+        if (heights[k] < 1 || widths[k] < 1 || heights[k] > kMaxDim || widths[k] > kMaxDim)
+            return fail(MDLSTM_ERR_INVALID_ARG, "example %d has size %dx%d", k, heights[k], widths[k]);
+        hm = std::max(hm, heights[k]);
+        wm = std::max(wm, widths[k]);
+    }
+    if ((int64_t)hm * n > kMaxDim) return fail(MDLSTM_ERR_UNSUPPORTED, "padded canvas exceeds %d rows", kMaxDim);
+    for (int32_t k = 0; k < n; ++k) {
+        tiles[k] = mdlstm_rect{k * hm, 0, hm, wm};
+        place[k] = mdlstm_rect{k * hm, 0, heights[k], widths[k]};
+    }
+    *canvas_h = n * hm;
+    *canvas_w = wm;
+    if (d_mask && n > 0) {
+        const size_t need = (size_t)(*canvas_h) * (size_t)wm;
+        if (mask_bytes < need) return fail(MDLSTM_ERR_WORKSPACE, "mask of %zu bytes, %zu needed", mask_bytes, need);
+        if (!d_workspace || workspace_bytes < pack_ws_bytes(n))
+            return fail(MDLSTM_ERR_WORKSPACE, "packing workspace of %zu bytes, %zu needed", workspace_bytes,
+                        pack_ws_bytes(n));
+        hipStream_t s = as_stream(stream);
+        int32_t* d_r = reinterpret_cast<int32_t*>(static_cast<char*>(d_workspace) + align_up((size_t)n * 8));
+        HIP_OR_FAIL(hipMemcpyAsync(d_r, place, (size_t)n * 16, hipMemcpyHostToDevice, s));
+        HIP_OR_FAIL(mdl::launch_mask(n, d_r, *canvas_h, wm, d_mask, s));
+    }
+    return MDLSTM_OK;
+}
+
+static mdlstm_status pack_io(bool pack, int32_t n, const void* const* ptrs, const mdlstm_rect* rects,
+                             int32_t canvas_h, int32_t canvas_w, int32_t c, int32_t dt, const void* d_canvas,
+                             void* d_workspace, size_t workspace_bytes, void* stream) {
+    if (n < 0 || c < 1) return fail(MDLSTM_ERR_INVALID_ARG, "n must be >= 0 and c >= 1");
+    if (dt != MDLSTM_F32 && dt != MDLSTM_BF16) return fail(MDLSTM_ERR_INVALID_ARG, "dtype %d unknown", dt);
+    if (canvas_h < 0 || canvas_w < 0 || canvas_h > kMaxDim || canvas_w > kMaxDim)
+        return fail(MDLSTM_ERR_INVALID_ARG, "canvas %dx%d out of range", canvas_h, canvas_w);
+    if ((int64_t)canvas_h * canvas_w > 0 && !d_canvas) return fail(MDLSTM_ERR_INVALID_ARG, "canvas is NULL");
+    if (n > 0 && (!ptrs || !rects)) return fail(MDLSTM_ERR_INVALID_ARG, "example or rect array is NULL");
+    int32_t max_h = 0;
+    for (int32_t k = 0; k < n; ++k) {
+        const mdlstm_rect& a = rects[k];
+        if (!ptrs[k]) return fail(MDLSTM_ERR_INVALID_ARG, "example %d pointer is NULL", k);
+        if (a.h < 1 || a.w < 1 || a.y0 < 0 || a.x0 < 0 || (int64_t)a.y0 + a.h > canvas_h ||
+            (int64_t)a.x0 + a.w > canvas_w)
+            return fail(MDLSTM_ERR_BAD_LAYOUT, "rect %d (%d,%d,%d,%d) leaves the %dx%d canvas", k, a.y0, a.x0, a.h,
+                        a.w, canvas_h, canvas_w);
+        max_h = std::max(max_h, a.h);
+    }
+    const int esize = dt == MDLSTM_BF16 ? 2 : 4;
+    hipStream_t s = as_stream(stream);
+    if (n == 0) {
+        if (pack) HIP_OR_FAIL(mdl::launch_scatter(0, nullptr, nullptr, canvas_h, canvas_w, c, esize,
+                                                  const_cast<void*>(d_canvas), 0, s));
+        return MDLSTM_OK;
+    }
+    if (!d_workspace || workspace_bytes < pack_ws_bytes(n))
+        return fail(MDLSTM_ERR_WORKSPACE, "packing workspace of %zu bytes, %zu needed", workspace_bytes,
+                    pack_ws_bytes(n));
+    char* ws = static_cast<char*>(d_workspace);
+    void** d_ptrs = reinterpret_cast<void**>(ws);
+    int32_t* d_r = reinterpret_cast<int32_t*>(ws + align_up((size_t)n * 8));
+    HIP_OR_FAIL(hipMemcpyAsync(d_ptrs, ptrs, (size_t)n * 8, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(hipMemcpyAsync(d_r, rects, (size_t)n * 16, hipMemcpyHostToDevice, s));
+    if (pack)
+        HIP_OR_FAIL(mdl::launch_scatter(n, d_ptrs, d_r, canvas_h, canvas_w, c, esize, const_cast<void*>(d_canvas),
+                                        max_h, s));
+    else
+        HIP_OR_FAIL(mdl::launch_gather(n, d_ptrs, d_r, canvas_w, c, esize, d_canvas, max_h, s));
+    return MDLSTM_OK;
+}
+
+mdlstm_status mdlstm_pack_data(int32_t n, const void* const* d_examples, const mdlstm_rect* rects, int32_t canvas_h,
+                               int32_t canvas_w, int32_t c, int32_t dt, void* d_canvas, void* d_workspace,
+                               size_t workspace_bytes, void* stream) {
+    return pack_io(true, n, d_examples, rects, canvas_h, canvas_w, c, dt, d_canvas, d_workspace, workspace_bytes,
+                   stream);
+}
+
+mdlstm_status mdlstm_unpack_data(int32_t n, void* const* d_examples, const mdlstm_rect* rects, int32_t canvas_h,
+                                 int32_t canvas_w, int32_t c, int32_t dt, const void* d_canvas, void* d_workspace,
+                                 size_t workspace_bytes, void* stream) {
+    return pack_io(false, n, reinterpret_cast<const void* const*>(d_examples), rects, canvas_h, canvas_w, c, dt,
+                   d_canvas, d_workspace, workspace_bytes, stream);
+}
+
+size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, int32_t n_rects) {
+    if (!desc || canvas_h < 0 || canvas_w < 0 || n_rects < 0) return 0;
+    if (desc->hidden < 1 || desc->c_in < 1) return 0;
+    return plan(desc, canvas_h, canvas_w, n_rects).total;
+}
+
+mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
+                             const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
+                             const void* d_u, const void* d_b, void* d_y, void* d_workspace, size_t workspace_bytes,
+                             void* stream) {
+    Common c;
+    mdlstm_status st = prepare(desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_workspace,
+                               workspace_bytes, &c);
+    if (st != MDLSTM_OK) return st;
+    if (c.g.n_cells > 0 && !d_y) return fail(MDLSTM_ERR_INVALID_ARG, "y is NULL");
+    if (c.g.n_cells == 0) return MDLSTM_OK;
+    hipStream_t s = as_stream(stream);
+    st = stage_layout(c, n_rects, rects, d_mask, s);
+    if (st != MDLSTM_OK) return st;
+    const int32_t* rid = reinterpret_cast<const int32_t*>(c.ws + c.p.rid);
+    HIP_OR_FAIL(mark(0, s));
+    HIP_OR_FAIL(mdl::launch_projection(c.g, d_x, d_wx, d_b, c.ws + c.p.z, s));
+    HIP_OR_FAIL(mark(1, s));
+    HIP_OR_FAIL(mdl::launch_zero_invalid(c.g, 4 * c.g.hidden, d_mask, rid, d_y, s));
+    HIP_OR_FAIL(mark(2, s));
+    HIP_OR_FAIL(mdl::launch_wavefront_fwd(c.g, c.nt, 4 * n_rects, reinterpret_cast<const int32_t*>(c.ws + c.p.units),
+                                          reinterpret_cast<const int32_t*>(c.ws + c.p.rects), d_mask, d_u,
+                                          c.ws + c.p.z, reinterpret_cast<float*>(c.ws + c.p.c), d_y, s));
+    HIP_OR_FAIL(mark(3, s));
+    return MDLSTM_OK;
+}
+
+mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
+                              const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
+                              const void* d_u, const void* d_b, const void* d_y, const void* d_dy, void* d_dx,
+                              float* d_dwx, float* d_du, float* d_db, void* d_workspace, size_t workspace_bytes,
+                              void* stream) {
+    Common c;
+    mdlstm_status st = prepare(desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_workspace,
+                               workspace_bytes, &c);
+    if (st != MDLSTM_OK) return st;
+    if (!d_dwx || !d_du || !d_db) return fail(MDLSTM_ERR_INVALID_ARG, "a weight-gradient pointer is NULL");
+    if (c.g.n_cells > 0 && (!d_y || !d_dy || !d_dx)) return fail(MDLSTM_ERR_INVALID_ARG, "y, dy or dx is NULL");
+    hipStream_t s = as_stream(stream);
+    st = stage_layout(c, n_rects, rects, d_mask, s);
+    if (st != MDLSTM_OK) return st;
+    const int32_t* rid = reinterpret_cast<const int32_t*>(c.ws + c.p.rid);
+    HIP_OR_FAIL(mark(4, s));
+    if (c.g.n_cells > 0) {
+        HIP_OR_FAIL(mdl::launch_wavefront_bwd(c.g, c.nt, 4 * n_rects,
+                                              reinterpret_cast<const int32_t*>(c.ws + c.p.units),
+                                              reinterpret_cast<const int32_t*>(c.ws + c.p.rects), d_mask, d_u, d_dy,
+                                              c.ws + c.p.z, reinterpret_cast<const float*>(c.ws + c.p.c), s));
+        HIP_OR_FAIL(mark(5, s));
+        HIP_OR_FAIL(mdl::launch_dx(c.g, c.ws + c.p.z, d_wx, d_mask, rid, d_dx, s));
+    } else {
+        HIP_OR_FAIL(mark(5, s));
+    }
+    HIP_OR_FAIL(mark(6, s));
+    HIP_OR_FAIL(mdl::launch_dw(c.g, c.ws + c.p.z, d_x, d_y, d_mask, rid,
+                               reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
+    HIP_OR_FAIL(mark(7, s));
+    return MDLSTM_OK;
+}
+
+}  // extern "C"

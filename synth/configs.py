@@ -54,7 +54,7 @@ class Workload:
     c_in: int
     hidden: int
     forward_only: bool
-    input_kind: str = "normal"  # "normal": N(0,1) features
+    forget_bias: float = -1.0  # centre of the two forget-gate biases (see params)
 
     @property
     def n(self) -> int:
@@ -80,6 +80,13 @@ class Workload:
         Gate order along the 5H axis: input gate, left forget gate, top forget
         gate, output gate, cell candidate. U's first H columns read the left
         predecessor's hidden state, the last H the top predecessor's.
+
+        Every weight and bias is U(-0.1, 0.1); the biases of the two forget
+        gates are then shifted by `forget_bias`. With a shift of 0 the two
+        forget gates sum to about 1 and the plain cell's state grows without
+        bound along long scans (|c| ~ 1e5 on 600-wide lines, ~1e16 on
+        1200-wide ones); a shift of -1 keeps f_L + f_T near 0.54 and the state
+        bounded.
         """
         H, C = self.hidden, self.c_in
         rng = _rng(self.cid, TAG_PARAMS, 0)
@@ -87,7 +94,9 @@ class Workload:
         for _d in range(4):
             wx.append(rng.uniform(-0.1, 0.1, (5 * H, C)))
             u.append(rng.uniform(-0.1, 0.1, (5 * H, 2 * H)))
-            b.append(rng.uniform(-0.1, 0.1, (5 * H,)))
+            bd = rng.uniform(-0.1, 0.1, (5 * H,))
+            bd[H:3 * H] += self.forget_bias
+            b.append(bd)
         return (_store(np.stack(wx), self.dtype), _store(np.stack(u), self.dtype),
                 _store(np.stack(b), self.dtype))
 
@@ -145,17 +154,20 @@ def workload(cid: int) -> Workload:
         raise ValueError(f"no single-layer workload {cid}; the three-layer stack is stack_workload()")
     name, dtype, sizes, cw, c_in, hidden, fwd_only = _LAYER_CONFIGS[cid]
     hs, ws = sizes()
+    # the tiny workload keeps all parameters U(-0.1, 0.1) as stated for it;
+    # the others centre the forget-gate biases at -1
     return Workload(cid=cid, name=name, dtype=dtype, heights=np.asarray(hs, np.int32),
                     widths=np.asarray(ws, np.int32), canvas_w=cw, c_in=c_in, hidden=hidden,
-                    forward_only=fwd_only)
+                    forward_only=fwd_only, forget_bias=0.0 if cid == 1 else -1.0)
 
 
 def custom_workload(cid: int, heights, widths, canvas_w: int, c_in: int, hidden: int,
-                    dtype: str = "f32") -> Workload:
+                    dtype: str = "f32", forget_bias: float = -1.0) -> Workload:
     """A workload with explicit sizes (used for small test cases); draws keyed by `cid`."""
     return Workload(cid=cid, name=f"custom {cid}", dtype=dtype,
                     heights=np.asarray(heights, np.int32), widths=np.asarray(widths, np.int32),
-                    canvas_w=int(canvas_w), c_in=int(c_in), hidden=int(hidden), forward_only=False)
+                    canvas_w=int(canvas_w), c_in=int(c_in), hidden=int(hidden), forward_only=False,
+                    forget_bias=float(forget_bias))
 
 
 @dataclass
@@ -198,7 +210,9 @@ class StackWorkload:
             for _d in range(4):
                 wx.append(rng.uniform(-0.1, 0.1, (5 * H, c_in)))
                 u.append(rng.uniform(-0.1, 0.1, (5 * H, 2 * H)))
-                b.append(rng.uniform(-0.1, 0.1, (5 * H,)))
+                bd = rng.uniform(-0.1, 0.1, (5 * H,))
+                bd[H:3 * H] -= 1.0  # forget-gate biases centred at -1, as for the single layers
+                b.append(bd)
             layers.append((_store(np.stack(wx), "f32"), _store(np.stack(u), "f32"),
                            _store(np.stack(b), "f32")))
             if li < 2:

@@ -1,0 +1,94 @@
+"""The C-ABI library loads, exports every declared entry point, and rejects
+bad arguments on the host before any HIP call (runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "mdlstm.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mdlstm_\w+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(built_lib):
+    from paper_1902_11208_amd import _lib
+
+    names = _declared()
+    assert "mdlstm_forward" in names and "mdlstm_backward" in names and "mdlstm_pack_layout" in names
+    L = ctypes.CDLL(built_lib)
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(_lib.SIGNATURES), "binding signatures out of sync with the header"
+
+
+FAKE = 0x100000  # never dereferenced: validation fails before any device access
+
+
+def _lib():
+    from paper_1902_11208_amd import _lib
+
+    return _lib
+
+
+def _call_pack(n, hs, ws, cw, ws_bytes=1 << 20):
+    L = _lib()
+    rects = (L.Rect * max(1, n))()
+    ch = ctypes.c_int32(-1)
+    arr_h = (ctypes.c_int32 * max(1, n))(*hs)
+    arr_w = (ctypes.c_int32 * max(1, n))(*ws)
+    st = L.lib().mdlstm_pack_layout(n, arr_h, arr_w, cw, rects, ctypes.byref(ch), None, 0, FAKE, ws_bytes, None)
+    return st, ch.value
+
+
+def test_pack_layout_errors(built_lib):
+    assert _call_pack(-1, [], [], 10)[0] == 1
+    assert _call_pack(2, [2, 2], [5, 11], 10)[0] == 2          # TOO_WIDE
+    assert b"wide" in _lib().lib().mdlstm_last_error()
+    assert _call_pack(1, [0], [3], 10)[0] == 1                 # INVALID_ARG
+    assert _call_pack(1, [2], [3], 0)[0] == 1
+    assert _call_pack(2, [2, 2], [5, 5], 10, ws_bytes=8)[0] == 4  # WORKSPACE
+    st, ch = _call_pack(0, [], [], 10)
+    assert st == 0 and ch == 0
+
+
+def _fwd(desc, ch, cw, rects, ws_bytes=None):
+    L = _lib()
+    arr = (L.Rect * max(1, len(rects)))(*[L.Rect(*r) for r in rects])
+    need = L.lib().mdlstm_workspace_bytes(ctypes.byref(desc), ch, cw, len(rects))
+    return L.lib().mdlstm_forward(ctypes.byref(desc), ch, cw, FAKE, FAKE, len(rects), arr, FAKE, FAKE, FAKE, FAKE,
+                                  FAKE, need if ws_bytes is None else ws_bytes, None)
+
+
+@pytest.mark.parametrize("c_in,hidden,dtype,code", [
+    (16, 12, 0, 5), (16, 128, 0, 5), (6, 16, 0, 5), (16, 16, 7, 1), (16, 16, 1, 5), (12, 32, 1, 5), (0, 16, 0, 1),
+])
+def test_forward_rejects_descriptor(built_lib, c_in, hidden, dtype, code):
+    d = _lib().LayerDesc(c_in, hidden, dtype)
+    assert _fwd(d, 10, 10, [(0, 0, 2, 2)]) == code
+
+
+def test_forward_rejects_layouts(built_lib):
+    d = _lib().LayerDesc(16, 16, 0)
+    assert _fwd(d, 10, 10, [(0, 0, 3, 3), (2, 2, 3, 3)]) == 3       # overlap
+    assert _fwd(d, 10, 10, [(0, 8, 3, 3)]) == 3                    # leaves canvas
+    assert _fwd(d, 10, 10, [(0, 0, 0, 3)]) == 3                    # empty rect
+    assert _fwd(d, 100, 10, [(0, 0, 65, 3)]) == 5                  # too tall for the kernels
+    assert _fwd(d, 10, 10, [(0, 0, 3, 3)], ws_bytes=16) == 4       # workspace
+    # disjoint rectangles pass the layout checks and stop at the (too small) workspace
+    assert _fwd(d, 10, 10, [(0, 0, 3, 3), (4, 0, 3, 3), (0, 4, 3, 6)], ws_bytes=16) == 4
+    assert b"workspace" in _lib().lib().mdlstm_last_error()
+
+
+def test_workspace_bytes_scale():
+    L = _lib()
+    d = L.LayerDesc(16, 16, 0)
+    a = L.lib().mdlstm_workspace_bytes(ctypes.byref(d), 100, 100, 4)
+    b = L.lib().mdlstm_workspace_bytes(ctypes.byref(d), 200, 100, 4)
+    assert a > 100 * 100 * (20 * 16 + 4 * 16) * 4
+    assert b > a
+    assert L.lib().mdlstm_workspace_bytes(None, 1, 1, 1) == 0

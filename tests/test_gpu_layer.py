@@ -1,0 +1,257 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Tolerance, per tensor and per example for Y and dX: both the normwise L2
+relative error ||gpu - oracle||_2 / ||oracle||_2 and the max-norm relative
+error max|gpu - oracle| / max|oracle| must be <= 1e-5 for fp32 storage and
+<= 2e-2 for bf16 storage (bf16 rounds Z, h, the gates and the gradients of
+the pre-activations to 8 significant bits).
+
+These workloads centre the forget-gate biases at -1, which keeps the plain
+cell's state bounded. With forget gates summing to about 1 the state grows
+without bound along long scans (Section III), |c| reaching 1e5 on 600-wide
+lines; there no fp32 evaluation tracks float64 to 1e-5 (a float32 NumPy
+evaluation of the same definition is 1.8e-4 off in dX), and
+test_exploding_state_regime checks the documented looser bounds instead.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+RTOL = {"f32": 1e-5, "bf16": 2e-2}
+GUARD = RTOL
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu(built_lib):
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _check(g, r, dtype, what):
+    from conftest import rel_err, rel_max
+
+    e, m = rel_err(g, r), rel_max(g, r)
+    assert e <= RTOL[dtype], f"{what}: L2 relative error {e:.3e}"
+    assert m <= GUARD[dtype], f"{what}: max-norm relative error {m:.3e}"
+    return e, m
+
+
+def _compare(gpu, ref, dtype, backward=True, label=""):
+    worst = {}
+
+    def upd(key, em):
+        e, m = worst.get(key, (0.0, 0.0))
+        worst[key] = (max(e, em[0]), max(m, em[1]))
+
+    for k, (g, r) in enumerate(zip(gpu["Y"], ref["Y"])):
+        upd("Y", _check(g, r, dtype, f"{label} Y example {k}"))
+    if backward:
+        for k, (g, r) in enumerate(zip(gpu["dX"], ref["dX"])):
+            upd("dX", _check(g, r, dtype, f"{label} dX example {k}"))
+        for nm in ("dWx", "dU", "db"):
+            upd(nm, _check(gpu[nm], ref[nm], dtype, f"{label} {nm}"))
+    _say(f"{label}: worst (L2, max) relative errors " +
+         ", ".join(f"{k} ({v[0]:.1e}, {v[1]:.1e})" for k, v in worst.items()))
+    return worst
+
+
+SMALL = [
+    # name, heights, widths, canvas_w, c_in, hidden, dtype
+    ("H4_ragged", [3, 5, 2, 1], [4, 7, 9, 1], 16, 4, 4, "f32"),
+    ("H8_two_tiles", [17, 5, 1], [20, 3, 30], 32, 8, 8, "f32"),
+    ("H16_tall_narrow", [40, 9, 16], [5, 40, 16], 64, 16, 16, "f32"),
+    ("H32_three_tiles", [40, 33, 2], [37, 50, 3], 96, 32, 32, "f32"),
+    ("H64_four_tiles", [64, 49], [20, 70], 96, 16, 64, "f32"),
+    ("bf16_H32", [20, 12], [30, 18], 64, 16, 32, "bf16"),
+    ("bf16_H64", [33, 12], [30, 41], 80, 32, 64, "bf16"),
+    ("bf16_H128", [48, 10], [30, 60], 128, 64, 128, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_small_cases_forward_backward(case):
+    import gpu_run
+    import oracle_run
+    from synth.configs import custom_workload
+
+    name, hs, ws, cw, c_in, H, dt = case
+    _say(f"case {name}: heights={hs} widths={ws} W={cw} C={c_in} H={H} {dt}")
+    wl = custom_workload(100 + SMALL.index(case), hs, ws, cw, c_in, H, dt)
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    gpu = gpu_run.run_layer(xs, params, dys, hs, ws, cw, dtype=dt)
+    ref = oracle_run.run_layer(xs, params, dys)
+    _compare(gpu, ref, dt, label=name)
+
+
+def test_config1_forward():
+    import gpu_run
+    import oracle_run
+    from synth import configs
+
+    wl = configs.workload(1)
+    _say(f"config 1: n={wl.n} H={wl.hidden} C={wl.c_in}")
+    xs, params = wl.examples(), wl.params()
+    gpu = gpu_run.run_layer(xs, params, None, wl.heights, wl.widths, wl.canvas_w, backward=False)
+    ref = oracle_run.run_layer(xs, params, None, backward=False)
+    _compare(gpu, ref, "f32", backward=False, label="config1")
+    # cells outside every example are exactly zero
+    m = gpu["mask"].cpu().numpy()
+    yc = gpu["y_canvas"].cpu().numpy()
+    assert np.all(yc[m == 0] == 0)
+
+
+@pytest.mark.parametrize("kind", ["packed", "padded"])
+def test_config2_words_forward_backward(kind):
+    import gpu_run
+    import oracle_run
+    from synth import configs
+
+    wl = configs.workload(2)
+    _say(f"config 2 ({kind}): n={wl.n} H={wl.hidden} C={wl.c_in}")
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    gpu = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w, kind=kind)
+    ref = oracle_run.run_layer(xs, params, dys, workers=oracle_run.default_workers())
+    _compare(gpu, ref, "f32", label=f"config2 {kind}")
+    m = gpu["mask"].cpu().numpy()
+    assert np.all(gpu["y_canvas"].cpu().numpy()[m == 0] == 0)
+    assert np.all(gpu["dx_canvas"].cpu().numpy()[m == 0] == 0)
+
+
+def test_config3_lines_forward_backward():
+    # full batch on the GPU; per-example Y and dX checked on a seeded sample of
+    # 12 examples (the oracle takes about 2 s per example), weight gradients on
+    # a second GPU run packing just that sample
+    import gpu_run
+    import oracle_run
+    from synth import configs
+
+    wl = configs.workload(3)
+    _say(f"config 3: n={wl.n} H={wl.hidden} C={wl.c_in}")
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    gpu = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w)
+    pick = sorted(np.random.default_rng(3).choice(wl.n, size=12, replace=False).tolist())
+    pick = sorted(set(pick) | {int(np.argmax(wl.widths)), int(np.argmin(wl.widths))})
+    ref = oracle_run.run_layer([xs[k] for k in pick], params, [dys[k] for k in pick],
+                               workers=oracle_run.default_workers())
+    sub = {"Y": [gpu["Y"][k] for k in pick], "dX": [gpu["dX"][k] for k in pick]}
+    _compare(sub, ref, "f32", backward=False, label="config3 sample Y")
+    _compare({"Y": sub["dX"]}, {"Y": ref["dX"]}, "f32", backward=False, label="config3 sample dX")
+    gsub = gpu_run.run_layer([xs[k] for k in pick], params, [dys[k] for k in pick], wl.heights[pick],
+                             wl.widths[pick], wl.canvas_w)
+    _compare(gsub, ref, "f32", label="config3 sample packed alone")
+
+
+def test_masked_holes_and_touching_rectangles():
+    # scheduling rectangles that touch (no separators) and mask holes inside
+    # them: the recurrence must restart at rectangle edges and at masked cells
+    import gpu_run
+    from oracle import mdlstm, pack
+    from paper_1902_11208_amd import api
+
+    rng = np.random.default_rng(5)
+    C, H = 8, 16  # parameters U(-0.3, 0.3): short scans, bounded state
+    rects = np.array([[0, 0, 5, 7], [0, 7, 5, 4], [5, 0, 3, 11], [8, 2, 2, 2]], np.int32)
+    ch, cw = 10, 11
+    mask = pack.make_mask(rects, ch, cw)
+    mask[1, 1] = mask[3, 8] = mask[6, 5] = 0
+    x = rng.standard_normal((ch, cw, C)).astype(np.float32)
+    dY = rng.standard_normal((ch, cw, 4 * H)).astype(np.float32)
+    params = [rng.uniform(-0.3, 0.3, s).astype(np.float32) for s in ((4, 5 * H, C), (4, 5 * H, 2 * H), (4, 5 * H))]
+    _say("case masked holes: 4 touching rects")
+    dmask = torch.from_numpy(mask).cuda()
+    layer = api.MDLSTMLayer(*(gpu_run.to_dev(p, "f32") for p in params), ch, cw, rects, dmask)
+    y = layer.forward(gpu_run.to_dev(x, "f32"))
+    dx, dwx, du, db = layer.backward(gpu_run.to_dev(dY, "f32"))
+    torch.cuda.synchronize()
+    Yr, caches = mdlstm.units_forward(x, mask, rects, params)
+    dXr, dWr, dUr, dbr = mdlstm.units_backward(x, mask, rects, params, caches, dY)
+    for got, ref, nm in ((y, Yr, "Y"), (dx, dXr, "dX"), (dwx, dWr, "dWx"), (du, dUr, "dU"), (db, dbr, "db")):
+        e, m = _check(gpu_run.to_np(got), ref, "f32", nm)
+        _say(f"  {nm}: L2 {e:.2e} max {m:.2e}")
+
+
+def test_flip_symmetry_is_bitexact():
+    # mirror the canvas left-right and swap the parameters of direction pairs
+    # (0,1), (2,3): every unit does identical arithmetic, so Y mirrors exactly
+    import gpu_run
+    from paper_1902_11208_amd import api
+    from synth.configs import custom_workload
+
+    wl = custom_workload(7, [12, 9, 16], [30, 21, 17], 64, 16, 16)
+    xs, params = wl.examples(), wl.params()
+    _say("case flip symmetry")
+    a = gpu_run.run_layer(xs, params, None, wl.heights, wl.widths, wl.canvas_w, backward=False)
+    perm = [1, 0, 3, 2]
+    pf = [p[perm] for p in params]
+    H = wl.hidden
+    b = gpu_run.run_layer([x[:, ::-1].copy() for x in xs], pf, None, wl.heights, wl.widths, wl.canvas_w,
+                          backward=False)
+    for ya, yb in zip(a["Y"], b["Y"]):
+        mirrored = np.concatenate([ya[:, ::-1, p * H:(p + 1) * H] for p in perm], axis=2)
+        assert np.array_equal(mirrored, yb)
+    del api
+
+
+def test_placement_invariance_and_determinism():
+    # an example's output does not depend on where it sits or on the canvas
+    # width; repeated runs are bitwise identical
+    import gpu_run
+    from synth.configs import custom_workload
+
+    wl = custom_workload(8, [16, 16, 16, 16], [40, 8, 25, 60], 64, 16, 16)
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    _say("case placement invariance")
+    r1 = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, 64)
+    r2 = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, 200)
+    r3 = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, 64)
+    assert not np.array_equal(r1["rects"], r2["rects"])
+    for k in range(wl.n):
+        assert np.array_equal(r1["Y"][k], r2["Y"][k])
+        assert np.array_equal(r1["dX"][k], r2["dX"][k])
+    for nm in ("Y", "dX"):
+        for k in range(wl.n):
+            assert np.array_equal(r1[nm][k], r3[nm][k])
+    for nm in ("dWx", "dU", "db"):
+        assert np.array_equal(r1[nm], r3[nm])
+
+
+def test_exploding_state_regime():
+    # forget-gate biases U(-0.1, 0.1): the state grows to |c| ~ 1e5 over these
+    # lines. Y still matches to 1e-5 (L2); in the gradients the fp32 floor of
+    # the problem itself is ~2e-4 (a float32 NumPy evaluation of the same
+    # definition), so they are held to 1e-3 L2 here.
+    import gpu_run
+    import oracle_run
+    from conftest import rel_err, rel_max
+    from synth.configs import custom_workload
+
+    wl = custom_workload(9, [32, 32, 64, 49], [600, 350, 20, 70], 2048, 32, 32, forget_bias=0.0)
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    _say("case exploding state: forget biases U(-0.1, 0.1)")
+    gpu = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w)
+    ref = oracle_run.run_layer(xs, params, dys, workers=oracle_run.default_workers())
+    for k in range(wl.n):
+        e = rel_err(gpu["Y"][k], ref["Y"][k])
+        _say(f"  example {k}: Y L2 {e:.1e} max {rel_max(gpu['Y'][k], ref['Y'][k]):.1e}, "
+             f"dX L2 {rel_err(gpu['dX'][k], ref['dX'][k]):.1e}")
+        assert e <= 1e-5
+        assert rel_err(gpu["dX"][k], ref["dX"][k]) <= 1e-3
+    for nm in ("dWx", "dU", "db"):
+        e = rel_err(gpu[nm], ref[nm])
+        _say(f"  {nm}: L2 {e:.1e}")
+        assert e <= 1e-3
