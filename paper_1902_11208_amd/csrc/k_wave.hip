@@ -107,14 +107,51 @@ struct WaveArgs {
     int canvas_w;
 };
 
+// Raw 4-element loads kept in registers until use (prefetched one step ahead).
+template <typename T>
+struct Raw;
+template <>
+struct Raw<float> {
+    using V = float4;
+    static __device__ __forceinline__ V load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+    static __device__ __forceinline__ floatx4 f(V v) { return floatx4{v.x, v.y, v.z, v.w}; }
+    static __device__ __forceinline__ V zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+};
+template <>
+struct Raw<bf16_t> {
+    using V = uint2;
+    static __device__ __forceinline__ V load(const bf16_t* p) { return *reinterpret_cast<const uint2*>(p); }
+    static __device__ __forceinline__ floatx4 f(V v) {
+        return floatx4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
+                       __uint_as_float(v.y & 0xffff0000u)};
+    }
+    static __device__ __forceinline__ V zero() { return make_uint2(0, 0); }
+};
+
+// Whether a unit keeps the next step's global loads in a second register set.
+// Large tiles (H = 128, or many N tiles at H = 64) would spill instead.
+template <int H, int NT, typename T>
+struct Prefetch {
+    static constexpr bool on = (H <= 32 && NT <= 2) || (H == 64 && NT == 1);
+};
+
 // ---------------------------------------------------------------------------
 // Forward.
 // ---------------------------------------------------------------------------
+template <int NT, typename T>
+struct FwdPre {
+    typename Raw<T>::V z[NT][5];
+    int64_t p[NT];
+    uint32_t m[NT];
+    bool live[NT];
+};
+
 template <int H, int NT, typename T>
 __global__ void __launch_bounds__(64 * ((H + 15) / 16))
 k_wave_fwd(WaveArgs a) {
     using Ops = WaveOps<T>;
     using Op = typename Ops::Op;
+    using R4 = Raw<T>;
     constexpr int G = 5 * H;             // gate rows per direction
     constexpr int KRUN = H / 2;          // hcat values per reduction slot
     constexpr int NSTEP = KRUN / Ops::PER_STEP;
@@ -135,6 +172,7 @@ k_wave_fwd(WaveArgs a) {
     T* __restrict__ Z = static_cast<T*>(a.z);
     T* __restrict__ Y = static_cast<T*>(a.y);
     float* __restrict__ Cs = a.c;
+    const int steps = R.h + R.w - 1;
 
     for (int i = threadIdx.x; i < 2 * ROWS * HP; i += blockDim.x) (&hbuf[0][0][0])[i] = T(0);
     for (int i = threadIdx.x; i < 2 * ROWS * H; i += blockDim.x) (&cbuf[0][0][0])[i] = 0.0f;
@@ -151,26 +189,36 @@ k_wave_fwd(WaveArgs a) {
     floatx4 cprev[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) cprev[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    __syncthreads();
 
-    const int steps = R.h + R.w - 1;
-    for (int s = 0; s < steps; ++s) {
+    // Global loads of step s (pre-activations and mask); they depend only on
+    // the position, never on the recurrence, so they can be issued early.
+    auto fetch = [&](int s, FwdPre<NT, T>& b) {
+        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            b.live[nt] = false;
+            if (s >= steps || 16 * nt > yhi || 16 * nt + 15 < ylo) continue;
+            const int yy = 16 * nt + n16, xx = s - yy;
+            const bool live = jok && yy < R.h && xx >= 0 && xx < R.w;
+            b.live[nt] = live;
+            if (live) {
+                const int64_t p = canvas_index(R, d, yy, xx, a.canvas_w);
+                b.p[nt] = p;
+                b.m[nt] = a.mask[p];
+                const T* zp = Z + p * (4 * G) + d * G + j0;
+#pragma unroll
+                for (int t = 0; t < 5; ++t) b.z[nt][t] = R4::load(zp + t * H);
+            }
+        }
+    };
+
+    auto compute = [&](int s, const FwdPre<NT, T>& b) {
         const int cur = s & 1, prv = cur ^ 1;
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;  // uniform over the workgroup
-            const int yy = 16 * nt + n16, xx = s - yy;
-            const bool act = yy < R.h && xx >= 0 && xx < R.w;
-            const int64_t p = act ? canvas_index(R, d, yy, xx, a.canvas_w) : 0;
-            const bool live = act && jok;
-            floatx4 zv[5];
-            uint8_t m = 0;
-            if (live) {
-                m = a.mask[p];
-#pragma unroll
-                for (int t = 0; t < 5; ++t) zv[t] = St<T>::ld4(Z + p * (4 * G) + d * G + t * H + j0);
-            }
+            const int yy = 16 * nt + n16;
             // B operand: slot q < 2 reads h_L (row yy of the previous diagonal),
             // q >= 2 reads h_T (row yy - 1); LDS row index is local row + 1.
             const T* brow = (q < 2) ? &hbuf[prv][yy + 1][q * KRUN] : &hbuf[prv][yy][(q - 2) * KRUN];
@@ -179,27 +227,28 @@ k_wave_fwd(WaveArgs a) {
             for (int t = 0; t < 5; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < NSTEP; ++ks) {
-                const Op b = Ops::lds_op(brow + ks * Ops::PER_STEP);
+                const Op bop = Ops::lds_op(brow + ks * Ops::PER_STEP);
 #pragma unroll
-                for (int t = 0; t < 5; ++t) acc[t] = Ops::mma(A[t][ks], b, acc[t]);
+                for (int t = 0; t < 5; ++t) acc[t] = Ops::mma(A[t][ks], bop, acc[t]);
             }
             floatx4 cn = floatx4{0.f, 0.f, 0.f, 0.f}, hn = cn;
-            if (live) {
+            if (b.live[nt]) {
                 const floatx4 cL = cprev[nt];
                 const floatx4 cT = lds_ld4f(&cbuf[prv][yy][j0]);
                 floatx4 gi, gfl, gft, go, gg;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    gi[r] = sigm(acc[0][r] + zv[0][r]);
-                    gfl[r] = sigm(acc[1][r] + zv[1][r]);
-                    gft[r] = sigm(acc[2][r] + zv[2][r]);
-                    go[r] = sigm(acc[3][r] + zv[3][r]);
-                    gg[r] = tanh_acc(acc[4][r] + zv[4][r]);
-                    float c = gi[r] * gg[r] + gfl[r] * cL[r] + gft[r] * cT[r];
+                    gi[r] = sigm_fast(acc[0][r] + R4::f(b.z[nt][0])[r]);
+                    gfl[r] = sigm_fast(acc[1][r] + R4::f(b.z[nt][1])[r]);
+                    gft[r] = sigm_fast(acc[2][r] + R4::f(b.z[nt][2])[r]);
+                    go[r] = sigm_fast(acc[3][r] + R4::f(b.z[nt][3])[r]);
+                    gg[r] = tanh_fast(acc[4][r] + R4::f(b.z[nt][4])[r]);
+                    const float c = gi[r] * gg[r] + gfl[r] * cL[r] + gft[r] * cT[r];
                     cn[r] = c;
-                    hn[r] = go[r] * tanh_acc(c);
+                    hn[r] = go[r] * tanh_fast(c);
                 }
-                if (m) {
+                const int64_t p = b.p[nt];
+                if (b.m[nt]) {
                     T* zp = Z + p * (4 * G) + d * G + j0;
                     St<T>::st4(zp + 0 * H, gi);
                     St<T>::st4(zp + 1 * H, gfl);
@@ -220,6 +269,27 @@ k_wave_fwd(WaveArgs a) {
             }
         }
         __syncthreads();
+    };
+
+    __syncthreads();
+    FwdPre<NT, T> b0, b1;
+    if constexpr (Prefetch<H, NT, T>::on) {
+        // two register sets in turn: step s computes from one while the loads
+        // of step s + 1 land in the other
+        fetch(0, b0);
+        int s = 0;
+        for (; s + 1 < steps; s += 2) {
+            fetch(s + 1, b1);
+            compute(s, b0);
+            fetch(s + 2, b0);
+            compute(s + 1, b1);
+        }
+        if (s < steps) compute(s, b0);
+    } else {
+        for (int s = 0; s < steps; ++s) {
+            fetch(s, b0);
+            compute(s, b0);
+        }
     }
 }
 
@@ -232,11 +302,21 @@ k_wave_fwd(WaveArgs a) {
 // Phase A does the cell update and writes da (over the saved gates, and to
 // LDS); phase B contracts da with U^T for the predecessors.
 // ---------------------------------------------------------------------------
+template <int NT, typename T>
+struct BwdPre {
+    typename Raw<T>::V g[NT][5], dy[NT];
+    float4 c[NT], cl[NT], ct[NT];
+    int64_t p[NT];
+    uint32_t m[NT];
+    bool live[NT];
+};
+
 template <int H, int NT, typename T>
 __global__ void __launch_bounds__(64 * ((H + 15) / 16))
 k_wave_bwd(WaveArgs a) {
     using Ops = WaveOps<T>;
     using Op = typename Ops::Op;
+    using R4 = Raw<T>;
     constexpr int G = 5 * H;
     constexpr int KRUN = G / 4;          // da values per reduction slot
     constexpr int NSTEP = KRUN / Ops::PER_STEP;
@@ -257,6 +337,7 @@ k_wave_bwd(WaveArgs a) {
     T* __restrict__ Z = static_cast<T*>(a.z);
     const T* __restrict__ DY = static_cast<const T*>(a.dy);
     const float* __restrict__ Cs = a.c;
+    const int steps = R.h + R.w - 1;
 
     for (int i = threadIdx.x; i < NT * 16 * GP; i += blockDim.x) (&dabuf[0][0])[i] = T(0);
     for (int i = threadIdx.x; i < (NT * 16 + 1) * H; i += blockDim.x) {
@@ -282,51 +363,67 @@ k_wave_bwd(WaveArgs a) {
         dcl[nt] = gl[nt];
         dct_new[nt] = gl[nt];
     }
-    __syncthreads();
 
-    const int steps = R.h + R.w - 1;
-    for (int s = steps - 1; s >= 0; --s) {
+    auto fetch = [&](int s, BwdPre<NT, T>& b) {
+        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            b.live[nt] = false;
+            if (s < 0 || 16 * nt > yhi || 16 * nt + 15 < ylo) continue;
+            const int yy = 16 * nt + n16, xx = s - yy;
+            const bool live = jok && yy < R.h && xx >= 0 && xx < R.w;
+            b.live[nt] = live;
+            if (live) {
+                const int64_t p = canvas_index(R, d, yy, xx, a.canvas_w);
+                b.p[nt] = p;
+                b.m[nt] = a.mask[p];
+                const T* zp = Z + p * (4 * G) + d * G + j0;
+#pragma unroll
+                for (int t = 0; t < 5; ++t) b.g[nt][t] = R4::load(zp + t * H);
+                b.dy[nt] = R4::load(DY + p * (4 * H) + d * H + j0);
+                b.c[nt] = Raw<float>::load(Cs + p * (4 * H) + d * H + j0);
+                b.cl[nt] = xx > 0 ? Raw<float>::load(Cs + canvas_index(R, d, yy, xx - 1, a.canvas_w) * (4 * H) + d * H + j0)
+                                  : Raw<float>::zero();
+                b.ct[nt] = yy > 0 ? Raw<float>::load(Cs + canvas_index(R, d, yy - 1, xx, a.canvas_w) * (4 * H) + d * H + j0)
+                                  : Raw<float>::zero();
+            }
+        }
+    };
+
+    auto compute = [&](int s, const BwdPre<NT, T>& b) {
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
         // Phase A: cell updates of diagonal s.
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;
-            const int yy = 16 * nt + n16, xx = s - yy;
-            const bool act = yy < R.h && xx >= 0 && xx < R.w;
+            const int yy = 16 * nt + n16;
             floatx4 da[5];
 #pragma unroll
             for (int t = 0; t < 5; ++t) da[t] = floatx4{0.f, 0.f, 0.f, 0.f};
             floatx4 ndl = da[0], ndt = da[0];
-            if (act && jok) {
-                const int64_t p = canvas_index(R, d, yy, xx, a.canvas_w);
-                if (a.mask[p]) {
-                    const T* zp = Z + p * (4 * G) + d * G + j0;
-                    const floatx4 gi = St<T>::ld4(zp), gfl = St<T>::ld4(zp + H), gft = St<T>::ld4(zp + 2 * H),
-                                  go = St<T>::ld4(zp + 3 * H), gg = St<T>::ld4(zp + 4 * H);
-                    const floatx4 dyv = St<T>::ld4(DY + p * (4 * H) + d * H + j0);
-                    const floatx4 cv = St<float>::ld4(Cs + p * (4 * H) + d * H + j0);
-                    floatx4 cL = floatx4{0.f, 0.f, 0.f, 0.f}, cT = cL;
-                    if (xx > 0) cL = St<float>::ld4(Cs + canvas_index(R, d, yy, xx - 1, a.canvas_w) * (4 * H) + d * H + j0);
-                    if (yy > 0) cT = St<float>::ld4(Cs + canvas_index(R, d, yy - 1, xx, a.canvas_w) * (4 * H) + d * H + j0);
-                    const floatx4 gt = lds_ld4f(&gtbuf[yy + 1][j0]);
-                    const floatx4 dcE = lds_ld4f(&dctbuf[yy + 1][j0]);
+            if (b.live[nt] && b.m[nt]) {
+                const floatx4 gi = R4::f(b.g[nt][0]), gfl = R4::f(b.g[nt][1]), gft = R4::f(b.g[nt][2]),
+                              go = R4::f(b.g[nt][3]), gg = R4::f(b.g[nt][4]);
+                const floatx4 dyv = R4::f(b.dy[nt]);
+                const floatx4 cv = Raw<float>::f(b.c[nt]), cL = Raw<float>::f(b.cl[nt]), cT = Raw<float>::f(b.ct[nt]);
+                const floatx4 gt = lds_ld4f(&gtbuf[yy + 1][j0]);
+                const floatx4 dcE = lds_ld4f(&dctbuf[yy + 1][j0]);
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        float dh = dyv[r] + gl[nt][r] + gt[r];
-                        float tc = tanh_acc(cv[r]);
-                        float dc = dcl[nt][r] + dcE[r] + dh * go[r] * (1.0f - tc * tc);
-                        da[0][r] = dc * gg[r] * gi[r] * (1.0f - gi[r]);
-                        da[1][r] = dc * cL[r] * gfl[r] * (1.0f - gfl[r]);
-                        da[2][r] = dc * cT[r] * gft[r] * (1.0f - gft[r]);
-                        da[3][r] = dh * tc * go[r] * (1.0f - go[r]);
-                        da[4][r] = dc * gi[r] * (1.0f - gg[r] * gg[r]);
-                        ndl[r] = dc * gfl[r];
-                        ndt[r] = dc * gft[r];
-                    }
-                    T* dz = Z + p * (4 * G) + d * G + j0;
-#pragma unroll
-                    for (int t = 0; t < 5; ++t) St<T>::st4(dz + t * H, da[t]);
+                for (int r = 0; r < 4; ++r) {
+                    const float dh = dyv[r] + gl[nt][r] + gt[r];
+                    const float tc = tanh_fast(cv[r]);
+                    const float dc = dcl[nt][r] + dcE[r] + dh * go[r] * (1.0f - tc * tc);
+                    da[0][r] = dc * gg[r] * gi[r] * (1.0f - gi[r]);
+                    da[1][r] = dc * cL[r] * gfl[r] * (1.0f - gfl[r]);
+                    da[2][r] = dc * cT[r] * gft[r] * (1.0f - gft[r]);
+                    da[3][r] = dh * tc * go[r] * (1.0f - go[r]);
+                    da[4][r] = dc * gi[r] * (1.0f - gg[r] * gg[r]);
+                    ndl[r] = dc * gfl[r];
+                    ndt[r] = dc * gft[r];
                 }
+                T* dz = Z + b.p[nt] * (4 * G) + d * G + j0;
+#pragma unroll
+                for (int t = 0; t < 5; ++t) St<T>::st4(dz + t * H, da[t]);
             }
             if (jok) {
 #pragma unroll
@@ -345,18 +442,37 @@ k_wave_bwd(WaveArgs a) {
             floatx4 accL = floatx4{0.f, 0.f, 0.f, 0.f}, accT = accL;
 #pragma unroll
             for (int ks = 0; ks < NSTEP; ++ks) {
-                const Op b = Ops::lds_op(brow + ks * Ops::PER_STEP);
-                accL = Ops::mma(AL[ks], b, accL);
-                accT = Ops::mma(AT[ks], b, accT);
+                const Op bop = Ops::lds_op(brow + ks * Ops::PER_STEP);
+                accL = Ops::mma(AL[ks], bop, accL);
+                accT = Ops::mma(AT[ks], bop, accT);
             }
             gl[nt] = accL;
             if (jok) {
                 *reinterpret_cast<float4*>(&gtbuf[yy][j0]) = make_float4(accT[0], accT[1], accT[2], accT[3]);
-                floatx4 v = dct_new[nt];
+                const floatx4 v = dct_new[nt];
                 *reinterpret_cast<float4*>(&dctbuf[yy][j0]) = make_float4(v[0], v[1], v[2], v[3]);
             }
         }
         __syncthreads();
+    };
+
+    __syncthreads();
+    BwdPre<NT, T> b0, b1;
+    if constexpr (Prefetch<H, NT, T>::on) {
+        fetch(steps - 1, b0);
+        int s = steps - 1;
+        for (; s - 1 >= 0; s -= 2) {
+            fetch(s - 1, b1);
+            compute(s, b0);
+            fetch(s - 2, b0);
+            compute(s - 1, b1);
+        }
+        if (s >= 0) compute(s, b0);
+    } else {
+        for (int s = steps - 1; s >= 0; --s) {
+            fetch(s, b0);
+            compute(s, b0);
+        }
     }
 }
 

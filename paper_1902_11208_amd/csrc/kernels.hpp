@@ -56,5 +56,12 @@ size_t dw_partial_bytes(const LayerGeom& g);
 hipError_t launch_dw(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y,
                      const uint8_t* d_mask, const int32_t* d_rid, float* d_part, float* d_dwx,
                      float* d_du, float* d_db, hipStream_t s);
+// Input and weight gradients together, staged through LDS by canvas-row
+// strips (hidden sizes up to 32 and c_in + 2H + 1 <= 128).
+bool strip_supported(const LayerGeom& g);
+size_t strip_partial_bytes(const LayerGeom& g);
+hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y,
+                            const void* d_wx, const uint8_t* d_mask, const int32_t* d_rid, void* d_dx,
+                            float* d_part, float* d_dwx, float* d_du, float* d_db, hipStream_t s);
 
 }  // namespace mdl

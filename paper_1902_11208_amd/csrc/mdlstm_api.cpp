@@ -104,7 +104,7 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
     p.units = off;
     off += align_up((size_t)(nr > 0 ? nr : 1) * 16);
     p.part = off;
-    off += align_up(mdl::dw_partial_bytes(g));
+    off += align_up(mdl::strip_supported(g) ? mdl::strip_partial_bytes(g) : mdl::dw_partial_bytes(g));
     p.total = off;
     return p;
 }
@@ -429,14 +429,19 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
                                               reinterpret_cast<const int32_t*>(c.ws + c.p.units),
                                               reinterpret_cast<const int32_t*>(c.ws + c.p.rects), d_mask, d_u, d_dy,
                                               c.ws + c.p.z, reinterpret_cast<const float*>(c.ws + c.p.c), s));
-        HIP_OR_FAIL(mark(5, s));
-        HIP_OR_FAIL(mdl::launch_dx(c.g, c.ws + c.p.z, d_wx, d_mask, rid, d_dx, s));
-    } else {
-        HIP_OR_FAIL(mark(5, s));
     }
-    HIP_OR_FAIL(mark(6, s));
-    HIP_OR_FAIL(mdl::launch_dw(c.g, c.ws + c.p.z, d_x, d_y, d_mask, rid,
-                               reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
+    HIP_OR_FAIL(mark(5, s));
+    if (c.g.n_cells > 0 && mdl::strip_supported(c.g)) {
+        // input and weight gradients in one pass (phase boundary 6 coincides with 5)
+        HIP_OR_FAIL(mark(6, s));
+        HIP_OR_FAIL(mdl::launch_bwd_strip(c.g, c.ws + c.p.z, d_x, d_y, d_wx, d_mask, rid, d_dx,
+                                          reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
+    } else {
+        if (c.g.n_cells > 0) HIP_OR_FAIL(mdl::launch_dx(c.g, c.ws + c.p.z, d_wx, d_mask, rid, d_dx, s));
+        HIP_OR_FAIL(mark(6, s));
+        HIP_OR_FAIL(mdl::launch_dw(c.g, c.ws + c.p.z, d_x, d_y, d_mask, rid,
+                                   reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
+    }
     HIP_OR_FAIL(mark(7, s));
     return MDLSTM_OK;
 }
