@@ -141,6 +141,8 @@ size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, i
 /*
  * Forward pass of the four-direction layer over a canvas.
  *
+ * Every device pointer of mdlstm_forward and mdlstm_backward must be 16-byte
+ * aligned (INVALID_ARG otherwise).
  * d_x: [canvas_h][canvas_w][c_in], storage dtype.
  * d_mask: uint8 [canvas_h][canvas_w]; a cell is valid iff its mask byte is
  *   nonzero AND it lies inside one of the rectangles.

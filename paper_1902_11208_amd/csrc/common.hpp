@@ -6,6 +6,7 @@
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // 16-byte chunk held in registers
 typedef uint16_t bf16_t;  // bfloat16 storage (upper half of an fp32)
 
 // ---------------------------------------------------------------------------
@@ -118,4 +119,12 @@ __device__ __forceinline__ int64_t canvas_index(const RectD& R, int d, int y, in
     int cy = R.y0 + ((d & 2) ? (R.h - 1 - y) : y);
     int cx = R.x0 + ((d & 1) ? (R.w - 1 - x) : x);
     return (int64_t)cy * canvas_w + cx;
+}
+
+// Workgroup barrier that orders LDS accesses only: global memory operations
+// of the waves stay in flight across it (__syncthreads also waits for them).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }

@@ -1,27 +1,26 @@
 // Anti-diagonal wavefront recurrence of the four-direction 2D MDLSTM
 // (Section III cell; Section IV-A: after input skewing every cell of an
-// anti-diagonal depends only on the previous anti-diagonal, so a whole
-// diagonal is computed at once; Section V: state from predecessors outside
-// the cell's rectangle or with mask 0 is blocked).
+// anti-diagonal depends only on the previous anti-diagonal; Section V: state
+// from predecessors outside the cell's rectangle or with mask 0 is blocked).
 //
 // One workgroup runs one unit = (rectangle, scan direction) and walks its
-// h + w - 1 local anti-diagonals in order (forward) or in reverse (backward).
-// Cells of a diagonal are indexed by their local row y, so a cell's left
-// predecessor is row y on the previous diagonal and its top predecessor is
-// row y - 1.
+// h + w - 1 local anti-diagonals. Cells of a diagonal are indexed by local
+// row y: the left predecessor is row y of the previous diagonal, the top
+// predecessor row y - 1.
 //
-// Per step, the recurrent contraction is a small dense product done on MFMA:
-//   forward   pre[r][cell] += sum_k U[r][k]   hcat[cell][k],  hcat = [h_L ; h_T]
-//   backward  g[k][cell]    = sum_r U[r][k]   da[cell][r]
-// The workgroup has one wave per block of 16 hidden units (jb). Wave jb keeps,
-// for its 16 hidden units, U's rows of all five gates (forward) or U's columns
-// for both predecessors (backward) in registers for the whole unit. Output
-// tile row 4q + r and column n of lane 16q + n map to hidden unit
-// j = 16 jb + 4q + r and the cell of local row 16 nt + n, so every lane holds
-// all five gates of four hidden units of one cell and does the cell update
-// without any exchange. Values that go to the same row on the next diagonal
-// (c_L forward; U_L^T da and dc f_L backward) stay in registers; values for
-// the neighbouring row and the full hidden vector go through LDS.
+// The unit's hidden units are split over NW waves in quads of four. Forward,
+// per step and 16-cell tile:
+//  * each wave computes, on MFMA, the pre-activations of the four sigmoid
+//    gates (i, f_L, f_T, o) of its quads from [h_L ; h_T]; the A operand rows
+//    are ordered (quad member, gate) so that lane 16q + n ends up holding all
+//    four gates of hidden unit 4*quad + q of cell n;
+//  * the cell-candidate pre-activations are split over the waves by
+//    reduction range and summed through LDS in a fixed order;
+//  * then every lane updates c and h of its (cell, hidden unit) pairs.
+// Backward, per step: every lane does the gate-gradient update of its pairs
+// (phase A), then the waves contract da with U^T on MFMA, split by output
+// tile and reduction range, partials summed through LDS in a fixed order
+// (phase B). The U operands stay in VGPRs for the whole unit.
 #include <type_traits>
 
 #include "common.hpp"
@@ -29,65 +28,51 @@
 
 namespace mdl {
 
-template <typename T>
-struct WaveOps;
+namespace {
 
-// fp32: 16x16x4 MFMA, slot q of the reduction holds a contiguous run of
-// KRUN values, one per K step.
+template <typename T>
+struct Ops;
 template <>
-struct WaveOps<float> {
+struct Ops<float> {  // 16x16x4 f32 MFMA: one reduction value per slot and step
     using Op = float;
-    static constexpr int PER_STEP = 1;
-    static __device__ __forceinline__ Op lds_op(const float* p) { return *p; }
+    static constexpr int PER = 1;
+    static __device__ __forceinline__ Op lds(const float* p) { return *p; }
     static __device__ __forceinline__ floatx4 mma(Op a, Op b, floatx4 c) { return mfma_f32(a, b, c); }
 };
-
-// bf16: 16x16x32 MFMA, eight consecutive values per K step.
 template <>
-struct WaveOps<bf16_t> {
+struct Ops<bf16_t> {  // 16x16x32 bf16 MFMA: eight consecutive values per slot and step
     using Op = bf16x8;
-    static constexpr int PER_STEP = 8;
-    static __device__ __forceinline__ Op lds_op(const bf16_t* p) {
-        return as_bf16x8(*reinterpret_cast<const uint4*>(p));
-    }
+    static constexpr int PER = 8;
+    static __device__ __forceinline__ Op lds(const bf16_t* p) { return as_bf16x8(*reinterpret_cast<const uint4*>(p)); }
     static __device__ __forceinline__ floatx4 mma(Op a, Op b, floatx4 c) { return mfma_bf16(a, b, c); }
 };
 
 template <typename T>
-__device__ __forceinline__ void lds_st4(T* p, floatx4 v);
-template <>
-__device__ __forceinline__ void lds_st4<float>(float* p, floatx4 v) {
-    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
-}
-template <>
-__device__ __forceinline__ void lds_st4<bf16_t>(bf16_t* p, floatx4 v) {
-    uint2 o;
-    o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-    o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-    *reinterpret_cast<uint2*>(p) = o;
-}
+__device__ __forceinline__ float ld1f(const T* p) { return St<T>::ld1(p); }
 
-__device__ __forceinline__ floatx4 lds_ld4f(const float* p) {
-    float4 v = *reinterpret_cast<const float4*>(p);
-    return floatx4{v.x, v.y, v.z, v.w};
-}
+template <typename T>
+__device__ __forceinline__ T from_f(float v);
+template <>
+__device__ __forceinline__ float from_f<float>(float v) { return v; }
+template <>
+__device__ __forceinline__ bf16_t from_f<bf16_t>(float v) { return f2bf(v); }
 
-// Load a K-slot of operand values from a row of U (global memory) with
-// element stride `es` between consecutive k (1: along a row; 2H: down a column).
+// A-operand values of one reduction slot from global memory: element stride
+// `es` between consecutive k.
 template <typename T, int NSTEP>
-__device__ __forceinline__ void load_u_slot(const T* __restrict__ base, int es, bool ok,
-                                            typename WaveOps<T>::Op (&v)[NSTEP]) {
+__device__ __forceinline__ void load_slot(const T* __restrict__ base, int64_t es, bool ok,
+                                          typename Ops<T>::Op (&v)[NSTEP]) {
     if constexpr (std::is_same<T, float>::value) {
 #pragma unroll
-        for (int ks = 0; ks < NSTEP; ++ks) v[ks] = ok ? base[(int64_t)ks * es] : 0.0f;
+        for (int ks = 0; ks < NSTEP; ++ks) v[ks] = ok ? base[ks * es] : 0.0f;
     } else {
 #pragma unroll
         for (int ks = 0; ks < NSTEP; ++ks) {
             uint32_t w[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                uint32_t lo = ok ? base[(int64_t)(8 * ks + 2 * e) * es] : 0;
-                uint32_t hi = ok ? base[(int64_t)(8 * ks + 2 * e + 1) * es] : 0;
+                const uint32_t lo = ok ? base[(8 * ks + 2 * e) * es] : 0;
+                const uint32_t hi = ok ? base[(8 * ks + 2 * e + 1) * es] : 0;
                 w[e] = lo | (hi << 16);
             }
             v[ks] = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
@@ -95,76 +80,128 @@ __device__ __forceinline__ void load_u_slot(const T* __restrict__ base, int es, 
     }
 }
 
+template <int H, typename T>
+struct Geo {
+    static constexpr int NW = H <= 4 ? 1 : (H <= 8 ? 2 : (H <= 64 ? 4 : 8));  // waves per unit
+    static constexpr int WQ = (H / 4) / NW;                                     // hidden-unit quads per wave
+    static constexpr int G = 5 * H;
+    static constexpr int PER = Ops<T>::PER;
+    // forward
+    static constexpr int KRUN = H / 2;                  // hcat values per reduction slot
+    static constexpr int NSTEP = KRUN / PER;
+    static constexpr int GT = (H + 15) / 16;            // cell-candidate tiles
+    static constexpr int SPL = NW / GT;                 // waves sharing one candidate tile
+    static constexpr int GSTEP = NSTEP / SPL;           // candidate K steps per wave
+    // backward
+    static constexpr int KRUNB = G / 4;                 // da values per reduction slot
+    static constexpr int NSTEPB = KRUNB / PER;
+    static constexpr int MT = (2 * H + 15) / 16;        // output tiles of U^T da
+    static constexpr int TPW = MT >= NW ? MT / NW : 1;  // output tiles per wave
+    static constexpr int SPLB = MT >= NW ? 1 : NW / MT;  // waves sharing one output tile
+    static constexpr int BSTEP = NSTEPB / SPLB;
+    static_assert(KRUN % PER == 0 && NSTEP % SPL == 0 && GT * SPL == NW, "forward split");
+    static_assert(KRUNB % PER == 0 && NSTEPB % SPLB == 0, "backward split");
+    static_assert(MT >= NW ? MT % NW == 0 : NW % MT == 0, "backward tiles");
+};
+
+// Per-step outputs of one cell, staged in LDS as 16-byte chunks and written
+// back by the whole workgroup with contiguous 16-byte stores: forward, the
+// 5H activated gates then the H outputs (storage type) then the H cell states
+// (fp32); backward, the 5H gate gradients.
+template <int H, typename T>
+struct OutQ {
+    static constexpr int QZ = 5 * H * (int)sizeof(T) / 16;
+    static constexpr int QY = H * (int)sizeof(T) / 16;
+    static constexpr int QC = H * 4 / 16;
+    static constexpr int QF = QZ + QY + QC;  // forward chunks per cell
+    static_assert(QZ * 16 == 5 * H * (int)sizeof(T) && QY * 16 == H * (int)sizeof(T), "chunking");
+};
+
+// LDS bytes of the forward kernel without and with staging of its inputs
+// (two diagonals of pre-activations) and outputs (one diagonal).
+template <int H, int NT, typename T>
+constexpr size_t fwd_lds_base() {
+    using Gm = Geo<H, T>;
+    return (size_t)2 * (NT * 16 + 1) * (H + 16 / sizeof(T)) * sizeof(T) + (size_t)2 * (NT * 16 + 1) * (H + 2) * 4 +
+           (size_t)Gm::SPL * NT * 16 * (H + 2) * 4 + (size_t)NT * 16 * 8;
+}
+template <int H, int NT, typename T>
+constexpr bool fwd_stage() {
+    using Q = OutQ<H, T>;
+    return fwd_lds_base<H, NT, T>() + (size_t)NT * 16 * 16 * ((Q::QF + 1) + 2 * (Q::QZ + 1)) <= 128 * 1024;
+}
+
+template <typename T>
+struct Prefetch2 {
+    template <int NT, int WQ>
+    static constexpr bool on() { return NT * WQ <= 2; }
+};
+
 struct WaveArgs {
     const int32_t* units;  // unit = rect*4 + direction, in launch order
     const int32_t* rects;  // [n_rects][4]
     const uint8_t* mask;   // [n_cells]
     const void* u;         // [4][5H][2H]
-    void* z;               // [n_cells][20H]: pre-activations in, activated gates out (fwd); dZ out (bwd)
+    void* z;               // [n_cells][20H]: pre-activations in, gates out (fwd); dZ out (bwd)
     float* c;              // [n_cells][4H] cell state
     void* y;               // [n_cells][4H] output (fwd)
     const void* dy;        // [n_cells][4H] upstream gradient (bwd)
     int canvas_w;
 };
 
-// Raw 4-element loads kept in registers until use (prefetched one step ahead).
-template <typename T>
-struct Raw;
-template <>
-struct Raw<float> {
-    using V = float4;
-    static __device__ __forceinline__ V load(const float* p) { return *reinterpret_cast<const float4*>(p); }
-    static __device__ __forceinline__ floatx4 f(V v) { return floatx4{v.x, v.y, v.z, v.w}; }
-    static __device__ __forceinline__ V zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
-};
-template <>
-struct Raw<bf16_t> {
-    using V = uint2;
-    static __device__ __forceinline__ V load(const bf16_t* p) { return *reinterpret_cast<const uint2*>(p); }
-    static __device__ __forceinline__ floatx4 f(V v) {
-        return floatx4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
-                       __uint_as_float(v.y & 0xffff0000u)};
-    }
-    static __device__ __forceinline__ V zero() { return make_uint2(0, 0); }
-};
-
-// Whether a unit keeps the next step's global loads in a second register set.
-// Large tiles (H = 128, or many N tiles at H = 64) would spill instead.
-template <int H, int NT, typename T>
-struct Prefetch {
-    static constexpr bool on = (H <= 32 && NT <= 2) || (H == 64 && NT == 1);
-};
-
-// ---------------------------------------------------------------------------
-// Forward.
-// ---------------------------------------------------------------------------
-template <int NT, typename T>
-struct FwdPre {
-    typename Raw<T>::V z[NT][5];
+template <int NT, int WQ, typename T>
+struct FPre {
+    T z[NT][WQ][5];
     int64_t p[NT];
     uint32_t m[NT];
     bool live[NT];
 };
 
-template <int H, int NT, typename T>
-__global__ void __launch_bounds__(64 * ((H + 15) / 16))
-k_wave_fwd(WaveArgs a) {
-    using Ops = WaveOps<T>;
-    using Op = typename Ops::Op;
-    using R4 = Raw<T>;
-    constexpr int G = 5 * H;             // gate rows per direction
-    constexpr int KRUN = H / 2;          // hcat values per reduction slot
-    constexpr int NSTEP = KRUN / Ops::PER_STEP;
-    constexpr int ROWS = NT * 16 + 1;    // +1: row 0 is the zero row above local row 0
-    constexpr int HP = H + 16 / (int)sizeof(T);  // padded LDS row pitch (elements)
-    static_assert(KRUN % Ops::PER_STEP == 0, "hidden size not supported for this storage type");
-    __shared__ __attribute__((aligned(16))) T hbuf[2][ROWS][HP];
-    __shared__ __attribute__((aligned(16))) float cbuf[2][ROWS][H];
+template <int NT, int WQ, typename T>
+struct BPre {
+    T g[NT][WQ][5], dy[NT][WQ];
+    float c[NT][WQ], cl[NT][WQ], ct[NT][WQ];
+    int64_t p[NT];
+    uint32_t m[NT];
+    bool live[NT], hasl[NT], hast[NT];
+};
 
-    const int lane = threadIdx.x & 63, jb = threadIdx.x >> 6;
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Forward.
+// ---------------------------------------------------------------------------
+template <int H, int NT, typename T>
+__global__ void __launch_bounds__((64 * Geo<H, T>::NW))
+k_wave_fwd(WaveArgs a) {
+    using Gm = Geo<H, T>;
+    using O = Ops<T>;
+    using Op = typename O::Op;
+    using Q = OutQ<H, T>;
+    constexpr int NW = Gm::NW, WQ = Gm::WQ, G = Gm::G, KRUN = Gm::KRUN, NSTEP = Gm::NSTEP;
+    constexpr int SPL = Gm::SPL, GSTEP = Gm::GSTEP, NTH = 64 * NW;
+    constexpr int ROWS = NT * 16 + 1;             // row 0: zero row above local row 0
+    constexpr int HP = H + 16 / (int)sizeof(T);   // padded LDS row pitch (elements)
+    // Staged: the pre-activations of the next diagonal are loaded as contiguous
+    // 16-byte chunks into registers one step ahead and pass through LDS to
+    // the lanes that use them; the outputs leave through LDS the same way.
+    // Otherwise every lane loads and stores its own values.
+    constexpr bool STAGE = fwd_stage<H, NT, T>();
+    constexpr int NC = STAGE ? NT * 16 : 1;
+    constexpr int PF = STAGE ? Q::QF + 1 : 1;     // chunk pitches; the extra chunk
+    constexpr int PZ = STAGE ? Q::QZ + 1 : 1;     // keeps rows in different LDS banks
+    // input slots, rounded up to whole workgroup passes so every lane loads
+    constexpr int NSL = STAGE ? (NT * 16 * PZ + NTH - 1) / NTH * NTH : 1;
+    constexpr int NITZ = STAGE ? NSL / NTH : 0;
+    __shared__ __attribute__((aligned(16))) T hbuf[2][ROWS][HP];
+    __shared__ __attribute__((aligned(16))) float cbuf[2][ROWS][H + 2];  // pitch H + 2: rows of a tile in different banks
+    __shared__ __attribute__((aligned(16))) float gpart[SPL][NT * 16][H + 2];
+    __shared__ __attribute__((aligned(16))) u32x4 ostage[NC][PF];
+    __shared__ __attribute__((aligned(16))) u32x4 zst[NSL];
+
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int q = lane >> 4, n16 = lane & 15;
-    const int j0 = 16 * jb + 4 * q;  // this lane's four hidden units (output rows)
-    const bool jok = j0 < H;
+    const int gt = w / SPL, sp = w % SPL;  // candidate tile and reduction slice of this wave
     const int unit = a.units[blockIdx.x];
     const int d = unit & 3;
     const RectD R = reinterpret_cast<const RectD*>(a.rects)[unit >> 2];
@@ -175,107 +212,220 @@ k_wave_fwd(WaveArgs a) {
     const int steps = R.h + R.w - 1;
 
     for (int i = threadIdx.x; i < 2 * ROWS * HP; i += blockDim.x) (&hbuf[0][0][0])[i] = T(0);
-    for (int i = threadIdx.x; i < 2 * ROWS * H; i += blockDim.x) (&cbuf[0][0][0])[i] = 0.0f;
+    for (int i = threadIdx.x; i < 2 * ROWS * (H + 2); i += blockDim.x) (&cbuf[0][0][0])[i] = 0.0f;
 
-    // A operand: U rows (gate t, hidden unit 16 jb + n16), reduction slot q
-    // holding hcat indices k = q*KRUN .. q*KRUN + KRUN - 1.
-    Op A[5][NSTEP];
-    {
-        const int jr = 16 * jb + n16;
+    // A operands. Own tiles: row n16 = 4*jj + gate -> U row gate*H + 4*quad + jj.
+    // Candidate tile gt: row n16 -> U row 4H + 16*gt + n16, K steps of slice sp only.
+    Op Aown[WQ][NSTEP], Ag[GSTEP];
 #pragma unroll
-        for (int t = 0; t < 5; ++t)
-            load_u_slot<T, NSTEP>(U + (int64_t)(t * H + (jr < H ? jr : 0)) * 2 * H + q * KRUN, 1, jr < H, A[t]);
+    for (int wq = 0; wq < WQ; ++wq) {
+        const int quad = w * WQ + wq;
+        const int row = (n16 & 3) * H + 4 * quad + (n16 >> 2);
+        load_slot<T, NSTEP>(U + (int64_t)row * 2 * H + q * KRUN, 1, true, Aown[wq]);
     }
-    floatx4 cprev[NT];
+    {
+        const int j = 16 * gt + n16;
+        const bool ok = j < H;
+        load_slot<T, GSTEP>(U + (int64_t)(4 * H + (ok ? j : 0)) * 2 * H + q * KRUN + sp * GSTEP * O::PER, 1, ok, Ag);
+    }
+    float cprev[NT][WQ];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) cprev[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int wq = 0; wq < WQ; ++wq) cprev[nt][wq] = 0.0f;
+    // The U operands are in registers before the step loop starts, so no wait
+    // inside the loop is attributed to them.
+    __builtin_amdgcn_s_waitcnt(0);
 
-    // Global loads of step s (pre-activations and mask); they depend only on
-    // the position, never on the recurrence, so they can be issued early.
-    auto fetch = [&](int s, FwdPre<NT, T>& b) {
-        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+    // Loads of step s: the lane's cells, their mask bytes and the
+    // pre-activations (staged: chunks into zr, else the lane's own values).
+    // They are issued for every lane from a valid cell of the rectangle (the
+    // row clamped into the diagonal's active range) so their number is the
+    // same on every path, which lets the compiler wait for exactly these loads
+    // one step later; `live` says whether they are used.
+    u32x4 zr[NITZ > 0 ? NITZ : 1];
+    auto fetch = [&](int s, FPre<NT, WQ, T>& b) {
+        const int sc = min(s, steps - 1);
+        const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            b.live[nt] = false;
-            if (s >= steps || 16 * nt > yhi || 16 * nt + 15 < ylo) continue;
-            const int yy = 16 * nt + n16, xx = s - yy;
-            const bool live = jok && yy < R.h && xx >= 0 && xx < R.w;
-            b.live[nt] = live;
-            if (live) {
-                const int64_t p = canvas_index(R, d, yy, xx, a.canvas_w);
-                b.p[nt] = p;
-                b.m[nt] = a.mask[p];
-                const T* zp = Z + p * (4 * G) + d * G + j0;
+            const int yy = 16 * nt + n16;
+            b.live[nt] = s < steps && yy >= ylo && yy <= yhi;
+            const int yc = min(max(yy, ylo), yhi);
+            const int64_t p = canvas_index(R, d, yc, sc - yc, a.canvas_w);
+            b.p[nt] = p;
+            b.m[nt] = a.mask[p];
+            if constexpr (!STAGE) {
+                const T* zp = Z + p * (4 * G) + d * G;
 #pragma unroll
-                for (int t = 0; t < 5; ++t) b.z[nt][t] = R4::load(zp + t * H);
+                for (int wq = 0; wq < WQ; ++wq) {
+                    const int j = 4 * (w * WQ + wq) + q;
+#pragma unroll
+                    for (int t = 0; t < 5; ++t) b.z[nt][wq][t] = zp[t * H + j];
+                }
+            }
+        }
+        if constexpr (STAGE) {
+            // slot S of zst is chunk S % PZ of the row of cell S / PZ (the
+            // padding chunk and the slots past the last cell repeat a valid one)
+#pragma unroll
+            for (int it = 0; it < NITZ; ++it) {
+                const int S = it * NTH + (int)threadIdx.x;
+                const int cell = min(S / PZ, NT * 16 - 1), r = min(S - (S / PZ) * PZ, Q::QZ - 1);
+                const int yc = min(max(cell, ylo), yhi);
+                const int64_t p = canvas_index(R, d, yc, sc - yc, a.canvas_w);
+                zr[it] = *reinterpret_cast<const u32x4*>(Z + p * (4 * G) + d * G + r * (16 / (int)sizeof(T)));
             }
         }
     };
+    // zr -> zst; the cell phase of the step reads zst after its first barrier.
+    auto stage_in = [&]() {
+#pragma unroll
+        for (int it = 0; it < NITZ; ++it) zst[it * NTH + threadIdx.x] = zr[it];
+    };
 
-    auto compute = [&](int s, const FwdPre<NT, T>& b) {
+    // Write back the outputs staged by diagonal sp. Runs between that step's
+    // closing barrier and the next cell phase's barrier. Every lane stores in
+    // every pass (rows outside the diagonal repeat its nearest cell, which
+    // writes the same bytes twice), so the number of stores is fixed. All LDS
+    // reads are issued before the first store: one LDS round trip.
+    constexpr int NITF = STAGE ? (NT * 16 * Q::QF + NTH - 1) / NTH : 0;
+    auto flush = [&](int sp) {
+        if constexpr (STAGE) {
+            constexpr int NCH = NT * 16 * Q::QF;
+            const int ylo = max(0, sp - R.w + 1), yhi = min(R.h - 1, sp);
+            u32x4 v[NITF];
+            char* dst[NITF];
+#pragma unroll
+            for (int it = 0; it < NITF; ++it) {
+                const int i = min(it * NTH + (int)threadIdx.x, NCH - 1);
+                const int cell = min(max(i / Q::QF, ylo), yhi), r = i - (i / Q::QF) * Q::QF;
+                v[it] = ostage[cell][r];
+                const int64_t p = canvas_index(R, d, cell, sp - cell, a.canvas_w);
+                char* zb = reinterpret_cast<char*>(Z + p * (4 * G) + d * G) + 16 * r;
+                char* yb = reinterpret_cast<char*>(Y + p * (4 * H) + d * H) + 16 * (r - Q::QZ);
+                char* cb = reinterpret_cast<char*>(Cs + p * (4 * H) + d * H) + 16 * (r - Q::QZ - Q::QY);
+                dst[it] = r < Q::QZ ? zb : (r < Q::QZ + Q::QY ? yb : cb);
+            }
+#pragma unroll
+            for (int it = 0; it < NITF; ++it) *reinterpret_cast<u32x4*>(dst[it]) = v[it];
+        }
+    };
+
+    auto compute = [&](int s, const FPre<NT, WQ, T>& b) {
         const int cur = s & 1, prv = cur ^ 1;
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+        floatx4 acc[NT][WQ];
+        // pre-activations from [h_L ; h_T] of the previous diagonal
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;  // uniform over the workgroup
             const int yy = 16 * nt + n16;
-            // B operand: slot q < 2 reads h_L (row yy of the previous diagonal),
-            // q >= 2 reads h_T (row yy - 1); LDS row index is local row + 1.
             const T* brow = (q < 2) ? &hbuf[prv][yy + 1][q * KRUN] : &hbuf[prv][yy][(q - 2) * KRUN];
-            floatx4 acc[5];
+            Op bop[NSTEP], bg[GSTEP];
 #pragma unroll
-            for (int t = 0; t < 5; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+            for (int ks = 0; ks < NSTEP; ++ks) bop[ks] = O::lds(brow + ks * O::PER);
 #pragma unroll
-            for (int ks = 0; ks < NSTEP; ++ks) {
-                const Op bop = Ops::lds_op(brow + ks * Ops::PER_STEP);
+            for (int ks = 0; ks < GSTEP; ++ks) bg[ks] = O::lds(brow + (sp * GSTEP + ks) * O::PER);
+            floatx4 ag = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int t = 0; t < 5; ++t) acc[t] = Ops::mma(A[t][ks], bop, acc[t]);
-            }
-            floatx4 cn = floatx4{0.f, 0.f, 0.f, 0.f}, hn = cn;
-            if (b.live[nt]) {
-                const floatx4 cL = cprev[nt];
-                const floatx4 cT = lds_ld4f(&cbuf[prv][yy][j0]);
-                floatx4 gi, gfl, gft, go, gg;
+            for (int wq = 0; wq < WQ; ++wq) acc[nt][wq] = ag;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    gi[r] = sigm_fast(acc[0][r] + R4::f(b.z[nt][0])[r]);
-                    gfl[r] = sigm_fast(acc[1][r] + R4::f(b.z[nt][1])[r]);
-                    gft[r] = sigm_fast(acc[2][r] + R4::f(b.z[nt][2])[r]);
-                    go[r] = sigm_fast(acc[3][r] + R4::f(b.z[nt][3])[r]);
-                    gg[r] = tanh_fast(acc[4][r] + R4::f(b.z[nt][4])[r]);
-                    const float c = gi[r] * gg[r] + gfl[r] * cL[r] + gft[r] * cT[r];
-                    cn[r] = c;
-                    hn[r] = go[r] * tanh_fast(c);
-                }
-                const int64_t p = b.p[nt];
-                if (b.m[nt]) {
-                    T* zp = Z + p * (4 * G) + d * G + j0;
-                    St<T>::st4(zp + 0 * H, gi);
-                    St<T>::st4(zp + 1 * H, gfl);
-                    St<T>::st4(zp + 2 * H, gft);
-                    St<T>::st4(zp + 3 * H, go);
-                    St<T>::st4(zp + 4 * H, gg);
-                    St<T>::st4(Y + p * (4 * H) + d * H + j0, hn);
-                } else {
-                    cn = floatx4{0.f, 0.f, 0.f, 0.f};
-                    hn = cn;
-                }
-                St<float>::st4(Cs + p * (4 * H) + d * H + j0, cn);
-            }
-            cprev[nt] = cn;
-            if (jok) {
-                lds_st4<T>(&hbuf[cur][yy + 1][j0], hn);
-                *reinterpret_cast<float4*>(&cbuf[cur][yy + 1][j0]) = make_float4(cn[0], cn[1], cn[2], cn[3]);
+            for (int ks = 0; ks < NSTEP; ++ks)
+#pragma unroll
+                for (int wq = 0; wq < WQ; ++wq) acc[nt][wq] = O::mma(Aown[wq][ks], bop[ks], acc[nt][wq]);
+#pragma unroll
+            for (int ks = 0; ks < GSTEP; ++ks) ag = O::mma(Ag[ks], bg[ks], ag);
+            const int j0 = 16 * gt + 4 * q;
+            if (j0 < H) {
+                *reinterpret_cast<float2*>(&gpart[sp][yy][j0]) = make_float2(ag[0], ag[1]);
+                *reinterpret_cast<float2*>(&gpart[sp][yy][j0 + 2]) = make_float2(ag[2], ag[3]);
             }
         }
-        __syncthreads();
+        lds_barrier();
+        // cell updates: lane owns (cell 16 nt + n16, hidden unit 4 (w WQ + wq) + q)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;
+            const int yy = 16 * nt + n16;
+#pragma unroll
+            for (int wq = 0; wq < WQ; ++wq) {
+                const int j = 4 * (w * WQ + wq) + q;
+                float cn = 0.0f, hn = 0.0f;
+                if (b.live[nt]) {
+                    float zv[5];
+#pragma unroll
+                    for (int t = 0; t < 5; ++t) {
+                        if constexpr (STAGE)
+                            zv[t] = ld1f<T>(reinterpret_cast<const T*>(&zst[yy * PZ]) + t * H + j);
+                        else
+                            zv[t] = ld1f<T>(&b.z[nt][wq][t]);
+                    }
+                    float gs = 0.0f;
+#pragma unroll
+                    for (int k = 0; k < SPL; ++k) gs += gpart[k][yy][j];
+                    const float gi = sigm_fast(acc[nt][wq][0] + zv[0]);
+                    const float gfl = sigm_fast(acc[nt][wq][1] + zv[1]);
+                    const float gft = sigm_fast(acc[nt][wq][2] + zv[2]);
+                    const float go = sigm_fast(acc[nt][wq][3] + zv[3]);
+                    const float gg = tanh_fast(gs + zv[4]);
+                    const float cT = cbuf[prv][yy][j];
+                    cn = gi * gg + gfl * cprev[nt][wq] + gft * cT;
+                    hn = go * tanh_fast(cn);
+                    const int64_t p = b.p[nt];
+                    if (!b.m[nt]) {
+                        cn = 0.0f;
+                        hn = 0.0f;
+                    }
+                    if constexpr (STAGE) {
+                        T* oz = reinterpret_cast<T*>(&ostage[yy][0]);
+                        oz[0 * H + j] = from_f<T>(gi);
+                        oz[1 * H + j] = from_f<T>(gfl);
+                        oz[2 * H + j] = from_f<T>(gft);
+                        oz[3 * H + j] = from_f<T>(go);
+                        oz[4 * H + j] = from_f<T>(gg);
+                        oz[5 * H + j] = from_f<T>(hn);
+                        reinterpret_cast<float*>(&ostage[yy][Q::QZ + Q::QY])[j] = cn;
+                    } else {
+                        if (b.m[nt]) {
+                            T* zp = Z + p * (4 * G) + d * G + j;
+                            zp[0 * H] = from_f<T>(gi);
+                            zp[1 * H] = from_f<T>(gfl);
+                            zp[2 * H] = from_f<T>(gft);
+                            zp[3 * H] = from_f<T>(go);
+                            zp[4 * H] = from_f<T>(gg);
+                            Y[p * (4 * H) + d * H + j] = from_f<T>(hn);
+                        }
+                        Cs[p * (4 * H) + d * H + j] = cn;
+                    }
+                }
+                cprev[nt][wq] = cn;
+                hbuf[cur][yy + 1][j] = from_f<T>(hn);
+                cbuf[cur][yy + 1][j] = cn;
+            }
+        }
+        lds_barrier();
     };
 
-    __syncthreads();
-    FwdPre<NT, T> b0, b1;
-    if constexpr (Prefetch<H, NT, T>::on) {
-        // two register sets in turn: step s computes from one while the loads
-        // of step s + 1 land in the other
+    lds_barrier();
+    FPre<NT, WQ, T> b0, b1;
+    if constexpr (STAGE) {
+        // Step s: move the staged inputs of step s into LDS, issue the loads of
+        // step s + 1 (past the last step they re-read valid cells), write back
+        // step s - 1, compute step s.
+        auto step = [&](int s, const FPre<NT, WQ, T>& cur, FPre<NT, WQ, T>& nxt) {
+            stage_in();
+            fetch(s + 1, nxt);
+            if (s > 0) flush(s - 1);
+            compute(s, cur);
+        };
+        fetch(0, b0);
+        for (int s = 0; s < steps; s += 2) {
+            step(s, b0, b1);
+            if (s + 1 < steps) step(s + 1, b1, b0);
+        }
+        flush(steps - 1);
+    } else if constexpr (Prefetch2<T>::template on<NT, WQ>()) {
         fetch(0, b0);
         int s = 0;
         for (; s + 1 < steps; s += 2) {
@@ -294,42 +444,30 @@ k_wave_fwd(WaveArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Backward (reverse anti-diagonals). For a cell with successors S (right,
-// same row, next diagonal) and E (below, row + 1, next diagonal):
+// Backward (reverse anti-diagonals). With successors S (right, same row, next
+// diagonal) and E (below, row + 1, next diagonal):
 //   dh = dY + (U^T da_S)[0:H] + (U^T da_E)[H:2H]
 //   dc = dh o (1 - tanh^2 c) + dc_S f_L(S) + dc_E f_T(E)
 //   da = (dc g i(1-i), dc c_L f_L(1-f_L), dc c_T f_T(1-f_T), dh tanh(c) o(1-o), dc i (1-g^2))
-// Phase A does the cell update and writes da (over the saved gates, and to
-// LDS); phase B contracts da with U^T for the predecessors.
 // ---------------------------------------------------------------------------
-template <int NT, typename T>
-struct BwdPre {
-    typename Raw<T>::V g[NT][5], dy[NT];
-    float4 c[NT], cl[NT], ct[NT];
-    int64_t p[NT];
-    uint32_t m[NT];
-    bool live[NT];
-};
-
 template <int H, int NT, typename T>
-__global__ void __launch_bounds__(64 * ((H + 15) / 16))
+__global__ void __launch_bounds__((64 * Geo<H, T>::NW))
 k_wave_bwd(WaveArgs a) {
-    using Ops = WaveOps<T>;
-    using Op = typename Ops::Op;
-    using R4 = Raw<T>;
-    constexpr int G = 5 * H;
-    constexpr int KRUN = G / 4;          // da values per reduction slot
-    constexpr int NSTEP = KRUN / Ops::PER_STEP;
+    using Gm = Geo<H, T>;
+    using O = Ops<T>;
+    using Op = typename O::Op;
+    constexpr int WQ = Gm::WQ, G = Gm::G, KRUNB = Gm::KRUNB;
+    constexpr int TPW = Gm::TPW, SPLB = Gm::SPLB, BSTEP = Gm::BSTEP;
     constexpr int GP = G + 16 / (int)sizeof(T);
-    static_assert(KRUN % Ops::PER_STEP == 0, "hidden size not supported for this storage type");
     __shared__ __attribute__((aligned(16))) T dabuf[NT * 16][GP];
-    __shared__ __attribute__((aligned(16))) float gtbuf[NT * 16 + 1][H];
-    __shared__ __attribute__((aligned(16))) float dctbuf[NT * 16 + 1][H];
+    __shared__ __attribute__((aligned(16))) float gbuf[SPLB][NT * 16 + 1][2 * H + 2];  // row NT*16 stays zero
+    __shared__ __attribute__((aligned(16))) float dct[NT * 16 + 1][H + 2];
+    __shared__ int64_t bpos[NT * 16];  // cell of dabuf row written back: p, or -1
+    constexpr int QZ = OutQ<H, T>::QZ;
 
-    const int lane = threadIdx.x & 63, jb = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int q = lane >> 4, n16 = lane & 15;
-    const int j0 = 16 * jb + 4 * q;
-    const bool jok = j0 < H;
+    const int mt0 = (w / SPLB) * TPW, sb = w % SPLB;  // output tiles and reduction slice of this wave
     const int unit = a.units[blockIdx.x];
     const int d = unit & 3;
     const RectD R = reinterpret_cast<const RectD*>(a.rects)[unit >> 2];
@@ -340,125 +478,152 @@ k_wave_bwd(WaveArgs a) {
     const int steps = R.h + R.w - 1;
 
     for (int i = threadIdx.x; i < NT * 16 * GP; i += blockDim.x) (&dabuf[0][0])[i] = T(0);
-    for (int i = threadIdx.x; i < (NT * 16 + 1) * H; i += blockDim.x) {
-        (&gtbuf[0][0])[i] = 0.0f;
-        (&dctbuf[0][0])[i] = 0.0f;
-    }
+    for (int i = threadIdx.x; i < SPLB * (NT * 16 + 1) * (2 * H + 2); i += blockDim.x) (&gbuf[0][0][0])[i] = 0.0f;
+    for (int i = threadIdx.x; i < (NT * 16 + 1) * (H + 2); i += blockDim.x) (&dct[0][0])[i] = 0.0f;
 
-    // A operands: U^T rows k (column k of U) for the left part (k = 16 jb + n16)
-    // and the top part (k = H + 16 jb + n16); slot q holds gate rows
-    // r = q*KRUN .. q*KRUN + KRUN - 1.
-    Op AL[NSTEP], AT[NSTEP];
-    {
-        const int kr = 16 * jb + n16;
-        const bool ok = kr < H;
-        const int kc = ok ? kr : 0;
-        load_u_slot<T, NSTEP>(U + (int64_t)(q * KRUN) * 2 * H + kc, 2 * H, ok, AL);
-        load_u_slot<T, NSTEP>(U + (int64_t)(q * KRUN) * 2 * H + H + kc, 2 * H, ok, AT);
-    }
-    floatx4 gl[NT], dcl[NT], dct_new[NT];
+    // A operands: U^T rows k = 16 mt + n16 (column k of U); slot q holds gate
+    // rows r = q*KRUNB + ..., slice sb of the K steps.
+    Op A[TPW][BSTEP];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-        gl[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-        dcl[nt] = gl[nt];
-        dct_new[nt] = gl[nt];
+    for (int tt = 0; tt < TPW; ++tt) {
+        const int k = 16 * (mt0 + tt) + n16;
+        const bool ok = k < 2 * H;
+        load_slot<T, BSTEP>(U + (int64_t)(q * KRUNB + sb * BSTEP * O::PER) * 2 * H + (ok ? k : 0), 2 * H, ok, A[tt]);
     }
+    float dcl[NT][WQ], dcn[NT][WQ];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int wq = 0; wq < WQ; ++wq) dcl[nt][wq] = dcn[nt][wq] = 0.0f;
+    __builtin_amdgcn_s_waitcnt(0);  // U operands in registers before the step loop
 
-    auto fetch = [&](int s, BwdPre<NT, T>& b) {
-        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+    // Loads of step s, issued for every lane from valid cells (see the forward
+    // pass); predecessors outside the rectangle read the cell itself and are
+    // zeroed on use.
+    auto fetch = [&](int s, BPre<NT, WQ, T>& b) {
+        const int sc = max(s, 0);
+        const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            b.live[nt] = false;
-            if (s < 0 || 16 * nt > yhi || 16 * nt + 15 < ylo) continue;
-            const int yy = 16 * nt + n16, xx = s - yy;
-            const bool live = jok && yy < R.h && xx >= 0 && xx < R.w;
-            b.live[nt] = live;
-            if (live) {
-                const int64_t p = canvas_index(R, d, yy, xx, a.canvas_w);
-                b.p[nt] = p;
-                b.m[nt] = a.mask[p];
-                const T* zp = Z + p * (4 * G) + d * G + j0;
+            const int yy = 16 * nt + n16;
+            b.live[nt] = s >= 0 && yy >= ylo && yy <= yhi;
+            const int yc = min(max(yy, ylo), yhi), xc = sc - yc;
+            const int64_t p = canvas_index(R, d, yc, xc, a.canvas_w);
+            const int64_t pl = xc > 0 ? canvas_index(R, d, yc, xc - 1, a.canvas_w) : p;
+            const int64_t pt = yc > 0 ? canvas_index(R, d, yc - 1, xc, a.canvas_w) : p;
+            b.p[nt] = p;
+            b.m[nt] = a.mask[p];
 #pragma unroll
-                for (int t = 0; t < 5; ++t) b.g[nt][t] = R4::load(zp + t * H);
-                b.dy[nt] = R4::load(DY + p * (4 * H) + d * H + j0);
-                b.c[nt] = Raw<float>::load(Cs + p * (4 * H) + d * H + j0);
-                b.cl[nt] = xx > 0 ? Raw<float>::load(Cs + canvas_index(R, d, yy, xx - 1, a.canvas_w) * (4 * H) + d * H + j0)
-                                  : Raw<float>::zero();
-                b.ct[nt] = yy > 0 ? Raw<float>::load(Cs + canvas_index(R, d, yy - 1, xx, a.canvas_w) * (4 * H) + d * H + j0)
-                                  : Raw<float>::zero();
+            for (int wq = 0; wq < WQ; ++wq) {
+                const int j = 4 * (w * WQ + wq) + q;
+                const T* zp = Z + p * (4 * G) + d * G + j;
+#pragma unroll
+                for (int t = 0; t < 5; ++t) b.g[nt][wq][t] = zp[t * H];
+                b.dy[nt][wq] = DY[p * (4 * H) + d * H + j];
+                b.c[nt][wq] = Cs[p * (4 * H) + d * H + j];
+                b.cl[nt][wq] = Cs[pl * (4 * H) + d * H + j];
+                b.ct[nt][wq] = Cs[pt * (4 * H) + d * H + j];
             }
+            b.hasl[nt] = xc > 0;
+            b.hast[nt] = yc > 0;
         }
     };
 
-    auto compute = [&](int s, const BwdPre<NT, T>& b) {
+    auto compute = [&](int s, const BPre<NT, WQ, T>& b) {
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
-        // Phase A: cell updates of diagonal s.
+        // Phase A: gate-gradient update of this lane's (cell, hidden unit) pairs.
+        if (w == 0 && q == 0) {
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) bpos[16 * nt + n16] = b.live[nt] && b.m[nt] ? b.p[nt] : -1;
+        }
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;
             const int yy = 16 * nt + n16;
-            floatx4 da[5];
 #pragma unroll
-            for (int t = 0; t < 5; ++t) da[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-            floatx4 ndl = da[0], ndt = da[0];
-            if (b.live[nt] && b.m[nt]) {
-                const floatx4 gi = R4::f(b.g[nt][0]), gfl = R4::f(b.g[nt][1]), gft = R4::f(b.g[nt][2]),
-                              go = R4::f(b.g[nt][3]), gg = R4::f(b.g[nt][4]);
-                const floatx4 dyv = R4::f(b.dy[nt]);
-                const floatx4 cv = Raw<float>::f(b.c[nt]), cL = Raw<float>::f(b.cl[nt]), cT = Raw<float>::f(b.ct[nt]);
-                const floatx4 gt = lds_ld4f(&gtbuf[yy + 1][j0]);
-                const floatx4 dcE = lds_ld4f(&dctbuf[yy + 1][j0]);
+            for (int wq = 0; wq < WQ; ++wq) {
+                const int j = 4 * (w * WQ + wq) + q;
+                float da[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+                float ndl = 0.0f, ndt = 0.0f;
+                if (b.live[nt] && b.m[nt]) {
+                    const float gi = ld1f<T>(&b.g[nt][wq][0]), gfl = ld1f<T>(&b.g[nt][wq][1]),
+                                gft = ld1f<T>(&b.g[nt][wq][2]), go = ld1f<T>(&b.g[nt][wq][3]),
+                                gg = ld1f<T>(&b.g[nt][wq][4]);
+                    float gl = 0.0f, gtv = 0.0f;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float dh = dyv[r] + gl[nt][r] + gt[r];
-                    const float tc = tanh_fast(cv[r]);
-                    const float dc = dcl[nt][r] + dcE[r] + dh * go[r] * (1.0f - tc * tc);
-                    da[0][r] = dc * gg[r] * gi[r] * (1.0f - gi[r]);
-                    da[1][r] = dc * cL[r] * gfl[r] * (1.0f - gfl[r]);
-                    da[2][r] = dc * cT[r] * gft[r] * (1.0f - gft[r]);
-                    da[3][r] = dh * tc * go[r] * (1.0f - go[r]);
-                    da[4][r] = dc * gi[r] * (1.0f - gg[r] * gg[r]);
-                    ndl[r] = dc * gfl[r];
-                    ndt[r] = dc * gft[r];
+                    for (int k = 0; k < SPLB; ++k) {
+                        gl += gbuf[k][yy][j];
+                        gtv += gbuf[k][yy + 1][H + j];
+                    }
+                    const float dh = ld1f<T>(&b.dy[nt][wq]) + gl + gtv;
+                    const float tc = tanh_fast(b.c[nt][wq]);
+                    const float dc = dcl[nt][wq] + dct[yy + 1][j] + dh * go * (1.0f - tc * tc);
+                    da[0] = dc * gg * gi * (1.0f - gi);
+                    const float cL = b.hasl[nt] ? b.cl[nt][wq] : 0.0f;
+                    const float cT = b.hast[nt] ? b.ct[nt][wq] : 0.0f;
+                    da[1] = dc * cL * gfl * (1.0f - gfl);
+                    da[2] = dc * cT * gft * (1.0f - gft);
+                    da[3] = dh * tc * go * (1.0f - go);
+                    da[4] = dc * gi * (1.0f - gg * gg);
+                    ndl = dc * gfl;
+                    ndt = dc * gft;
                 }
-                T* dz = Z + b.p[nt] * (4 * G) + d * G + j0;
 #pragma unroll
-                for (int t = 0; t < 5; ++t) St<T>::st4(dz + t * H, da[t]);
+                for (int t = 0; t < 5; ++t) dabuf[yy][t * H + j] = from_f<T>(da[t]);
+                dcl[nt][wq] = ndl;
+                dcn[nt][wq] = ndt;
             }
-            if (jok) {
-#pragma unroll
-                for (int t = 0; t < 5; ++t) lds_st4<T>(&dabuf[yy][t * H + j0], da[t]);
-            }
-            dcl[nt] = ndl;
-            dct_new[nt] = ndt;
         }
-        __syncthreads();
-        // Phase B: contributions U^T da for the left and top predecessors.
+        lds_barrier();
+        // The rows of dabuf are the gate gradients of the diagonal's cells:
+        // write them back with contiguous 16-byte stores.
+        {
+            constexpr int NCH = NT * 16 * QZ, NTH = 64 * Gm::NW, NIT = (NCH + NTH - 1) / NTH;
+            u32x4 v[NIT];
+            u32x4* dst[NIT];
+            bool ok[NIT];
+#pragma unroll
+            for (int it = 0; it < NIT; ++it) {
+                const int i = min(it * NTH + (int)threadIdx.x, NCH - 1);
+                const int cell = i / QZ, r = i - cell * QZ;
+                const int64_t p = bpos[cell];
+                v[it] = reinterpret_cast<const u32x4*>(&dabuf[cell][0])[r];
+                dst[it] = reinterpret_cast<u32x4*>(Z + (p >= 0 ? p : 0) * (4 * G) + d * G) + r;
+                ok[it] = it * NTH + (int)threadIdx.x < NCH && p >= 0;
+            }
+#pragma unroll
+            for (int it = 0; it < NIT; ++it)
+                if (ok[it]) *dst[it] = v[it];
+        }
+        // Phase B: U^T da for the left (rows k < H) and top (k >= H) predecessors.
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;
             const int yy = 16 * nt + n16;
-            const T* brow = &dabuf[yy][q * KRUN];
-            floatx4 accL = floatx4{0.f, 0.f, 0.f, 0.f}, accT = accL;
+            const T* brow = &dabuf[yy][q * KRUNB + sb * BSTEP * O::PER];
+            Op bop[BSTEP];
 #pragma unroll
-            for (int ks = 0; ks < NSTEP; ++ks) {
-                const Op bop = Ops::lds_op(brow + ks * Ops::PER_STEP);
-                accL = Ops::mma(AL[ks], bop, accL);
-                accT = Ops::mma(AT[ks], bop, accT);
+            for (int ks = 0; ks < BSTEP; ++ks) bop[ks] = O::lds(brow + ks * O::PER);
+#pragma unroll
+            for (int tt = 0; tt < TPW; ++tt) {
+                floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < BSTEP; ++ks) acc = O::mma(A[tt][ks], bop[ks], acc);
+                const int k0 = 16 * (mt0 + tt) + 4 * q;
+                if (k0 < 2 * H) {
+                    *reinterpret_cast<float2*>(&gbuf[sb][yy][k0]) = make_float2(acc[0], acc[1]);
+                    *reinterpret_cast<float2*>(&gbuf[sb][yy][k0 + 2]) = make_float2(acc[2], acc[3]);
+                }
             }
-            gl[nt] = accL;
-            if (jok) {
-                *reinterpret_cast<float4*>(&gtbuf[yy][j0]) = make_float4(accT[0], accT[1], accT[2], accT[3]);
-                const floatx4 v = dct_new[nt];
-                *reinterpret_cast<float4*>(&dctbuf[yy][j0]) = make_float4(v[0], v[1], v[2], v[3]);
-            }
+#pragma unroll
+            for (int wq = 0; wq < WQ; ++wq) dct[yy][4 * (w * WQ + wq) + q] = dcn[nt][wq];
         }
-        __syncthreads();
+        lds_barrier();
     };
 
-    __syncthreads();
-    BwdPre<NT, T> b0, b1;
-    if constexpr (Prefetch<H, NT, T>::on) {
+    lds_barrier();
+    BPre<NT, WQ, T> b0, b1;
+    if constexpr (Prefetch2<T>::template on<NT, WQ>()) {
         fetch(steps - 1, b0);
         int s = steps - 1;
         for (; s - 1 >= 0; s -= 2) {
@@ -479,20 +644,31 @@ k_wave_bwd(WaveArgs a) {
 // ---------------------------------------------------------------------------
 // Dispatch over (hidden size, N tiles, storage type).
 // ---------------------------------------------------------------------------
+// LDS of the backward kernel; shapes beyond the 160 KB of a CU are not built.
 template <int H, int NT, typename T>
-static void launch_pair(bool fwd, int n_units, const WaveArgs& a, hipStream_t s) {
-    const dim3 grid(n_units), block(64 * ((H + 15) / 16));
+constexpr bool bwd_fits() {
+    using Gm = Geo<H, T>;
+    return (size_t)NT * 16 * (Gm::G + 16 / sizeof(T)) * sizeof(T) +
+               (size_t)Gm::SPLB * (NT * 16 + 1) * (2 * H + 2) * 4 + (size_t)(NT * 16 + 1) * (H + 2) * 4 +
+               (size_t)NT * 16 * 8 <=
+           160 * 1024;
+}
+
+template <int H, int NT, typename T>
+static void launch_unit(bool fwd, int n_units, const WaveArgs& a, hipStream_t s) {
+    const dim3 grid(n_units), block(64 * Geo<H, T>::NW);
     if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_wave_bwd<H, NT, T>), grid, block, 0, s, a);
+    else if constexpr (bwd_fits<H, NT, T>()) hipLaunchKernelGGL((k_wave_bwd<H, NT, T>), grid, block, 0, s, a);
 }
 
 template <int H, typename T>
 static hipError_t launch_nt(bool fwd, int nt, int n_units, const WaveArgs& a, hipStream_t s) {
+    if (nt == 4 && !bwd_fits<H, 4, T>()) return hipErrorInvalidValue;  // host rejects these rectangles
     switch (nt) {
-        case 1: launch_pair<H, 1, T>(fwd, n_units, a, s); break;
-        case 2: launch_pair<H, 2, T>(fwd, n_units, a, s); break;
-        case 3: launch_pair<H, 3, T>(fwd, n_units, a, s); break;
-        case 4: launch_pair<H, 4, T>(fwd, n_units, a, s); break;
+        case 1: launch_unit<H, 1, T>(fwd, n_units, a, s); break;
+        case 2: launch_unit<H, 2, T>(fwd, n_units, a, s); break;
+        case 3: launch_unit<H, 3, T>(fwd, n_units, a, s); break;
+        case 4: launch_unit<H, 4, T>(fwd, n_units, a, s); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -46,6 +46,9 @@ constexpr int32_t kMaxPackN = 4096;         // placement keys + skip list fit 48
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Device buffers are accessed with 16-byte vector loads and stores.
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; }
+
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 // ---------------------------------------------------------------------------
@@ -176,11 +179,15 @@ mdlstm_status prepare(const mdlstm_layer_desc* desc, int32_t ch, int32_t cw, con
     int32_t max_h = 0;
     st = check_rects(n_rects, rects, ch, cw, &max_h);
     if (st != MDLSTM_OK) return st;
+    if (desc->dtype == MDLSTM_BF16 && desc->hidden == 128 && max_h > 48)
+        return fail(MDLSTM_ERR_UNSUPPORTED, "bf16 hidden 128 supports rectangles up to 48 high, got %d", max_h);
     const int64_t cells = (int64_t)ch * cw;
     if (cells > 0 && (!d_x || !d_mask)) return fail(MDLSTM_ERR_INVALID_ARG, "x or mask is NULL");
     if (!d_wx || !d_u || !d_b) return fail(MDLSTM_ERR_INVALID_ARG, "a weight pointer is NULL");
     Plan p = plan(desc, ch, cw, n_rects);
     if (!d_workspace) return fail(MDLSTM_ERR_INVALID_ARG, "workspace is NULL");
+    if (misaligned(d_x) || misaligned(d_wx) || misaligned(d_u) || misaligned(d_b) || misaligned(d_workspace))
+        return fail(MDLSTM_ERR_INVALID_ARG, "x, weights and workspace must be 16-byte aligned");
     if (ws_bytes < p.total)
         return fail(MDLSTM_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, p.total);
     out->g = geom(desc, ch, cw);
@@ -391,6 +398,7 @@ mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, in
                                workspace_bytes, &c);
     if (st != MDLSTM_OK) return st;
     if (c.g.n_cells > 0 && !d_y) return fail(MDLSTM_ERR_INVALID_ARG, "y is NULL");
+    if (misaligned(d_y)) return fail(MDLSTM_ERR_INVALID_ARG, "y must be 16-byte aligned");
     if (c.g.n_cells == 0) return MDLSTM_OK;
     hipStream_t s = as_stream(stream);
     st = stage_layout(c, n_rects, rects, d_mask, s);
@@ -419,6 +427,9 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
     if (st != MDLSTM_OK) return st;
     if (!d_dwx || !d_du || !d_db) return fail(MDLSTM_ERR_INVALID_ARG, "a weight-gradient pointer is NULL");
     if (c.g.n_cells > 0 && (!d_y || !d_dy || !d_dx)) return fail(MDLSTM_ERR_INVALID_ARG, "y, dy or dx is NULL");
+    if (misaligned(d_y) || misaligned(d_dy) || misaligned(d_dx) || misaligned(d_dwx) || misaligned(d_du) ||
+        misaligned(d_db))
+        return fail(MDLSTM_ERR_INVALID_ARG, "y, dy, dx and the weight gradients must be 16-byte aligned");
     hipStream_t s = as_stream(stream);
     st = stage_layout(c, n_rects, rects, d_mask, s);
     if (st != MDLSTM_OK) return st;

@@ -92,3 +92,18 @@ def test_workspace_bytes_scale():
     assert a > 100 * 100 * (20 * 16 + 4 * 16) * 4
     assert b > a
     assert L.lib().mdlstm_workspace_bytes(None, 1, 1, 1) == 0
+
+
+@pytest.mark.parametrize("which", ["x", "wx", "workspace", "y"])
+def test_forward_rejects_misaligned_pointers(built_lib, which):
+    L = _lib()
+    d = L.LayerDesc(16, 16, 0)
+    rects = [(0, 0, 3, 3)]
+    arr = (L.Rect * 1)(*[L.Rect(*r) for r in rects])
+    need = L.lib().mdlstm_workspace_bytes(ctypes.byref(d), 10, 10, 1)
+    ptr = {k: FAKE for k in ("x", "mask", "wx", "u", "b", "y", "workspace")}
+    ptr[which] = FAKE + 4  # the alignment check fails before any device access
+    st = L.lib().mdlstm_forward(ctypes.byref(d), 10, 10, ptr["x"], ptr["mask"], 1, arr, ptr["wx"], ptr["u"],
+                                ptr["b"], ptr["y"], ptr["workspace"], need, None)
+    assert st == 1
+    assert b"aligned" in L.lib().mdlstm_last_error()
