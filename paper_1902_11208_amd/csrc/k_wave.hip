@@ -131,6 +131,24 @@ constexpr bool fwd_stage() {
     return fwd_lds_base<H, NT, T>() + (size_t)NT * 16 * 16 * ((Q::QF + 1) + 2 * (Q::QZ + 1)) <= 128 * 1024;
 }
 
+// LDS bytes of the backward kernel without and with staging of its inputs
+// (two diagonals of gates, upstream gradients and cell states).
+template <int H, int NT, typename T>
+constexpr size_t bwd_lds_base() {
+    using Gm = Geo<H, T>;
+    return (size_t)NT * 16 * (Gm::G + 16 / sizeof(T)) * sizeof(T) +
+           (size_t)Gm::SPLB * (NT * 16 + 1) * (2 * H + 2) * 4 + (size_t)(NT * 16 + 1) * (H + 2) * 4;
+}
+template <int H, int NT, typename T>
+constexpr size_t bwd_lds_stage() {
+    constexpr size_t nth = 64 * Geo<H, T>::NW;
+    return 2 * ((NT * 16 * (OutQ<H, T>::QF + 1) + nth - 1) / nth * nth) * 16;
+}
+template <int H, int NT, typename T>
+constexpr bool bwd_stage() {
+    return bwd_lds_base<H, NT, T>() + bwd_lds_stage<H, NT, T>() <= 128 * 1024;
+}
+
 template <typename T>
 struct Prefetch2 {
     template <int NT, int WQ>
@@ -456,14 +474,24 @@ k_wave_bwd(WaveArgs a) {
     using Gm = Geo<H, T>;
     using O = Ops<T>;
     using Op = typename O::Op;
-    constexpr int WQ = Gm::WQ, G = Gm::G, KRUNB = Gm::KRUNB;
+    using Q = OutQ<H, T>;
+    constexpr int WQ = Gm::WQ, G = Gm::G, KRUNB = Gm::KRUNB, NTH = 64 * Gm::NW;
     constexpr int TPW = Gm::TPW, SPLB = Gm::SPLB, BSTEP = Gm::BSTEP;
     constexpr int GP = G + 16 / (int)sizeof(T);
+    // Staged: the gates, upstream gradients and cell states of a diagonal are
+    // loaded as contiguous 16-byte chunks into registers two steps ahead and
+    // kept in LDS for two steps (own cells, then left/top predecessors of the
+    // next diagonal). Otherwise every lane loads its own values.
+    constexpr bool STAGE = bwd_stage<H, NT, T>();
+    constexpr int PB = STAGE ? Q::QF + 1 : 1;  // row pitch in chunks; the extra chunk spreads LDS banks
+    constexpr int NSL = STAGE ? (NT * 16 * PB + NTH - 1) / NTH * NTH : 1;
+    constexpr int NITZ = STAGE ? NSL / NTH : 0;
+    constexpr int NITF = (NT * 16 * Q::QZ + NTH - 1) / NTH;  // passes writing back the gate gradients
+    constexpr int CC = Q::QZ + Q::QY;                        // first cell-state chunk of a row
     __shared__ __attribute__((aligned(16))) T dabuf[NT * 16][GP];
     __shared__ __attribute__((aligned(16))) float gbuf[SPLB][NT * 16 + 1][2 * H + 2];  // row NT*16 stays zero
     __shared__ __attribute__((aligned(16))) float dct[NT * 16 + 1][H + 2];
-    __shared__ int64_t bpos[NT * 16];  // cell of dabuf row written back: p, or -1
-    constexpr int QZ = OutQ<H, T>::QZ;
+    __shared__ __attribute__((aligned(16))) u32x4 ist[STAGE ? 2 : 1][NSL];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int q = lane >> 4, n16 = lane & 15;
@@ -497,9 +525,10 @@ k_wave_bwd(WaveArgs a) {
         for (int wq = 0; wq < WQ; ++wq) dcl[nt][wq] = dcn[nt][wq] = 0.0f;
     __builtin_amdgcn_s_waitcnt(0);  // U operands in registers before the step loop
 
-    // Loads of step s, issued for every lane from valid cells (see the forward
-    // pass); predecessors outside the rectangle read the cell itself and are
-    // zeroed on use.
+    // Cells of diagonal s, their mask bytes and (unstaged) the lane's inputs,
+    // issued for every lane from valid cells (see the forward pass);
+    // predecessors outside the rectangle read the cell itself and are zeroed
+    // on use.
     auto fetch = [&](int s, BPre<NT, WQ, T>& b) {
         const int sc = max(s, 0);
         const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
@@ -509,33 +538,58 @@ k_wave_bwd(WaveArgs a) {
             b.live[nt] = s >= 0 && yy >= ylo && yy <= yhi;
             const int yc = min(max(yy, ylo), yhi), xc = sc - yc;
             const int64_t p = canvas_index(R, d, yc, xc, a.canvas_w);
-            const int64_t pl = xc > 0 ? canvas_index(R, d, yc, xc - 1, a.canvas_w) : p;
-            const int64_t pt = yc > 0 ? canvas_index(R, d, yc - 1, xc, a.canvas_w) : p;
             b.p[nt] = p;
             b.m[nt] = a.mask[p];
-#pragma unroll
-            for (int wq = 0; wq < WQ; ++wq) {
-                const int j = 4 * (w * WQ + wq) + q;
-                const T* zp = Z + p * (4 * G) + d * G + j;
-#pragma unroll
-                for (int t = 0; t < 5; ++t) b.g[nt][wq][t] = zp[t * H];
-                b.dy[nt][wq] = DY[p * (4 * H) + d * H + j];
-                b.c[nt][wq] = Cs[p * (4 * H) + d * H + j];
-                b.cl[nt][wq] = Cs[pl * (4 * H) + d * H + j];
-                b.ct[nt][wq] = Cs[pt * (4 * H) + d * H + j];
-            }
             b.hasl[nt] = xc > 0;
             b.hast[nt] = yc > 0;
+            if constexpr (!STAGE) {
+                const int64_t pl = xc > 0 ? canvas_index(R, d, yc, xc - 1, a.canvas_w) : p;
+                const int64_t pt = yc > 0 ? canvas_index(R, d, yc - 1, xc, a.canvas_w) : p;
+#pragma unroll
+                for (int wq = 0; wq < WQ; ++wq) {
+                    const int j = 4 * (w * WQ + wq) + q;
+                    const T* zp = Z + p * (4 * G) + d * G + j;
+#pragma unroll
+                    for (int t = 0; t < 5; ++t) b.g[nt][wq][t] = zp[t * H];
+                    b.dy[nt][wq] = DY[p * (4 * H) + d * H + j];
+                    b.c[nt][wq] = Cs[p * (4 * H) + d * H + j];
+                    b.cl[nt][wq] = Cs[pl * (4 * H) + d * H + j];
+                    b.ct[nt][wq] = Cs[pt * (4 * H) + d * H + j];
+                }
+            }
         }
+    };
+
+    // Staged rows of diagonal s (clamped at 0) into zr: slot S is chunk S % PB
+    // of the row of cell S / PB, a row being the 5H gates, the H upstream
+    // gradients and the H cell states of the cell (padding chunk and slots
+    // past the last cell repeat a valid chunk).
+    u32x4 zr[NITZ > 0 ? NITZ : 1];
+    auto fetch_rows = [&](int s) {
+        if constexpr (STAGE) {
+            const int sc = max(s, 0);
+            const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
+#pragma unroll
+            for (int it = 0; it < NITZ; ++it) {
+                const int S = it * NTH + (int)threadIdx.x;
+                const int cell = min(S / PB, NT * 16 - 1), r = min(S - (S / PB) * PB, Q::QF - 1);
+                const int yc = min(max(cell, ylo), yhi);
+                const int64_t p = canvas_index(R, d, yc, sc - yc, a.canvas_w);
+                const char* zs = reinterpret_cast<const char*>(Z + p * (4 * G) + d * G) + 16 * r;
+                const char* ys = reinterpret_cast<const char*>(DY + p * (4 * H) + d * H) + 16 * (r - Q::QZ);
+                const char* cs = reinterpret_cast<const char*>(Cs + p * (4 * H) + d * H) + 16 * (r - CC);
+                zr[it] = *reinterpret_cast<const u32x4*>(r < Q::QZ ? zs : (r < CC ? ys : cs));
+            }
+        }
+    };
+    auto stage_in = [&](int s) {
+#pragma unroll
+        for (int it = 0; it < NITZ; ++it) ist[s & 1][it * NTH + threadIdx.x] = zr[it];
     };
 
     auto compute = [&](int s, const BPre<NT, WQ, T>& b) {
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
         // Phase A: gate-gradient update of this lane's (cell, hidden unit) pairs.
-        if (w == 0 && q == 0) {
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) bpos[16 * nt + n16] = b.live[nt] && b.m[nt] ? b.p[nt] : -1;
-        }
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;
@@ -546,21 +600,35 @@ k_wave_bwd(WaveArgs a) {
                 float da[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
                 float ndl = 0.0f, ndt = 0.0f;
                 if (b.live[nt] && b.m[nt]) {
-                    const float gi = ld1f<T>(&b.g[nt][wq][0]), gfl = ld1f<T>(&b.g[nt][wq][1]),
-                                gft = ld1f<T>(&b.g[nt][wq][2]), go = ld1f<T>(&b.g[nt][wq][3]),
-                                gg = ld1f<T>(&b.g[nt][wq][4]);
+                    float g[5], dyv, cv, cL, cT;
+                    if constexpr (STAGE) {
+                        const T* row = reinterpret_cast<const T*>(&ist[s & 1][yy * PB]);
+#pragma unroll
+                        for (int t = 0; t < 5; ++t) g[t] = ld1f<T>(row + t * H + j);
+                        dyv = ld1f<T>(row + 5 * H + j);
+                        cv = reinterpret_cast<const float*>(&ist[s & 1][yy * PB + CC])[j];
+                        const u32x4* prv = &ist[(s - 1) & 1][0];
+                        cL = b.hasl[nt] ? reinterpret_cast<const float*>(prv + yy * PB + CC)[j] : 0.0f;
+                        cT = b.hast[nt] ? reinterpret_cast<const float*>(prv + max(yy - 1, 0) * PB + CC)[j] : 0.0f;
+                    } else {
+#pragma unroll
+                        for (int t = 0; t < 5; ++t) g[t] = ld1f<T>(&b.g[nt][wq][t]);
+                        dyv = ld1f<T>(&b.dy[nt][wq]);
+                        cv = b.c[nt][wq];
+                        cL = b.hasl[nt] ? b.cl[nt][wq] : 0.0f;
+                        cT = b.hast[nt] ? b.ct[nt][wq] : 0.0f;
+                    }
+                    const float gi = g[0], gfl = g[1], gft = g[2], go = g[3], gg = g[4];
                     float gl = 0.0f, gtv = 0.0f;
 #pragma unroll
                     for (int k = 0; k < SPLB; ++k) {
                         gl += gbuf[k][yy][j];
                         gtv += gbuf[k][yy + 1][H + j];
                     }
-                    const float dh = ld1f<T>(&b.dy[nt][wq]) + gl + gtv;
-                    const float tc = tanh_fast(b.c[nt][wq]);
+                    const float dh = dyv + gl + gtv;
+                    const float tc = tanh_fast(cv);
                     const float dc = dcl[nt][wq] + dct[yy + 1][j] + dh * go * (1.0f - tc * tc);
                     da[0] = dc * gg * gi * (1.0f - gi);
-                    const float cL = b.hasl[nt] ? b.cl[nt][wq] : 0.0f;
-                    const float cT = b.hast[nt] ? b.ct[nt][wq] : 0.0f;
                     da[1] = dc * cL * gfl * (1.0f - gfl);
                     da[2] = dc * cT * gft * (1.0f - gft);
                     da[3] = dh * tc * go * (1.0f - go);
@@ -575,25 +643,29 @@ k_wave_bwd(WaveArgs a) {
             }
         }
         lds_barrier();
+        // Staged rows of diagonal s - 2 replace those of diagonal s, which no
+        // lane reads any more; the rows of diagonal s - 3 start loading.
+        if constexpr (STAGE) {
+            stage_in(s - 2);
+            fetch_rows(s - 3);
+        }
         // The rows of dabuf are the gate gradients of the diagonal's cells:
-        // write them back with contiguous 16-byte stores.
+        // write them back with contiguous 16-byte stores. Every lane stores in
+        // every pass (rows outside the diagonal repeat its nearest cell; cells
+        // with mask 0 get zero gradients), so the number of stores is fixed.
         {
-            constexpr int NCH = NT * 16 * QZ, NTH = 64 * Gm::NW, NIT = (NCH + NTH - 1) / NTH;
-            u32x4 v[NIT];
-            u32x4* dst[NIT];
-            bool ok[NIT];
+            constexpr int NCH = NT * 16 * Q::QZ;
+            u32x4 v[NITF];
+            u32x4* dst[NITF];
 #pragma unroll
-            for (int it = 0; it < NIT; ++it) {
+            for (int it = 0; it < NITF; ++it) {
                 const int i = min(it * NTH + (int)threadIdx.x, NCH - 1);
-                const int cell = i / QZ, r = i - cell * QZ;
-                const int64_t p = bpos[cell];
+                const int cell = min(max(i / Q::QZ, ylo), yhi), r = i - (i / Q::QZ) * Q::QZ;
                 v[it] = reinterpret_cast<const u32x4*>(&dabuf[cell][0])[r];
-                dst[it] = reinterpret_cast<u32x4*>(Z + (p >= 0 ? p : 0) * (4 * G) + d * G) + r;
-                ok[it] = it * NTH + (int)threadIdx.x < NCH && p >= 0;
+                dst[it] = reinterpret_cast<u32x4*>(Z + canvas_index(R, d, cell, s - cell, a.canvas_w) * (4 * G) + d * G) + r;
             }
 #pragma unroll
-            for (int it = 0; it < NIT; ++it)
-                if (ok[it]) *dst[it] = v[it];
+            for (int it = 0; it < NITF; ++it) *dst[it] = v[it];
         }
         // Phase B: U^T da for the left (rows k < H) and top (k >= H) predecessors.
 #pragma unroll
@@ -621,9 +693,27 @@ k_wave_bwd(WaveArgs a) {
         lds_barrier();
     };
 
-    lds_barrier();
     BPre<NT, WQ, T> b0, b1;
-    if constexpr (Prefetch2<T>::template on<NT, WQ>()) {
+    if constexpr (STAGE) {
+        // Before step s: rows of diagonals s and s - 1 in LDS, rows of s - 2
+        // loading, cells of s in registers.
+        fetch_rows(steps - 1);
+        stage_in(steps - 1);
+        fetch_rows(steps - 2);
+        stage_in(steps - 2);
+        fetch_rows(steps - 3);
+        fetch(steps - 1, b0);
+        lds_barrier();
+        auto step = [&](int s, const BPre<NT, WQ, T>& cur, BPre<NT, WQ, T>& nxt) {
+            fetch(s - 1, nxt);
+            compute(s, cur);
+        };
+        for (int s = steps - 1; s >= 0; s -= 2) {
+            step(s, b0, b1);
+            if (s - 1 >= 0) step(s - 1, b1, b0);
+        }
+    } else if constexpr (Prefetch2<T>::template on<NT, WQ>()) {
+        lds_barrier();
         fetch(steps - 1, b0);
         int s = steps - 1;
         for (; s - 1 >= 0; s -= 2) {
@@ -634,6 +724,7 @@ k_wave_bwd(WaveArgs a) {
         }
         if (s >= 0) compute(s, b0);
     } else {
+        lds_barrier();
         for (int s = steps - 1; s >= 0; --s) {
             fetch(s, b0);
             compute(s, b0);
@@ -647,11 +738,7 @@ k_wave_bwd(WaveArgs a) {
 // LDS of the backward kernel; shapes beyond the 160 KB of a CU are not built.
 template <int H, int NT, typename T>
 constexpr bool bwd_fits() {
-    using Gm = Geo<H, T>;
-    return (size_t)NT * 16 * (Gm::G + 16 / sizeof(T)) * sizeof(T) +
-               (size_t)Gm::SPLB * (NT * 16 + 1) * (2 * H + 2) * 4 + (size_t)(NT * 16 + 1) * (H + 2) * 4 +
-               (size_t)NT * 16 * 8 <=
-           160 * 1024;
+    return bwd_lds_base<H, NT, T>() + (bwd_stage<H, NT, T>() ? bwd_lds_stage<H, NT, T>() : 0) <= 160 * 1024;
 }
 
 template <int H, int NT, typename T>
