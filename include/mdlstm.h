@@ -185,6 +185,67 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
                               void* d_dx, float* d_dwx, float* d_du, float* d_db,
                               void* d_workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Stack glue (Section V-B, Fig. 1): a multi-layer network keeps every layer
+ * on a packed canvas. Between two MDLSTM layers a block-strided convolution
+ * (stride equal to its bh x bw kernel, so blocks never overlap) with tanh maps
+ * one layer's output canvas onto the next layer's input canvas, where each
+ * example occupies a rectangle bh times lower and bw times narrower (packed
+ * again with mdlstm_pack_layout). It is grouped by scan direction: group d
+ * reads the H channels d*H + j of the block's pixels, input index
+ * (dy*bw + dx)*H + j, and writes og channels d*og + o:
+ *   out[p'][d*og + o] = tanh(b[d][o] + sum_{dy,dx,j} W[d][o][(dy*bw+dx)*H + j]
+ *                                      * y[pixel (by*bh + dy, bx*bw + dx)][d*H + j])
+ * All glue tensors are fp32. The convolutions support bh x bw = 2 x 4 (the
+ * paper's block), hidden in {4, 8, 16, 32, 64} and og in {4, 8, 16, 32} with
+ * 4*og*bh*bw*hidden <= 16384 (else UNSUPPORTED).
+ */
+
+/* Workspace of mdlstm_pack_blocks (hidden = og = 0) and of the block
+ * convolutions for n examples. */
+size_t mdlstm_blocks_workspace_bytes(int32_t n, int32_t hidden, int32_t og);
+
+/*
+ * Block reshape of the stack input: image k (device, HWC fp32
+ * [rects[k].h*bh][rects[k].w*bw][c]) becomes [rects[k].h][rects[k].w][bh*bw*c],
+ * channel (dy*bw + dx)*c + ch, written into rectangle rects[k] of d_canvas
+ * [canvas_h][canvas_w][bh*bw*c]; the rest of the canvas is set to zero.
+ * d_images: host array of n device pointers. Rectangles must be disjoint and
+ * inside the canvas (BAD_LAYOUT).
+ */
+mdlstm_status mdlstm_pack_blocks(int32_t n, const float* const* d_images, int32_t c, int32_t bh, int32_t bw,
+                                 const mdlstm_rect* rects, int32_t canvas_h, int32_t canvas_w, float* d_canvas,
+                                 void* d_workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Grouped block convolution forward. in_rects[k] (host) is example k on the
+ * input canvas d_y [in_h][in_w][4*hidden]; out_rects[k] (host) on the output
+ * canvas d_out [out_h][out_w][4*og], with in_rects[k].h == bh*out_rects[k].h
+ * and in_rects[k].w == bw*out_rects[k].w (BAD_LAYOUT otherwise). d_w
+ * [4][og][bh*bw*hidden], d_b [4][og]. d_out is overwritten: the formula above
+ * inside the output rectangles, zero elsewhere.
+ */
+mdlstm_status mdlstm_block_conv_forward(int32_t n, int32_t hidden, int32_t og, int32_t bh, int32_t bw,
+                                        const mdlstm_rect* in_rects, int32_t in_h, int32_t in_w, const float* d_y,
+                                        const float* d_w, const float* d_b, const mdlstm_rect* out_rects,
+                                        int32_t out_h, int32_t out_w, float* d_out, void* d_workspace,
+                                        size_t workspace_bytes, void* stream);
+
+/*
+ * Grouped block convolution backward: gradients of sum(out * dout).
+ * d_out: the forward output; d_dout: its gradient (read inside the output
+ * rectangles only). d_dy (out) [in_h][in_w][4*hidden]: input gradient inside
+ * the input rectangles, zero elsewhere. d_dw [4][og][bh*bw*hidden] and d_db
+ * [4][og] (out): OVERWRITTEN, summed over all blocks of all examples in a fixed
+ * order (bitwise reproducible).
+ */
+mdlstm_status mdlstm_block_conv_backward(int32_t n, int32_t hidden, int32_t og, int32_t bh, int32_t bw,
+                                         const mdlstm_rect* in_rects, int32_t in_h, int32_t in_w, const float* d_y,
+                                         const float* d_w, const mdlstm_rect* out_rects, int32_t out_h,
+                                         int32_t out_w, const float* d_out, const float* d_dout, float* d_dy,
+                                         float* d_dw, float* d_db, void* d_workspace, size_t workspace_bytes,
+                                         void* stream);
+
 /* Message for the last non-OK status returned on the calling thread. */
 const char* mdlstm_last_error(void);
 

@@ -43,6 +43,14 @@ SIGNATURES = {
                                 c_void, c_void, c_void, c_void, c_void, c_void, c_size, c_void]),
     "mdlstm_last_error": (c_char_p, []),
     "mdlstm_set_phase_events": (c_i32, [c_i32, P_VOIDP]),
+    "mdlstm_blocks_workspace_bytes": (c_size, [c_i32, c_i32, c_i32]),
+    "mdlstm_pack_blocks": (c_i32, [c_i32, P_VOIDP, c_i32, c_i32, c_i32, P_RECT, c_i32, c_i32, c_void, c_void, c_size,
+                                   c_void]),
+    "mdlstm_block_conv_forward": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_i32, P_RECT, c_i32, c_i32, c_void, c_void,
+                                          c_void, P_RECT, c_i32, c_i32, c_void, c_void, c_size, c_void]),
+    "mdlstm_block_conv_backward": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_i32, P_RECT, c_i32, c_i32, c_void, c_void,
+                                           P_RECT, c_i32, c_i32, c_void, c_void, c_void, c_void, c_void, c_void, c_size,
+                                           c_void]),
 }
 
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "TOO_WIDE", 3: "BAD_LAYOUT", 4: "WORKSPACE", 5: "UNSUPPORTED", 6: "DEVICE"}

@@ -219,3 +219,74 @@ class MDLSTMLayer:
         backward(self.prep, self.x, self.mask, self.wx, self.u, self.b, self.y, dy, self.dx, self.dwx, self.du,
                  self.db, self.workspace, stream)
         return self.dx, self.dwx, self.du, self.db
+
+
+# ---------------------------------------------------------------------------
+# Stack glue (block reshape, grouped block convolution)
+# ---------------------------------------------------------------------------
+def blocks_workspace_bytes(n: int, hidden: int = 0, og: int = 0) -> int:
+    return int(lib().mdlstm_blocks_workspace_bytes(int(n), int(hidden), int(og)))
+
+
+def pack_blocks(images, rects, canvas_h: int, canvas_w: int, bh: int, bw: int, out=None, stream=None):
+    """Block-reshape fp32 HWC images into their rectangles of a [canvas_h, canvas_w, bh*bw*c] canvas."""
+    n = len(images)
+    r = np.asarray(rects, np.int32).reshape(-1, 4)
+    c = int(images[0].shape[2]) if n else 1
+    dev = images[0].device if n else torch.device("cuda")
+    for k, im in enumerate(images):
+        _check_dev(im, f"image {k}")
+        if im.dtype != torch.float32 or tuple(im.shape) != (r[k, 2] * bh, r[k, 3] * bw, c):
+            raise ValueError(f"image {k} has shape {tuple(im.shape)}, rect says {r[k, 2] * bh}x{r[k, 3] * bw}x{c}")
+    canvas = out if out is not None else torch.empty((canvas_h, canvas_w, bh * bw * c), dtype=torch.float32,
+                                                     device=dev)
+    ptrs = (ctypes.c_void_p * max(1, n))(*[im.data_ptr() for im in images])
+    work = torch.empty(blocks_workspace_bytes(n), dtype=torch.uint8, device=dev)
+    s = stream if stream is not None else torch.cuda.current_stream()
+    check(lib().mdlstm_pack_blocks(n, ctypes.cast(ptrs, P_VOIDP), c, bh, bw, _rect_array(r), canvas_h, canvas_w,
+                                   _ptr(canvas), _ptr(work), work.numel(), _stream(s)))
+    s.synchronize()  # the pointer table in the workspace is released on return
+    return canvas
+
+
+class BlockConv:
+    """Grouped block convolution + tanh from one packed canvas to the next."""
+
+    def __init__(self, w: torch.Tensor, b: torch.Tensor, in_rects, in_hw, out_rects, out_hw, bh: int = 2,
+                 bw: int = 4):
+        _check_dev(w, "w")
+        _check_dev(b, "b")
+        self.w, self.b = w, b
+        self.og = int(w.shape[1])
+        self.hidden = int(w.shape[2]) // (bh * bw)
+        self.bh, self.bw = int(bh), int(bw)
+        self.in_np = np.asarray(in_rects, np.int32).reshape(-1, 4)
+        self.out_np = np.asarray(out_rects, np.int32).reshape(-1, 4)
+        self.n = int(self.in_np.shape[0])
+        self.in_rects, self.out_rects = _rect_array(self.in_np), _rect_array(self.out_np)
+        self.in_h, self.in_w = (int(v) for v in in_hw)
+        self.out_h, self.out_w = (int(v) for v in out_hw)
+        dev = w.device
+        self.work = torch.empty(blocks_workspace_bytes(self.n, self.hidden, self.og), dtype=torch.uint8, device=dev)
+        self.out = torch.empty((self.out_h, self.out_w, 4 * self.og), dtype=torch.float32, device=dev)
+        self.dy = torch.empty((self.in_h, self.in_w, 4 * self.hidden), dtype=torch.float32, device=dev)
+        self.dw = torch.empty_like(w)
+        self.db = torch.empty_like(b)
+
+    def forward(self, y: torch.Tensor, stream=None) -> torch.Tensor:
+        _check_dev(y, "y")
+        self.y = y
+        check(lib().mdlstm_block_conv_forward(self.n, self.hidden, self.og, self.bh, self.bw, self.in_rects, self.in_h,
+                                              self.in_w, _ptr(y), _ptr(self.w), _ptr(self.b), self.out_rects,
+                                              self.out_h, self.out_w, _ptr(self.out), _ptr(self.work),
+                                              self.work.numel(), _stream(stream)))
+        return self.out
+
+    def backward(self, dout: torch.Tensor, stream=None):
+        _check_dev(dout, "dout")
+        check(lib().mdlstm_block_conv_backward(self.n, self.hidden, self.og, self.bh, self.bw, self.in_rects,
+                                               self.in_h, self.in_w, _ptr(self.y), _ptr(self.w), self.out_rects,
+                                               self.out_h, self.out_w, _ptr(self.out), _ptr(dout), _ptr(self.dy),
+                                               _ptr(self.dw), _ptr(self.db), _ptr(self.work), self.work.numel(),
+                                               _stream(stream)))
+        return self.dy, self.dw, self.db

@@ -64,4 +64,33 @@ hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_
                             const void* d_wx, const uint8_t* d_mask, const int32_t* d_rid, void* d_dx,
                             float* d_part, float* d_dwx, float* d_du, float* d_db, hipStream_t s);
 
+// --- stack glue (block reshape, grouped block convolution) -----------------
+// d_blk_off[n + 1]: first block of each example (prefix sum of out_h*out_w).
+hipError_t launch_pack_blocks(int n, const float* const* d_imgs, const int32_t* d_blk_off, int total_blocks,
+                              const int32_t* d_rects, int canvas_w, int c, int bh, int bw, float* d_canvas,
+                              hipStream_t s);
+struct ConvArgs {
+    int n, total_blocks, hidden, og, bh, bw;
+    const int32_t* blk_off;
+    const int32_t* in_rects;
+    int in_w;
+    const int32_t* out_rects;
+    int out_w;
+    const float* y;     // [in canvas][4H]
+    const float* w;     // [4][og][bh*bw*H]
+    const float* b;     // [4][og]
+    float* out;         // [out canvas][4*og] (forward output; backward input)
+    const float* dout;  // backward: gradient of out
+    float* dy;          // backward: gradient of y (only rectangle pixels written)
+    float* dw;          // backward: [4][og][bh*bw*H]
+    float* db;          // backward: [4][og]
+    float* partial;     // backward: conv_partial_bytes
+};
+bool conv_supported(int hidden, int og, int bh, int bw);
+int conv_chunks(int total_blocks);
+size_t conv_partial_bytes(int hidden, int og, int bh, int bw, int total_blocks);
+hipError_t launch_block_conv(bool fwd, const ConvArgs& a, hipStream_t s);
+// Fill n floats with zero.
+hipError_t launch_zero_f32(float* d, int64_t n, hipStream_t s);
+
 }  // namespace mdl

@@ -117,7 +117,8 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
 // pairwise disjoint. Sorted by y0, a rectangle can only overlap those that
 // start fewer than MDLSTM_MAX_RECT_H rows before it.
 // ---------------------------------------------------------------------------
-mdlstm_status check_rects(int32_t n, const mdlstm_rect* r, int32_t ch, int32_t cw, int32_t* max_h) {
+mdlstm_status check_rects(int32_t n, const mdlstm_rect* r, int32_t ch, int32_t cw, int32_t* max_h,
+                          int32_t limit_h = MDLSTM_MAX_RECT_H) {
     if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n_rects is negative");
     if (n > 0 && !r) return fail(MDLSTM_ERR_INVALID_ARG, "rects is NULL");
     int32_t mh = 0;
@@ -127,9 +128,8 @@ mdlstm_status check_rects(int32_t n, const mdlstm_rect* r, int32_t ch, int32_t c
         if (a.y0 < 0 || a.x0 < 0 || (int64_t)a.y0 + a.h > ch || (int64_t)a.x0 + a.w > cw)
             return fail(MDLSTM_ERR_BAD_LAYOUT, "rect %d (%d,%d,%d,%d) leaves the %dx%d canvas", k, a.y0, a.x0, a.h,
                         a.w, ch, cw);
-        if (a.h > MDLSTM_MAX_RECT_H)
-            return fail(MDLSTM_ERR_UNSUPPORTED, "rect %d is %d high; at most %d is supported", k, a.h,
-                        MDLSTM_MAX_RECT_H);
+        if (a.h > limit_h)
+            return fail(MDLSTM_ERR_UNSUPPORTED, "rect %d is %d high; at most %d is supported", k, a.h, limit_h);
         mh = std::max(mh, a.h);
     }
     std::vector<int32_t> order(n);
@@ -454,6 +454,213 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
                                    reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
     }
     HIP_OR_FAIL(mark(7, s));
+    return MDLSTM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Stack glue: block reshape and grouped block convolution between layers.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr int kMaxConvChunks = 512;
+
+size_t blocks_ws_bytes(int32_t n, int32_t hidden, int32_t og) {
+    const size_t nn = n > 0 ? (size_t)n : 1;
+    size_t b = align_up(nn * 8) + 2 * align_up(nn * 16) + align_up((nn + 1) * 4);
+    if (hidden > 0 && og > 0) b += align_up((size_t)kMaxConvChunks * (4 * og * 8 * hidden + 4 * og) * 4);
+    return b;
+}
+
+struct BlockWs {
+    void** ptrs;
+    int32_t* in_rects;
+    int32_t* out_rects;
+    int32_t* blk_off;
+    float* partial;
+};
+
+BlockWs block_ws(void* d_workspace, int32_t n) {
+    const size_t nn = n > 0 ? (size_t)n : 1;
+    char* ws = static_cast<char*>(d_workspace);
+    BlockWs w;
+    w.ptrs = reinterpret_cast<void**>(ws);
+    ws += align_up(nn * 8);
+    w.in_rects = reinterpret_cast<int32_t*>(ws);
+    ws += align_up(nn * 16);
+    w.out_rects = reinterpret_cast<int32_t*>(ws);
+    ws += align_up(nn * 16);
+    w.blk_off = reinterpret_cast<int32_t*>(ws);
+    ws += align_up((nn + 1) * 4);
+    w.partial = reinterpret_cast<float*>(ws);
+    return w;
+}
+
+// Block offsets (prefix sums of the block rectangles' areas) into off[n + 1].
+mdlstm_status block_offsets(int32_t n, const mdlstm_rect* r, std::vector<int32_t>& off) {
+    off.assign((size_t)n + 1, 0);
+    int64_t t = 0;
+    for (int32_t k = 0; k < n; ++k) {
+        off[k] = (int32_t)t;
+        t += (int64_t)r[k].h * r[k].w;
+        if (t > INT32_MAX / 64) return fail(MDLSTM_ERR_UNSUPPORTED, "too many blocks (%lld)", (long long)t);
+    }
+    off[n] = (int32_t)t;
+    return MDLSTM_OK;
+}
+
+// Shared validation of the convolution calls; fills the kernel arguments.
+mdlstm_status conv_prepare(int32_t n, int32_t hidden, int32_t og, int32_t bh, int32_t bw, const mdlstm_rect* in_rects,
+                           int32_t in_h, int32_t in_w, const float* d_y, const float* d_w,
+                           const mdlstm_rect* out_rects, int32_t out_h, int32_t out_w, void* d_workspace,
+                           size_t workspace_bytes, std::vector<int32_t>& off, mdl::ConvArgs& a) {
+    if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n is negative");
+    if (!mdl::conv_supported(hidden, og, bh, bw))
+        return fail(MDLSTM_ERR_UNSUPPORTED, "block convolution hidden %d, og %d, block %dx%d not built", hidden, og,
+                    bh, bw);
+    if (in_h < 0 || in_w < 0 || out_h < 0 || out_w < 0 || in_h > kMaxDim || in_w > kMaxDim || out_h > kMaxDim ||
+        out_w > kMaxDim)
+        return fail(MDLSTM_ERR_INVALID_ARG, "canvas size out of range");
+    int32_t mh = 0;
+    mdlstm_status st = check_rects(n, in_rects, in_h, in_w, &mh, kMaxDim);
+    if (st != MDLSTM_OK) return st;
+    st = check_rects(n, out_rects, out_h, out_w, &mh, kMaxDim);
+    if (st != MDLSTM_OK) return st;
+    for (int32_t k = 0; k < n; ++k)
+        if (in_rects[k].h != bh * out_rects[k].h || in_rects[k].w != bw * out_rects[k].w)
+            return fail(MDLSTM_ERR_BAD_LAYOUT, "example %d: input %dx%d is not %dx%d blocks of %dx%d", k,
+                        in_rects[k].h, in_rects[k].w, out_rects[k].h, out_rects[k].w, bh, bw);
+    if (!d_w) return fail(MDLSTM_ERR_INVALID_ARG, "weights are NULL");
+    if ((int64_t)in_h * in_w > 0 && !d_y) return fail(MDLSTM_ERR_INVALID_ARG, "input canvas is NULL");
+    if (!d_workspace || workspace_bytes < blocks_ws_bytes(n, hidden, og))
+        return fail(MDLSTM_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes,
+                    blocks_ws_bytes(n, hidden, og));
+    if (misaligned(d_y) || misaligned(d_w) || misaligned(d_workspace))
+        return fail(MDLSTM_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+    st = block_offsets(n, out_rects, off);
+    if (st != MDLSTM_OK) return st;
+    const BlockWs w = block_ws(d_workspace, n);
+    a = mdl::ConvArgs{};
+    a.n = n;
+    a.total_blocks = off[n];
+    a.hidden = hidden;
+    a.og = og;
+    a.bh = bh;
+    a.bw = bw;
+    a.blk_off = w.blk_off;
+    a.in_rects = w.in_rects;
+    a.in_w = in_w;
+    a.out_rects = w.out_rects;
+    a.out_w = out_w;
+    a.y = d_y;
+    a.w = d_w;
+    a.partial = w.partial;
+    return MDLSTM_OK;
+}
+
+mdlstm_status conv_stage(int32_t n, const mdlstm_rect* in_rects, const mdlstm_rect* out_rects,
+                         const std::vector<int32_t>& off, void* d_workspace, hipStream_t s) {
+    if (n == 0) return MDLSTM_OK;
+    const BlockWs w = block_ws(d_workspace, n);
+    HIP_OR_FAIL(hipMemcpyAsync(w.in_rects, in_rects, (size_t)n * 16, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(hipMemcpyAsync(w.out_rects, out_rects, (size_t)n * 16, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(hipMemcpyAsync(w.blk_off, off.data(), ((size_t)n + 1) * 4, hipMemcpyHostToDevice, s));
+    return MDLSTM_OK;
+}
+
+}  // namespace
+
+size_t mdlstm_blocks_workspace_bytes(int32_t n, int32_t hidden, int32_t og) {
+    if (n < 0 || hidden < 0 || og < 0) return 0;
+    return blocks_ws_bytes(n, hidden, og);
+}
+
+mdlstm_status mdlstm_pack_blocks(int32_t n, const float* const* d_images, int32_t c, int32_t bh, int32_t bw,
+                                 const mdlstm_rect* rects, int32_t canvas_h, int32_t canvas_w, float* d_canvas,
+                                 void* d_workspace, size_t workspace_bytes, void* stream) {
+    if (n < 0 || c < 1 || bh < 1 || bw < 1 || (int64_t)bh * bw * c > 4096)
+        return fail(MDLSTM_ERR_INVALID_ARG, "n %d, c %d, block %dx%d out of range", n, c, bh, bw);
+    if (canvas_h < 0 || canvas_w < 0 || canvas_h > kMaxDim || canvas_w > kMaxDim)
+        return fail(MDLSTM_ERR_INVALID_ARG, "canvas %dx%d out of range", canvas_h, canvas_w);
+    if ((int64_t)canvas_h * canvas_w > 0 && !d_canvas) return fail(MDLSTM_ERR_INVALID_ARG, "canvas is NULL");
+    int32_t mh = 0;
+    mdlstm_status st = check_rects(n, rects, canvas_h, canvas_w, &mh, kMaxDim);
+    if (st != MDLSTM_OK) return st;
+    if (n > 0 && !d_images) return fail(MDLSTM_ERR_INVALID_ARG, "image array is NULL");
+    for (int32_t k = 0; k < n; ++k)
+        if (!d_images[k]) return fail(MDLSTM_ERR_INVALID_ARG, "image %d is NULL", k);
+    if (!d_workspace || workspace_bytes < blocks_ws_bytes(n, 0, 0))
+        return fail(MDLSTM_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes,
+                    blocks_ws_bytes(n, 0, 0));
+    std::vector<int32_t> off;
+    st = block_offsets(n, rects, off);
+    if (st != MDLSTM_OK) return st;
+    hipStream_t s = as_stream(stream);
+    HIP_OR_FAIL(mdl::launch_zero_f32(d_canvas, (int64_t)canvas_h * canvas_w * bh * bw * c, s));
+    if (n == 0) return MDLSTM_OK;
+    const BlockWs w = block_ws(d_workspace, n);
+    HIP_OR_FAIL(hipMemcpyAsync(w.ptrs, d_images, (size_t)n * 8, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(hipMemcpyAsync(w.out_rects, rects, (size_t)n * 16, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(hipMemcpyAsync(w.blk_off, off.data(), ((size_t)n + 1) * 4, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(mdl::launch_pack_blocks(n, reinterpret_cast<const float* const*>(w.ptrs), w.blk_off, off[n],
+                                        w.out_rects, canvas_w, c, bh, bw, d_canvas, s));
+    return MDLSTM_OK;
+}
+
+mdlstm_status mdlstm_block_conv_forward(int32_t n, int32_t hidden, int32_t og, int32_t bh, int32_t bw,
+                                        const mdlstm_rect* in_rects, int32_t in_h, int32_t in_w, const float* d_y,
+                                        const float* d_w, const float* d_b, const mdlstm_rect* out_rects,
+                                        int32_t out_h, int32_t out_w, float* d_out, void* d_workspace,
+                                        size_t workspace_bytes, void* stream) {
+    std::vector<int32_t> off;
+    mdl::ConvArgs a;
+    mdlstm_status st = conv_prepare(n, hidden, og, bh, bw, in_rects, in_h, in_w, d_y, d_w, out_rects, out_h, out_w,
+                                    d_workspace, workspace_bytes, off, a);
+    if (st != MDLSTM_OK) return st;
+    if (!d_b) return fail(MDLSTM_ERR_INVALID_ARG, "bias is NULL");
+    if ((int64_t)out_h * out_w > 0 && !d_out) return fail(MDLSTM_ERR_INVALID_ARG, "output canvas is NULL");
+    if (misaligned(d_b) || misaligned(d_out)) return fail(MDLSTM_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+    a.b = d_b;
+    a.out = d_out;
+    hipStream_t s = as_stream(stream);
+    HIP_OR_FAIL(mdl::launch_zero_f32(d_out, (int64_t)out_h * out_w * 4 * og, s));
+    st = conv_stage(n, in_rects, out_rects, off, d_workspace, s);
+    if (st != MDLSTM_OK) return st;
+    HIP_OR_FAIL(mdl::launch_block_conv(true, a, s));
+    return MDLSTM_OK;
+}
+
+mdlstm_status mdlstm_block_conv_backward(int32_t n, int32_t hidden, int32_t og, int32_t bh, int32_t bw,
+                                         const mdlstm_rect* in_rects, int32_t in_h, int32_t in_w, const float* d_y,
+                                         const float* d_w, const mdlstm_rect* out_rects, int32_t out_h,
+                                         int32_t out_w, const float* d_out, const float* d_dout, float* d_dy,
+                                         float* d_dw, float* d_db, void* d_workspace, size_t workspace_bytes,
+                                         void* stream) {
+    std::vector<int32_t> off;
+    mdl::ConvArgs a;
+    mdlstm_status st = conv_prepare(n, hidden, og, bh, bw, in_rects, in_h, in_w, d_y, d_w, out_rects, out_h, out_w,
+                                    d_workspace, workspace_bytes, off, a);
+    if (st != MDLSTM_OK) return st;
+    if (!d_dw || !d_db) return fail(MDLSTM_ERR_INVALID_ARG, "a weight-gradient pointer is NULL");
+    if ((int64_t)out_h * out_w > 0 && (!d_out || !d_dout))
+        return fail(MDLSTM_ERR_INVALID_ARG, "output or its gradient is NULL");
+    if ((int64_t)in_h * in_w > 0 && !d_dy) return fail(MDLSTM_ERR_INVALID_ARG, "input gradient is NULL");
+    if (misaligned(d_out) || misaligned(d_dout) || misaligned(d_dy) || misaligned(d_dw) || misaligned(d_db))
+        return fail(MDLSTM_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+    a.out = const_cast<float*>(d_out);
+    a.dout = d_dout;
+    a.dy = d_dy;
+    a.dw = d_dw;
+    a.db = d_db;
+    hipStream_t s = as_stream(stream);
+    HIP_OR_FAIL(mdl::launch_zero_f32(d_dy, (int64_t)in_h * in_w * 4 * hidden, s));
+    if (a.total_blocks == 0) {  // empty batch: zero gradients
+        HIP_OR_FAIL(mdl::launch_zero_f32(d_dw, (int64_t)4 * og * bh * bw * hidden, s));
+        HIP_OR_FAIL(mdl::launch_zero_f32(d_db, (int64_t)4 * og, s));
+        return MDLSTM_OK;
+    }
+    st = conv_stage(n, in_rects, out_rects, off, d_workspace, s);
+    if (st != MDLSTM_OK) return st;
+    HIP_OR_FAIL(mdl::launch_block_conv(false, a, s));
     return MDLSTM_OK;
 }
 

@@ -46,3 +46,34 @@ def run_layer(xs, params, dys, backward=True, workers=1):
             acc = [a + b for a, b in zip(acc, (dWx, dU, db))]
         out["dWx"], out["dU"], out["db"] = acc
     return out
+
+
+def _stack_one(args):
+    from oracle import stack
+
+    image, layers, convs, dy3, block = args
+    Y3, cache = stack.stack_forward(image, layers, convs, block)
+    lg, cg, g = stack.stack_backward(cache, dy3, layers, convs, block)
+    return Y3, lg, cg, g
+
+
+def run_stack(images, layers, convs, dys, block=(2, 4), workers=1):
+    """Per image, alone: last output Y3, input-block gradient, and the summed layer/conv gradients."""
+    l64 = [tuple(np.asarray(t, np.float64) for t in p) for p in layers]
+    c64 = [tuple(np.asarray(t, np.float64) for t in p) for p in convs]
+    jobs = [(np.asarray(im, np.float64), l64, c64, dys[k], block) for k, im in enumerate(images)]
+    if workers > 1 and len(jobs) > 1:
+        with cf.ProcessPoolExecutor(workers, mp_context=mp.get_context("fork")) as ex:
+            results = list(ex.map(_stack_one, jobs))
+    else:
+        results = [_stack_one(j) for j in jobs]
+    out = {"Y": [r[0] for r in results], "dX0": [r[3] for r in results]}
+    lsum = [[np.zeros_like(a) for a in results[0][1][i]] for i in range(len(layers))]
+    csum = [[np.zeros_like(a) for a in results[0][2][i]] for i in range(len(convs))]
+    for _, lg, cg, _ in results:
+        for i in range(len(layers)):
+            lsum[i] = [a + b for a, b in zip(lsum[i], lg[i])]
+        for i in range(len(convs)):
+            csum[i] = [a + b for a, b in zip(csum[i], cg[i])]
+    out["layer_grads"], out["conv_grads"] = lsum, csum
+    return out

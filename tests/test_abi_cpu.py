@@ -107,3 +107,37 @@ def test_forward_rejects_misaligned_pointers(built_lib, which):
                                 ptr["b"], ptr["y"], ptr["workspace"], need, None)
     assert st == 1
     assert b"aligned" in L.lib().mdlstm_last_error()
+
+
+def _conv_fwd(n, hidden, og, bh, bw, in_rects, in_hw, out_rects, out_hw, ws_bytes=None, ptr=FAKE):
+    L = _lib()
+    ia = (L.Rect * max(1, n))(*[L.Rect(*r) for r in in_rects])
+    oa = (L.Rect * max(1, n))(*[L.Rect(*r) for r in out_rects])
+    need = L.lib().mdlstm_blocks_workspace_bytes(n, hidden, og)
+    return L.lib().mdlstm_block_conv_forward(n, hidden, og, bh, bw, ia, in_hw[0], in_hw[1], ptr, FAKE, FAKE, oa,
+                                             out_hw[0], out_hw[1], FAKE, FAKE,
+                                             need if ws_bytes is None else ws_bytes, None)
+
+
+def test_block_conv_rejects_bad_arguments(built_lib):
+    ok_in, ok_out = [(0, 0, 4, 8)], [(0, 0, 2, 2)]
+    assert _conv_fwd(1, 16, 8, 2, 4, ok_in, (4, 8), ok_out, (2, 2), ws_bytes=16) == 4      # workspace
+    assert _conv_fwd(1, 16, 8, 3, 4, [(0, 0, 6, 8)], (6, 8), ok_out, (2, 2)) == 5         # block not built
+    assert _conv_fwd(1, 16, 12, 2, 4, ok_in, (4, 8), ok_out, (2, 2)) == 5                 # og not built
+    assert _conv_fwd(1, 128, 8, 2, 4, ok_in, (4, 8), ok_out, (2, 2)) == 5                 # hidden not built
+    assert _conv_fwd(1, 16, 8, 2, 4, [(0, 0, 4, 4)], (4, 8), ok_out, (2, 2)) == 3         # not bh x bw blocks
+    assert _conv_fwd(1, 16, 8, 2, 4, ok_in, (4, 8), [(1, 1, 2, 2)], (2, 2)) == 3          # leaves the canvas
+    assert _conv_fwd(2, 16, 8, 2, 4, ok_in * 2, (4, 16), [(0, 0, 2, 2), (0, 1, 2, 2)], (2, 4)) == 3  # overlap
+    assert _conv_fwd(1, 16, 8, 2, 4, ok_in, (4, 8), ok_out, (2, 2), ptr=FAKE + 4) == 1    # misaligned
+    assert b"aligned" in _lib().lib().mdlstm_last_error()
+
+
+def test_pack_blocks_rejects_bad_arguments(built_lib):
+    L = _lib()
+    r = (L.Rect * 1)(L.Rect(0, 0, 2, 2))
+    imgs = (ctypes.c_void_p * 1)(FAKE)
+    need = L.lib().mdlstm_blocks_workspace_bytes(1, 0, 0)
+    f = L.lib().mdlstm_pack_blocks
+    assert f(1, ctypes.cast(imgs, L.P_VOIDP), 1, 2, 4, r, 2, 2, FAKE, FAKE, 16, None) == 4     # workspace
+    assert f(1, ctypes.cast(imgs, L.P_VOIDP), 1, 2, 4, r, 1, 2, FAKE, FAKE, need, None) == 3   # leaves canvas
+    assert f(1, ctypes.cast(imgs, L.P_VOIDP), 0, 2, 4, r, 2, 2, FAKE, FAKE, need, None) == 1   # c < 1

@@ -1,0 +1,97 @@
+"""Packed three-layer stack (Section V-B) on the GPU against the oracle, which
+runs every image alone: block reshape, MDLSTM layers, grouped block
+convolutions with tanh and the re-packing between layers, forward and
+backward, all through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+from conftest import rel_err, rel_max
+from synth import configs
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5  # fp32, normwise (L2) and max-norm relative
+
+
+def _gpu_stack(wl, sample=None):
+    from paper_1902_11208_amd import api, stack
+    import gpu_run
+
+    layers, convs = wl.params()
+    dl = [tuple(gpu_run.to_dev(t, "f32") for t in p) for p in layers]
+    dc = [tuple(gpu_run.to_dev(t, "f32") for t in p) for p in convs]
+    st = stack.MDLSTMStack(dl, dc, wl.heights, wl.widths, wl.canvas_w, block=wl.block)
+    x0 = st.pack_input([gpu_run.to_dev(wl.image(k), "f32") for k in range(wl.n)])
+    y3 = st.forward(x0)
+    ch, cw = st.canvas[-1]
+    dy3 = api.pack_data([gpu_run.to_dev(wl.dy(k), "f32") for k in range(wl.n)], st.rects[-1], ch, cw)
+    g0 = st.backward(dy3)
+    torch.cuda.synchronize()
+    ks = range(wl.n) if sample is None else sample
+    Y = api.unpack_data(y3, st.rects[-1])
+    G = api.unpack_data(g0, st.rects[0])
+    out = {"Y": [gpu_run.to_np(Y[k]) for k in ks], "dX0": [gpu_run.to_np(G[k]) for k in ks],
+           "layer_grads": [(gpu_run.to_np(l.dwx), gpu_run.to_np(l.du), gpu_run.to_np(l.db)) for l in st.layers],
+           "conv_grads": [(gpu_run.to_np(c.dw), gpu_run.to_np(c.db)) for c in st.convs], "stack": st}
+    return out, layers, convs
+
+
+def _oracle(wl, layers, convs, ks):
+    import oracle_run
+
+    return oracle_run.run_stack([wl.image(k) for k in ks], layers, convs, [wl.dy(k) for k in ks], wl.block,
+                                workers=oracle_run.default_workers())
+
+
+def _check(name, got, want):
+    e2, em = rel_err(got, want), rel_max(got, want)
+    print(f"  {name}: L2 {e2:.2e} max {em:.2e}", flush=True)
+    assert e2 <= TOL and em <= TOL, (name, e2, em)
+
+
+def test_small_stack_forward_backward():
+    """Three images of different widths, several per canvas row, every output and gradient compared."""
+    wl = configs.StackWorkload(cid=41, heights=np.array([16, 32, 16], np.int32),
+                               widths=np.array([192, 64, 128], np.int32), canvas_w=(128, 32, 8))
+    print("case: small stack, 3 images", flush=True)
+    got, layers, convs = _gpu_stack(wl)
+    want = _oracle(wl, layers, convs, range(wl.n))
+    for k in range(wl.n):
+        _check(f"Y3[{k}]", got["Y"][k], want["Y"][k])
+        _check(f"dX0[{k}]", got["dX0"][k], want["dX0"][k])
+    for i, (g, w) in enumerate(zip(got["layer_grads"], want["layer_grads"])):
+        for nm, a, b in zip(("dWx", "dU", "db"), g, w):
+            _check(f"layer{i}.{nm}", a, b)
+    for i, (g, w) in enumerate(zip(got["conv_grads"], want["conv_grads"])):
+        for nm, a, b in zip(("dW", "db"), g, w):
+            _check(f"conv{i}.{nm}", a, b)
+
+
+def test_stack_config4_sampled():
+    """The 32-image line batch at full size: outputs and input gradients of
+    the widest, the narrowest and two more images, each computed alone by the
+    oracle."""
+    wl = configs.stack_workload()
+    order = np.argsort(wl.widths, kind="stable")
+    ks = sorted({int(order[-1]), int(order[0]), 5, 17})
+    print(f"case: config 4 stack, sampled images {ks}", flush=True)
+    got, layers, convs = _gpu_stack(wl, sample=ks)
+    want = _oracle(wl, layers, convs, ks)
+    for i, k in enumerate(ks):
+        _check(f"Y3[{k}]", got["Y"][i], want["Y"][i])
+        _check(f"dX0[{k}]", got["dX0"][i], want["dX0"][i])
+    st = got["stack"]
+    # every layer's canvas holds all 32 images, several per row
+    assert all(r.shape[0] == wl.n for r in st.rects)
+    assert st.canvas[0][0] < wl.n * (int(wl.heights.max()) // 2)
+
+
+def test_stack_weight_gradients_are_deterministic():
+    wl = configs.StackWorkload(cid=42, heights=np.array([16, 16], np.int32), widths=np.array([128, 64], np.int32),
+                               canvas_w=(64, 16, 4))
+    a, _, _ = _gpu_stack(wl)
+    b, _, _ = _gpu_stack(wl)
+    for ga, gb in zip(a["conv_grads"] + a["layer_grads"], b["conv_grads"] + b["layer_grads"]):
+        for x, y in zip(ga, gb):
+            assert np.array_equal(x, y)
