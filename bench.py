@@ -9,8 +9,14 @@ example padded to the batch maximum) for the packed-vs-padded speed-up.
 Metric: useful cell-updates/s = 4 directions x sum(h*w) / step time, the same
 useful count for both layouts. Inputs are resident in HBM before timing.
 
+--config 4 times the three-layer stack on packed canvases instead (forward
++ backward of all layers and block convolutions; useful cells summed over
+the layers). Per-step times are also given as median and minimum; the
+packing time (placement + scatter) is reported separately and folded into
+a second "with layout" rate.
+
 Prints one JSON line. Options: --gpus N (only 1 is supported), --steps K,
---warmup W, --config {1,2,3,5}, --no-cpu, --no-padded.
+--warmup W, --config {1,2,3,4,5}, --no-cpu, --no-padded.
 """
 from __future__ import annotations
 
@@ -38,7 +44,7 @@ def _parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 5])
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-padded", action="store_true", help="skip the padded-layout comparison")
     return ap.parse_args()
@@ -78,21 +84,27 @@ class Run:
         def to_dev(a):
             return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(tdt).to(dev)
 
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        if kind == "packed":
-            units, ch, mask = api.pack_layout(wl.heights, wl.widths, wl.canvas_w)
-            place, cw = units, wl.canvas_w
-        else:
-            units, place, ch, cw, mask = api.pad_layout(wl.heights, wl.widths)
-        torch.cuda.synchronize()
-        self.layout_ms = (time.perf_counter() - t0) * 1e3
         xs = [to_dev(x) for x in wl.examples()]
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        self.x = api.pack_data(xs, place, ch, cw)
-        torch.cuda.synchronize()
-        self.scatter_ms = (time.perf_counter() - t0) * 1e3
+
+        def layout():
+            if kind == "packed":
+                units, ch, mask = api.pack_layout(wl.heights, wl.widths, wl.canvas_w)
+                return units, units, ch, wl.canvas_w, mask
+            return api.pad_layout(wl.heights, wl.widths)
+
+        # placement + mask, then the scatter of the examples: timed warm (median of 5)
+        t_lay, t_sc = [], []
+        for _ in range(6):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            units, place, ch, cw, mask = layout()
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            self.x = api.pack_data(xs, place, ch, cw)
+            torch.cuda.synchronize()
+            t_lay.append((t1 - t0) * 1e3)
+            t_sc.append((time.perf_counter() - t1) * 1e3)
+        self.layout_ms, self.scatter_ms = float(np.median(t_lay[1:])), float(np.median(t_sc[1:]))
         wx, u, b = (to_dev(p) for p in wl.params())
         self.dy = api.pack_data([to_dev(wl.dy(k)) for k in range(wl.n)], place, ch, cw)
         del xs
@@ -138,7 +150,94 @@ class Run:
             if not self.backward and a >= 4:
                 continue
             phase[name] = float(np.mean([evs[k][a].elapsed_time(evs[k][b]) for k in range(steps)]))
-        return ev_ms / steps, wall_ms / steps, phase
+        last = 7 if self.backward else 3
+        per_step = [evs[k][0].elapsed_time(evs[k][last]) for k in range(steps)]
+        return ev_ms / steps, wall_ms / steps, phase, per_step
+
+
+class StackRun:
+    """The three-layer stack (block reshape, MDLSTM layers, block convolutions) resident on the GPU."""
+
+    def __init__(self, wl, kind: str):
+        import torch
+
+        from paper_1902_11208_amd import api, stack
+
+        self.torch = torch
+        dev = "cuda"
+
+        def to_dev(a):
+            return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+        layers, convs = wl.params()
+        dl = [tuple(to_dev(t) for t in p) for p in layers]
+        dc = [tuple(to_dev(t) for t in p) for p in convs]
+        imgs = [to_dev(wl.image(k)) for k in range(wl.n)]
+        # layouts of all layers (+ buffers), then the block reshape of the images: timed warm (median of 3)
+        t_lay, t_sc = [], []
+        for _ in range(4):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            self.st = stack.MDLSTMStack(dl, dc, wl.heights, wl.widths, wl.canvas_w, block=wl.block, kind=kind)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            self.x = self.st.pack_input(imgs)
+            torch.cuda.synchronize()
+            t_lay.append((t1 - t0) * 1e3)
+            t_sc.append((time.perf_counter() - t1) * 1e3)
+        self.layout_ms, self.scatter_ms = float(np.median(t_lay[1:])), float(np.median(t_sc[1:]))
+        ch, cw = self.st.canvas[-1]
+        self.dy = api.pack_data([to_dev(wl.dy(k)) for k in range(wl.n)], self.st.rects[-1], ch, cw)
+        self.canvas_h, self.canvas_w = self.st.canvas[0]
+        self.n_cells = sum(h * w for h, w in self.st.canvas)
+        self.unit_cells = sum(int(np.sum(l.prep.rects_np[:, 2].astype(np.int64) * l.prep.rects_np[:, 3]))
+                              for l in self.st.layers)
+        self.backward = True
+
+    def step(self):
+        self.st.forward(self.x)
+        self.st.backward(self.dy)
+
+    def time(self, steps: int, warmup: int):
+        torch = self.torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        start.record()
+        for k in range(steps):
+            evs[k][0].record()
+            self.step()
+            evs[k][1].record()
+        stop.record()
+        torch.cuda.synchronize()
+        wall_ms = (time.perf_counter() - t0) * 1e3
+        per_step = [a.elapsed_time(b) for a, b in evs]
+        return start.elapsed_time(stop) / steps, wall_ms / steps, {}, per_step
+
+
+def cpu_baseline_stack(wl, max_images: int = 8):
+    """The oracle on a bounded sample of the stack batch (each image alone, float64)."""
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import oracle_run
+
+    workers = oracle_run.default_workers()
+    ks = list(range(min(max_images, wl.n)))
+    layers, convs = wl.params()
+    t0 = time.perf_counter()
+    oracle_run.run_stack([wl.image(k) for k in ks], layers, convs, [wl.dy(k) for k in ks], wl.block,
+                         workers=workers)
+    dt = time.perf_counter() - t0
+    useful = 0
+    for k in ks:
+        h, w = int(wl.heights[k]), int(wl.widths[k])
+        useful += 4 * sum((h // wl.block[0] ** (l + 1)) * (w // wl.block[1] ** (l + 1)) for l in range(3))
+    return {"value": useful / dt, "unit": "cell-updates/s", "cores": workers, "kind": "oracle",
+            "sample": f"{len(ks)} of {wl.n} images, all three layers and convolutions, forward+backward, "
+                      f"float64 NumPy, process pool of {workers} over images, {dt:.1f} s wall"}
 
 
 def cpu_baseline(wl):
@@ -180,50 +279,43 @@ def main():
         from paper_1902_11208_amd import build
 
         build.build()
-    wl = configs.workload(args.config)
-    useful = 4 * wl.useful_cells
-    print(f"[bench] workload: {wl.name}, {wl.n} examples, useful cell-directions {useful}", file=sys.stderr,
-          flush=True)
+    if args.config == 4:
+        wl = configs.stack_workload()
+        wl.name, wl.dtype, wl.forward_only = ("line stack: 32 x h64 widths 400-1600, MDLSTM 16/32/64 with 2x4 "
+                                              "block convolutions", "f32", False)
+        RunCls = StackRun
+    else:
+        wl = configs.workload(args.config)
+        RunCls = Run
+    print(f"[bench] workload: {wl.name}, {wl.n} examples", file=sys.stderr, flush=True)
 
-    packed = Run(wl, "packed")
-    ms, wall_ms, phase = packed.time(args.steps, args.warmup)
-    print(f"[bench] packed: {ms:.3f} ms/step (wall {wall_ms:.3f})", file=sys.stderr, flush=True)
+    packed = RunCls(wl, "packed")
+    useful = 4 * packed.unit_cells
+    ms, wall_ms, phase, per_step = packed.time(args.steps, args.warmup)
+    print(f"[bench] packed: {ms:.3f} ms/step (wall {wall_ms:.3f}), useful cell-directions {useful}",
+          file=sys.stderr, flush=True)
+    pack_ms = packed.layout_ms + packed.scatter_ms
 
-    alg = algorithmic(wl, packed.n_cells, packed.unit_cells)
-    phases_out = {}
-    for name, t in phase.items():
-        by, fl = alg[name]
-        phases_out[name] = {"ms": round(t, 4), "GB_s": round(by / (t * 1e-3) / 1e9, 1) if t > 0 else None,
-                            "TFLOP_s": round(fl / (t * 1e-3) / 1e12, 2) if t > 0 else None}
-    dom = max(phase, key=lambda k: phase[k])
-    by, fl = alg[dom]
-    achieved = by / (phase[dom] * 1e-3) / 1e9
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None, "kernel": dom,
-                "bytes_per_launch": int(by)}
-    # the projection is a dense contraction: report its MFMA-peak fraction too
-    proj_t = phase.get("projection")
-    peak_mm = PEAK_BF16_MFMA_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
-    proj = None
-    if proj_t:
-        pf = alg["projection"][1] / (proj_t * 1e-3) / 1e12
-        pb = alg["projection"][0] / (proj_t * 1e-3) / 1e9
-        proj = {"TFLOP_s": round(pf, 2), "frac_mfma_peak": round(pf / peak_mm, 4), "GB_s": round(pb, 1),
-                "frac_hbm_peak": round(pb / PEAK_HBM_GBS, 4)}
+    if args.config == 4:
+        roofline, proj, phases_out = None, None, {}
+    else:
+        roofline, proj, phases_out = _rooflines(wl, packed, phase)
 
     padded = None
     if not args.no_padded:
-        pr = Run(wl, "padded")
-        pms, pwall, pphase = pr.time(max(3, args.steps // 2), args.warmup)
-        padded = {"ms_per_step": round(pms, 4), "value": useful / (pms * 1e-3), "canvas_cells": pr.n_cells,
+        pr = RunCls(wl, "padded")
+        pms, pwall, pphase, pper = pr.time(max(3, args.steps // 2), args.warmup)
+        padded = {"ms_per_step": round(pms, 4), "median_ms": round(float(np.median(pper)), 4),
+                  "value": useful / (pms * 1e-3), "canvas_cells": pr.n_cells,
                   "unit_cells": pr.unit_cells, "speedup_packed_vs_padded": round(pms / ms, 3),
+                  "layout_ms": round(pr.layout_ms + pr.scatter_ms, 3),
                   "phases_ms": {k: round(v, 4) for k, v in pphase.items()}}
         print(f"[bench] padded: {pms:.3f} ms/step", file=sys.stderr, flush=True)
         del pr
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(wl)
+        cpu = cpu_baseline_stack(wl) if args.config == 4 else cpu_baseline(wl)
         print(f"[bench] cpu oracle: {cpu['value']:.3e} cell-updates/s on {cpu['cores']} cores", file=sys.stderr,
               flush=True)
 
@@ -247,11 +339,40 @@ def main():
         "padded": padded,
         "projection": proj,
         "phases": phases_out,
+        "median_ms": round(float(np.median(per_step)), 4),
+        "min_ms": round(float(np.min(per_step)), 4),
         "layout_ms": round(packed.layout_ms, 3),
         "scatter_ms": round(packed.scatter_ms, 3),
+        "value_with_layout": useful / ((ms + pack_ms) * 1e-3),
         "wall_ms_per_step": round(wall_ms, 4),
     }
     print(json.dumps(out), flush=True)
+
+
+def _rooflines(wl, packed, phase):
+    """Per-phase rates, the dominant kernel's HBM roofline and the projection's MFMA fraction."""
+    alg = algorithmic(wl, packed.n_cells, packed.unit_cells)
+    phases_out = {}
+    for name, t in phase.items():
+        by, fl = alg[name]
+        phases_out[name] = {"ms": round(t, 4), "GB_s": round(by / (t * 1e-3) / 1e9, 1) if t > 0 else None,
+                            "TFLOP_s": round(fl / (t * 1e-3) / 1e12, 2) if t > 0 else None}
+    dom = max(phase, key=lambda k: phase[k])
+    by, fl = alg[dom]
+    achieved = by / (phase[dom] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None, "kernel": dom,
+                "bytes_per_launch": int(by)}
+    # the projection is a dense contraction: report its MFMA-peak fraction too
+    proj_t = phase.get("projection")
+    peak_mm = PEAK_BF16_MFMA_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
+    proj = None
+    if proj_t:
+        pf = alg["projection"][1] / (proj_t * 1e-3) / 1e12
+        pb = alg["projection"][0] / (proj_t * 1e-3) / 1e9
+        proj = {"TFLOP_s": round(pf, 2), "frac_mfma_peak": round(pf / peak_mm, 4), "GB_s": round(pb, 1),
+                "frac_hbm_peak": round(pb / PEAK_HBM_GBS, 4)}
+    return roofline, proj, phases_out
 
 
 if __name__ == "__main__":

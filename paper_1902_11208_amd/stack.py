@@ -21,10 +21,12 @@ class MDLSTMStack:
     layers: [(wx, u, b)] device tensors per MDLSTM layer; convs: [(w, b)] per
     block convolution (len(layers) - 1). heights/widths: image sizes, each a
     multiple of the total block reduction. canvas_w: canvas width per layer.
+    kind "padded" lays every layer out last-minute padded instead (tiles of
+    the batch maximum, mask = true extents) for comparison.
     """
 
     def __init__(self, layers, convs, heights, widths, canvas_w, block=(2, 4), in_channels: int = 1,
-                 device="cuda"):
+                 device="cuda", kind: str = "packed"):
         if len(convs) != len(layers) - 1 or len(canvas_w) != len(layers):
             raise ValueError("need one convolution between consecutive layers and one canvas width per layer")
         self.bh, self.bw = block
@@ -38,10 +40,14 @@ class MDLSTMStack:
             f = (self.bh ** (li + 1), self.bw ** (li + 1))
             if np.any(hs % f[0]) or np.any(ws % f[1]):
                 raise ValueError(f"image sizes must be multiples of {f[0]}x{f[1]}")
-            rects, ch, mask = api.pack_layout(hs // f[0], ws // f[1], int(canvas_w[li]), device=device)
+            if kind == "packed":
+                rects, ch, mask = api.pack_layout(hs // f[0], ws // f[1], int(canvas_w[li]), device=device)
+                units, cw = rects, int(canvas_w[li])
+            else:
+                units, rects, ch, cw, mask = api.pad_layout(hs // f[0], ws // f[1], device=device)
             self.rects.append(rects)
-            self.canvas.append((ch, int(canvas_w[li])))
-            self.layers.append(api.MDLSTMLayer(wx, u, b, ch, int(canvas_w[li]), rects, mask))
+            self.canvas.append((ch, cw))
+            self.layers.append(api.MDLSTMLayer(wx, u, b, ch, cw, units, mask))
         for li, (w, b) in enumerate(convs):
             self.convs.append(api.BlockConv(w, b, self.rects[li], self.canvas[li], self.rects[li + 1],
                                             self.canvas[li + 1], self.bh, self.bw))
