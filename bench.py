@@ -154,6 +154,27 @@ class Run:
         per_step = [evs[k][0].elapsed_time(evs[k][last]) for k in range(steps)]
         return ev_ms / steps, wall_ms / steps, phase, per_step
 
+    def time_stepwise_forward(self, steps: int, warmup: int) -> float:
+        """Mean forward-wavefront time when it runs as one launch per diagonal from a HIP graph."""
+        torch = self.torch
+        from paper_1902_11208_amd import _lib
+
+        for _ in range(warmup):
+            self.layer.forward_stepwise(self.x)
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(steps)]
+        for row in evs:
+            for e in row:
+                e.record()
+        torch.cuda.synchronize()
+        L = _lib.lib()
+        for k in range(steps):
+            _lib.check(L.mdlstm_set_phase_events(8, (_lib.c_void * 8)(*[e.cuda_event for e in evs[k]])))
+            self.layer.forward_stepwise(self.x)
+        torch.cuda.synchronize()
+        _lib.check(L.mdlstm_set_phase_events(0, None))
+        return float(np.mean([evs[k][2].elapsed_time(evs[k][3]) for k in range(steps)]))
+
 
 class StackRun:
     """The three-layer stack (block reshape, MDLSTM layers, block convolutions) resident on the GPU."""
@@ -297,9 +318,12 @@ def main():
     pack_ms = packed.layout_ms + packed.scatter_ms
 
     if args.config == 4:
-        roofline, proj, phases_out = None, None, {}
+        roofline, proj, phases_out, stepwise = None, None, {}, None
     else:
         roofline, proj, phases_out = _rooflines(wl, packed, phase)
+        stepwise = packed.time_stepwise_forward(max(3, args.steps // 2), args.warmup)
+        print(f"[bench] forward wavefront, one launch per diagonal from a HIP graph: {stepwise:.3f} ms",
+              file=sys.stderr, flush=True)
 
     padded = None
     if not args.no_padded:
@@ -339,6 +363,7 @@ def main():
         "padded": padded,
         "projection": proj,
         "phases": phases_out,
+        "wavefront_fwd_stepwise_graph_ms": None if stepwise is None else round(stepwise, 4),
         "median_ms": round(float(np.median(per_step)), 4),
         "min_ms": round(float(np.min(per_step)), 4),
         "layout_ms": round(packed.layout_ms, 3),

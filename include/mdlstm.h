@@ -166,6 +166,23 @@ mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, in
                              void* d_y, void* d_workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The same forward pass with the wavefront run as one kernel launch per local
+ * anti-diagonal (launch s advances every unit by its diagonal s, reading the
+ * state of diagonal s - 1 back from y and the workspace) instead of one
+ * persistent launch: the alternative schedule of Section IV-A, kept for
+ * comparison. Same arguments, contract and results (bit for bit) as
+ * mdlstm_forward. The launches are recorded once into a HIP graph, which is
+ * replayed while the arguments (pointers, sizes, rectangles) stay the same; the
+ * graph of the last call is kept per calling thread until the next call with
+ * different arguments.
+ */
+mdlstm_status mdlstm_forward_stepwise(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
+                                      const void* d_x, const uint8_t* d_mask,
+                                      int32_t n_rects, const mdlstm_rect* rects,
+                                      const void* d_wx, const void* d_u, const void* d_b,
+                                      void* d_y, void* d_workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Backward pass: gradients of L = sum(Y * dY) after an mdlstm_forward with the
  * same arguments and workspace (reverse anti-diagonal sweep, then weight and
  * input gradient reductions).

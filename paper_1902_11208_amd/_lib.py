@@ -39,6 +39,8 @@ SIGNATURES = {
     "mdlstm_workspace_bytes": (c_size, [P_DESC, c_i32, c_i32, c_i32]),
     "mdlstm_forward": (c_i32, [P_DESC, c_i32, c_i32, c_void, c_void, c_i32, P_RECT, c_void, c_void, c_void, c_void,
                                c_void, c_size, c_void]),
+    "mdlstm_forward_stepwise": (c_i32, [P_DESC, c_i32, c_i32, c_void, c_void, c_i32, P_RECT, c_void, c_void, c_void,
+                                        c_void, c_void, c_size, c_void]),
     "mdlstm_backward": (c_i32, [P_DESC, c_i32, c_i32, c_void, c_void, c_i32, P_RECT, c_void, c_void, c_void, c_void,
                                 c_void, c_void, c_void, c_void, c_void, c_void, c_size, c_void]),
     "mdlstm_last_error": (c_char_p, []),

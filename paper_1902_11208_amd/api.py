@@ -175,6 +175,14 @@ def forward(prep: Prepared, x, mask, wx, u, b, y, workspace, stream=None):
                                prep.ws_bytes if workspace is not None else 0, _stream(stream)))
 
 
+def forward_stepwise(prep: Prepared, x, mask, wx, u, b, y, workspace, stream=None):
+    """Forward pass with one wavefront launch per diagonal, replayed from a HIP graph (comparison variant)."""
+    check(lib().mdlstm_forward_stepwise(ctypes.byref(prep.desc), prep.canvas_h, prep.canvas_w, _ptr(x), _ptr(mask),
+                                        prep.n_rects, prep.rects, _ptr(wx), _ptr(u), _ptr(b), _ptr(y),
+                                        _ptr(workspace), prep.ws_bytes if workspace is not None else 0,
+                                        _stream(stream)))
+
+
 def backward(prep: Prepared, x, mask, wx, u, b, y, dy, dx, dwx, du, db, workspace, stream=None):
     """Enqueue the backward pass; all outputs caller-allocated, overwritten."""
     check(lib().mdlstm_backward(ctypes.byref(prep.desc), prep.canvas_h, prep.canvas_w, _ptr(x), _ptr(mask),
@@ -212,6 +220,12 @@ class MDLSTMLayer:
         _check_dev(x, "x")
         self.x = x
         forward(self.prep, x, self.mask, self.wx, self.u, self.b, self.y, self.workspace, stream)
+        return self.y
+
+    def forward_stepwise(self, x: torch.Tensor, stream=None) -> torch.Tensor:
+        _check_dev(x, "x")
+        self.x = x
+        forward_stepwise(self.prep, x, self.mask, self.wx, self.u, self.b, self.y, self.workspace, stream)
         return self.y
 
     def backward(self, dy: torch.Tensor, stream=None):

@@ -21,6 +21,7 @@
 // (phase A), then the waves contract da with U^T on MFMA, split by output
 // tile and reduction range, partials summed through LDS in a fixed order
 // (phase B). The U operands stay in VGPRs for the whole unit.
+#include <climits>
 #include <type_traits>
 
 #include "common.hpp"
@@ -165,6 +166,7 @@ struct WaveArgs {
     void* y;               // [n_cells][4H] output (fwd)
     const void* dy;        // [n_cells][4H] upstream gradient (bwd)
     int canvas_w;
+    int s0, s1;            // forward: local diagonals [s0, s1) of every unit
 };
 
 template <int NT, int WQ, typename T>
@@ -228,9 +230,25 @@ k_wave_fwd(WaveArgs a) {
     T* __restrict__ Y = static_cast<T*>(a.y);
     float* __restrict__ Cs = a.c;
     const int steps = R.h + R.w - 1;
+    // Diagonals [sb, se) of the unit: all of them in one launch, or one per
+    // launch, in which case the state of diagonal sb - 1 is read back from the
+    // outputs and cell states the previous launch wrote.
+    const int sb = a.s0, se = min(a.s1, steps);
+    if (sb >= se) return;
 
     for (int i = threadIdx.x; i < 2 * ROWS * HP; i += blockDim.x) (&hbuf[0][0][0])[i] = T(0);
     for (int i = threadIdx.x; i < 2 * ROWS * (H + 2); i += blockDim.x) (&cbuf[0][0][0])[i] = 0.0f;
+    if (sb > 0) {
+        const int pb = (sb & 1) ^ 1;  // buffer of diagonal sb - 1
+        for (int i = threadIdx.x; i < NT * 16 * H; i += blockDim.x) {
+            const int yy = i / H, j = i - yy * H, xx = sb - 1 - yy;
+            if (yy < R.h && xx >= 0 && xx < R.w) {
+                const int64_t p = canvas_index(R, d, yy, xx, a.canvas_w);
+                hbuf[pb][yy + 1][j] = Y[p * (4 * H) + d * H + j];
+                cbuf[pb][yy + 1][j] = Cs[p * (4 * H) + d * H + j];
+            }
+        }
+    }
 
     // A operands. Own tiles: row n16 = 4*jj + gate -> U row gate*H + 4*quad + jj.
     // Candidate tile gt: row n16 -> U row 4H + 16*gt + n16, K steps of slice sp only.
@@ -246,11 +264,16 @@ k_wave_fwd(WaveArgs a) {
         const bool ok = j < H;
         load_slot<T, GSTEP>(U + (int64_t)(4 * H + (ok ? j : 0)) * 2 * H + q * KRUN + sp * GSTEP * O::PER, 1, ok, Ag);
     }
-    float cprev[NT][WQ];
+    float cprev[NT][WQ];  // c_L: the lane's cell state of the previous diagonal
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int wq = 0; wq < WQ; ++wq) cprev[nt][wq] = 0.0f;
+        for (int wq = 0; wq < WQ; ++wq) {
+            const int yy = 16 * nt + n16, j = 4 * (w * WQ + wq) + q, xx = sb - 1 - yy;
+            cprev[nt][wq] = sb > 0 && yy < R.h && xx >= 0 && xx < R.w
+                                ? Cs[canvas_index(R, d, yy, xx, a.canvas_w) * (4 * H) + d * H + j]
+                                : 0.0f;
+        }
     // The U operands are in registers before the step loop starts, so no wait
     // inside the loop is attributed to them.
     __builtin_amdgcn_s_waitcnt(0);
@@ -434,27 +457,27 @@ k_wave_fwd(WaveArgs a) {
         auto step = [&](int s, const FPre<NT, WQ, T>& cur, FPre<NT, WQ, T>& nxt) {
             stage_in();
             fetch(s + 1, nxt);
-            if (s > 0) flush(s - 1);
+            if (s > sb) flush(s - 1);
             compute(s, cur);
         };
-        fetch(0, b0);
-        for (int s = 0; s < steps; s += 2) {
+        fetch(sb, b0);
+        for (int s = sb; s < se; s += 2) {
             step(s, b0, b1);
-            if (s + 1 < steps) step(s + 1, b1, b0);
+            if (s + 1 < se) step(s + 1, b1, b0);
         }
-        flush(steps - 1);
+        flush(se - 1);
     } else if constexpr (Prefetch2<T>::template on<NT, WQ>()) {
-        fetch(0, b0);
-        int s = 0;
-        for (; s + 1 < steps; s += 2) {
+        fetch(sb, b0);
+        int s = sb;
+        for (; s + 1 < se; s += 2) {
             fetch(s + 1, b1);
             compute(s, b0);
             fetch(s + 2, b0);
             compute(s + 1, b1);
         }
-        if (s < steps) compute(s, b0);
+        if (s < se) compute(s, b0);
     } else {
-        for (int s = 0; s < steps; ++s) {
+        for (int s = sb; s < se; ++s) {
             fetch(s, b0);
             compute(s, b0);
         }
@@ -784,15 +807,75 @@ static hipError_t launch_wave(bool fwd, const LayerGeom& g, int nt, int n_units,
 hipError_t launch_wavefront_fwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u, void* d_z,
                                 float* d_c, void* d_y, hipStream_t s) {
-    WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w};
+    WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w, 0, INT_MAX};
     return launch_wave(true, g, nt, n_units, a, s);
 }
 
 hipError_t launch_wavefront_bwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u, const void* d_dy,
                                 void* d_z, const float* d_c, hipStream_t s) {
-    WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, const_cast<float*>(d_c), nullptr, d_dy, g.canvas_w};
+    WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, const_cast<float*>(d_c), nullptr, d_dy, g.canvas_w, 0, INT_MAX};
     return launch_wave(false, g, nt, n_units, a, s);
+}
+
+// Forward kernel of a shape and its workgroup size, for graph nodes.
+template <int H, typename T>
+static bool fwd_kernel(int nt, const void** fn, int* threads) {
+    *threads = 64 * Geo<H, T>::NW;
+    switch (nt) {
+        case 1: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 1, T>); return true;
+        case 2: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 2, T>); return true;
+        case 3: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 3, T>); return true;
+        case 4: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 4, T>); return true;
+        default: return false;
+    }
+}
+
+hipError_t build_wavefront_fwd_graph(const LayerGeom& g, int nt, int n_units, int max_steps, const int32_t* d_units,
+                                     const int32_t* d_rects, const uint8_t* d_mask, const void* d_u, void* d_z,
+                                     float* d_c, void* d_y, hipGraphExec_t* exec) {
+    const void* fn = nullptr;
+    int threads = 0;
+    bool ok = false;
+    if (g.dtype == 0) {
+        switch (g.hidden) {
+            case 4: ok = fwd_kernel<4, float>(nt, &fn, &threads); break;
+            case 8: ok = fwd_kernel<8, float>(nt, &fn, &threads); break;
+            case 16: ok = fwd_kernel<16, float>(nt, &fn, &threads); break;
+            case 32: ok = fwd_kernel<32, float>(nt, &fn, &threads); break;
+            case 64: ok = fwd_kernel<64, float>(nt, &fn, &threads); break;
+            default: break;
+        }
+    } else {
+        switch (g.hidden) {
+            case 32: ok = fwd_kernel<32, bf16_t>(nt, &fn, &threads); break;
+            case 64: ok = fwd_kernel<64, bf16_t>(nt, &fn, &threads); break;
+            case 128: ok = fwd_kernel<128, bf16_t>(nt, &fn, &threads); break;
+            default: break;
+        }
+    }
+    if (!ok || n_units <= 0 || max_steps <= 0) return hipErrorInvalidValue;
+    hipGraph_t graph;
+    hipError_t e = hipGraphCreate(&graph, 0);
+    if (e != hipSuccess) return e;
+    hipGraphNode_t prev = nullptr;
+    for (int st = 0; st < max_steps && e == hipSuccess; ++st) {
+        WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w, st, st + 1};
+        void* params[] = {&a};
+        hipKernelNodeParams p{};
+        p.func = const_cast<void*>(fn);
+        p.gridDim = dim3(n_units);
+        p.blockDim = dim3(threads);
+        p.sharedMemBytes = 0;
+        p.kernelParams = params;
+        p.extra = nullptr;
+        hipGraphNode_t node;
+        e = hipGraphAddKernelNode(&node, graph, prev ? &prev : nullptr, prev ? 1 : 0, &p);
+        prev = node;
+    }
+    if (e == hipSuccess) e = hipGraphInstantiate(exec, graph, nullptr, nullptr, 0);
+    const hipError_t e2 = hipGraphDestroy(graph);
+    return e != hipSuccess ? e : e2;
 }
 
 }  // namespace mdl

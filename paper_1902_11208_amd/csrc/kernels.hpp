@@ -43,6 +43,13 @@ hipError_t launch_wavefront_fwd(const LayerGeom& g, int nt, int n_units, const i
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u,
                                 void* d_z, float* d_c, void* d_y, hipStream_t s);
 
+// The forward wavefront as one launch per local diagonal (diagonal s of every
+// unit in launch s), recorded as a chain of max_steps kernel nodes into an
+// instantiated graph; same results as launch_wavefront_fwd.
+hipError_t build_wavefront_fwd_graph(const LayerGeom& g, int nt, int n_units, int max_steps, const int32_t* d_units,
+                                     const int32_t* d_rects, const uint8_t* d_mask, const void* d_u, void* d_z,
+                                     float* d_c, void* d_y, hipGraphExec_t* exec);
+
 // --- backward --------------------------------------------------------------
 hipError_t launch_wavefront_bwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u,

@@ -389,10 +389,20 @@ size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, i
     return plan(desc, canvas_h, canvas_w, n_rects).total;
 }
 
-mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
-                             const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
-                             const void* d_u, const void* d_b, void* d_y, void* d_workspace, size_t workspace_bytes,
-                             void* stream) {
+namespace {
+
+// The per-diagonal graph of the last mdlstm_forward_stepwise call on this
+// thread and the arguments it was recorded for. Deliberately never freed at
+// exit: destroying a graph after the HIP runtime has shut down is unsafe.
+struct StepGraph {
+    std::vector<uintptr_t> key;
+    hipGraphExec_t exec = nullptr;
+};
+
+mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
+                           const void* d_x, const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects,
+                           const void* d_wx, const void* d_u, const void* d_b, void* d_y, void* d_workspace,
+                           size_t workspace_bytes, void* stream) {
     Common c;
     mdlstm_status st = prepare(desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_workspace,
                                workspace_bytes, &c);
@@ -404,16 +414,59 @@ mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, in
     st = stage_layout(c, n_rects, rects, d_mask, s);
     if (st != MDLSTM_OK) return st;
     const int32_t* rid = reinterpret_cast<const int32_t*>(c.ws + c.p.rid);
+    const int32_t* units = reinterpret_cast<const int32_t*>(c.ws + c.p.units);
+    const int32_t* drects = reinterpret_cast<const int32_t*>(c.ws + c.p.rects);
+    float* cs = reinterpret_cast<float*>(c.ws + c.p.c);
     HIP_OR_FAIL(mark(0, s));
     HIP_OR_FAIL(mdl::launch_projection(c.g, d_x, d_wx, d_b, c.ws + c.p.z, s));
     HIP_OR_FAIL(mark(1, s));
     HIP_OR_FAIL(mdl::launch_zero_invalid(c.g, 4 * c.g.hidden, d_mask, rid, d_y, s));
     HIP_OR_FAIL(mark(2, s));
-    HIP_OR_FAIL(mdl::launch_wavefront_fwd(c.g, c.nt, 4 * n_rects, reinterpret_cast<const int32_t*>(c.ws + c.p.units),
-                                          reinterpret_cast<const int32_t*>(c.ws + c.p.rects), d_mask, d_u,
-                                          c.ws + c.p.z, reinterpret_cast<float*>(c.ws + c.p.c), d_y, s));
+    if (!stepwise) {
+        HIP_OR_FAIL(mdl::launch_wavefront_fwd(c.g, c.nt, 4 * n_rects, units, drects, d_mask, d_u, c.ws + c.p.z, cs,
+                                              d_y, s));
+    } else if (n_rects > 0) {
+        int32_t max_steps = 0;
+        for (int32_t k = 0; k < n_rects; ++k) max_steps = std::max(max_steps, rects[k].h + rects[k].w - 1);
+        static thread_local StepGraph* cache = new StepGraph;
+        std::vector<uintptr_t> key = {(uintptr_t)desc->c_in, (uintptr_t)desc->hidden, (uintptr_t)desc->dtype,
+                                      (uintptr_t)canvas_h, (uintptr_t)canvas_w, (uintptr_t)d_mask, (uintptr_t)d_u,
+                                      (uintptr_t)d_y, (uintptr_t)d_workspace, (uintptr_t)n_rects};
+        for (int32_t k = 0; k < n_rects; ++k) {
+            key.push_back(((uintptr_t)(uint32_t)rects[k].y0 << 32) | (uint32_t)rects[k].x0);
+            key.push_back(((uintptr_t)(uint32_t)rects[k].h << 32) | (uint32_t)rects[k].w);
+        }
+        if (!cache->exec || cache->key != key) {
+            if (cache->exec) {
+                HIP_OR_FAIL(hipGraphExecDestroy(cache->exec));
+                cache->exec = nullptr;
+            }
+            HIP_OR_FAIL(mdl::build_wavefront_fwd_graph(c.g, c.nt, 4 * n_rects, max_steps, units, drects, d_mask, d_u,
+                                                       c.ws + c.p.z, cs, d_y, &cache->exec));
+            cache->key = std::move(key);
+        }
+        HIP_OR_FAIL(hipGraphLaunch(cache->exec, s));
+    }
     HIP_OR_FAIL(mark(3, s));
     return MDLSTM_OK;
+}
+
+}  // namespace
+
+mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
+                             const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
+                             const void* d_u, const void* d_b, void* d_y, void* d_workspace, size_t workspace_bytes,
+                             void* stream) {
+    return forward_impl(false, desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_y,
+                        d_workspace, workspace_bytes, stream);
+}
+
+mdlstm_status mdlstm_forward_stepwise(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
+                                      const void* d_x, const uint8_t* d_mask, int32_t n_rects,
+                                      const mdlstm_rect* rects, const void* d_wx, const void* d_u, const void* d_b,
+                                      void* d_y, void* d_workspace, size_t workspace_bytes, void* stream) {
+    return forward_impl(true, desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_y,
+                        d_workspace, workspace_bytes, stream);
 }
 
 mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,

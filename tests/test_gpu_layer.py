@@ -255,3 +255,32 @@ def test_exploding_state_regime():
         e = rel_err(gpu[nm], ref[nm])
         _say(f"  {nm}: L2 {e:.1e}")
         assert e <= 1e-3
+
+
+@pytest.mark.parametrize("case", ["H16_words", "H32_tall", "bf16_H64"])
+def test_stepwise_forward_matches_persistent(case):
+    """One launch per diagonal, replayed from a HIP graph, gives the persistent
+    kernel's outputs bit for bit (twice, to cover the graph's replay)."""
+    from paper_1902_11208_amd import api
+    from synth import configs
+    import gpu_run
+
+    if case == "H16_words":
+        wl = configs.workload(2)
+    elif case == "H32_tall":
+        wl = configs.custom_workload(61, [40, 7, 33], [50, 64, 9], 128, 8, 32)
+    else:
+        wl = configs.custom_workload(62, [16, 48, 5], [70, 20, 33], 96, 16, 64, dtype="bf16")
+    print(f"case: stepwise forward {case}", flush=True)
+    units, ch, mask = api.pack_layout(wl.heights, wl.widths, wl.canvas_w)
+    x = api.pack_data([gpu_run.to_dev(e, wl.dtype) for e in wl.examples()], units, ch, wl.canvas_w)
+    params = [gpu_run.to_dev(p, wl.dtype) for p in wl.params()]
+    a = api.MDLSTMLayer(*params, ch, wl.canvas_w, units, mask)
+    ref = a.forward(x).clone()
+    c_ref = a.workspace.clone()
+    b = api.MDLSTMLayer(*params, ch, wl.canvas_w, units, mask)
+    for _ in range(2):
+        out = b.forward_stepwise(x).clone()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref)
+        assert torch.equal(b.workspace, c_ref)  # gates and cell states too
