@@ -154,6 +154,33 @@ def test_config3_lines_forward_backward():
     _compare(gsub, ref, "f32", label="config3 sample packed alone")
 
 
+def test_config5_bf16_forward_backward():
+    # the bf16 stress batch (128 x h48, widths 300-1200, C_in 64, H 128) at full
+    # size on the GPU; the oracle (float64 on the bf16-representable inputs)
+    # takes 15-60 s per example, so Y and dX are checked on the narrowest
+    # example and one of about 600 columns, weight gradients on a second GPU
+    # run that packs just those two
+    import gpu_run
+    import oracle_run
+    from synth import configs
+
+    wl = configs.workload(5)
+    _say(f"config 5: n={wl.n} H={wl.hidden} C={wl.c_in} bf16, full batch")
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    gpu = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w, dtype="bf16")
+    pick = sorted({int(np.argmin(wl.widths)), int(np.argmin(np.abs(wl.widths - 600)))})
+    _say(f"config 5: oracle on examples {pick} (widths {wl.widths[pick].tolist()})")
+    ref = oracle_run.run_layer([xs[k] for k in pick], params, [dys[k] for k in pick],
+                               workers=oracle_run.default_workers())
+    sub = {"Y": [gpu["Y"][k] for k in pick], "dX": [gpu["dX"][k] for k in pick]}
+    _compare(sub, ref, "bf16", backward=False, label="config5 sample Y")
+    _compare({"Y": sub["dX"]}, {"Y": ref["dX"]}, "bf16", backward=False, label="config5 sample dX")
+    gsub = gpu_run.run_layer([xs[k] for k in pick], params, [dys[k] for k in pick], wl.heights[pick],
+                             wl.widths[pick], wl.canvas_w, dtype="bf16")
+    _compare(gsub, ref, "bf16", label="config5 sample packed alone")
+
+
 def test_masked_holes_and_touching_rectangles():
     # scheduling rectangles that touch (no separators) and mask holes inside
     # them: the recurrence must restart at rectangle edges and at masked cells
