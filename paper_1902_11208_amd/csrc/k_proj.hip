@@ -4,112 +4,146 @@
 // directions are folded into the same GEMM):
 //     Z[p][n] = b_all[n] + sum_k Wx_all[n][k] X[p][k],  n = d*5H + gate*H + j.
 // MFMA 16x16 tiles: M = gate columns (A = Wx rows), N = cells (B = X rows),
-// K = input channels. Each wave owns 64 cells (four N tiles) and sweeps all
-// gate-column tiles, so a lane stores four consecutive gate columns of one
-// cell per tile.
+// K = input channels. A workgroup stages a chunk of Wx rows (gate columns) in
+// LDS once and its four waves sweep the chunk for 64 cells each, B operands in
+// registers. The stores are write-bandwidth bound: every 16-cell x 64-column
+// output block passes through a small per-wave LDS tile so that one store
+// instruction writes four cells x 64 contiguous columns instead of sixteen
+// cells x 4 columns.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace mdl {
 
-// Reduction-slot layouts. fp32: slot g holds k = g*KS + ks (one value per
-// K step). bf16: K step ks covers k = 32*ks + 8*g + e, e = 0..7.
-template <int KS>
-__device__ __forceinline__ void load_slot_f32(const float* __restrict__ row, int g, int C, bool ok, float (&v)[KS]) {
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-        int k = g * KS + ks;
-        v[ks] = (ok && k < C) ? row[k] : 0.0f;
+namespace {
+
+constexpr int PCELLS = 64;             // cells per wave
+constexpr int PW_LDS = 48 * 1024;      // LDS bytes for the Wx chunk
+
+template <typename T>
+struct PK;
+template <>
+struct PK<float> {  // 16x16x4 f32: K step ks, slot g holds k = g*KS + ks
+    using Op = float;
+    static constexpr int PERK = 4;  // k values per K step
+    static constexpr int PAD = 4;   // LDS row padding (elements)
+    static __device__ __forceinline__ int koff(int g, int ks, int KS) { return g * KS + ks; }
+    static __device__ __forceinline__ Op lds(const float* p) { return *p; }
+    static __device__ __forceinline__ Op gload(const float* row, int k, int C) { return k < C ? row[k] : 0.0f; }
+    static __device__ __forceinline__ floatx4 mma(Op a, Op b, floatx4 c) { return mfma_f32(a, b, c); }
+    static __device__ __forceinline__ void st4(float* p, floatx4 v) { St<float>::st4(p, v); }
+};
+template <>
+struct PK<bf16_t> {  // 16x16x32 bf16: K step ks, slot g holds k = 32 ks + 8 g + e
+    using Op = bf16x8;
+    static constexpr int PERK = 32;
+    static constexpr int PAD = 8;
+    static __device__ __forceinline__ int koff(int g, int ks, int) { return 32 * ks + 8 * g; }
+    static __device__ __forceinline__ Op lds(const bf16_t* p) { return as_bf16x8(*reinterpret_cast<const uint4*>(p)); }
+    static __device__ __forceinline__ Op gload(const bf16_t* row, int k, int C) {
+        return as_bf16x8(k < C ? *reinterpret_cast<const uint4*>(row + k) : make_uint4(0, 0, 0, 0));
     }
-}
+    static __device__ __forceinline__ floatx4 mma(Op a, Op b, floatx4 c) { return mfma_bf16(a, b, c); }
+    static __device__ __forceinline__ void st4(bf16_t* p, floatx4 v) { St<bf16_t>::st4(p, v); }
+};
 
-template <int KS>
-__device__ __forceinline__ void load_slot_bf16(const bf16_t* __restrict__ row, int g, int C, bool ok,
-                                               bf16x8 (&v)[KS]) {
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-        int k = 32 * ks + 8 * g;
-        uint4 u = make_uint4(0, 0, 0, 0);
-        if (ok && k < C) u = *reinterpret_cast<const uint4*>(row + k);
-        v[ks] = as_bf16x8(u);
-    }
-}
+}  // namespace
 
-constexpr int PROJ_CELLS_PER_WAVE = 64;
-
-template <int KS>
+template <typename T, int KS>
 __global__ void __launch_bounds__(256)
-k_projection_f32(int64_t n_cells, int C, int N, const float* __restrict__ X, const float* __restrict__ Wx,
-                 const float* __restrict__ bias, float* __restrict__ Z) {
+k_projection(int64_t n_cells, int C, int N, int nch, const T* __restrict__ X, const T* __restrict__ Wx,
+             const T* __restrict__ bias, T* __restrict__ Z) {
+    using K = PK<T>;
+    using Op = typename K::Op;
+    constexpr int RW = K::PERK * KS;  // staged k values per row
+    constexpr int P = RW + K::PAD;    // LDS row pitch (elements); the pad spreads rows over banks
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    T* sW = reinterpret_cast<T*>(smem);
+    __shared__ __attribute__((aligned(16))) float sO[4][16][64 + 4];
+
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int g = lane >> 4, n16 = lane & 15;
-    const int64_t cell0 = ((int64_t)blockIdx.x * 4 + wave) * PROJ_CELLS_PER_WAVE;
+    const int n0 = blockIdx.y * nch, nc = min(nch, N - n0);
+    for (int i = threadIdx.x; i < nc * RW; i += 256) {
+        const int r = i / RW, k = i - r * RW;
+        sW[r * P + k] = k < C ? Wx[(int64_t)(n0 + r) * C + k] : T(0);
+    }
+    __syncthreads();
+    const int64_t cell0 = ((int64_t)blockIdx.x * 4 + wave) * PCELLS;
     if (cell0 >= n_cells) return;
-    float b[4][KS];
+    Op b[4][KS];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-        int64_t cell = cell0 + 16 * t + n16;
-        load_slot_f32<KS>(X + cell * C, g, C, cell < n_cells, b[t]);
+        const int64_t cell = cell0 + 16 * t + n16;
+        const T* row = X + min(cell, n_cells - 1) * C;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) b[t][ks] = K::gload(row, K::koff(g, ks, KS), C);
     }
-    for (int mt = 0; mt < N / 16; ++mt) {
-        float a[KS];
-        load_slot_f32<KS>(Wx + (int64_t)(mt * 16 + n16) * C, g, C, true, a);
-        floatx4 acc[4];
+    float(*so)[64 + 4] = sO[wave];
+    const int ntiles = nc / 16;
+    for (int mg = 0; mg * 4 < ntiles; ++mg) {
+        const int mc = min(4, ntiles - 4 * mg);  // column tiles in this group
+        floatx4 acc[4][4];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int m = 0; m < 4; ++m) {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
+            for (int t = 0; t < 4; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+            if (m < mc) {
+                Op a[KS];
+                const T* ar = sW + ((mg * 4 + m) * 16 + n16) * P;
 #pragma unroll
-            for (int t = 0; t < 4; ++t) acc[t] = mfma_f32(a[ks], b[t][ks], acc[t]);
-        const int col = mt * 16 + 4 * g;
-        floatx4 bb = St<float>::ld4(bias + col);
+                for (int ks = 0; ks < KS; ++ks) a[ks] = K::lds(ar + K::koff(g, ks, KS));
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) acc[m][t] = K::mma(a[ks], b[t][ks], acc[m][t]);
+            }
+        }
+        // lane (r, c) of the store pass writes cell 4 r' + lane/16 of the tile,
+        // columns 4 (lane % 16) .. + 3 of the group
+        const int c4 = 4 * (lane & 15);
+        const int colb = n0 + mg * 64;
+        const bool colok = c4 < 16 * mc;
+        const floatx4 bb = colok ? St<T>::ld4(bias + colb + c4) : floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            int64_t cell = cell0 + 16 * t + n16;
-            if (cell < n_cells) St<float>::st4(Z + cell * N + col, acc[t] + bb);
+#pragma unroll
+            for (int m = 0; m < 4; ++m) *reinterpret_cast<floatx4*>(&so[n16][m * 16 + 4 * g]) = acc[m][t];
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int cl = 4 * r + (lane >> 4);
+                const floatx4 v = *reinterpret_cast<const floatx4*>(&so[cl][c4]) + bb;
+                const int64_t cell = cell0 + 16 * t + cl;
+                if (colok && cell < n_cells) K::st4(Z + cell * N + colb + c4, v);
+            }
+            __builtin_amdgcn_wave_barrier();
         }
     }
 }
 
-template <int KS>
-__global__ void __launch_bounds__(256)
-k_projection_bf16(int64_t n_cells, int C, int N, const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wx,
-                  const bf16_t* __restrict__ bias, bf16_t* __restrict__ Z) {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int g = lane >> 4, n16 = lane & 15;
-    const int64_t cell0 = ((int64_t)blockIdx.x * 4 + wave) * PROJ_CELLS_PER_WAVE;
-    if (cell0 >= n_cells) return;
-    bf16x8 b[4][KS];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        int64_t cell = cell0 + 16 * t + n16;
-        load_slot_bf16<KS>(X + cell * C, g, C, cell < n_cells, b[t]);
-    }
-    for (int mt = 0; mt < N / 16; ++mt) {
-        bf16x8 a[KS];
-        load_slot_bf16<KS>(Wx + (int64_t)(mt * 16 + n16) * C, g, C, true, a);
-        floatx4 acc[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-            for (int t = 0; t < 4; ++t) acc[t] = mfma_bf16(a[ks], b[t][ks], acc[t]);
-        const int col = mt * 16 + 4 * g;
-        floatx4 bb = St<bf16_t>::ld4(bias + col);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            int64_t cell = cell0 + 16 * t + n16;
-            if (cell < n_cells) St<bf16_t>::st4(Z + cell * N + col, acc[t] + bb);
-        }
-    }
+template <typename T, int KS>
+static hipError_t launch_proj(const LayerGeom& g, const T* X, const T* W, const T* B, T* Z, hipStream_t s) {
+    constexpr int RW = PK<T>::PERK * KS, P = RW + PK<T>::PAD;
+    const int N = 20 * g.hidden;
+    // columns per workgroup: as many as the LDS budget holds (a multiple of 16,
+    // of 64 when possible), split evenly over the chunks
+    const int cap = PW_LDS / (P * (int)sizeof(T)) / 16 * 16;
+    const int unit = cap >= 64 ? 64 : 16;
+    const int nchunks = (N + cap / unit * unit - 1) / (cap / unit * unit);
+    int nch = ((N + nchunks - 1) / nchunks + unit - 1) / unit * unit;
+    nch = std::min(std::min(nch, cap / unit * unit), N);
+    const int64_t waves = (g.n_cells + PCELLS - 1) / PCELLS;
+    const dim3 grid((unsigned)((waves + 3) / 4), (unsigned)((N + nch - 1) / nch)), block(256);
+    hipLaunchKernelGGL((k_projection<T, KS>), grid, block, (size_t)nch * P * sizeof(T), s, g.n_cells, g.c_in, N, nch,
+                       X, W, B, Z);
+    return hipGetLastError();
 }
 
 hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_wx, const void* d_b, void* d_z,
                              hipStream_t s) {
-    const int N = 20 * g.hidden;
-    const int64_t waves = (g.n_cells + PROJ_CELLS_PER_WAVE - 1) / PROJ_CELLS_PER_WAVE;
-    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
     if (g.n_cells == 0) return hipSuccess;
     if (g.dtype == 0) {
         const int ks = (g.c_in + 3) / 4;
@@ -117,27 +151,25 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
         auto W = static_cast<const float*>(d_wx);
         auto B = static_cast<const float*>(d_b);
         auto Z = static_cast<float*>(d_z);
-        if (ks <= 1) hipLaunchKernelGGL(k_projection_f32<1>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else if (ks <= 2) hipLaunchKernelGGL(k_projection_f32<2>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else if (ks <= 4) hipLaunchKernelGGL(k_projection_f32<4>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else if (ks <= 8) hipLaunchKernelGGL(k_projection_f32<8>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else if (ks <= 16) hipLaunchKernelGGL(k_projection_f32<16>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else if (ks <= 32) hipLaunchKernelGGL(k_projection_f32<32>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else if (ks <= 64) hipLaunchKernelGGL(k_projection_f32<64>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else return hipErrorInvalidValue;
-    } else {
-        const int ks = (g.c_in + 31) / 32;
-        auto X = static_cast<const bf16_t*>(d_x);
-        auto W = static_cast<const bf16_t*>(d_wx);
-        auto B = static_cast<const bf16_t*>(d_b);
-        auto Z = static_cast<bf16_t*>(d_z);
-        if (ks <= 1) hipLaunchKernelGGL(k_projection_bf16<1>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else if (ks <= 2) hipLaunchKernelGGL(k_projection_bf16<2>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else if (ks <= 4) hipLaunchKernelGGL(k_projection_bf16<4>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else if (ks <= 8) hipLaunchKernelGGL(k_projection_bf16<8>, grid, block, 0, s, g.n_cells, g.c_in, N, X, W, B, Z);
-        else return hipErrorInvalidValue;
+        if (ks <= 1) return launch_proj<float, 1>(g, X, W, B, Z, s);
+        if (ks <= 2) return launch_proj<float, 2>(g, X, W, B, Z, s);
+        if (ks <= 4) return launch_proj<float, 4>(g, X, W, B, Z, s);
+        if (ks <= 8) return launch_proj<float, 8>(g, X, W, B, Z, s);
+        if (ks <= 16) return launch_proj<float, 16>(g, X, W, B, Z, s);
+        if (ks <= 32) return launch_proj<float, 32>(g, X, W, B, Z, s);
+        if (ks <= 64) return launch_proj<float, 64>(g, X, W, B, Z, s);
+        return hipErrorInvalidValue;
     }
-    return hipGetLastError();
+    const int ks = (g.c_in + 31) / 32;
+    auto X = static_cast<const bf16_t*>(d_x);
+    auto W = static_cast<const bf16_t*>(d_wx);
+    auto B = static_cast<const bf16_t*>(d_b);
+    auto Z = static_cast<bf16_t*>(d_z);
+    if (ks <= 1) return launch_proj<bf16_t, 1>(g, X, W, B, Z, s);
+    if (ks <= 2) return launch_proj<bf16_t, 2>(g, X, W, B, Z, s);
+    if (ks <= 4) return launch_proj<bf16_t, 4>(g, X, W, B, Z, s);
+    if (ks <= 8) return launch_proj<bf16_t, 8>(g, X, W, B, Z, s);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace mdl

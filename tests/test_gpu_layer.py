@@ -303,9 +303,11 @@ def test_stepwise_forward_matches_persistent(case):
     x = api.pack_data([gpu_run.to_dev(e, wl.dtype) for e in wl.examples()], units, ch, wl.canvas_w)
     params = [gpu_run.to_dev(p, wl.dtype) for p in wl.params()]
     a = api.MDLSTMLayer(*params, ch, wl.canvas_w, units, mask)
+    b = api.MDLSTMLayer(*params, ch, wl.canvas_w, units, mask)
+    a.workspace.zero_()  # the forward pass leaves the gradient scratch of the workspace untouched
+    b.workspace.zero_()
     ref = a.forward(x).clone()
     c_ref = a.workspace.clone()
-    b = api.MDLSTMLayer(*params, ch, wl.canvas_w, units, mask)
     for _ in range(2):
         out = b.forward_stepwise(x).clone()
         torch.cuda.synchronize()
