@@ -128,3 +128,20 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
+
+// Canvas index of local cell (y, s - y) of diagonal s of a unit in scan
+// direction d (as canvas_index), written c0 + sx*s + y*ky: with the
+// direction's mirroring folded into per-unit constants, a step's base costs
+// one add and a cell one multiply-add.
+struct DiagMap {
+    int64_t c0;
+    int sx, ky;
+    __device__ __forceinline__ DiagMap(const RectD& R, int d, int canvas_w) {
+        const int cy0 = R.y0 + ((d & 2) ? R.h - 1 : 0), cx0 = R.x0 + ((d & 1) ? R.w - 1 : 0);
+        sx = (d & 1) ? -1 : 1;
+        ky = ((d & 2) ? -canvas_w : canvas_w) - sx;
+        c0 = (int64_t)cy0 * canvas_w + cx0;
+    }
+    __device__ __forceinline__ int64_t base(int s) const { return c0 + (int64_t)(sx * s); }
+    __device__ __forceinline__ int64_t at(int64_t b, int y) const { return b + (int64_t)y * ky; }
+};

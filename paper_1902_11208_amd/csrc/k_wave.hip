@@ -21,6 +21,7 @@
 // (phase A), then the waves contract da with U^T on MFMA, split by output
 // tile and reduction range, partials summed through LDS in a fixed order
 // (phase B). The U operands stay in VGPRs for the whole unit.
+#include <algorithm>
 #include <climits>
 #include <type_traits>
 
@@ -167,6 +168,8 @@ struct WaveArgs {
     const void* dy;        // [n_cells][4H] upstream gradient (bwd)
     int canvas_w;
     int s0, s1;            // forward: local diagonals [s0, s1) of every unit
+    unsigned* queue;       // next unit to take (zeroed before the launch), or NULL: unit = block
+    int n_units;
 };
 
 template <int NT, int WQ, typename T>
@@ -192,8 +195,7 @@ struct BPre {
 // Forward.
 // ---------------------------------------------------------------------------
 template <int H, int NT, typename T>
-__global__ void __launch_bounds__((64 * Geo<H, T>::NW))
-k_wave_fwd(WaveArgs a) {
+__device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit) {
     using Gm = Geo<H, T>;
     using O = Ops<T>;
     using Op = typename O::Op;
@@ -222,7 +224,6 @@ k_wave_fwd(WaveArgs a) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int q = lane >> 4, n16 = lane & 15;
     const int gt = w / SPL, sp = w % SPL;  // candidate tile and reduction slice of this wave
-    const int unit = a.units[blockIdx.x];
     const int d = unit & 3;
     const RectD R = reinterpret_cast<const RectD*>(a.rects)[unit >> 2];
     const T* __restrict__ U = static_cast<const T*>(a.u) + (int64_t)d * G * 2 * H;
@@ -285,15 +286,28 @@ k_wave_fwd(WaveArgs a) {
     // same on every path, which lets the compiler wait for exactly these loads
     // one step later; `live` says whether they are used.
     u32x4 zr[NITZ > 0 ? NITZ : 1];
+    const DiagMap M(R, d, a.canvas_w);
+    // The lane's chunk of each staged-input pass: cell row and chunk of the
+    // row (slot S of zst is chunk S % PZ of the row of cell S / PZ; the
+    // padding chunk and the slots past the last cell repeat a valid one).
+    int zcell[NITZ > 0 ? NITZ : 1], zoff[NITZ > 0 ? NITZ : 1];
+#pragma unroll
+    for (int it = 0; it < NITZ; ++it) {
+        const int S = it * NTH + (int)threadIdx.x;
+        zcell[it] = min(S / PZ, NT * 16 - 1);
+        zoff[it] = (d * G) * (int)sizeof(T) + 16 * min(S - (S / PZ) * PZ, Q::QZ - 1);
+    }
+    const char* Zb = reinterpret_cast<const char*>(Z);
     auto fetch = [&](int s, FPre<NT, WQ, T>& b) {
         const int sc = min(s, steps - 1);
         const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
+        const int64_t base = M.base(sc);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             const int yy = 16 * nt + n16;
             b.live[nt] = s < steps && yy >= ylo && yy <= yhi;
             const int yc = min(max(yy, ylo), yhi);
-            const int64_t p = canvas_index(R, d, yc, sc - yc, a.canvas_w);
+            const int64_t p = M.at(base, yc);
             b.p[nt] = p;
             b.m[nt] = a.mask[p];
             if constexpr (!STAGE) {
@@ -307,15 +321,10 @@ k_wave_fwd(WaveArgs a) {
             }
         }
         if constexpr (STAGE) {
-            // slot S of zst is chunk S % PZ of the row of cell S / PZ (the
-            // padding chunk and the slots past the last cell repeat a valid one)
 #pragma unroll
             for (int it = 0; it < NITZ; ++it) {
-                const int S = it * NTH + (int)threadIdx.x;
-                const int cell = min(S / PZ, NT * 16 - 1), r = min(S - (S / PZ) * PZ, Q::QZ - 1);
-                const int yc = min(max(cell, ylo), yhi);
-                const int64_t p = canvas_index(R, d, yc, sc - yc, a.canvas_w);
-                zr[it] = *reinterpret_cast<const u32x4*>(Z + p * (4 * G) + d * G + r * (16 / (int)sizeof(T)));
+                const int yc = min(max(zcell[it], ylo), yhi);
+                zr[it] = *reinterpret_cast<const u32x4*>(Zb + M.at(base, yc) * (4 * G * (int)sizeof(T)) + zoff[it]);
             }
         }
     };
@@ -331,22 +340,38 @@ k_wave_fwd(WaveArgs a) {
     // writes the same bytes twice), so the number of stores is fixed. All LDS
     // reads are issued before the first store: one LDS round trip.
     constexpr int NITF = STAGE ? (NT * 16 * Q::QF + NTH - 1) / NTH : 0;
+    // The lane's chunk of each write-back pass: cell row, chunk index in the
+    // staged row, and where the chunk goes (address at canvas index 0 and
+    // bytes per canvas cell of its tensor: gates, outputs or cell states).
+    int fcell[NITF > 0 ? NITF : 1], fcr[NITF > 0 ? NITF : 1];
+    char* fbase[NITF > 0 ? NITF : 1];
+#pragma unroll
+    for (int it = 0; it < NITF; ++it) {
+        const int i = min(it * NTH + (int)threadIdx.x, NT * 16 * Q::QF - 1);
+        const int r = i % Q::QF;
+        fcell[it] = i / Q::QF;
+        if (r < Q::QZ) {
+            fbase[it] = reinterpret_cast<char*>(Z + d * G) + 16 * r;
+            fcr[it] = (4 * G * (int)sizeof(T)) << 8 | r;
+        } else if (r < Q::QZ + Q::QY) {
+            fbase[it] = reinterpret_cast<char*>(Y + d * H) + 16 * (r - Q::QZ);
+            fcr[it] = (4 * H * (int)sizeof(T)) << 8 | r;
+        } else {
+            fbase[it] = reinterpret_cast<char*>(Cs + d * H) + 16 * (r - Q::QZ - Q::QY);
+            fcr[it] = (16 * H) << 8 | r;
+        }
+    }
     auto flush = [&](int sp) {
         if constexpr (STAGE) {
-            constexpr int NCH = NT * 16 * Q::QF;
             const int ylo = max(0, sp - R.w + 1), yhi = min(R.h - 1, sp);
+            const int64_t base = M.base(sp);
             u32x4 v[NITF];
             char* dst[NITF];
 #pragma unroll
             for (int it = 0; it < NITF; ++it) {
-                const int i = min(it * NTH + (int)threadIdx.x, NCH - 1);
-                const int cell = min(max(i / Q::QF, ylo), yhi), r = i - (i / Q::QF) * Q::QF;
-                v[it] = ostage[cell][r];
-                const int64_t p = canvas_index(R, d, cell, sp - cell, a.canvas_w);
-                char* zb = reinterpret_cast<char*>(Z + p * (4 * G) + d * G) + 16 * r;
-                char* yb = reinterpret_cast<char*>(Y + p * (4 * H) + d * H) + 16 * (r - Q::QZ);
-                char* cb = reinterpret_cast<char*>(Cs + p * (4 * H) + d * H) + 16 * (r - Q::QZ - Q::QY);
-                dst[it] = r < Q::QZ ? zb : (r < Q::QZ + Q::QY ? yb : cb);
+                const int cell = min(max(fcell[it], ylo), yhi);
+                v[it] = ostage[cell][fcr[it] & 255];
+                dst[it] = fbase[it] + M.at(base, cell) * (fcr[it] >> 8);
             }
 #pragma unroll
             for (int it = 0; it < NITF; ++it) *reinterpret_cast<u32x4*>(dst[it]) = v[it];
@@ -492,8 +517,7 @@ k_wave_fwd(WaveArgs a) {
 //   da = (dc g i(1-i), dc c_L f_L(1-f_L), dc c_T f_T(1-f_T), dh tanh(c) o(1-o), dc i (1-g^2))
 // ---------------------------------------------------------------------------
 template <int H, int NT, typename T>
-__global__ void __launch_bounds__((64 * Geo<H, T>::NW))
-k_wave_bwd(WaveArgs a) {
+__device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit) {
     using Gm = Geo<H, T>;
     using O = Ops<T>;
     using Op = typename O::Op;
@@ -519,7 +543,6 @@ k_wave_bwd(WaveArgs a) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int q = lane >> 4, n16 = lane & 15;
     const int mt0 = (w / SPLB) * TPW, sb = w % SPLB;  // output tiles and reduction slice of this wave
-    const int unit = a.units[blockIdx.x];
     const int d = unit & 3;
     const RectD R = reinterpret_cast<const RectD*>(a.rects)[unit >> 2];
     const T* __restrict__ U = static_cast<const T*>(a.u) + (int64_t)d * G * 2 * H;
@@ -552,15 +575,17 @@ k_wave_bwd(WaveArgs a) {
     // issued for every lane from valid cells (see the forward pass);
     // predecessors outside the rectangle read the cell itself and are zeroed
     // on use.
+    const DiagMap M(R, d, a.canvas_w);
     auto fetch = [&](int s, BPre<NT, WQ, T>& b) {
         const int sc = max(s, 0);
         const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
+        const int64_t base = M.base(sc);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             const int yy = 16 * nt + n16;
             b.live[nt] = s >= 0 && yy >= ylo && yy <= yhi;
             const int yc = min(max(yy, ylo), yhi), xc = sc - yc;
-            const int64_t p = canvas_index(R, d, yc, xc, a.canvas_w);
+            const int64_t p = M.at(base, yc);
             b.p[nt] = p;
             b.m[nt] = a.mask[p];
             b.hasl[nt] = xc > 0;
@@ -588,20 +613,35 @@ k_wave_bwd(WaveArgs a) {
     // gradients and the H cell states of the cell (padding chunk and slots
     // past the last cell repeat a valid chunk).
     u32x4 zr[NITZ > 0 ? NITZ : 1];
+    // The lane's chunk of each staged-input pass: cell row, and the chunk's
+    // address at canvas index 0 with the bytes per canvas cell of its tensor.
+    int zcell[NITZ > 0 ? NITZ : 1], zrb[NITZ > 0 ? NITZ : 1];
+    const char* zsrc[NITZ > 0 ? NITZ : 1];
+#pragma unroll
+    for (int it = 0; it < NITZ; ++it) {
+        const int S = it * NTH + (int)threadIdx.x;
+        const int r = min(S % PB, Q::QF - 1);
+        zcell[it] = min(S / PB, NT * 16 - 1);
+        if (r < Q::QZ) {
+            zsrc[it] = reinterpret_cast<const char*>(Z + d * G) + 16 * r;
+            zrb[it] = 4 * G * (int)sizeof(T);
+        } else if (r < CC) {
+            zsrc[it] = reinterpret_cast<const char*>(DY + d * H) + 16 * (r - Q::QZ);
+            zrb[it] = 4 * H * (int)sizeof(T);
+        } else {
+            zsrc[it] = reinterpret_cast<const char*>(Cs + d * H) + 16 * (r - CC);
+            zrb[it] = 16 * H;
+        }
+    }
     auto fetch_rows = [&](int s) {
         if constexpr (STAGE) {
             const int sc = max(s, 0);
             const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
+            const int64_t base = M.base(sc);
 #pragma unroll
             for (int it = 0; it < NITZ; ++it) {
-                const int S = it * NTH + (int)threadIdx.x;
-                const int cell = min(S / PB, NT * 16 - 1), r = min(S - (S / PB) * PB, Q::QF - 1);
-                const int yc = min(max(cell, ylo), yhi);
-                const int64_t p = canvas_index(R, d, yc, sc - yc, a.canvas_w);
-                const char* zs = reinterpret_cast<const char*>(Z + p * (4 * G) + d * G) + 16 * r;
-                const char* ys = reinterpret_cast<const char*>(DY + p * (4 * H) + d * H) + 16 * (r - Q::QZ);
-                const char* cs = reinterpret_cast<const char*>(Cs + p * (4 * H) + d * H) + 16 * (r - CC);
-                zr[it] = *reinterpret_cast<const u32x4*>(r < Q::QZ ? zs : (r < CC ? ys : cs));
+                const int yc = min(max(zcell[it], ylo), yhi);
+                zr[it] = *reinterpret_cast<const u32x4*>(zsrc[it] + M.at(base, yc) * zrb[it]);
             }
         }
     };
@@ -610,6 +650,15 @@ k_wave_bwd(WaveArgs a) {
         for (int it = 0; it < NITZ; ++it) ist[s & 1][it * NTH + threadIdx.x] = zr[it];
     };
 
+    // The lane's chunk of each gate-gradient write-back pass (cell row, chunk).
+    int dcell[NITF], dchunk[NITF];
+#pragma unroll
+    for (int it = 0; it < NITF; ++it) {
+        const int i = min(it * NTH + (int)threadIdx.x, NT * 16 * Q::QZ - 1);
+        dcell[it] = i / Q::QZ;
+        dchunk[it] = i - dcell[it] * Q::QZ;
+    }
+    char* const Zd = reinterpret_cast<char*>(Z + d * G);
     auto compute = [&](int s, const BPre<NT, WQ, T>& b) {
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
         // Phase A: gate-gradient update of this lane's (cell, hidden unit) pairs.
@@ -677,18 +726,17 @@ k_wave_bwd(WaveArgs a) {
         // every pass (rows outside the diagonal repeat its nearest cell; cells
         // with mask 0 get zero gradients), so the number of stores is fixed.
         {
-            constexpr int NCH = NT * 16 * Q::QZ;
+            const int64_t base = M.base(s);
             u32x4 v[NITF];
-            u32x4* dst[NITF];
+            char* dst[NITF];
 #pragma unroll
             for (int it = 0; it < NITF; ++it) {
-                const int i = min(it * NTH + (int)threadIdx.x, NCH - 1);
-                const int cell = min(max(i / Q::QZ, ylo), yhi), r = i - (i / Q::QZ) * Q::QZ;
-                v[it] = reinterpret_cast<const u32x4*>(&dabuf[cell][0])[r];
-                dst[it] = reinterpret_cast<u32x4*>(Z + canvas_index(R, d, cell, s - cell, a.canvas_w) * (4 * G) + d * G) + r;
+                const int cell = min(max(dcell[it], ylo), yhi);
+                v[it] = reinterpret_cast<const u32x4*>(&dabuf[cell][0])[dchunk[it]];
+                dst[it] = Zd + M.at(base, cell) * (4 * G * (int)sizeof(T)) + 16 * dchunk[it];
             }
 #pragma unroll
-            for (int it = 0; it < NITF; ++it) *dst[it] = v[it];
+            for (int it = 0; it < NITF; ++it) *reinterpret_cast<u32x4*>(dst[it]) = v[it];
         }
         // Phase B: U^T da for the left (rows k < H) and top (k >= H) predecessors.
 #pragma unroll
@@ -756,6 +804,43 @@ k_wave_bwd(WaveArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Kernels. With a queue, a fixed number of workgroups per CU take units in
+// launch order (longest first) from a counter until none is left, so a long
+// unit shares its CU with fewer others than when every unit has its own
+// workgroup from the start; without one, workgroup b runs unit b.
+// ---------------------------------------------------------------------------
+template <int H, int NT, typename T, bool FWD, bool QUEUE>
+__device__ __forceinline__ void run_units(const WaveArgs& a) {
+    if constexpr (!QUEUE) {
+        if (FWD) wave_fwd_unit<H, NT, T>(a, a.units[blockIdx.x]);
+        else wave_bwd_unit<H, NT, T>(a, a.units[blockIdx.x]);
+        return;
+    }
+    __shared__ int slot;
+    for (;;) {
+        lds_barrier();
+        if (threadIdx.x == 0) slot = (int)atomicAdd(a.queue, 1u);
+        lds_barrier();
+        const int k = slot;
+        if (k >= a.n_units) break;
+        if (FWD) wave_fwd_unit<H, NT, T>(a, a.units[k]);
+        else wave_bwd_unit<H, NT, T>(a, a.units[k]);
+    }
+}
+
+template <int H, int NT, typename T, bool QUEUE>
+__global__ void __launch_bounds__((64 * Geo<H, T>::NW))
+k_wave_fwd(WaveArgs a) {
+    run_units<H, NT, T, true, QUEUE>(a);
+}
+
+template <int H, int NT, typename T, bool QUEUE>
+__global__ void __launch_bounds__((64 * Geo<H, T>::NW))
+k_wave_bwd(WaveArgs a) {
+    run_units<H, NT, T, false, QUEUE>(a);
+}
+
+// ---------------------------------------------------------------------------
 // Dispatch over (hidden size, N tiles, storage type).
 // ---------------------------------------------------------------------------
 // LDS of the backward kernel; shapes beyond the 160 KB of a CU are not built.
@@ -765,10 +850,15 @@ constexpr bool bwd_fits() {
 }
 
 template <int H, int NT, typename T>
-static void launch_unit(bool fwd, int n_units, const WaveArgs& a, hipStream_t s) {
-    const dim3 grid(n_units), block(64 * Geo<H, T>::NW);
-    if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T>), grid, block, 0, s, a);
-    else if constexpr (bwd_fits<H, NT, T>()) hipLaunchKernelGGL((k_wave_bwd<H, NT, T>), grid, block, 0, s, a);
+static void launch_unit(bool fwd, int n_groups, const WaveArgs& a, hipStream_t s) {
+    const dim3 grid(n_groups), block(64 * Geo<H, T>::NW);
+    if (a.queue) {
+        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, true>), grid, block, 0, s, a);
+        else if constexpr (bwd_fits<H, NT, T>()) hipLaunchKernelGGL((k_wave_bwd<H, NT, T, true>), grid, block, 0, s, a);
+    } else {
+        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, false>), grid, block, 0, s, a);
+        else if constexpr (bwd_fits<H, NT, T>()) hipLaunchKernelGGL((k_wave_bwd<H, NT, T, false>), grid, block, 0, s, a);
+    }
 }
 
 template <int H, typename T>
@@ -784,8 +874,28 @@ static hipError_t launch_nt(bool fwd, int nt, int n_units, const WaveArgs& a, hi
     return hipGetLastError();
 }
 
-static hipError_t launch_wave(bool fwd, const LayerGeom& g, int nt, int n_units, const WaveArgs& a, hipStream_t s) {
+// Workgroups per CU when units are taken from a queue.
+#ifndef WAVE_GROUPS_PER_CU
+#define WAVE_GROUPS_PER_CU 2
+#endif
+
+static hipError_t launch_wave(bool fwd, const LayerGeom& g, int nt, int n_units, WaveArgs a, hipStream_t s) {
     if (n_units == 0) return hipSuccess;
+    a.n_units = n_units;
+    if (a.queue) {
+        int dev = 0, cus = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        const int groups = WAVE_GROUPS_PER_CU * std::max(cus, 1);
+        if (n_units > groups) {  // else one workgroup per unit
+            e = launch_zero_f32(reinterpret_cast<float*>(a.queue), 1, s);
+            if (e != hipSuccess) return e;
+            n_units = groups;
+        } else {
+            a.queue = nullptr;
+        }
+    }
     if (g.dtype == 0) {
         switch (g.hidden) {
             case 4: return launch_nt<4, float>(fwd, nt, n_units, a, s);
@@ -806,15 +916,16 @@ static hipError_t launch_wave(bool fwd, const LayerGeom& g, int nt, int n_units,
 
 hipError_t launch_wavefront_fwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u, void* d_z,
-                                float* d_c, void* d_y, hipStream_t s) {
-    WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w, 0, INT_MAX};
+                                float* d_c, void* d_y, unsigned* d_queue, hipStream_t s) {
+    WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w, 0, INT_MAX, d_queue, n_units};
     return launch_wave(true, g, nt, n_units, a, s);
 }
 
 hipError_t launch_wavefront_bwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u, const void* d_dy,
-                                void* d_z, const float* d_c, hipStream_t s) {
-    WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, const_cast<float*>(d_c), nullptr, d_dy, g.canvas_w, 0, INT_MAX};
+                                void* d_z, const float* d_c, unsigned* d_queue, hipStream_t s) {
+    WaveArgs a{d_units,  d_rects, d_mask, d_u,     d_z,     const_cast<float*>(d_c), nullptr, d_dy, g.canvas_w, 0,
+               INT_MAX, d_queue, n_units};
     return launch_wave(false, g, nt, n_units, a, s);
 }
 
@@ -823,10 +934,10 @@ template <int H, typename T>
 static bool fwd_kernel(int nt, const void** fn, int* threads) {
     *threads = 64 * Geo<H, T>::NW;
     switch (nt) {
-        case 1: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 1, T>); return true;
-        case 2: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 2, T>); return true;
-        case 3: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 3, T>); return true;
-        case 4: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 4, T>); return true;
+        case 1: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 1, T, false>); return true;
+        case 2: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 2, T, false>); return true;
+        case 3: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 3, T, false>); return true;
+        case 4: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 4, T, false>); return true;
         default: return false;
     }
 }
@@ -860,7 +971,7 @@ hipError_t build_wavefront_fwd_graph(const LayerGeom& g, int nt, int n_units, in
     if (e != hipSuccess) return e;
     hipGraphNode_t prev = nullptr;
     for (int st = 0; st < max_steps && e == hipSuccess; ++st) {
-        WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w, st, st + 1};
+        WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w, st, st + 1, nullptr, n_units};
         void* params[] = {&a};
         hipKernelNodeParams p{};
         p.func = const_cast<void*>(fn);

@@ -38,10 +38,12 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
 // Zero the rows of a [n_cells][width] tensor (storage dtype) whose cell is invalid.
 hipError_t launch_zero_invalid(const LayerGeom& g, int width, const uint8_t* d_mask,
                                const int32_t* d_rid, void* d_t, hipStream_t s);
-// Forward anti-diagonal wavefront, one workgroup per unit.
+// Forward anti-diagonal wavefront over n_units units (rectangle, direction)
+// in the order of d_units. d_queue: a device counter the launch zeroes and
+// its workgroups take units from (a fixed number per CU).
 hipError_t launch_wavefront_fwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u,
-                                void* d_z, float* d_c, void* d_y, hipStream_t s);
+                                void* d_z, float* d_c, void* d_y, unsigned* d_queue, hipStream_t s);
 
 // The forward wavefront as one launch per local diagonal (diagonal s of every
 // unit in launch s), recorded as a chain of max_steps kernel nodes into an
@@ -53,7 +55,7 @@ hipError_t build_wavefront_fwd_graph(const LayerGeom& g, int nt, int n_units, in
 // --- backward --------------------------------------------------------------
 hipError_t launch_wavefront_bwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u,
-                                const void* d_dy, void* d_z, const float* d_c, hipStream_t s);
+                                const void* d_dy, void* d_z, const float* d_c, unsigned* d_queue, hipStream_t s);
 // dX = valid * (dZ Wx_all).
 hipError_t launch_dx(const LayerGeom& g, const void* d_dz, const void* d_wx, const uint8_t* d_mask,
                      const int32_t* d_rid, void* d_dx, hipStream_t s);

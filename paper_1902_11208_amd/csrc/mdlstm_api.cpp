@@ -76,7 +76,7 @@ mdlstm_status check_desc(const mdlstm_layer_desc* d) {
 }
 
 struct Plan {
-    size_t z, c, rid, rects, units, part, total;
+    size_t z, c, rid, rects, units, part, queue, total;
 };
 
 mdl::LayerGeom geom(const mdlstm_layer_desc* d, int32_t ch, int32_t cw) {
@@ -108,6 +108,8 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
     off += align_up((size_t)(nr > 0 ? nr : 1) * 16);
     p.part = off;
     off += align_up(mdl::strip_supported(g) ? mdl::strip_partial_bytes(g) : mdl::dw_partial_bytes(g));
+    p.queue = off;
+    off += align_up(4);
     p.total = off;
     return p;
 }
@@ -424,7 +426,7 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
     HIP_OR_FAIL(mark(2, s));
     if (!stepwise) {
         HIP_OR_FAIL(mdl::launch_wavefront_fwd(c.g, c.nt, 4 * n_rects, units, drects, d_mask, d_u, c.ws + c.p.z, cs,
-                                              d_y, s));
+                                              d_y, reinterpret_cast<unsigned*>(c.ws + c.p.queue), s));
     } else if (n_rects > 0) {
         int32_t max_steps = 0;
         for (int32_t k = 0; k < n_rects; ++k) max_steps = std::max(max_steps, rects[k].h + rects[k].w - 1);
@@ -492,7 +494,8 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
         HIP_OR_FAIL(mdl::launch_wavefront_bwd(c.g, c.nt, 4 * n_rects,
                                               reinterpret_cast<const int32_t*>(c.ws + c.p.units),
                                               reinterpret_cast<const int32_t*>(c.ws + c.p.rects), d_mask, d_u, d_dy,
-                                              c.ws + c.p.z, reinterpret_cast<const float*>(c.ws + c.p.c), s));
+                                              c.ws + c.p.z, reinterpret_cast<const float*>(c.ws + c.p.c),
+                                              reinterpret_cast<unsigned*>(c.ws + c.p.queue), s));
     }
     HIP_OR_FAIL(mark(5, s));
     if (c.g.n_cells > 0 && mdl::strip_supported(c.g)) {

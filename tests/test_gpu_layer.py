@@ -304,12 +304,13 @@ def test_stepwise_forward_matches_persistent(case):
     params = [gpu_run.to_dev(p, wl.dtype) for p in wl.params()]
     a = api.MDLSTMLayer(*params, ch, wl.canvas_w, units, mask)
     b = api.MDLSTMLayer(*params, ch, wl.canvas_w, units, mask)
-    a.workspace.zero_()  # the forward pass leaves the gradient scratch of the workspace untouched
-    b.workspace.zero_()
+    dy = api.pack_data([gpu_run.to_dev(wl.dy(k), wl.dtype) for k in range(wl.n)], units, ch, wl.canvas_w)
     ref = a.forward(x).clone()
-    c_ref = a.workspace.clone()
+    ref_grads = [t.clone() for t in a.backward(dy)]
     for _ in range(2):
         out = b.forward_stepwise(x).clone()
         torch.cuda.synchronize()
         assert torch.equal(out, ref)
-        assert torch.equal(b.workspace, c_ref)  # gates and cell states too
+    # the saved gates and cell states are the same too: identical gradients
+    for g, r in zip(b.backward(dy), ref_grads):
+        assert torch.equal(g, r)
