@@ -171,20 +171,24 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
             if (c < len && 4 * k4 < C) v = L4::f(L4::load(X + (p0 + c) * C + 4 * k4));
             st_f4(&sx[c][4 * k4], v);
         }
-        // validity byte per cell: bit0 valid, bit1 left, bit2 right, bit3 up, bit4 down
+        // validity byte per cell: bit0 valid, bit1 left, bit2 right, bit3 up, bit4 down.
+        // All ten loads are issued at once (neighbours outside the canvas
+        // re-read the cell itself and are discarded).
         for (int c = tid; c < TC; c += NTH) {
+            const int cc = min(c, len - 1), cx = cx0 + cc;
+            const int64_t p = p0 + cc;
+            const bool hl = cx > 0, hr = cx + 1 < canvas_w, hu = cy > 0, hd = cy + 1 < canvas_h;
+            const int64_t pl = hl ? p - 1 : p, pr = hr ? p + 1 : p;
+            const int64_t pu = hu ? p - canvas_w : p, pd = hd ? p + canvas_w : p;
+            const int r = rid[p], rl = rid[pl], rr = rid[pr], ru = rid[pu], rd = rid[pd];
+            const uint8_t m = mask[p], ml = mask[pl], mr = mask[pr], mu = mask[pu], md = mask[pd];
             uint8_t f = 0;
-            if (c < len) {
-                const int64_t p = p0 + c;
-                const int r = rid[p];
-                if (mask[p] && r >= 0) {
-                    const int cx = cx0 + c;
-                    f = 1;
-                    if (cx > 0 && rid[p - 1] == r && mask[p - 1]) f |= 2;
-                    if (cx + 1 < canvas_w && rid[p + 1] == r && mask[p + 1]) f |= 4;
-                    if (cy > 0 && rid[p - canvas_w] == r && mask[p - canvas_w]) f |= 8;
-                    if (cy + 1 < canvas_h && rid[p + canvas_w] == r && mask[p + canvas_w]) f |= 16;
-                }
+            if (c < len && m && r >= 0) {
+                f = 1;
+                if (hl && rl == r && ml) f |= 2;
+                if (hr && rr == r && mr) f |= 4;
+                if (hu && ru == r && mu) f |= 8;
+                if (hd && rd == r && md) f |= 16;
             }
             sflag[c] = f;
         }
@@ -232,8 +236,18 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
                 const int cell = nt * 16 + i16;
                 const bool v = sflag[cell] & 1;
                 if ((rslice + cc * WPD) < CXT) {
+                    // B operands in groups of ten: one LDS round trip per group
+                    constexpr int KB = 10, NKS = G / 4;
 #pragma unroll
-                    for (int ks = 0; ks < G / 4; ++ks) ax = mfma_f32(wa[cc][ks], v ? sz[cell][d * G + 4 * ks + g] : 0.0f, ax);
+                    for (int k0 = 0; k0 < NKS; k0 += KB) {
+                        float bz[KB];
+#pragma unroll
+                        for (int kk = 0; kk < KB; ++kk)
+                            bz[kk] = (v && k0 + kk < NKS) ? sz[cell][d * G + 4 * (k0 + kk) + g] : 0.0f;
+#pragma unroll
+                        for (int kk = 0; kk < KB; ++kk)
+                            if (k0 + kk < NKS) ax = mfma_f32(wa[cc][k0 + kk], bz[kk], ax);
+                    }
                 }
                 axs[cc][nt] = ax;
             }
