@@ -84,7 +84,12 @@ __device__ __forceinline__ void load_slot(const T* __restrict__ base, int64_t es
 
 template <int H, typename T>
 struct Geo {
-    static constexpr int NW = H <= 4 ? 1 : (H <= 8 ? 2 : (H <= 64 ? 4 : 8));  // waves per unit
+    // Waves per unit: fp32, one hidden-unit quad per wave up to eight waves.
+    // The waves of a workgroup share the four SIMDs of a CU, and a wave alone
+    // on its SIMD leaves MFMA and VALU issue slots idle, so more waves with
+    // less work each shorten every step (beyond eight the VGPR budget spills).
+    static constexpr int NW = std::is_same<T, float>::value ? (H <= 4 ? 1 : (H <= 32 ? H / 4 : 8))
+                                                             : (H <= 8 ? 2 : (H <= 32 ? 4 : 8));
     static constexpr int WQ = (H / 4) / NW;                                     // hidden-unit quads per wave
     static constexpr int G = 5 * H;
     static constexpr int PER = Ops<T>::PER;
@@ -194,7 +199,7 @@ struct BPre {
 // ---------------------------------------------------------------------------
 // Forward.
 // ---------------------------------------------------------------------------
-template <int H, int NT, typename T>
+template <int H, int NT, typename T, int PFD>
 __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit) {
     using Gm = Geo<H, T>;
     using O = Ops<T>;
@@ -219,7 +224,10 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
     __shared__ __attribute__((aligned(16))) float cbuf[2][ROWS][H + 2];  // pitch H + 2: rows of a tile in different banks
     __shared__ __attribute__((aligned(16))) float gpart[SPL][NT * 16][H + 2];
     __shared__ __attribute__((aligned(16))) u32x4 ostage[NC][PF];
-    __shared__ __attribute__((aligned(16))) u32x4 zst[NSL];
+    __shared__ __attribute__((aligned(16))) u32x4 zst[STAGE ? 2 : 1][NSL];  // by diagonal parity
+    // mask bytes by diagonal parity; a slot per thread so that every lane
+    // writes (rows below 16 NT are read)
+    __shared__ uint32_t mst[STAGE ? 2 : 1][STAGE ? NTH : 1];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int q = lane >> 4, n16 = lane & 15;
@@ -285,32 +293,48 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
     // row clamped into the diagonal's active range) so their number is the
     // same on every path, which lets the compiler wait for exactly these loads
     // one step later; `live` says whether they are used.
-    u32x4 zr[NITZ > 0 ? NITZ : 1];
+    // Staged chunks and mask bytes loaded PFD steps ahead of their diagonal's
+    // staging step (set k holds diagonals sb + k, sb + k + PFD, ...).
+    static_assert(PFD == 1 || PFD == 2, "prefetch distance");
+    u32x4 zr[PFD][NITZ > 0 ? NITZ : 1];
+    uint32_t mr[PFD];
     const DiagMap M(R, d, a.canvas_w);
-    // The lane's chunk of each staged-input pass: cell row and chunk of the
-    // row (slot S of zst is chunk S % PZ of the row of cell S / PZ; the
-    // padding chunk and the slots past the last cell repeat a valid one).
-    int zcell[NITZ > 0 ? NITZ : 1], zoff[NITZ > 0 ? NITZ : 1];
+    constexpr int RBZ = 4 * G * (int)sizeof(T);  // bytes per canvas cell of Z
+    // Cell (y, s - y) of the unit is canvas index M.c0 + idx with
+    // idx = sx*s + y*ky, which fits 32 bits; the lanes keep 64-bit pointers to
+    // their chunks at idx = 0 and add idx times the tensor's row bytes.
+    const uint8_t* mrow = a.mask + M.c0;
+    // The lane's chunk of each staged-input pass: cell row and address (slot S
+    // of zst is chunk S % PZ of the row of cell S / PZ; the padding chunk and
+    // the slots past the last cell repeat a valid one).
+    int zcell[NITZ > 0 ? NITZ : 1];
+    const char* zptr[NITZ > 0 ? NITZ : 1];
 #pragma unroll
     for (int it = 0; it < NITZ; ++it) {
         const int S = it * NTH + (int)threadIdx.x;
         zcell[it] = min(S / PZ, NT * 16 - 1);
-        zoff[it] = (d * G) * (int)sizeof(T) + 16 * min(S - (S / PZ) * PZ, Q::QZ - 1);
+        zptr[it] = reinterpret_cast<const char*>(Z) + M.c0 * RBZ + (d * G) * (int)sizeof(T) +
+                   16 * min(S - (S / PZ) * PZ, Q::QZ - 1);
     }
-    const char* Zb = reinterpret_cast<const char*>(Z);
+    // Loads of step s: the lanes' mask bytes and the pre-activations (staged:
+    // chunks into zr, else the lane's own values). They are issued for every
+    // lane from a valid cell of the rectangle (the row clamped into the
+    // diagonal's active range) so their number is the same on every path,
+    // which lets the compiler wait for exactly these loads one step later;
+    // `live` says whether they are used.
     auto fetch = [&](int s, FPre<NT, WQ, T>& b) {
         const int sc = min(s, steps - 1);
         const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
-        const int64_t base = M.base(sc);
+        const int sxs = M.sx * sc;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             const int yy = 16 * nt + n16;
             b.live[nt] = s < steps && yy >= ylo && yy <= yhi;
-            const int yc = min(max(yy, ylo), yhi);
-            const int64_t p = M.at(base, yc);
-            b.p[nt] = p;
-            b.m[nt] = a.mask[p];
+            const int idx = sxs + min(max(yy, ylo), yhi) * M.ky;
+            b.m[nt] = mrow[idx];
             if constexpr (!STAGE) {
+                const int64_t p = M.c0 + idx;
+                b.p[nt] = p;
                 const T* zp = Z + p * (4 * G) + d * G;
 #pragma unroll
                 for (int wq = 0; wq < WQ; ++wq) {
@@ -320,72 +344,91 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
                 }
             }
         }
+    };
+    // Staged pre-activation chunks and the mask byte of row threadIdx.x (of
+    // the last row above 16 NT, unused there) of diagonal s into register set k.
+    auto fetch_z = [&](int s, int k) {
+        const int sc = min(s, steps - 1);
+        const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
+        const int sxs = M.sx * sc;
         if constexpr (STAGE) {
 #pragma unroll
             for (int it = 0; it < NITZ; ++it) {
-                const int yc = min(max(zcell[it], ylo), yhi);
-                zr[it] = *reinterpret_cast<const u32x4*>(Zb + M.at(base, yc) * (4 * G * (int)sizeof(T)) + zoff[it]);
+                const int idx = sxs + min(max(zcell[it], ylo), yhi) * M.ky;
+                zr[k][it] = *reinterpret_cast<const u32x4*>(zptr[it] + (int64_t)idx * RBZ);
             }
+            // every lane loads (a valid byte), which keeps the number of loads per step fixed
+            mr[k] = mrow[sxs + min(max(min((int)threadIdx.x, NT * 16 - 1), ylo), yhi) * M.ky];
         }
     };
-    // zr -> zst; the cell phase of the step reads zst after its first barrier.
-    auto stage_in = [&]() {
+    // Register set k -> LDS buffers of diagonal s's parity.
+    auto stage_in = [&](int s, int k) {
 #pragma unroll
-        for (int it = 0; it < NITZ; ++it) zst[it * NTH + threadIdx.x] = zr[it];
+        for (int it = 0; it < NITZ; ++it) zst[s & 1][it * NTH + threadIdx.x] = zr[k][it];
+        if constexpr (STAGE) mst[s & 1][threadIdx.x] = mr[k];
     };
 
-    // Write back the outputs staged by diagonal sp. Runs between that step's
-    // closing barrier and the next cell phase's barrier. Every lane stores in
-    // every pass (rows outside the diagonal repeat its nearest cell, which
-    // writes the same bytes twice), so the number of stores is fixed. All LDS
-    // reads are issued before the first store: one LDS round trip.
+    // Write back the outputs staged by diagonal sp. Every lane stores in every
+    // pass (rows outside the diagonal repeat its nearest cell, which writes
+    // the same bytes twice), so the number of stores is fixed. All LDS reads
+    // are issued before the first store: one LDS round trip.
     constexpr int NITF = STAGE ? (NT * 16 * Q::QF + NTH - 1) / NTH : 0;
     // The lane's chunk of each write-back pass: cell row, chunk index in the
-    // staged row, and where the chunk goes (address at canvas index 0 and
-    // bytes per canvas cell of its tensor: gates, outputs or cell states).
+    // staged row and bytes per canvas cell of its tensor (gates, outputs or
+    // cell states) packed as rowbytes << 8 | chunk, and its address at idx = 0.
     int fcell[NITF > 0 ? NITF : 1], fcr[NITF > 0 ? NITF : 1];
-    char* fbase[NITF > 0 ? NITF : 1];
+    char* fptr[NITF > 0 ? NITF : 1];
 #pragma unroll
     for (int it = 0; it < NITF; ++it) {
         const int i = min(it * NTH + (int)threadIdx.x, NT * 16 * Q::QF - 1);
         const int r = i % Q::QF;
         fcell[it] = i / Q::QF;
         if (r < Q::QZ) {
-            fbase[it] = reinterpret_cast<char*>(Z + d * G) + 16 * r;
-            fcr[it] = (4 * G * (int)sizeof(T)) << 8 | r;
+            fptr[it] = reinterpret_cast<char*>(Z + d * G) + 16 * r + M.c0 * RBZ;
+            fcr[it] = RBZ << 8 | r;
         } else if (r < Q::QZ + Q::QY) {
-            fbase[it] = reinterpret_cast<char*>(Y + d * H) + 16 * (r - Q::QZ);
+            fptr[it] = reinterpret_cast<char*>(Y + d * H) + 16 * (r - Q::QZ) + M.c0 * (4 * H * (int)sizeof(T));
             fcr[it] = (4 * H * (int)sizeof(T)) << 8 | r;
         } else {
-            fbase[it] = reinterpret_cast<char*>(Cs + d * H) + 16 * (r - Q::QZ - Q::QY);
+            fptr[it] = reinterpret_cast<char*>(Cs + d * H) + 16 * (r - Q::QZ - Q::QY) + M.c0 * (16 * H);
             fcr[it] = (16 * H) << 8 | r;
         }
     }
+    auto flush_read = [&](int sp, u32x4 (&v)[NITF > 0 ? NITF : 1]) {
+        const int ylo = max(0, sp - R.w + 1), yhi = min(R.h - 1, sp);
+#pragma unroll
+        for (int it = 0; it < NITF; ++it) v[it] = ostage[min(max(fcell[it], ylo), yhi)][fcr[it] & 255];
+    };
+    auto flush_store = [&](int sp, const u32x4 (&v)[NITF > 0 ? NITF : 1]) {
+        const int ylo = max(0, sp - R.w + 1), yhi = min(R.h - 1, sp);
+        const int sxs = M.sx * sp;
+#pragma unroll
+        for (int it = 0; it < NITF; ++it) {
+            const int cell = min(max(fcell[it], ylo), yhi);
+            *reinterpret_cast<u32x4*>(fptr[it] + (int64_t)(sxs + cell * M.ky) * (fcr[it] >> 8)) = v[it];
+        }
+    };
     auto flush = [&](int sp) {
         if constexpr (STAGE) {
-            const int ylo = max(0, sp - R.w + 1), yhi = min(R.h - 1, sp);
-            const int64_t base = M.base(sp);
-            u32x4 v[NITF];
-            char* dst[NITF];
-#pragma unroll
-            for (int it = 0; it < NITF; ++it) {
-                const int cell = min(max(fcell[it], ylo), yhi);
-                v[it] = ostage[cell][fcr[it] & 255];
-                dst[it] = fbase[it] + M.at(base, cell) * (fcr[it] >> 8);
-            }
-#pragma unroll
-            for (int it = 0; it < NITF; ++it) *reinterpret_cast<u32x4*>(dst[it]) = v[it];
+            u32x4 v[NITF > 0 ? NITF : 1];
+            flush_read(sp, v);
+            flush_store(sp, v);
         }
     };
 
-    auto compute = [&](int s, const FPre<NT, WQ, T>& b) {
-        const int cur = s & 1, prv = cur ^ 1;
+    // Recurrent contraction of step s on MFMA from [h_L ; h_T] of the previous
+    // diagonal: the lane's own sigmoid gates (acc) and this wave's reduction
+    // slice of the candidate tile (ag). Staged, tiles outside the diagonal are
+    // computed too (their results are not used), which keeps a step's MFMAs
+    // in one block with the memory work issued behind them; otherwise they
+    // are skipped.
+    constexpr bool SKIP = !STAGE;
+    auto mma = [&](int s, floatx4 (&acc)[NT][WQ], floatx4 (&ag)[NT]) {
+        const int prv = (s & 1) ^ 1;
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
-        floatx4 acc[NT][WQ];
-        // pre-activations from [h_L ; h_T] of the previous diagonal
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;  // uniform over the workgroup
+            if (SKIP && (16 * nt > yhi || 16 * nt + 15 < ylo)) continue;  // uniform over the workgroup
             const int yy = 16 * nt + n16;
             const T* brow = (q < 2) ? &hbuf[prv][yy + 1][q * KRUN] : &hbuf[prv][yy][(q - 2) * KRUN];
             Op bop[NSTEP], bg[GSTEP];
@@ -393,23 +436,62 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
             for (int ks = 0; ks < NSTEP; ++ks) bop[ks] = O::lds(brow + ks * O::PER);
 #pragma unroll
             for (int ks = 0; ks < GSTEP; ++ks) bg[ks] = O::lds(brow + (sp * GSTEP + ks) * O::PER);
-            floatx4 ag = floatx4{0.f, 0.f, 0.f, 0.f};
+            ag[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int wq = 0; wq < WQ; ++wq) acc[nt][wq] = ag;
+            for (int ks = 0; ks < GSTEP; ++ks) ag[nt] = O::mma(Ag[ks], bg[ks], ag[nt]);
+#pragma unroll
+            for (int wq = 0; wq < WQ; ++wq) acc[nt][wq] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < NSTEP; ++ks)
 #pragma unroll
                 for (int wq = 0; wq < WQ; ++wq) acc[nt][wq] = O::mma(Aown[wq][ks], bop[ks], acc[nt][wq]);
+        }
+    };
+    // The candidate slices go to LDS for the cell phase to sum.
+    auto partials = [&](int s, const floatx4 (&ag)[NT]) {
+        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+        const int j0 = 16 * gt + 4 * q;
 #pragma unroll
-            for (int ks = 0; ks < GSTEP; ++ks) ag = O::mma(Ag[ks], bg[ks], ag);
-            const int j0 = 16 * gt + 4 * q;
+        for (int nt = 0; nt < NT; ++nt) {
+            if (SKIP && (16 * nt > yhi || 16 * nt + 15 < ylo)) continue;
+            const int yy = 16 * nt + n16;
             if (j0 < H) {
-                *reinterpret_cast<float2*>(&gpart[sp][yy][j0]) = make_float2(ag[0], ag[1]);
-                *reinterpret_cast<float2*>(&gpart[sp][yy][j0 + 2]) = make_float2(ag[2], ag[3]);
+                *reinterpret_cast<float2*>(&gpart[sp][yy][j0]) = make_float2(ag[nt][0], ag[nt][1]);
+                *reinterpret_cast<float2*>(&gpart[sp][yy][j0 + 2]) = make_float2(ag[nt][2], ag[nt][3]);
             }
         }
-        lds_barrier();
-        // cell updates: lane owns (cell 16 nt + n16, hidden unit 4 (w WQ + wq) + q)
+    };
+    // Inputs of the cell updates of step s that are ready before its
+    // contraction: the pre-activations and the top neighbours' cell states.
+    auto pre_read = [&](int s, const FPre<NT, WQ, T>& b, float (&zv)[NT][WQ][5], float (&ct)[NT][WQ],
+                        uint32_t (&mk)[NT]) {
+        const int prv = (s & 1) ^ 1;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const int yy = 16 * nt + n16;
+            if constexpr (STAGE)
+                mk[nt] = mst[s & 1][yy];
+            else
+                mk[nt] = b.m[nt];
+#pragma unroll
+            for (int wq = 0; wq < WQ; ++wq) {
+                const int j = 4 * (w * WQ + wq) + q;
+#pragma unroll
+                for (int t = 0; t < 5; ++t) {
+                    if constexpr (STAGE)
+                        zv[nt][wq][t] = ld1f<T>(reinterpret_cast<const T*>(&zst[s & 1][yy * PZ]) + t * H + j);
+                    else
+                        zv[nt][wq][t] = ld1f<T>(&b.z[nt][wq][t]);
+                }
+                ct[nt][wq] = cbuf[prv][yy][j];
+            }
+        }
+    };
+    // Cell updates: the lane owns (cell 16 nt + n16, hidden unit 4 (w WQ + wq) + q).
+    auto update = [&](int s, const FPre<NT, WQ, T>& b, const floatx4 (&acc)[NT][WQ], const float (&zv0)[NT][WQ][5],
+                      const float (&ct)[NT][WQ], const uint32_t (&mk)[NT]) {
+        const int cur = s & 1, prv = cur ^ 1;
+        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;
@@ -418,15 +500,8 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
             for (int wq = 0; wq < WQ; ++wq) {
                 const int j = 4 * (w * WQ + wq) + q;
                 float cn = 0.0f, hn = 0.0f;
-                if (b.live[nt]) {
-                    float zv[5];
-#pragma unroll
-                    for (int t = 0; t < 5; ++t) {
-                        if constexpr (STAGE)
-                            zv[t] = ld1f<T>(reinterpret_cast<const T*>(&zst[yy * PZ]) + t * H + j);
-                        else
-                            zv[t] = ld1f<T>(&b.z[nt][wq][t]);
-                    }
+                if (yy >= ylo && yy <= yhi) {
+                    const float* zv = zv0[nt][wq];
                     float gs = 0.0f;
 #pragma unroll
                     for (int k = 0; k < SPL; ++k) gs += gpart[k][yy][j];
@@ -435,11 +510,9 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
                     const float gft = sigm_fast(acc[nt][wq][2] + zv[2]);
                     const float go = sigm_fast(acc[nt][wq][3] + zv[3]);
                     const float gg = tanh_fast(gs + zv[4]);
-                    const float cT = cbuf[prv][yy][j];
-                    cn = gi * gg + gfl * cprev[nt][wq] + gft * cT;
+                    cn = gi * gg + gfl * cprev[nt][wq] + gft * ct[nt][wq];
                     hn = go * tanh_fast(cn);
-                    const int64_t p = b.p[nt];
-                    if (!b.m[nt]) {
+                    if (!mk[nt]) {
                         cn = 0.0f;
                         hn = 0.0f;
                     }
@@ -453,7 +526,8 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
                         oz[5 * H + j] = from_f<T>(hn);
                         reinterpret_cast<float*>(&ostage[yy][Q::QZ + Q::QY])[j] = cn;
                     } else {
-                        if (b.m[nt]) {
+                        const int64_t p = b.p[nt];
+                        if (mk[nt]) {
                             T* zp = Z + p * (4 * G) + d * G + j;
                             zp[0 * H] = from_f<T>(gi);
                             zp[1 * H] = from_f<T>(gfl);
@@ -470,26 +544,61 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
                 cbuf[cur][yy + 1][j] = cn;
             }
         }
+    };
+    auto compute = [&](int s, const FPre<NT, WQ, T>& b) {
+        floatx4 acc[NT][WQ], ag[NT];
+        float zv[NT][WQ][5], ct[NT][WQ];
+        uint32_t mk[NT];
+        pre_read(s, b, zv, ct, mk);
+        mma(s, acc, ag);
+        partials(s, ag);
+        lds_barrier();
+        update(s, b, acc, zv, ct, mk);
         lds_barrier();
     };
 
     lds_barrier();
     FPre<NT, WQ, T> b0, b1;
     if constexpr (STAGE) {
-        // Step s: move the staged inputs of step s into LDS, issue the loads of
-        // step s + 1 (past the last step they re-read valid cells), write back
-        // step s - 1, compute step s.
-        auto step = [&](int s, const FPre<NT, WQ, T>& cur, FPre<NT, WQ, T>& nxt) {
-            stage_in();
-            fetch(s + 1, nxt);
-            if (s > sb) flush(s - 1);
-            compute(s, cur);
+        // Step s: the MFMAs first, then the LDS reads that the previous step
+        // made ready (the outputs of step s - 1 to write back, the
+        // pre-activations and mask bytes staged for step s, the top cell
+        // states); behind them the registers loaded for step s + 1 PFD steps
+        // ago go to LDS, the loads of step s + 1 + PFD are issued into them
+        // (past the last step they re-read valid cells) and step s - 1 is
+        // written back; the candidate partials go to LDS once their MFMAs are
+        // done; then the cell phase. Two steps of prefetch cover the load
+        // latency when the whole chip streams to and from memory.
+        auto step = [&](int s, int k, auto with_flush) {
+            constexpr bool WF = decltype(with_flush)::value;
+            floatx4 acc[NT][WQ], ag[NT];
+            mma(s, acc, ag);
+            u32x4 fv[NITF > 0 ? NITF : 1];
+            if constexpr (WF) flush_read(s - 1, fv);
+            float zv[NT][WQ][5], ct[NT][WQ];
+            uint32_t mk[NT];
+            pre_read(s, b0, zv, ct, mk);
+            stage_in(s + 1, k);
+            fetch_z(s + 1 + PFD, k);
+            if constexpr (WF) flush_store(s - 1, fv);
+            partials(s, ag);
+            lds_barrier();
+            update(s, b0, acc, zv, ct, mk);
+            lds_barrier();
         };
-        fetch(sb, b0);
-        for (int s = sb; s < se; s += 2) {
-            step(s, b0, b1);
-            if (s + 1 < se) step(s + 1, b1, b0);
+        constexpr int K1 = PFD - 1;  // register set of diagonals sb + 1, sb + 3, ...
+        fetch_z(sb, 0);
+        stage_in(sb, 0);
+        fetch_z(sb + PFD, 0);
+        if constexpr (PFD == 2) fetch_z(sb + 1, 1);
+        lds_barrier();
+        step(sb, K1, std::false_type{});
+        int s = sb + 1;
+        for (; s + 1 < se; s += 2) {
+            step(s, 0, std::true_type{});
+            step(s + 1, K1, std::true_type{});
         }
+        if (s < se) step(s, 0, std::true_type{});
         flush(se - 1);
     } else if constexpr (Prefetch2<T>::template on<NT, WQ>()) {
         fetch(sb, b0);
@@ -809,10 +918,13 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
 // unit shares its CU with fewer others than when every unit has its own
 // workgroup from the start; without one, workgroup b runs unit b.
 // ---------------------------------------------------------------------------
+// Forward loads run one step ahead with one workgroup per unit, two steps
+// ahead when several workgroups per CU take units from the queue (the load
+// latency grows while every CU streams to and from memory).
 template <int H, int NT, typename T, bool FWD, bool QUEUE>
 __device__ __forceinline__ void run_units(const WaveArgs& a) {
     if constexpr (!QUEUE) {
-        if (FWD) wave_fwd_unit<H, NT, T>(a, a.units[blockIdx.x]);
+        if (FWD) wave_fwd_unit<H, NT, T, 1>(a, a.units[blockIdx.x]);
         else wave_bwd_unit<H, NT, T>(a, a.units[blockIdx.x]);
         return;
     }
@@ -823,7 +935,7 @@ __device__ __forceinline__ void run_units(const WaveArgs& a) {
         lds_barrier();
         const int k = slot;
         if (k >= a.n_units) break;
-        if (FWD) wave_fwd_unit<H, NT, T>(a, a.units[k]);
+        if (FWD) wave_fwd_unit<H, NT, T, 2>(a, a.units[k]);
         else wave_bwd_unit<H, NT, T>(a, a.units[k]);
     }
 }
