@@ -4,17 +4,26 @@
 // A strip is TC consecutive cells of one canvas row. For each strip the
 // workgroup loads, with independent coalesced loads, dZ [TC][20H], X
 // [TC][C_in], the layer output Y of the strip's row (one cell of halo on each
-// side) and of the rows above and below, and per cell a validity byte (cell
+// side) and of the rows above and below, and the rectangle ids and mask bytes
+// of the same halo block, from which a validity byte per cell follows (cell
 // valid; left/right/up/down neighbour in the same rectangle and unmasked).
-// Then, from LDS:
+// Cells outside every rectangle or masked, and predecessors outside the
+// cell's rectangle or masked, are zeroed in LDS once staged, so the MFMA
+// loops below read plain operands. Then, from LDS:
 //   dW_d[r][col] += sum_cells dZ[cell][d*5H + r] * B_d[cell][col],
-//     B_d = [X | h_L,d | h_T,d | 1]  (the layer output shifted one cell in
+//     B_d = [X | h_L,d | h_T,d]  (the layer output shifted one cell in
 //     direction d's frame: the shifted recurrent operand of Appendix A)
+//   db_d[r] += sum_cells dZ[cell][d*5H + r]
 //   dX[cell] = sum_d dZ_d[cell] Wx_d
 // Wave w of the workgroup owns direction d = w / WPD and a slice of the gate
-// rows; the dW tiles stay in its registers across all strips of the
-// workgroup, and are written once as the workgroup's partial. A fixed-order
-// reduction over workgroups gives deterministic weight gradients.
+// rows; the dW tiles (MFMA) and bias sums (VALU) stay in its registers across
+// all strips of the workgroup, and are written once as the workgroup's
+// partial. A fixed-order reduction over workgroups gives deterministic weight
+// gradients.
+//
+// The loads of the next strip are issued into registers before the current
+// strip is computed, so their latency is hidden behind the MFMA work; the
+// workgroup's barriers order LDS only and leave them in flight.
 #include <algorithm>
 #include <type_traits>
 
@@ -25,22 +34,33 @@ namespace mdl {
 
 namespace {
 
-constexpr int STRIP_WGS = 512;  // workgroups (two per CU)
-
 template <int H, int C>
 struct StripCfg {
     static constexpr int G = 5 * H, N = 20 * H;
     static constexpr int RT = (G + 15) / 16;          // gate-row tiles per direction
-    static constexpr int CT = (C + 2 * H + 1 + 15) / 16;  // dW column tiles
+    static constexpr int NB = C + 2 * H;              // dW columns (the bias is summed apart)
+    static constexpr int CT = (NB + 15) / 16;         // dW column tiles
+    static constexpr int PP = CT * 16 + 4;            // partial row pitch; column CT*16 holds the bias
+    static constexpr bool ALIGNED = C % 16 == 0 && H % 16 == 0;  // column tiles never straddle X / h_L / h_T
     static constexpr int CXT = (C + 15) / 16;         // dX channel tiles
     static constexpr int WPD = H >= 32 ? 2 : 1;       // waves per direction
     static constexpr int RTW = (RT + WPD - 1) / WPD;  // gate-row tiles per wave
     static constexpr int TC = H >= 32 ? 16 : 32;      // cells per strip
     static constexpr int THREADS = 256 * WPD;
-    static constexpr int ZP = N + 16;                 // LDS pitch of dZ rows: 4 cell slots hit distinct banks
+    static constexpr int ZP = N + 4;                  // LDS pitch of dZ rows (4 mod 16: the cells read by one MFMA hit distinct banks)
     static constexpr int YP = 4 * H + 4;              // LDS pitch of Y rows
     static constexpr int XP = CXT * 16 + 4;           // LDS pitch of X rows and dX partials
     static constexpr int SY = 3 * (TC + 2) * YP, SDX = 4 * TC * XP;
+    static constexpr int HW = TC + 2;                 // halo block width
+    // The next strip's loads are prefetched into registers where the dW tiles
+    // leave room; those shapes use over 256 registers per lane (one
+    // workgroup per CU), the others run two workgroups per CU.
+    static constexpr bool PREFETCH = H <= 16;
+    static constexpr int WGS = H == 16 ? 256 : 512;
+    // register budget of the H = 32 shapes: dW steps unrolled by two, dX
+    // operands read five blocks at a time
+    static constexpr int DW_UNROLL = H >= 32 ? 2 : TC / 4;
+    static constexpr int DXB = H >= 32 ? 5 : (G + 15) / 16;
 };
 
 // 4 consecutive elements of storage type T as fp32.
@@ -51,7 +71,7 @@ struct V4<float> {
     using R = float4;
     static __device__ __forceinline__ R load(const float* p) { return *reinterpret_cast<const float4*>(p); }
     static __device__ __forceinline__ float4 f(R v) { return v; }
-    static __device__ __forceinline__ R zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+    static __device__ __forceinline__ void store(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
 };
 template <>
 struct V4<bf16_t> {
@@ -61,7 +81,10 @@ struct V4<bf16_t> {
         return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
                            __uint_as_float(v.y & 0xffff0000u));
     }
-    static __device__ __forceinline__ R zero() { return make_uint2(0, 0); }
+    static __device__ __forceinline__ void store(bf16_t* p, float4 v) {
+        *reinterpret_cast<uint2*>(p) = make_uint2((uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16),
+                                                  (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+    }
 };
 
 template <typename T>
@@ -82,15 +105,16 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
             const int32_t* __restrict__ rid, T* __restrict__ dX, float* __restrict__ part) {
     using Cf = StripCfg<H, C>;
     using L4 = V4<T>;
-    constexpr int TC = Cf::TC, RTW = Cf::RTW, WPD = Cf::WPD, CT = Cf::CT, CXT = Cf::CXT;
+    constexpr int TC = Cf::TC, RTW = Cf::RTW, WPD = Cf::WPD, CT = Cf::CT, CXT = Cf::CXT, HW = Cf::HW;
     constexpr int N = Cf::N, G = Cf::G, ZP = Cf::ZP, YP = Cf::YP, XP = Cf::XP, NTH = Cf::THREADS;
-    __shared__ __attribute__((aligned(16))) float sz[TC][ZP];
+    __shared__ __attribute__((aligned(16))) float sz[TC * ZP + 16];
     __shared__ __attribute__((aligned(16))) float sx[TC][XP];
     // Y rows above, same (with one cell of halo each side), below; later the
     // per-direction dX partials
     __shared__ __attribute__((aligned(16))) float sy_raw[Cf::SY > Cf::SDX ? Cf::SY : Cf::SDX];
-    __shared__ uint8_t sflag[TC];
-    auto sy = reinterpret_cast<float(*)[TC + 2][YP]>(sy_raw);
+    __shared__ int32_t srid[3][HW];
+    __shared__ uint32_t smask[3][HW];
+    auto sy = reinterpret_cast<float(*)[HW][YP]>(sy_raw);
     auto sdx = reinterpret_cast<float(*)[TC][XP]>(sy_raw);
 
     const int tid = threadIdx.x;
@@ -99,134 +123,225 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
     const int d = wave / WPD, rslice = wave % WPD;
     const int rt0 = rslice * RTW;
 
+    // The dZ row padding and the 16 floats after the last row are read
+    // (times zero weights) where 5H is not a multiple of 16; they stay zero.
+    for (int e = tid; e < TC * (ZP - N) + 16; e += NTH) {
+        const int c = e / (ZP - N);
+        sz[c < TC ? c * ZP + N + (e - c * (ZP - N)) : TC * ZP + (e - TC * (ZP - N))] = 0.0f;
+    }
+
     floatx4 acc[RTW][CT];
 #pragma unroll
     for (int a = 0; a < RTW; ++a)
 #pragma unroll
         for (int b = 0; b < CT; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // bias sums: the dW A operands summed per lane (its cell slots), the four
+    // slots added across lanes at the end
+    float dbp[RTW];
+#pragma unroll
+    for (int a = 0; a < RTW; ++a) dbp[a] = 0.0f;
 
     // dX: wave (d, rslice) owns channel tiles ct = rslice, rslice + WPD, ...;
-    // its A operand Wx_d^T (row = channel, K = gate rows 4 ks + g) stays in registers.
-    constexpr int CXW = (CXT + WPD - 1) / WPD;
-    float wa[CXW][G / 4];
+    // M = channels, N = cells, K = the direction's gate rows in blocks of 16:
+    // in MFMA j of block m, K slot g is gate row 16 m + 4 g + j, so that a
+    // lane reads its four rows of a block as one 16-byte LDS load. The A
+    // operand Wx_d^T stays in registers.
+    constexpr int CXW = (CXT + WPD - 1) / WPD, KBL = (G + 15) / 16;
+    float wa[CXW][KBL][4];
 #pragma unroll
     for (int cc = 0; cc < CXW; ++cc) {
         const int ch = (rslice + cc * WPD) * 16 + i16;
 #pragma unroll
-        for (int ks = 0; ks < G / 4; ++ks)
-            wa[cc][ks] = ch < C ? to_f<T>(Wx[((int64_t)d * G + 4 * ks + g) * C + ch]) : 0.0f;
+        for (int m = 0; m < KBL; ++m)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * m + 4 * g + j;
+                wa[cc][m][j] = (ch < C && r < G) ? to_f<T>(Wx[((int64_t)d * G + r) * C + ch]) : 0.0f;
+            }
     }
 
-    for (int strip = blockIdx.x; strip < n_strips; strip += gridDim.x) {
-        const int cy = strip / segs;
-        const int cx0 = (strip - cy * segs) * TC;
-        const int len = min(TC, canvas_w - cx0);
-        const int64_t p0 = (int64_t)cy * canvas_w + cx0;
+    // --- loads of one strip into registers. Every lane issues the same
+    // number of loads from valid addresses (slots past the end repeat the last
+    // element, cells past the row's end repeat its last cell, halo cells
+    // outside the canvas re-read the nearest cell and are marked invalid when
+    // staged), so the waits for them are exact.
+    constexpr int NZ = TC * N / 4, PZ = (NZ + NTH - 1) / NTH;
+    constexpr int NYR = HW * H, NY = 3 * NYR, PY = (NY + NTH - 1) / NTH;
+    constexpr int NX = TC * C / 4, PX = (NX + NTH - 1) / NTH;
+    constexpr int NHALO = 3 * HW, PH = (NHALO + NTH - 1) / NTH;
+    typename L4::R vz[PZ], vy[PY], vx[PX];
+    int32_t vr[PH];
+    uint32_t vm[PH];
+    auto strip_pos = [&](int strip, int& cy, int& cx0, int& len, int64_t& p0) {
+        cy = strip / segs;
+        cx0 = (strip - cy * segs) * TC;
+        len = min(TC, canvas_w - cx0);
+        p0 = (int64_t)cy * canvas_w + cx0;
+    };
+    // part bits: 1 dZ, 2 Y, 4 X, 8 ids and mask bytes
+    auto issue = [&](int strip, int parts) {
+        int cy, cx0, len;
+        int64_t p0;
+        strip_pos(strip, cy, cx0, len, p0);
+#pragma unroll
+        for (int k = 0; k < PZ * (parts & 1); ++k) {
+            const int e = min(tid + k * NTH, NZ - 1);
+            const int c = (4 * e) / N, n = 4 * e - c * N;
+            vz[k] = L4::load(dZ + (p0 + min(c, len - 1)) * N + n);
+        }
+#pragma unroll
+        for (int k = 0; k < PY * ((parts >> 1) & 1); ++k) {
+            const int e = min(tid + k * NTH, NY - 1);
+            const int row = e / NYR, rem = e - row * NYR;
+            const int c = rem / H, k4 = rem - c * H;
+            const int yy = min(max(cy + row - 1, 0), canvas_h - 1), xx = min(max(cx0 + c - 1, 0), canvas_w - 1);
+            vy[k] = L4::load(Y + ((int64_t)yy * canvas_w + xx) * (4 * H) + 4 * k4);
+        }
+#pragma unroll
+        for (int k = 0; k < PX * ((parts >> 2) & 1); ++k) {
+            const int e = min(tid + k * NTH, NX - 1);
+            const int c = e / (C / 4), k4 = e - c * (C / 4);
+            vx[k] = L4::load(X + (p0 + min(c, len - 1)) * C + 4 * k4);
+        }
+#pragma unroll
+        for (int k = 0; k < PH * ((parts >> 3) & 1); ++k) {
+            const int e = min(tid + k * NTH, NHALO - 1);
+            const int row = e / HW, c = e - row * HW;
+            const int yy = min(max(cy + row - 1, 0), canvas_h - 1), xx = min(max(cx0 + c - 1, 0), canvas_w - 1);
+            const int64_t p = (int64_t)yy * canvas_w + xx;
+            vr[k] = rid[p];
+            vm[k] = mask[p];
+        }
+    };
+    // registers -> LDS; slots past the end store the last element again
+    auto commit = [&](int strip, int parts) {
+        int cy, cx0, len;
+        int64_t p0;
+        strip_pos(strip, cy, cx0, len, p0);
+#pragma unroll
+        for (int k = 0; k < PZ * (parts & 1); ++k) {
+            const int e = min(tid + k * NTH, NZ - 1);
+            const int c = (4 * e) / N, n = 4 * e - c * N;
+            st_f4(&sz[c * ZP + n], L4::f(vz[k]));
+        }
+#pragma unroll
+        for (int k = 0; k < PY * ((parts >> 1) & 1); ++k) {
+            const int e = min(tid + k * NTH, NY - 1);
+            const int row = e / NYR, rem = e - row * NYR;
+            const int c = rem / H, k4 = rem - c * H;
+            st_f4(&sy[row][c][4 * k4], L4::f(vy[k]));
+        }
+#pragma unroll
+        for (int k = 0; k < PX * ((parts >> 2) & 1); ++k) {
+            const int e = min(tid + k * NTH, NX - 1);
+            const int c = e / (C / 4), k4 = e - c * (C / 4);
+            st_f4(&sx[c][4 * k4], L4::f(vx[k]));
+        }
+#pragma unroll
+        for (int k = 0; k < PH * ((parts >> 3) & 1); ++k) {
+            const int e = min(tid + k * NTH, NHALO - 1);
+            const int row = e / HW, c = e - row * HW;
+            const int yy = cy + row - 1, xx = cx0 + c - 1;
+            const bool inside = yy >= 0 && yy < canvas_h && xx >= 0 && xx < canvas_w;
+            srid[row][c] = inside ? vr[k] : -2;  // -2 matches no rectangle id
+            smask[row][c] = inside ? vm[k] : 0u;
+        }
+    };
 
-        // --- stage (all loads independent; issued in batches before the LDS stores)
-        {
-            constexpr int NZ = TC * N / 4, PZ = (NZ + NTH - 1) / NTH;
-            typename L4::R v[PZ];
+    // With the prefetch the next strip's loads occupy registers during the
+    // compute; shapes whose dW tiles fill the register file load each strip
+    // just before staging it, one tensor at a time.
+    constexpr bool PREFETCH = Cf::PREFETCH;
+    int strip = blockIdx.x;
+    if constexpr (PREFETCH) issue(strip, 15);
+    for (; strip < n_strips; strip += gridDim.x) {
+        int cy, cx0, len;
+        int64_t p0;
+        strip_pos(strip, cy, cx0, len, p0);
+        if constexpr (PREFETCH) {
+            commit(strip, 15);
+        } else {
 #pragma unroll
-            for (int k = 0; k < PZ; ++k) {
-                const int e = tid + k * NTH;
-                const int c = (4 * e) / N;
-                v[k] = (e < NZ && c < len) ? L4::load(dZ + p0 * N + 4 * e) : L4::zero();
-            }
-#pragma unroll
-            for (int k = 0; k < PZ; ++k) {
-                const int e = tid + k * NTH;
-                if (e < NZ) {
-                    const int c = (4 * e) / N, n = 4 * e - c * N;
-                    st_f4(&sz[c][n], L4::f(v[k]));
-                }
+            for (int part = 1; part < 16; part <<= 1) {
+                issue(strip, part);
+                commit(strip, part);
             }
         }
-        {
-            constexpr int NYR = (TC + 2) * H, NY = 3 * NYR, PY = (NY + NTH - 1) / NTH;  // float4 units
-            typename L4::R v[PY];
+        lds_barrier();
+        // Validity, folded into the staged data: the dZ and X rows of an
+        // invalid cell (outside every rectangle, masked, or past the row's
+        // end) and every predecessor output that is not in the cell's
+        // rectangle or is masked become zero. Each predecessor segment (row,
+        // halo cell, direction) has one consumer cell.
+        // Lanes 0..TC-1 of every wave find the invalid cells (same ballot in every wave).
+        bool cv = false;
+        if (lane < TC) {
+            const int r = srid[1][lane + 1];
+            cv = lane < len && smask[1][lane + 1] && r >= 0;
+        }
+        const uint64_t valid = __ballot(cv);
+        const uint64_t bad = ~valid & ((TC == 64) ? ~0ull : ((1ull << TC) - 1));
+        for (uint64_t bm = bad; bm; bm &= bm - 1) {  // uniform loop over the invalid cells
+            const int c = __builtin_ctzll(bm);
+            for (int e = tid; e < N / 4; e += NTH) st_f4(&sz[c * ZP + 4 * e], make_float4(0.f, 0.f, 0.f, 0.f));
+            if (tid < C / 4) st_f4(&sx[c][4 * tid], make_float4(0.f, 0.f, 0.f, 0.f));
+        }
+        for (int e = tid; e < 8 * TC; e += NTH) {
+            // e = (direction, left or top, consumer cell)
+            const int c = e % TC, lt = (e / TC) & 1, dd = e / (2 * TC);
+            const int row = lt ? ((dd & 2) ? 2 : 0) : 1;
+            const int k = lt ? c + 1 : ((dd & 1) ? c + 2 : c);
+            const int r = srid[1][c + 1];
+            if (!(srid[row][k] == r && smask[row][k])) {
 #pragma unroll
-            for (int k = 0; k < PY; ++k) {
-                const int e = tid + k * NTH;
-                const int row = e / NYR, rem = e - row * NYR;
-                const int c = rem / H, k4 = rem - c * H;
-                const int yy = cy + row - 1, xx = cx0 + c - 1;
-                v[k] = (e < NY && yy >= 0 && yy < canvas_h && xx >= 0 && xx < canvas_w && c <= len + 1)
-                           ? L4::load(Y + ((int64_t)yy * canvas_w + xx) * (4 * H) + 4 * k4)
-                           : L4::zero();
-            }
-#pragma unroll
-            for (int k = 0; k < PY; ++k) {
-                const int e = tid + k * NTH;
-                if (e < NY) {
-                    const int row = e / NYR, rem = e - row * NYR;
-                    const int c = rem / H, k4 = rem - c * H;
-                    st_f4(&sy[row][c][4 * k4], L4::f(v[k]));
-                }
+                for (int j = 0; j < H; j += 4) st_f4(&sy[row][k][dd * H + j], make_float4(0.f, 0.f, 0.f, 0.f));
             }
         }
-        for (int e = tid; e < TC * CXT * 4; e += NTH) {
-            const int c = e / (CXT * 4), k4 = e - c * (CXT * 4);
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (c < len && 4 * k4 < C) v = L4::f(L4::load(X + (p0 + c) * C + 4 * k4));
-            st_f4(&sx[c][4 * k4], v);
-        }
-        // validity byte per cell: bit0 valid, bit1 left, bit2 right, bit3 up, bit4 down.
-        // All ten loads are issued at once (neighbours outside the canvas
-        // re-read the cell itself and are discarded).
-        for (int c = tid; c < TC; c += NTH) {
-            const int cc = min(c, len - 1), cx = cx0 + cc;
-            const int64_t p = p0 + cc;
-            const bool hl = cx > 0, hr = cx + 1 < canvas_w, hu = cy > 0, hd = cy + 1 < canvas_h;
-            const int64_t pl = hl ? p - 1 : p, pr = hr ? p + 1 : p;
-            const int64_t pu = hu ? p - canvas_w : p, pd = hd ? p + canvas_w : p;
-            const int r = rid[p], rl = rid[pl], rr = rid[pr], ru = rid[pu], rd = rid[pd];
-            const uint8_t m = mask[p], ml = mask[pl], mr = mask[pr], mu = mask[pu], md = mask[pd];
-            uint8_t f = 0;
-            if (c < len && m && r >= 0) {
-                f = 1;
-                if (hl && rl == r && ml) f |= 2;
-                if (hr && rr == r && mr) f |= 4;
-                if (hu && ru == r && mu) f |= 8;
-                if (hd && rd == r && md) f |= 16;
-            }
-            sflag[c] = f;
-        }
-        __syncthreads();
+        // the next strip's loads (the last strip re-reads itself) stay in flight
+        if constexpr (PREFETCH) issue(min(strip + (int)gridDim.x, n_strips - 1), 15);
+        lds_barrier();
 
-        // --- dW: K = cells of the strip, 4 per MFMA step (slot g = cell offset)
-#pragma unroll 2
+        // --- dW: K = cells of the strip, 4 per MFMA step; in step ks, K slot g
+        // is cell 16 (ks / 4) + 4 g + ks % 4 (the four slots of a step hit
+        // distinct LDS banks)
+#pragma unroll Cf::DW_UNROLL
         for (int ks = 0; ks < TC / 4; ++ks) {
-            const int c = 4 * ks + g;
-            const uint8_t f = sflag[c];
-            const bool v = f & 1;
-            const bool vl = (d & 1) ? (f & 4) : (f & 2);
-            const bool vt = (d & 2) ? (f & 16) : (f & 8);
+            const int c = 16 * (ks >> 2) + 4 * g + (ks & 3);
             const int lc = (d & 1) ? c + 2 : c;  // left predecessor in the halo-shifted same row
             const int trow = (d & 2) ? 2 : 0;    // row of the top predecessor
             float av[RTW], bv[CT];
 #pragma unroll
             for (int a = 0; a < RTW; ++a) {
                 const int r = (rt0 + a) * 16 + i16;
-                av[a] = (v && r < G) ? sz[c][d * G + r] : 0.0f;
+                const float z = sz[c * ZP + d * G + r];  // in bounds for r < RT * 16
+                av[a] = r < G ? z : 0.0f;
             }
 #pragma unroll
             for (int b = 0; b < CT; ++b) {
-                const int col = b * 16 + i16;
-                float x = 0.0f;
-                if (col < C) x = sx[c][col];
-                else if (col < C + H) x = vl ? sy[1][lc][d * H + col - C] : 0.0f;
-                else if (col < C + 2 * H) x = vt ? sy[trow][c + 1][d * H + col - C - H] : 0.0f;
-                else if (col == C + 2 * H) x = 1.0f;
-                bv[b] = v ? x : 0.0f;
+                float x;
+                if constexpr (Cf::ALIGNED) {
+                    // tile b lies in one of X, h_L, h_T
+                    if (b < C / 16) x = sx[c][b * 16 + i16];
+                    else if (b < (C + H) / 16) x = sy[1][lc][d * H + (b - C / 16) * 16 + i16];
+                    else x = sy[trow][c + 1][d * H + (b - (C + H) / 16) * 16 + i16];
+                } else {
+                    const int col = b * 16 + i16;
+                    x = 0.0f;
+                    if (col < C) x = sx[c][col];
+                    else if (col < C + H) x = sy[1][lc][d * H + col - C];
+                    else if (col < C + 2 * H) x = sy[trow][c + 1][d * H + col - C - H];
+                }
+                bv[b] = x;
             }
 #pragma unroll
-            for (int a = 0; a < RTW; ++a)
+            for (int a = 0; a < RTW; ++a) {
+                dbp[a] += av[a];
 #pragma unroll
                 for (int b = 0; b < CT; ++b) acc[a][b] = mfma_f32(av[a], bv[b], acc[a][b]);
+            }
         }
 
-        // --- dX partial of direction d: M = channels, N = cells, K = 5H gate rows
+        // --- dX partial of direction d
         floatx4 axs[CXW][TC / 16];
 #pragma unroll
         for (int cc = 0; cc < CXW; ++cc) {
@@ -234,25 +349,31 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
             for (int nt = 0; nt < TC / 16; ++nt) {
                 floatx4 ax = floatx4{0.f, 0.f, 0.f, 0.f};
                 const int cell = nt * 16 + i16;
-                const bool v = sflag[cell] & 1;
                 if ((rslice + cc * WPD) < CXT) {
-                    // B operands in groups of ten: one LDS round trip per group
-                    constexpr int KB = 10, NKS = G / 4;
+                    // operands in groups of DXB blocks: one LDS round trip per group
+                    constexpr int DXB = Cf::DXB;
 #pragma unroll
-                    for (int k0 = 0; k0 < NKS; k0 += KB) {
-                        float bz[KB];
+                    for (int m0 = 0; m0 < KBL; m0 += DXB) {
+                        float4 bz[DXB];
 #pragma unroll
-                        for (int kk = 0; kk < KB; ++kk)
-                            bz[kk] = (v && k0 + kk < NKS) ? sz[cell][d * G + 4 * (k0 + kk) + g] : 0.0f;
+                        for (int m = 0; m < DXB; ++m)
+                            if (m0 + m < KBL)
+                                bz[m] = *reinterpret_cast<const float4*>(&sz[cell * ZP + d * G + 16 * (m0 + m) + 4 * g]);
 #pragma unroll
-                        for (int kk = 0; kk < KB; ++kk)
-                            if (k0 + kk < NKS) ax = mfma_f32(wa[cc][k0 + kk], bz[kk], ax);
+                        for (int m = 0; m < DXB; ++m) {
+                            if (m0 + m < KBL) {
+                                ax = mfma_f32(wa[cc][m0 + m][0], bz[m].x, ax);
+                                ax = mfma_f32(wa[cc][m0 + m][1], bz[m].y, ax);
+                                ax = mfma_f32(wa[cc][m0 + m][2], bz[m].z, ax);
+                                ax = mfma_f32(wa[cc][m0 + m][3], bz[m].w, ax);
+                            }
+                        }
                     }
                 }
                 axs[cc][nt] = ax;
             }
         }
-        __syncthreads();  // every wave is done reading the staged Y rows
+        lds_barrier();  // every wave is done reading the staged Y rows
 #pragma unroll
         for (int cc = 0; cc < CXW; ++cc) {
             const int ct = rslice + cc * WPD;
@@ -263,20 +384,31 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
                     for (int r = 0; r < 4; ++r) sdx[d][nt * 16 + i16][ct * 16 + 4 * g + r] = axs[cc][nt][r];
             }
         }
-        __syncthreads();
-        // sum the four directions in a fixed order; dX is 0 at invalid cells
-        for (int e = tid; e < TC * C; e += NTH) {
-            const int c = e / C, k = e - c * C;
-            if (c < len) {
-                const float s4 = ((sdx[0][c][k] + sdx[1][c][k]) + sdx[2][c][k]) + sdx[3][c][k];
-                St<T>::st1(dX + (p0 + c) * C + k, (sflag[c] & 1) ? s4 : 0.0f);
+        lds_barrier();
+        // sum the four directions in a fixed order (0 at invalid cells, whose
+        // dZ rows are zero). Every lane stores 4 channels of one cell in every
+        // pass (cells past the row's end and slots past the last repeat the
+        // row's last cell).
+        {
+            constexpr int NXS = TC * C / 4, PXS = (NXS + NTH - 1) / NTH;
+#pragma unroll
+            for (int k = 0; k < PXS; ++k) {
+                const int e = min(tid + k * NTH, NXS - 1);
+                const int c = min(e / (C / 4), len - 1), k4 = 4 * (e - (e / (C / 4)) * (C / 4));
+                const float4 a0 = *reinterpret_cast<const float4*>(&sdx[0][c][k4]);
+                const float4 a1 = *reinterpret_cast<const float4*>(&sdx[1][c][k4]);
+                const float4 a2 = *reinterpret_cast<const float4*>(&sdx[2][c][k4]);
+                const float4 a3 = *reinterpret_cast<const float4*>(&sdx[3][c][k4]);
+                L4::store(dX + (p0 + c) * C + k4,
+                          make_float4(((a0.x + a1.x) + a2.x) + a3.x, ((a0.y + a1.y) + a2.y) + a3.y,
+                                      ((a0.z + a1.z) + a2.z) + a3.z, ((a0.w + a1.w) + a2.w) + a3.w));
             }
         }
-        __syncthreads();
+        lds_barrier();
     }
 
-    // partial of this workgroup: [wg][4][RT*16][CT*16]
-    float* out = part + (int64_t)blockIdx.x * 4 * (Cf::RT * 16) * (CT * 16) + (int64_t)d * (Cf::RT * 16) * (CT * 16);
+    // partial of this workgroup: [wg][4][RT*16][PP], bias in column CT*16
+    float* out = part + ((int64_t)blockIdx.x * 4 + d) * (Cf::RT * 16) * Cf::PP;
 #pragma unroll
     for (int a = 0; a < RTW; ++a) {
         if (rt0 + a >= Cf::RT) continue;
@@ -284,36 +416,56 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
         for (int b = 0; b < CT; ++b)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                out[(int64_t)((rt0 + a) * 16 + 4 * g + r) * (CT * 16) + b * 16 + i16] = acc[a][b][r];
+                out[(int64_t)((rt0 + a) * 16 + 4 * g + r) * Cf::PP + b * 16 + i16] = acc[a][b][r];
+    }
+#pragma unroll
+    for (int a = 0; a < RTW; ++a) {
+        // lanes i16, i16 + 16, i16 + 32, i16 + 48 hold the four cell slots of row (rt0 + a) * 16 + i16
+        float sb = dbp[a];
+        sb += __shfl_xor(sb, 16);
+        sb += __shfl_xor(sb, 32);
+        if (g == 0 && rt0 + a < Cf::RT) out[(int64_t)((rt0 + a) * 16 + i16) * Cf::PP + CT * 16] = sb;
     }
 }
 
-// Fixed-order sum over workgroup partials; one thread per output element,
-// loads batched so the sum is bandwidth- rather than latency-bound.
-__global__ void k_strip_reduce(int C, int H, int RT, int CT, int nwg, const float* __restrict__ part,
-                               float* __restrict__ dwx, float* __restrict__ du, float* __restrict__ db) {
-    const int G = 5 * H, NB = C + 2 * H + 1;
-    const int64_t total = (int64_t)4 * G * NB;
-    const int64_t stride = (int64_t)4 * (RT * 16) * (CT * 16);
-    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-         idx += (int64_t)gridDim.x * blockDim.x) {
-        const int d = (int)(idx / ((int64_t)G * NB));
-        const int rem = (int)(idx - (int64_t)d * G * NB);
-        const int r = rem / NB, col = rem - r * NB;
-        const float* src = part + (int64_t)d * (RT * 16) * (CT * 16) + (int64_t)r * (CT * 16) + col;
-        float s = 0.0f;
-        int w = 0;
-        for (; w + 8 <= nwg; w += 8) {
+// Fixed-order sum over workgroup partials. A block takes 64 consecutive
+// outputs; its four thread groups sum every fourth workgroup each (loads
+// batched), and the four sums are added in a fixed order.
+__global__ void __launch_bounds__(256)
+k_strip_reduce(int C, int H, int RT, int PP, int CT, int nwg, const float* __restrict__ part,
+               float* __restrict__ dwx, float* __restrict__ du, float* __restrict__ db) {
+    __shared__ float ps[4][64];
+    const int G = 5 * H, NB = C + 2 * H + 1;  // columns: X, h_L, h_T, bias
+    const int total = 4 * G * NB;
+    const int oi = blockIdx.x * 64 + (threadIdx.x & 63), grp = threadIdx.x >> 6;
+    const int64_t stride = (int64_t)4 * (RT * 16) * PP;
+    float s = 0.0f;
+    int d = 0, r = 0, col = 0;
+    if (oi < total) {
+        d = oi / (G * NB);
+        const int rem = oi - d * G * NB;
+        r = rem / NB;
+        col = rem - r * NB;
+        const int pc = col < NB - 1 ? col : CT * 16;
+        const float* src = part + (int64_t)d * (RT * 16) * PP + (int64_t)r * PP + pc;
+        int w = grp;
+        for (; w + 28 < nwg; w += 32) {
             float v[8];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) v[k] = src[(int64_t)(w + k) * stride];
+            for (int k = 0; k < 8; ++k) v[k] = src[(int64_t)(w + 4 * k) * stride];
 #pragma unroll
             for (int k = 0; k < 8; ++k) s += v[k];
         }
-        for (; w < nwg; ++w) s += src[(int64_t)w * stride];
-        if (col < C) dwx[((int64_t)d * G + r) * C + col] = s;
-        else if (col < C + 2 * H) du[((int64_t)d * G + r) * (2 * H) + (col - C)] = s;
-        else db[(int64_t)d * G + r] = s;
+        for (; w < nwg; w += 4) s += src[(int64_t)w * stride];
+    }
+    ps[grp][threadIdx.x & 63] = s;
+    __syncthreads();
+    if (grp == 0 && oi < total) {
+        const int t = threadIdx.x;
+        const float v = ((ps[0][t] + ps[1][t]) + ps[2][t]) + ps[3][t];
+        if (col < C) dwx[((int64_t)d * G + r) * C + col] = v;
+        else if (col < C + 2 * H) du[((int64_t)d * G + r) * (2 * H) + (col - C)] = v;
+        else db[(int64_t)d * G + r] = v;
     }
 }
 
@@ -335,12 +487,19 @@ bool strip_supported(const LayerGeom& g) {
 static int strip_wgs(const LayerGeom& g) {
     const int tc = strip_tc(g.hidden);
     const int64_t strips = (int64_t)g.canvas_h * ((g.canvas_w + tc - 1) / tc);
-    return (int)std::max<int64_t>(1, std::min<int64_t>(STRIP_WGS, strips));
+    int wgs = 0;
+#define MDL_STRIP_WGS(T, H, C) \
+    if (!wgs && (g.dtype == 1) == std::is_same<T, bf16_t>::value && g.hidden == H && g.c_in == C) wgs = StripCfg<H, C>::WGS;
+    MDL_STRIP_SHAPES(MDL_STRIP_WGS)
+#undef MDL_STRIP_WGS
+    return (int)std::max<int64_t>(1, std::min<int64_t>(wgs, strips));
 }
 
+static int strip_pp(const LayerGeom& g) { return (g.c_in + 2 * g.hidden + 15) / 16 * 16 + 4; }
+
 size_t strip_partial_bytes(const LayerGeom& g) {
-    const int RT = (5 * g.hidden + 15) / 16, CT = (g.c_in + 2 * g.hidden + 1 + 15) / 16;
-    return (size_t)strip_wgs(g) * 4 * RT * 16 * CT * 16 * sizeof(float);
+    const int RT = (5 * g.hidden + 15) / 16;
+    return (size_t)strip_wgs(g) * 4 * RT * 16 * strip_pp(g) * sizeof(float);
 }
 
 hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y, const void* d_wx,
@@ -350,7 +509,7 @@ hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_
     const int segs = (g.canvas_w + tc - 1) / tc;
     const int n_strips = g.canvas_h * segs;
     const int nwg = strip_wgs(g);
-    const int RT = (5 * g.hidden + 15) / 16, CT = (g.c_in + 2 * g.hidden + 1 + 15) / 16;
+    const int RT = (5 * g.hidden + 15) / 16, CT = (g.c_in + 2 * g.hidden + 15) / 16;
     bool ok = false;
 #define MDL_STRIP_LAUNCH(T, H, C)                                                                                  \
     if (!ok && (g.dtype == 1) == std::is_same<T, bf16_t>::value && g.hidden == H && g.c_in == C) {                 \
@@ -363,11 +522,9 @@ hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_
     MDL_STRIP_SHAPES(MDL_STRIP_LAUNCH)
 #undef MDL_STRIP_LAUNCH
     if (!ok) return hipErrorInvalidValue;
-    const int64_t total = (int64_t)4 * 5 * g.hidden * (g.c_in + 2 * g.hidden + 1);
-    int blocks = (int)((total + 255) / 256);
-    if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(k_strip_reduce, dim3(blocks), dim3(256), 0, s, g.c_in, g.hidden, RT, CT, nwg, d_part, d_dwx,
-                       d_du, d_db);
+    const int total = 4 * 5 * g.hidden * (g.c_in + 2 * g.hidden + 1);
+    hipLaunchKernelGGL(k_strip_reduce, dim3((total + 63) / 64), dim3(256), 0, s, g.c_in, g.hidden, RT, strip_pp(g),
+                       CT, nwg, d_part, d_dwx, d_du, d_db);
     return hipGetLastError();
 }
 
