@@ -26,7 +26,8 @@
  *     the kernels.
  *   - Pointers named d_* are DEVICE memory of the current HIP device; all
  *     other pointers are HOST memory. The caller owns every buffer; the library
- *     allocates no memory of its own and keeps no pointer after returning.
+ *     allocates no memory of its own and keeps no pointer after returning
+ *     (workspace addresses serve as lookup keys only, never dereferenced).
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream). Work
  *     is enqueued on it asynchronously unless stated otherwise.
  *   - Every argument is validated on the host before any HIP call; on error
@@ -191,7 +192,10 @@ mdlstm_status mdlstm_forward_stepwise(const mdlstm_layer_desc* desc, int32_t can
  * d_dwx [4][5H][c_in], d_du [4][5H][2H], d_db [4][5H] (out, fp32): sums over
  *   all valid cells, OVERWRITTEN (not accumulated); fixed reduction order, so
  *   repeated calls give bitwise-identical results.
- * The gates saved in the workspace are overwritten by their gradients.
+ * The gates saved in the workspace are overwritten by their gradients. The
+ * rectangle ids the forward call staged in the workspace are reused when the
+ * layer shape, canvas and rectangles are the same (the library remembers, per
+ * workspace address, what the last forward call staged there).
  * Asynchronous on `stream`.
  */
 mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,

@@ -139,8 +139,10 @@ __global__ void k_fill(V* __restrict__ p, int64_t count, V v) {
 }
 
 template <typename V, bool USE_INDEX>
-__global__ void k_paint_rects(const int32_t* __restrict__ rects, int canvas_w, V* __restrict__ out, V v) {
+__global__ void k_paint_rects(const int32_t* __restrict__ rects, int canvas_w, V* __restrict__ out, V v,
+                              unsigned* __restrict__ zero2) {
     const int k = blockIdx.x;
+    if (zero2 && k == 0 && threadIdx.x < 2) zero2[threadIdx.x] = 0u;
     const int y0 = rects[4 * k], x0 = rects[4 * k + 1], h = rects[4 * k + 2], w = rects[4 * k + 3];
     const V val = USE_INDEX ? (V)k : v;
     for (int i = threadIdx.x; i < h * w; i += blockDim.x) {
@@ -161,18 +163,18 @@ hipError_t launch_mask(int n, const int32_t* d_rects, int canvas_h, int canvas_w
         hipLaunchKernelGGL(k_fill<uint8_t>, dim3(fill_blocks(cells)), dim3(256), 0, s, d_mask, cells, (uint8_t)0);
     if (n > 0)
         hipLaunchKernelGGL((k_paint_rects<uint8_t, false>), dim3(n), dim3(256), 0, s, d_rects, canvas_w, d_mask,
-                           (uint8_t)1);
+                           (uint8_t)1, nullptr);
     return hipGetLastError();
 }
 
 hipError_t launch_rect_ids(int n, const int32_t* d_rects, int canvas_h, int canvas_w, int32_t* d_rid,
-                           hipStream_t s) {
+                           unsigned* d_zero2, hipStream_t s) {
     int64_t cells = (int64_t)canvas_h * canvas_w;
     if (cells > 0)
         hipLaunchKernelGGL(k_fill<int32_t>, dim3(fill_blocks(cells)), dim3(256), 0, s, d_rid, cells, (int32_t)-1);
     if (n > 0)
         hipLaunchKernelGGL((k_paint_rects<int32_t, true>), dim3(n), dim3(256), 0, s, d_rects, canvas_w, d_rid,
-                           (int32_t)0);
+                           (int32_t)0, d_zero2);
     return hipGetLastError();
 }
 

@@ -938,6 +938,16 @@ __device__ __forceinline__ void run_units(const WaveArgs& a) {
         if (FWD) wave_fwd_unit<H, NT, T, 2>(a, a.units[k]);
         else wave_bwd_unit<H, NT, T>(a, a.units[k]);
     }
+    // Count the workgroup out; the last one leaves both counters at zero for
+    // the next launch (every other workgroup's last take precedes its count).
+    if (threadIdx.x == 0) {
+        __threadfence();
+        if (atomicAdd(a.queue + 1, 1u) == gridDim.x - 1) {
+            __threadfence();
+            atomicExch(a.queue, 0u);
+            atomicExch(a.queue + 1, 0u);
+        }
+    }
 }
 
 template <int H, int NT, typename T, bool QUEUE>
@@ -1001,8 +1011,6 @@ static hipError_t launch_wave(bool fwd, const LayerGeom& g, int nt, int n_units,
         if (e != hipSuccess) return e;
         const int groups = WAVE_GROUPS_PER_CU * std::max(cus, 1);
         if (n_units > groups) {  // else one workgroup per unit
-            e = launch_zero_f32(reinterpret_cast<float*>(a.queue), 1, s);
-            if (e != hipSuccess) return e;
             n_units = groups;
         } else {
             a.queue = nullptr;

@@ -22,9 +22,10 @@ hipError_t launch_pack_place(int n, int canvas_w, const int32_t* d_hw, int32_t* 
 // mask[canvas] = 1 inside any of the rects, else 0.
 hipError_t launch_mask(int n, const int32_t* d_rects, int canvas_h, int canvas_w, uint8_t* d_mask,
                        hipStream_t s);
-// rect id per cell (-1 outside every rect).
+// rect id per cell (-1 outside every rect); also zeroes the two counters at
+// d_zero2 (the wavefront unit queue) when n > 0 and d_zero2 is not NULL.
 hipError_t launch_rect_ids(int n, const int32_t* d_rects, int canvas_h, int canvas_w, int32_t* d_rid,
-                           hipStream_t s);
+                           unsigned* d_zero2, hipStream_t s);
 // scatter/gather of n HWC examples of c channels, element size esize (2 or 4).
 hipError_t launch_scatter(int n, const void* const* d_ptrs, const int32_t* d_rects, int canvas_h,
                           int canvas_w, int c, int esize, void* d_canvas, int max_h, hipStream_t s);
@@ -39,8 +40,9 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
 hipError_t launch_zero_invalid(const LayerGeom& g, int width, const uint8_t* d_mask,
                                const int32_t* d_rid, void* d_t, hipStream_t s);
 // Forward anti-diagonal wavefront over n_units units (rectangle, direction)
-// in the order of d_units. d_queue: a device counter the launch zeroes and
-// its workgroups take units from (a fixed number per CU).
+// in the order of d_units. d_queue: two device counters, zero on entry (the
+// workgroups take units from the first, a fixed number per CU, and count
+// themselves out on the second; the last one out zeroes both again).
 hipError_t launch_wavefront_fwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u,
                                 void* d_z, float* d_c, void* d_y, unsigned* d_queue, hipStream_t s);

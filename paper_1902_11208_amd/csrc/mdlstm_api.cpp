@@ -8,7 +8,10 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstring>
+#include <mutex>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "kernels.hpp"
@@ -108,8 +111,8 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
     off += align_up((size_t)(nr > 0 ? nr : 1) * 16);
     p.part = off;
     off += align_up(mdl::strip_supported(g) ? mdl::strip_partial_bytes(g) : mdl::dw_partial_bytes(g));
-    p.queue = off;
-    off += align_up(4);
+    p.queue = off;  // unit queue: next unit, workgroups done
+    off += align_up(8);
     p.total = off;
     return p;
 }
@@ -200,15 +203,65 @@ mdlstm_status prepare(const mdlstm_layer_desc* desc, int32_t ch, int32_t cw, con
     return MDLSTM_OK;
 }
 
-mdlstm_status stage_layout(const Common& c, int32_t n_rects, const mdlstm_rect* rects, const uint8_t*,
-                           hipStream_t s) {
+// Identity of what a workspace holds after layout staging: the layer shape,
+// canvas and rectangles (with a hash of the rectangle list).
+struct StagedKey {
+    int32_t c_in = 0, hidden = 0, dtype = 0, canvas_h = 0, canvas_w = 0, n_rects = -1, device = -1;
+    uint64_t hash = 0;
+    bool operator==(const StagedKey& o) const {
+        return c_in == o.c_in && hidden == o.hidden && dtype == o.dtype && canvas_h == o.canvas_h &&
+               canvas_w == o.canvas_w && n_rects == o.n_rects && device == o.device && hash == o.hash;
+    }
+};
+
+StagedKey staged_key(const Common& c, int32_t n_rects, const mdlstm_rect* rects) {
+    StagedKey k;
+    k.c_in = c.g.c_in;
+    k.hidden = c.g.hidden;
+    k.dtype = c.g.dtype;
+    k.canvas_h = c.g.canvas_h;
+    k.canvas_w = c.g.canvas_w;
+    k.n_rects = n_rects;
+    if (hipGetDevice(&k.device) != hipSuccess) k.device = -2;
+    uint64_t h = 1469598103934665603ull;  // FNV-1a over the rectangle bytes
+    const unsigned char* b = reinterpret_cast<const unsigned char*>(rects);
+    for (size_t i = 0; i < (size_t)(n_rects > 0 ? n_rects : 0) * sizeof(mdlstm_rect); ++i) {
+        h ^= b[i];
+        h *= 1099511628211ull;
+    }
+    k.hash = h;
+    return k;
+}
+
+// Workspaces staged by the last forward call on them. A backward call, whose
+// workspace must be untouched since its forward, skips restaging when its
+// layout is the one staged there.
+std::mutex g_staged_mu;
+std::unordered_map<uintptr_t, StagedKey> g_staged;
+
+mdlstm_status stage_layout(const Common& c, int32_t n_rects, const mdlstm_rect* rects, bool reuse, hipStream_t s) {
+    const StagedKey key = staged_key(c, n_rects, rects);
+    const uintptr_t ws = reinterpret_cast<uintptr_t>(c.ws);
+    if (reuse) {
+        std::lock_guard<std::mutex> lock(g_staged_mu);
+        auto it = g_staged.find(ws);
+        if (it != g_staged.end() && it->second == key) return MDLSTM_OK;
+    }
     if (n_rects > 0) {
+        // rectangles and unit order in one copy (adjacent workspace sections)
         std::vector<int32_t> units = unit_order(n_rects, rects);
-        HIP_OR_FAIL(hipMemcpyAsync(c.ws + c.p.rects, rects, (size_t)n_rects * 16, hipMemcpyHostToDevice, s));
-        HIP_OR_FAIL(hipMemcpyAsync(c.ws + c.p.units, units.data(), units.size() * 4, hipMemcpyHostToDevice, s));
+        const size_t ubytes = units.size() * 4, span = c.p.units - c.p.rects + ubytes;
+        std::vector<unsigned char> host(span, 0);
+        std::memcpy(host.data(), rects, (size_t)n_rects * 16);
+        std::memcpy(host.data() + (c.p.units - c.p.rects), units.data(), ubytes);
+        HIP_OR_FAIL(hipMemcpyAsync(c.ws + c.p.rects, host.data(), span, hipMemcpyHostToDevice, s));
     }
     HIP_OR_FAIL(mdl::launch_rect_ids(n_rects, reinterpret_cast<const int32_t*>(c.ws + c.p.rects), c.g.canvas_h,
-                                     c.g.canvas_w, reinterpret_cast<int32_t*>(c.ws + c.p.rid), s));
+                                     c.g.canvas_w, reinterpret_cast<int32_t*>(c.ws + c.p.rid),
+                                     reinterpret_cast<unsigned*>(c.ws + c.p.queue), s));
+    std::lock_guard<std::mutex> lock(g_staged_mu);
+    if (g_staged.size() >= 4096) g_staged.clear();  // bound the table; a miss only restages
+    g_staged[ws] = key;
     return MDLSTM_OK;
 }
 
@@ -413,7 +466,7 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
     if (misaligned(d_y)) return fail(MDLSTM_ERR_INVALID_ARG, "y must be 16-byte aligned");
     if (c.g.n_cells == 0) return MDLSTM_OK;
     hipStream_t s = as_stream(stream);
-    st = stage_layout(c, n_rects, rects, d_mask, s);
+    st = stage_layout(c, n_rects, rects, false, s);
     if (st != MDLSTM_OK) return st;
     const int32_t* rid = reinterpret_cast<const int32_t*>(c.ws + c.p.rid);
     const int32_t* units = reinterpret_cast<const int32_t*>(c.ws + c.p.units);
@@ -486,7 +539,7 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
         misaligned(d_db))
         return fail(MDLSTM_ERR_INVALID_ARG, "y, dy, dx and the weight gradients must be 16-byte aligned");
     hipStream_t s = as_stream(stream);
-    st = stage_layout(c, n_rects, rects, d_mask, s);
+    st = stage_layout(c, n_rects, rects, true, s);
     if (st != MDLSTM_OK) return st;
     const int32_t* rid = reinterpret_cast<const int32_t*>(c.ws + c.p.rid);
     HIP_OR_FAIL(mark(4, s));
