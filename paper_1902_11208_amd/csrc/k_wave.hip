@@ -144,7 +144,7 @@ template <int H, int NT, typename T>
 constexpr size_t bwd_lds_base() {
     using Gm = Geo<H, T>;
     return (size_t)NT * 16 * (Gm::G + 16 / sizeof(T)) * sizeof(T) +
-           (size_t)Gm::SPLB * (NT * 16 + 1) * (2 * H + 2) * 4 + (size_t)(NT * 16 + 1) * (H + 2) * 4;
+           (size_t)Gm::SPLB * (NT * 16 + 2) * (2 * H + 2) * 4 + (size_t)(NT * 16 + 2) * (H + 2) * 4;
 }
 template <int H, int NT, typename T>
 constexpr size_t bwd_lds_stage() {
@@ -645,8 +645,10 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
     constexpr int NITF = (NT * 16 * Q::QZ + NTH - 1) / NTH;  // passes writing back the gate gradients
     constexpr int CC = Q::QZ + Q::QY;                        // first cell-state chunk of a row
     __shared__ __attribute__((aligned(16))) T dabuf[NT * 16][GP];
-    __shared__ __attribute__((aligned(16))) float gbuf[SPLB][NT * 16 + 1][2 * H + 2];  // row NT*16 stays zero
-    __shared__ __attribute__((aligned(16))) float dct[NT * 16 + 1][H + 2];
+    // row NT*16 stays zero; row NT*16 + 1 takes the writes of tiles outside
+    // the diagonal (and of padding columns), which nobody reads
+    __shared__ __attribute__((aligned(16))) float gbuf[SPLB][NT * 16 + 2][2 * H + 2];
+    __shared__ __attribute__((aligned(16))) float dct[NT * 16 + 2][H + 2];
     __shared__ __attribute__((aligned(16))) u32x4 ist[STAGE ? 2 : 1][NSL];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -661,8 +663,8 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
     const int steps = R.h + R.w - 1;
 
     for (int i = threadIdx.x; i < NT * 16 * GP; i += blockDim.x) (&dabuf[0][0])[i] = T(0);
-    for (int i = threadIdx.x; i < SPLB * (NT * 16 + 1) * (2 * H + 2); i += blockDim.x) (&gbuf[0][0][0])[i] = 0.0f;
-    for (int i = threadIdx.x; i < (NT * 16 + 1) * (H + 2); i += blockDim.x) (&dct[0][0])[i] = 0.0f;
+    for (int i = threadIdx.x; i < SPLB * (NT * 16 + 2) * (2 * H + 2); i += blockDim.x) (&gbuf[0][0][0])[i] = 0.0f;
+    for (int i = threadIdx.x; i < (NT * 16 + 2) * (H + 2); i += blockDim.x) (&dct[0][0])[i] = 0.0f;
 
     // A operands: U^T rows k = 16 mt + n16 (column k of U); slot q holds gate
     // rows r = q*KRUNB + ..., slice sb of the K steps.
@@ -824,11 +826,25 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
             }
         }
         lds_barrier();
-        // Staged rows of diagonal s - 2 replace those of diagonal s, which no
-        // lane reads any more; the rows of diagonal s - 3 start loading.
-        if constexpr (STAGE) {
-            stage_in(s - 2);
-            fetch_rows(s - 3);
+        // Phase B: U^T da for the left (rows k < H) and top (k >= H)
+        // predecessors, on MFMA; issued first so that the memory work below
+        // runs behind it. Staged, tiles outside the diagonal are computed too
+        // (their results are not used), which keeps the MFMAs in one block.
+        floatx4 acc[NT][TPW];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            if (!STAGE && (16 * nt > yhi || 16 * nt + 15 < ylo)) continue;
+            const int yy = 16 * nt + n16;
+            const T* brow = &dabuf[yy][q * KRUNB + sb * BSTEP * O::PER];
+            Op bop[BSTEP];
+#pragma unroll
+            for (int ks = 0; ks < BSTEP; ++ks) bop[ks] = O::lds(brow + ks * O::PER);
+#pragma unroll
+            for (int tt = 0; tt < TPW; ++tt) {
+                acc[nt][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < BSTEP; ++ks) acc[nt][tt] = O::mma(A[tt][ks], bop[ks], acc[nt][tt]);
+            }
         }
         // The rows of dabuf are the gate gradients of the diagonal's cells:
         // write them back with contiguous 16-byte stores. Every lane stores in
@@ -844,31 +860,32 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
                 v[it] = reinterpret_cast<const u32x4*>(&dabuf[cell][0])[dchunk[it]];
                 dst[it] = Zd + M.at(base, cell) * (4 * G * (int)sizeof(T)) + 16 * dchunk[it];
             }
+            // Staged rows of diagonal s - 2 replace those of diagonal s, which
+            // no lane reads any more; the rows of diagonal s - 3 start loading.
+            if constexpr (STAGE) {
+                stage_in(s - 2);
+                fetch_rows(s - 3);
+            }
 #pragma unroll
             for (int it = 0; it < NITF; ++it) *reinterpret_cast<u32x4*>(dst[it]) = v[it];
         }
-        // Phase B: U^T da for the left (rows k < H) and top (k >= H) predecessors.
+        // The products and the dc of the top predecessors go to LDS without
+        // branches (tiles outside the diagonal and padding columns write to
+        // the unread last rows), so the MFMA results are read in the same
+        // straight-line block that produced them.
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;
-            const int yy = 16 * nt + n16;
-            const T* brow = &dabuf[yy][q * KRUNB + sb * BSTEP * O::PER];
-            Op bop[BSTEP];
-#pragma unroll
-            for (int ks = 0; ks < BSTEP; ++ks) bop[ks] = O::lds(brow + ks * O::PER);
+            const bool act = !(16 * nt > yhi || 16 * nt + 15 < ylo);
+            const int yy = act ? 16 * nt + n16 : NT * 16 + 1;
 #pragma unroll
             for (int tt = 0; tt < TPW; ++tt) {
-                floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < BSTEP; ++ks) acc = O::mma(A[tt][ks], bop[ks], acc);
                 const int k0 = 16 * (mt0 + tt) + 4 * q;
-                if (k0 < 2 * H) {
-                    *reinterpret_cast<float2*>(&gbuf[sb][yy][k0]) = make_float2(acc[0], acc[1]);
-                    *reinterpret_cast<float2*>(&gbuf[sb][yy][k0 + 2]) = make_float2(acc[2], acc[3]);
-                }
+                float* gp = (act && k0 < 2 * H) ? &gbuf[sb][yy][k0] : &gbuf[sb][NT * 16 + 1][0];
+                *reinterpret_cast<float2*>(gp) = make_float2(acc[nt][tt][0], acc[nt][tt][1]);
+                *reinterpret_cast<float2*>(gp + 2) = make_float2(acc[nt][tt][2], acc[nt][tt][3]);
             }
 #pragma unroll
-            for (int wq = 0; wq < WQ; ++wq) dct[yy][4 * (w * WQ + wq) + q] = dcn[nt][wq];
+            for (int wq = 0; wq < WQ; ++wq) dct[yy][act ? 4 * (w * WQ + wq) + q : 0] = dcn[nt][wq];
         }
         lds_barrier();
     };
