@@ -18,7 +18,7 @@ LIB = os.path.join(PKG, "libmdlstm.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["mdlstm_api.cpp", "k_pack.hip", "k_proj.hip", "k_wave.hip", "k_bwd_gemm.hip", "k_bwd_strip.hip",
+SOURCES = ["mdlstm_api.cpp", "k_pack.hip", "k_proj.hip", "k_wave.hip", "k_bwd_big.hip", "k_bwd_strip.hip",
            "k_stack.hip"]
 
 FLAGS = [

@@ -79,7 +79,7 @@ mdlstm_status check_desc(const mdlstm_layer_desc* d) {
 }
 
 struct Plan {
-    size_t z, c, rid, rects, units, part, queue, total;
+    size_t z, c, rid, rects, units, part, flags, wxt, queue, total;
 };
 
 mdl::LayerGeom geom(const mdlstm_layer_desc* d, int32_t ch, int32_t cw) {
@@ -110,7 +110,12 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
     p.units = off;
     off += align_up((size_t)(nr > 0 ? nr : 1) * 16);
     p.part = off;
-    off += align_up(mdl::strip_supported(g) ? mdl::strip_partial_bytes(g) : mdl::dw_partial_bytes(g));
+    const bool strip = mdl::strip_supported(g);
+    off += align_up(strip ? mdl::strip_partial_bytes(g) : mdl::big_partial_bytes(g));
+    p.flags = off;  // the tiled gradient path only
+    off += strip ? 0 : align_up(mdl::big_flags_bytes(g));
+    p.wxt = off;
+    off += strip ? 0 : align_up(mdl::big_wxt_bytes(g));
     p.queue = off;  // unit queue: next unit, workgroups done
     off += align_up(8);
     p.total = off;
@@ -557,10 +562,17 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
         HIP_OR_FAIL(mdl::launch_bwd_strip(c.g, c.ws + c.p.z, d_x, d_y, d_wx, d_mask, rid, d_dx,
                                           reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
     } else {
-        if (c.g.n_cells > 0) HIP_OR_FAIL(mdl::launch_dx(c.g, c.ws + c.p.z, d_wx, d_mask, rid, d_dx, s));
+        // tiled products (phase boundary 6 coincides with 5)
         HIP_OR_FAIL(mark(6, s));
-        HIP_OR_FAIL(mdl::launch_dw(c.g, c.ws + c.p.z, d_x, d_y, d_mask, rid,
-                                   reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
+        if (c.g.n_cells > 0) {
+            HIP_OR_FAIL(mdl::launch_bwd_big(c.g, c.ws + c.p.z, d_x, d_y, d_wx, d_mask, rid, d_dx,
+                                            reinterpret_cast<uint8_t*>(c.ws + c.p.flags), c.ws + c.p.wxt,
+                                            reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
+        } else {
+            HIP_OR_FAIL(mdl::launch_zero_f32(d_dwx, (int64_t)4 * 5 * c.g.hidden * c.g.c_in, s));
+            HIP_OR_FAIL(mdl::launch_zero_f32(d_du, (int64_t)4 * 5 * c.g.hidden * 2 * c.g.hidden, s));
+            HIP_OR_FAIL(mdl::launch_zero_f32(d_db, (int64_t)4 * 5 * c.g.hidden, s));
+        }
     }
     HIP_OR_FAIL(mark(7, s));
     return MDLSTM_OK;
