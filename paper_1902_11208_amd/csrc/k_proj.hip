@@ -5,8 +5,9 @@
 //     Z[p][n] = b_all[n] + sum_k Wx_all[n][k] X[p][k],  n = d*5H + gate*H + j.
 // MFMA 16x16 tiles: M = gate columns (A = Wx rows), N = cells (B = X rows),
 // K = input channels. A workgroup stages a chunk of Wx rows (gate columns) in
-// LDS once and its four waves sweep the chunk for 64 cells each, B operands in
-// registers. The stores are write-bandwidth bound: every 16-cell x 64-column
+// LDS once and then loops over blocks of 256 cells (its four waves take 64
+// cells each, B operands in registers, the next block's loaded while the
+// current one is stored). The stores are write-bandwidth bound: every 16-cell x 64-column
 // output block passes through a small per-wave LDS tile so that one store
 // instruction writes four cells x 64 contiguous columns instead of sixteen
 // cells x 4 columns.
@@ -53,8 +54,8 @@ struct PK<bf16_t> {  // 16x16x32 bf16: K step ks, slot g holds k = 32 ks + 8 g +
 
 template <typename T, int KS>
 __global__ void __launch_bounds__(256)
-k_projection(int64_t n_cells, int C, int N, int nch, const T* __restrict__ X, const T* __restrict__ Wx,
-             const T* __restrict__ bias, T* __restrict__ Z) {
+k_projection(int64_t n_cells, int64_t n_blocks, int C, int N, int nch, const T* __restrict__ X,
+             const T* __restrict__ Wx, const T* __restrict__ bias, T* __restrict__ Z) {
     using K = PK<T>;
     using Op = typename K::Op;
     constexpr int RW = K::PERK * KS;  // staged k values per row
@@ -71,55 +72,63 @@ k_projection(int64_t n_cells, int C, int N, int nch, const T* __restrict__ X, co
         sW[r * P + k] = k < C ? Wx[(int64_t)(n0 + r) * C + k] : T(0);
     }
     __syncthreads();
-    const int64_t cell0 = ((int64_t)blockIdx.x * 4 + wave) * PCELLS;
-    if (cell0 >= n_cells) return;
-    Op b[4][KS];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        const int64_t cell = cell0 + 16 * t + n16;
-        const T* row = X + min(cell, n_cells - 1) * C;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) b[t][ks] = K::gload(row, K::koff(g, ks, KS), C);
-    }
     float(*so)[64 + 4] = sO[wave];
     const int ntiles = nc / 16;
-    for (int mg = 0; mg * 4 < ntiles; ++mg) {
-        const int mc = min(4, ntiles - 4 * mg);  // column tiles in this group
-        floatx4 acc[4][4];
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-#pragma unroll
-            for (int t = 0; t < 4; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-            if (m < mc) {
-                Op a[KS];
-                const T* ar = sW + ((mg * 4 + m) * 16 + n16) * P;
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) a[ks] = K::lds(ar + K::koff(g, ks, KS));
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) acc[m][t] = K::mma(a[ks], b[t][ks], acc[m][t]);
-            }
-        }
-        // lane (r, c) of the store pass writes cell 4 r' + lane/16 of the tile,
-        // columns 4 (lane % 16) .. + 3 of the group
-        const int c4 = 4 * (lane & 15);
-        const int colb = n0 + mg * 64;
-        const bool colok = c4 < 16 * mc;
-        const floatx4 bb = colok ? St<T>::ld4(bias + colb + c4) : floatx4{0.f, 0.f, 0.f, 0.f};
+    // B operands of a block's 64 cells of this wave (rows past the canvas
+    // re-read its last cell; their results are not stored)
+    Op b[4][KS];
+    auto load_b = [&](int64_t blk) {
+        const int64_t cell0 = (blk * 4 + wave) * PCELLS;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
+            const T* row = X + min(cell0 + 16 * t + n16, n_cells - 1) * C;
 #pragma unroll
-            for (int m = 0; m < 4; ++m) *reinterpret_cast<floatx4*>(&so[n16][m * 16 + 4 * g]) = acc[m][t];
-            __builtin_amdgcn_wave_barrier();
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int cl = 4 * r + (lane >> 4);
-                const floatx4 v = *reinterpret_cast<const floatx4*>(&so[cl][c4]) + bb;
-                const int64_t cell = cell0 + 16 * t + cl;
-                if (colok && cell < n_cells) K::st4(Z + cell * N + colb + c4, v);
+            for (int ks = 0; ks < KS; ++ks) b[t][ks] = K::gload(row, K::koff(g, ks, KS), C);
+        }
+    };
+    load_b(blockIdx.x);
+    for (int64_t blk = blockIdx.x; blk < n_blocks; blk += gridDim.x) {
+        const int64_t cell0 = (blk * 4 + wave) * PCELLS;
+        for (int mg = 0; mg * 4 < ntiles; ++mg) {
+            const int mc = min(4, ntiles - 4 * mg);  // column tiles in this group
+            floatx4 acc[4][4];
+    #pragma unroll
+            for (int m = 0; m < 4; ++m) {
+    #pragma unroll
+                for (int t = 0; t < 4; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+                if (m < mc) {
+                    Op a[KS];
+                    const T* ar = sW + ((mg * 4 + m) * 16 + n16) * P;
+    #pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) a[ks] = K::lds(ar + K::koff(g, ks, KS));
+    #pragma unroll
+                    for (int ks = 0; ks < KS; ++ks)
+    #pragma unroll
+                        for (int t = 0; t < 4; ++t) acc[m][t] = K::mma(a[ks], b[t][ks], acc[m][t]);
+                }
             }
-            __builtin_amdgcn_wave_barrier();
+            // lane (r, c) of the store pass writes cell 4 r' + lane/16 of the tile,
+            // columns 4 (lane % 16) .. + 3 of the group
+            // the last column group's MFMAs are issued: load the next block's operands
+            if (mg * 4 + 4 >= ntiles) load_b(min(blk + (int64_t)gridDim.x, n_blocks - 1));
+            const int c4 = 4 * (lane & 15);
+            const int colb = n0 + mg * 64;
+            const bool colok = c4 < 16 * mc;
+            const floatx4 bb = colok ? St<T>::ld4(bias + colb + c4) : floatx4{0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+            for (int t = 0; t < 4; ++t) {
+    #pragma unroll
+                for (int m = 0; m < 4; ++m) *reinterpret_cast<floatx4*>(&so[n16][m * 16 + 4 * g]) = acc[m][t];
+                __builtin_amdgcn_wave_barrier();
+    #pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int cl = 4 * r + (lane >> 4);
+                    const floatx4 v = *reinterpret_cast<const floatx4*>(&so[cl][c4]) + bb;
+                    const int64_t cell = cell0 + 16 * t + cl;
+                    if (colok && cell < n_cells) K::st4(Z + cell * N + colb + c4, v);
+                }
+                __builtin_amdgcn_wave_barrier();
+            }
         }
     }
 }
@@ -136,9 +145,19 @@ static hipError_t launch_proj(const LayerGeom& g, const T* X, const T* W, const 
     int nch = ((N + nchunks - 1) / nchunks + unit - 1) / unit * unit;
     nch = std::min(std::min(nch, cap / unit * unit), N);
     const int64_t waves = (g.n_cells + PCELLS - 1) / PCELLS;
-    const dim3 grid((unsigned)((waves + 3) / 4), (unsigned)((N + nch - 1) / nch)), block(256);
-    hipLaunchKernelGGL((k_projection<T, KS>), grid, block, (size_t)nch * P * sizeof(T), s, g.n_cells, g.c_in, N, nch,
-                       X, W, B, Z);
+    const int64_t blocks = (waves + 3) / 4;
+    const int nchunks_col = (N + nch - 1) / nch;
+    // workgroups that loop over the cell blocks: as many as fit on the CUs at
+    // once (LDS-limited, at most four per CU)
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        cus = 256;
+    const size_t lds = (size_t)nch * P * sizeof(T) + 4 * 16 * (64 + 4) * sizeof(float);
+    const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(4, 160 * 1024 / lds));
+    const int64_t want = std::max<int64_t>(1, (int64_t)per_cu * std::max(cus, 1) / nchunks_col);
+    const dim3 grid((unsigned)std::min<int64_t>(blocks, want), (unsigned)nchunks_col), block(256);
+    hipLaunchKernelGGL((k_projection<T, KS>), grid, block, (size_t)nch * P * sizeof(T), s, g.n_cells, blocks, g.c_in,
+                       N, nch, X, W, B, Z);
     return hipGetLastError();
 }
 
