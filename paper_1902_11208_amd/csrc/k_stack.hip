@@ -238,14 +238,34 @@ k_conv_bwd_dw(const float* __restrict__ y, const float* __restrict__ out, const 
     if ((int)threadIdx.x < 4 * OG) pc[M + threadIdx.x] = accb;
 }
 
-__global__ void k_sum_partials(const float* __restrict__ partial, int chunks, int m, float* __restrict__ dw,
-                               float* __restrict__ db, int mw) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= m) return;
+// Fixed-order sum of the chunk partials: a block takes 64 consecutive
+// outputs; its four thread groups sum every fourth chunk each (loads batched
+// eight at a time), and the four sums are added in a fixed order.
+__global__ void __launch_bounds__(256)
+k_sum_partials(const float* __restrict__ partial, int chunks, int m, float* __restrict__ dw,
+               float* __restrict__ db, int mw) {
+    __shared__ float ps[4][64];
+    const int t = threadIdx.x & 63, grp = threadIdx.x >> 6;
+    const int i = blockIdx.x * 64 + t;
     float s = 0.0f;
-    for (int c = 0; c < chunks; ++c) s += partial[(size_t)c * m + i];
-    if (i < mw) dw[i] = s;
-    else db[i - mw] = s;
+    if (i < m) {
+        int c = grp;
+        for (; c + 28 < chunks; c += 32) {
+            float v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = partial[(size_t)(c + 4 * k) * m + i];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) s += v[k];
+        }
+        for (; c < chunks; c += 4) s += partial[(size_t)c * m + i];
+    }
+    ps[grp][t] = s;
+    __syncthreads();
+    if (grp == 0 && i < m) {
+        const float v = ((ps[0][t] + ps[1][t]) + ps[2][t]) + ps[3][t];
+        if (i < mw) dw[i] = v;
+        else db[i - mw] = v;
+    }
 }
 
 __global__ void k_zero_f32(float* __restrict__ d, int64_t n) {
@@ -305,7 +325,7 @@ static hipError_t conv_launch(bool fwd, const ConvArgs& a, hipStream_t s) {
         hipLaunchKernelGGL((k_conv_bwd_dw<H, OG>), dim3(chunks), dim3(256), 0, s, a.y, a.out, a.dout, a.blk_off,
                            a.n, a.in_rects, a.in_w, a.out_rects, a.out_w, per, a.partial);
         const int m = 4 * OG * K + 4 * OG;
-        hipLaunchKernelGGL(k_sum_partials, dim3((m + 255) / 256), dim3(256), 0, s, a.partial, chunks, m, a.dw,
+        hipLaunchKernelGGL(k_sum_partials, dim3((m + 63) / 64), dim3(256), 0, s, a.partial, chunks, m, a.dw,
                            a.db, 4 * OG * K);
         return hipGetLastError();
     }
