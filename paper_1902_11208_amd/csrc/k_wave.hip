@@ -619,6 +619,184 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
 }
 
 // ---------------------------------------------------------------------------
+// Forward for wide layers (bf16, H = 128: four quads per wave, where the
+// staged kernel's LDS buffers do not fit and its registers spill).
+//
+// Lane 16q + n of wave w owns the four consecutive hidden units
+// u0 = 16w + 4q .. u0 + 3 of cell n of a tile. The rows of own MFMA tile k
+// are ordered (unit offset jj, gate) -> U row gate*H + 16w + 4jj + k, so the
+// lane ends with the four sigmoid gates of unit u0 + k in tile k; the rows of
+// the candidate tile are the wave's sixteen units in order, so its register
+// k is the candidate of unit u0 + k. No value crosses lanes: the cell update
+// follows each tile's MFMAs without a barrier, both neighbours' cell states
+// come from LDS, and pre-activations, gates, outputs and cell states move as
+// 8- and 16-byte vectors. Tiles of a diagonal run one after another (the
+// accumulators of one tile only), their pre-activations loaded two tiles
+// ahead; one barrier per diagonal publishes h and c.
+// ---------------------------------------------------------------------------
+template <int H, typename T>
+struct FwdBig {
+    static constexpr bool on = sizeof(T) == 2 && Geo<H, T>::NW == 8 && Geo<H, T>::WQ == 4;
+};
+
+template <int H, int NT, typename T>
+__device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) {
+    using O = Ops<T>;
+    using Op = typename O::Op;
+    constexpr int G = 5 * H, KRUN = H / 2, NSTEP = KRUN / O::PER;
+    constexpr int ROWS = NT * 16 + 1;            // row 0: zero row above local row 0
+    constexpr int HP = H + 16 / (int)sizeof(T);  // padded LDS row pitches
+    constexpr int CP = H + 4;
+    __shared__ __attribute__((aligned(16))) T hbuf[2][ROWS][HP];
+    __shared__ __attribute__((aligned(16))) float cbuf[2][ROWS][CP];
+
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int q = lane >> 4, n16 = lane & 15;
+    const int u0 = 16 * w + 4 * q;
+    const int d = unit & 3;
+    const RectD R = reinterpret_cast<const RectD*>(a.rects)[unit >> 2];
+    const T* __restrict__ U = static_cast<const T*>(a.u) + (int64_t)d * G * 2 * H;
+    T* __restrict__ Z = static_cast<T*>(a.z);
+    T* __restrict__ Y = static_cast<T*>(a.y);
+    float* __restrict__ Cs = a.c;
+    const int steps = R.h + R.w - 1;
+    const int sb = a.s0, se = min(a.s1, steps);
+    if (sb >= se) return;
+
+    for (int i = threadIdx.x; i < 2 * ROWS * HP; i += blockDim.x) (&hbuf[0][0][0])[i] = T(0);
+    for (int i = threadIdx.x; i < 2 * ROWS * CP; i += blockDim.x) (&cbuf[0][0][0])[i] = 0.0f;
+    if (sb > 0) {  // state of diagonal sb - 1 from the previous launch's outputs
+        const int pb = (sb & 1) ^ 1;
+        for (int i = threadIdx.x; i < NT * 16 * H; i += blockDim.x) {
+            const int yy = i / H, j = i - yy * H, xx = sb - 1 - yy;
+            if (yy < R.h && xx >= 0 && xx < R.w) {
+                const int64_t p = canvas_index(R, d, yy, xx, a.canvas_w);
+                hbuf[pb][yy + 1][j] = Y[p * (4 * H) + d * H + j];
+                cbuf[pb][yy + 1][j] = Cs[p * (4 * H) + d * H + j];
+            }
+        }
+    }
+
+    Op Aown[4][NSTEP], Ag[NSTEP];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int row = (n16 & 3) * H + 16 * w + 4 * (n16 >> 2) + k;
+        load_slot<T, NSTEP>(U + (int64_t)row * 2 * H + q * KRUN, 1, true, Aown[k]);
+    }
+    load_slot<T, NSTEP>(U + (int64_t)(4 * H + 16 * w + n16) * 2 * H + q * KRUN, 1, true, Ag);
+    __builtin_amdgcn_s_waitcnt(0);
+
+    const DiagMap M(R, d, a.canvas_w);
+    const uint8_t* mrow = a.mask + M.c0;
+    // the lane's elements at diagonal index idx = 0 (cell = c0 + idx)
+    T* const zb = Z + M.c0 * (4 * G) + d * G + u0;
+    T* const yb = Y + M.c0 * (4 * H) + d * H + u0;
+    float* const cb = Cs + M.c0 * (4 * H) + d * H + u0;
+
+    // Pre-activations (5 gates x 4 units) and mask byte of the lane's cell of
+    // tile nt of diagonal s; past the last diagonal, or for rows outside the
+    // diagonal, a valid cell of the rectangle is read instead (fixed number of
+    // loads on every path).
+    auto load = [&](int s, int nt, uint2 (&zr)[5], uint32_t& m) {
+        const int sc = min(s, se - 1);
+        const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
+        const int idx = M.sx * sc + min(max(16 * nt + n16, ylo), yhi) * M.ky;
+        const T* zp = zb + (int64_t)idx * (4 * G);
+#pragma unroll
+        for (int t = 0; t < 5; ++t) zr[t] = *reinterpret_cast<const uint2*>(zp + t * H);
+        m = mrow[idx];
+    };
+    // Next tile of the walk: the next active tile of the diagonal, else the
+    // first active tile of the next one.
+    auto advance = [&](int& s, int& nt) {
+        const int yhi = min(R.h - 1, s);
+        if (16 * (nt + 1) <= yhi) {
+            ++nt;
+        } else {
+            ++s;
+            nt = max(0, s - R.w + 1) >> 4;
+        }
+    };
+    auto tile = [&](int s, int nt, const uint2 (&zr)[5], uint32_t m) {
+        const int cur = s & 1, prv = cur ^ 1;
+        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+        const int yy = 16 * nt + n16;
+        const T* brow = (q < 2) ? &hbuf[prv][yy + 1][q * KRUN] : &hbuf[prv][yy][(q - 2) * KRUN];
+        floatx4 acc[4], ag = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc[k] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < NSTEP; ++ks) {
+            const Op b = O::lds(brow + ks * O::PER);
+            ag = O::mma(Ag[ks], b, ag);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) acc[k] = O::mma(Aown[k][ks], b, acc[k]);
+        }
+        const float4 cl = *reinterpret_cast<const float4*>(&cbuf[prv][yy + 1][u0]);
+        const float4 ct = *reinterpret_cast<const float4*>(&cbuf[prv][yy][u0]);
+        const float clv[4] = {cl.x, cl.y, cl.z, cl.w}, ctv[4] = {ct.x, ct.y, ct.z, ct.w};
+        const bool inr = yy >= ylo && yy <= yhi;
+        const bool live = inr && m != 0;
+        float gv[5][4], hv[4], cv[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            float zv[5];
+#pragma unroll
+            for (int t = 0; t < 5; ++t) {
+                const uint32_t wd = (k < 2) ? zr[t].x : zr[t].y;
+                zv[t] = __uint_as_float((k & 1) ? (wd & 0xffff0000u) : (wd << 16));
+            }
+            gv[0][k] = sigm_fast(acc[k][0] + zv[0]);
+            gv[1][k] = sigm_fast(acc[k][1] + zv[1]);
+            gv[2][k] = sigm_fast(acc[k][2] + zv[2]);
+            gv[3][k] = sigm_fast(acc[k][3] + zv[3]);
+            gv[4][k] = tanh_fast(ag[k] + zv[4]);
+            const float cn = gv[0][k] * gv[4][k] + gv[1][k] * clv[k] + gv[2][k] * ctv[k];
+            const float hn = gv[3][k] * tanh_fast(cn);
+            cv[k] = live ? cn : 0.0f;
+            hv[k] = live ? hn : 0.0f;
+        }
+        auto pack = [](const float (&v)[4]) {
+            return make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
+                              (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+        };
+        *reinterpret_cast<uint2*>(&hbuf[cur][yy + 1][u0]) = pack(hv);
+        *reinterpret_cast<float4*>(&cbuf[cur][yy + 1][u0]) = make_float4(cv[0], cv[1], cv[2], cv[3]);
+        const int64_t idx = (int64_t)(M.sx * s + yy * M.ky);
+        if (live) {
+            T* zp = zb + idx * (4 * G);
+#pragma unroll
+            for (int t = 0; t < 5; ++t) *reinterpret_cast<uint2*>(zp + t * H) = pack(gv[t]);
+            *reinterpret_cast<uint2*>(yb + idx * (4 * H)) = pack(hv);
+        }
+        if (inr) *reinterpret_cast<float4*>(cb + idx * (4 * H)) = make_float4(cv[0], cv[1], cv[2], cv[3]);
+        if (16 * nt + 16 > yhi) lds_barrier();  // last tile of the diagonal
+    };
+
+    lds_barrier();
+    uint2 z0[5], z1[5];
+    uint32_t m0, m1;
+    int s = sb, nt = max(0, sb - R.w + 1) >> 4;
+    int ls = s, lnt = nt;
+    load(ls, lnt, z0, m0);
+    advance(ls, lnt);
+    load(ls, lnt, z1, m1);
+    advance(ls, lnt);
+    for (;;) {
+        tile(s, nt, z0, m0);
+        load(ls, lnt, z0, m0);
+        advance(ls, lnt);
+        advance(s, nt);
+        if (s >= se) break;
+        tile(s, nt, z1, m1);
+        load(ls, lnt, z1, m1);
+        advance(ls, lnt);
+        advance(s, nt);
+        if (s >= se) break;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Backward (reverse anti-diagonals). With successors S (right, same row, next
 // diagonal) and E (below, row + 1, next diagonal):
 //   dh = dY + (U^T da_S)[0:H] + (U^T da_E)[H:2H]
@@ -941,7 +1119,8 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
 template <int H, int NT, typename T, bool FWD, bool QUEUE>
 __device__ __forceinline__ void run_units(const WaveArgs& a) {
     if constexpr (!QUEUE) {
-        if (FWD) wave_fwd_unit<H, NT, T, 1>(a, a.units[blockIdx.x]);
+        if constexpr (FWD && FwdBig<H, T>::on) wave_fwd_big<H, NT, T>(a, a.units[blockIdx.x]);
+        else if (FWD) wave_fwd_unit<H, NT, T, 1>(a, a.units[blockIdx.x]);
         else wave_bwd_unit<H, NT, T>(a, a.units[blockIdx.x]);
         return;
     }
@@ -952,7 +1131,8 @@ __device__ __forceinline__ void run_units(const WaveArgs& a) {
         lds_barrier();
         const int k = slot;
         if (k >= a.n_units) break;
-        if (FWD) wave_fwd_unit<H, NT, T, 2>(a, a.units[k]);
+        if constexpr (FWD && FwdBig<H, T>::on) wave_fwd_big<H, NT, T>(a, a.units[k]);
+        else if (FWD) wave_fwd_unit<H, NT, T, 2>(a, a.units[k]);
         else wave_bwd_unit<H, NT, T>(a, a.units[k]);
     }
     // Count the workgroup out; the last one leaves both counters at zero for

@@ -286,7 +286,7 @@ def test_exploding_state_regime():
         assert e <= 1e-3
 
 
-@pytest.mark.parametrize("case", ["H16_words", "H32_tall", "bf16_H64"])
+@pytest.mark.parametrize("case", ["H16_words", "H32_tall", "bf16_H64", "bf16_H128"])
 def test_stepwise_forward_matches_persistent(case):
     """One launch per diagonal, replayed from a HIP graph, gives the persistent
     kernel's outputs bit for bit (twice, to cover the graph's replay)."""
@@ -298,8 +298,10 @@ def test_stepwise_forward_matches_persistent(case):
         wl = configs.workload(2)
     elif case == "H32_tall":
         wl = configs.custom_workload(61, [40, 7, 33], [50, 64, 9], 128, 8, 32)
-    else:
+    elif case == "bf16_H64":
         wl = configs.custom_workload(62, [16, 48, 5], [70, 20, 33], 96, 16, 64, dtype="bf16")
+    else:
+        wl = configs.custom_workload(63, [48, 10, 20], [30, 60, 17], 128, 64, 128, dtype="bf16")
     print(f"case: stepwise forward {case}", flush=True)
     units, ch, mask = api.pack_layout(wl.heights, wl.widths, wl.canvas_w)
     x = api.pack_data([gpu_run.to_dev(e, wl.dtype) for e in wl.examples()], units, ch, wl.canvas_w)
