@@ -1108,6 +1108,170 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
 }
 
 // ---------------------------------------------------------------------------
+// Backward for wide layers (bf16, H = 128), with the forward's lane mapping:
+// lane 16q + n of wave w owns units u0 = 16w + 4q .. u0 + 3 of cell n of a
+// tile. The wave computes the two U^T da output tiles of its own units, the
+// left-predecessor part (rows u0 + r) and the top-predecessor part
+// (rows H + u0 + r), so the left part lands in the lane that needs it on the
+// next diagonal (the cell's left predecessor is on the same row) and stays in
+// registers; the top part and dc f_T go one row up through LDS, within the
+// wave. Only the gate gradients cross waves (all of them are the reduction
+// operand), so a diagonal runs as segments [A(t0)] [B(t0) A(t1)] ... [B(t1)]
+// with a barrier after each: A = gate-gradient update of a tile, B = its
+// U^T da products on MFMA.
+// ---------------------------------------------------------------------------
+template <int H, typename T>
+struct BwdBig {
+    static constexpr bool on = sizeof(T) == 2 && Geo<H, T>::NW == 8 && Geo<H, T>::WQ == 4 && 2 * H == 256;
+};
+
+template <int H, int NT, typename T>
+__device__ __forceinline__ void wave_bwd_big(const WaveArgs& a, const int unit) {
+    using O = Ops<T>;
+    using Op = typename O::Op;
+    constexpr int G = 5 * H, KRUNB = G / 4, NSTEPB = KRUNB / O::PER;
+    constexpr int GP = G + 16 / (int)sizeof(T);  // padded LDS row pitches
+    constexpr int CP = H + 4;
+    __shared__ __attribute__((aligned(16))) T dabuf[NT * 16][GP];
+    // per cell row: the top-predecessor part of U^T da, and dc f_T (row NT*16 stays zero)
+    __shared__ __attribute__((aligned(16))) float gtop[NT * 16 + 1][CP];
+    __shared__ __attribute__((aligned(16))) float dct[NT * 16 + 1][CP];
+
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int q = lane >> 4, n16 = lane & 15;
+    const int u0 = 16 * w + 4 * q;
+    const int d = unit & 3;
+    const RectD R = reinterpret_cast<const RectD*>(a.rects)[unit >> 2];
+    const T* __restrict__ U = static_cast<const T*>(a.u) + (int64_t)d * G * 2 * H;
+    T* __restrict__ Z = static_cast<T*>(a.z);
+    const T* __restrict__ DY = static_cast<const T*>(a.dy);
+    const float* __restrict__ Cs = a.c;
+    const int steps = R.h + R.w - 1;
+
+    for (int i = threadIdx.x; i < NT * 16 * GP; i += blockDim.x) (&dabuf[0][0])[i] = T(0);
+    for (int i = threadIdx.x; i < (NT * 16 + 1) * CP; i += blockDim.x) {
+        (&gtop[0][0])[i] = 0.0f;
+        (&dct[0][0])[i] = 0.0f;
+    }
+    // A operands: U^T rows k = u-part + 16w + n16 (column k of U); slot q
+    // holds gate rows q*KRUNB + 8 ks + e.
+    Op A[2][NSTEPB];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+        load_slot<T, NSTEPB>(U + (int64_t)(q * KRUNB) * 2 * H + tt * H + 16 * w + n16, 2 * H, true, A[tt]);
+    floatx4 gl[NT], dcl[NT];  // left-successor parts of dh and dc, per tile row
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) gl[nt] = dcl[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    __builtin_amdgcn_s_waitcnt(0);
+
+    const DiagMap M(R, d, a.canvas_w);
+    const uint8_t* mrow = a.mask + M.c0;
+    T* const zb = Z + M.c0 * (4 * G) + d * G + u0;
+    const T* const dyb = DY + M.c0 * (4 * H) + d * H + u0;
+    const float* const cb = Cs + M.c0 * (4 * H) + d * H + u0;
+
+    struct In {
+        uint2 g[5], dy;
+        float4 c, cl, ct;
+        uint32_t m;
+    };
+    // Inputs of the lane's cell of tile nt of diagonal s (rows outside the
+    // diagonal read its nearest cell; a missing predecessor reads the cell).
+    auto load = [&](int s, int nt, In& in) {
+        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+        const int yc = min(max(16 * nt + n16, ylo), yhi), xc = s - yc;
+        const int idx = M.sx * s + yc * M.ky;
+        const int il = xc > 0 ? idx - M.sx : idx;
+        const int it = yc > 0 ? idx - M.sx - M.ky : idx;
+        const T* zp = zb + (int64_t)idx * (4 * G);
+#pragma unroll
+        for (int t = 0; t < 5; ++t) in.g[t] = *reinterpret_cast<const uint2*>(zp + t * H);
+        in.dy = *reinterpret_cast<const uint2*>(dyb + (int64_t)idx * (4 * H));
+        in.c = *reinterpret_cast<const float4*>(cb + (int64_t)idx * (4 * H));
+        in.cl = *reinterpret_cast<const float4*>(cb + (int64_t)il * (4 * H));
+        in.ct = *reinterpret_cast<const float4*>(cb + (int64_t)it * (4 * H));
+        in.m = mrow[idx];
+    };
+    auto bf = [](const uint2& v, int k) {
+        const uint32_t wd = (k < 2) ? v.x : v.y;
+        return __uint_as_float((k & 1) ? (wd & 0xffff0000u) : (wd << 16));
+    };
+    auto pack = [](const float (&v)[4]) {
+        return make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
+                          (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+    };
+    // Phase A of tile nt: gate gradients of the lane's four units.
+    auto phase_a = [&](int s, int nt, const In& in) {
+        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+        const int yy = 16 * nt + n16;
+        const bool inr = yy >= ylo && yy <= yhi;
+        const bool live = inr && in.m != 0;
+        const bool hasl = s - yy > 0, hast = yy > 0;
+        const float4 gt4 = *reinterpret_cast<const float4*>(&gtop[yy + 1][u0]);
+        const float4 dt4 = *reinterpret_cast<const float4*>(&dct[yy + 1][u0]);
+        const float gtv[4] = {gt4.x, gt4.y, gt4.z, gt4.w}, dtv[4] = {dt4.x, dt4.y, dt4.z, dt4.w};
+        const float cv4[4] = {in.c.x, in.c.y, in.c.z, in.c.w};
+        const float cl4[4] = {in.cl.x, in.cl.y, in.cl.z, in.cl.w};
+        const float ct4[4] = {in.ct.x, in.ct.y, in.ct.z, in.ct.w};
+        float da[5][4], ndl[4], ndt[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const float gi = bf(in.g[0], k), gfl = bf(in.g[1], k), gft = bf(in.g[2], k), go = bf(in.g[3], k),
+                        gg = bf(in.g[4], k);
+            const float cL = hasl ? cl4[k] : 0.0f, cT = hast ? ct4[k] : 0.0f;
+            const float dh = bf(in.dy, k) + gl[nt][k] + gtv[k];
+            const float tc = tanh_fast(cv4[k]);
+            const float dc = dcl[nt][k] + dtv[k] + dh * go * (1.0f - tc * tc);
+            da[0][k] = live ? dc * gg * gi * (1.0f - gi) : 0.0f;
+            da[1][k] = live ? dc * cL * gfl * (1.0f - gfl) : 0.0f;
+            da[2][k] = live ? dc * cT * gft * (1.0f - gft) : 0.0f;
+            da[3][k] = live ? dh * tc * go * (1.0f - go) : 0.0f;
+            da[4][k] = live ? dc * gi * (1.0f - gg * gg) : 0.0f;
+            ndl[k] = live ? dc * gfl : 0.0f;
+            ndt[k] = live ? dc * gft : 0.0f;
+        }
+        dcl[nt] = floatx4{ndl[0], ndl[1], ndl[2], ndl[3]};
+        *reinterpret_cast<float4*>(&dct[yy][u0]) = make_float4(ndt[0], ndt[1], ndt[2], ndt[3]);
+#pragma unroll
+        for (int t = 0; t < 5; ++t) *reinterpret_cast<uint2*>(&dabuf[yy][t * H + u0]) = pack(da[t]);
+        if (inr) {
+            T* zp = zb + (int64_t)(M.sx * s + yy * M.ky) * (4 * G);
+#pragma unroll
+            for (int t = 0; t < 5; ++t) *reinterpret_cast<uint2*>(zp + t * H) = pack(da[t]);
+        }
+    };
+    // Phase B of tile nt: U^T da of its cells for the wave's units.
+    auto phase_b = [&](int nt) {
+        const T* brow = &dabuf[16 * nt + n16][q * KRUNB];
+        floatx4 al = floatx4{0.f, 0.f, 0.f, 0.f}, at = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < NSTEPB; ++ks) {
+            const Op b = O::lds(brow + ks * O::PER);
+            al = O::mma(A[0][ks], b, al);
+            at = O::mma(A[1][ks], b, at);
+        }
+        gl[nt] = al;
+        *reinterpret_cast<float4*>(&gtop[16 * nt + n16][u0]) = make_float4(at[0], at[1], at[2], at[3]);
+    };
+
+    lds_barrier();
+    for (int s = steps - 1; s >= 0; --s) {
+        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+        const int t0 = ylo >> 4, t1 = yhi >> 4;
+#pragma unroll
+        for (int k = 0; k <= NT; ++k) {
+            const bool pa = k < NT && k >= t0 && k <= t1;      // A(k) in this segment
+            const bool pb = k >= 1 && k - 1 >= t0 && k - 1 <= t1;  // B(k - 1) in this segment
+            In in;
+            if (pa) load(s, k, in);
+            if (pb) phase_b(k - 1);
+            if (pa) phase_a(s, k, in);
+            if (pa || pb) lds_barrier();
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Kernels. With a queue, a fixed number of workgroups per CU take units in
 // launch order (longest first) from a counter until none is left, so a long
 // unit shares its CU with fewer others than when every unit has its own
@@ -1121,6 +1285,7 @@ __device__ __forceinline__ void run_units(const WaveArgs& a) {
     if constexpr (!QUEUE) {
         if constexpr (FWD && FwdBig<H, T>::on) wave_fwd_big<H, NT, T>(a, a.units[blockIdx.x]);
         else if (FWD) wave_fwd_unit<H, NT, T, 1>(a, a.units[blockIdx.x]);
+        else if constexpr (BwdBig<H, T>::on) wave_bwd_big<H, NT, T>(a, a.units[blockIdx.x]);
         else wave_bwd_unit<H, NT, T>(a, a.units[blockIdx.x]);
         return;
     }
@@ -1133,6 +1298,7 @@ __device__ __forceinline__ void run_units(const WaveArgs& a) {
         if (k >= a.n_units) break;
         if constexpr (FWD && FwdBig<H, T>::on) wave_fwd_big<H, NT, T>(a, a.units[k]);
         else if (FWD) wave_fwd_unit<H, NT, T, 2>(a, a.units[k]);
+        else if constexpr (BwdBig<H, T>::on) wave_bwd_big<H, NT, T>(a, a.units[k]);
         else wave_bwd_unit<H, NT, T>(a, a.units[k]);
     }
     // Count the workgroup out; the last one leaves both counters at zero for
@@ -1165,6 +1331,9 @@ k_wave_bwd(WaveArgs a) {
 // LDS of the backward kernel; shapes beyond the 160 KB of a CU are not built.
 template <int H, int NT, typename T>
 constexpr bool bwd_fits() {
+    if constexpr (BwdBig<H, T>::on)
+        return (size_t)NT * 16 * (5 * H + 16 / sizeof(T)) * sizeof(T) + (size_t)2 * (NT * 16 + 1) * (H + 4) * 4 <=
+               160 * 1024;
     return bwd_lds_base<H, NT, T>() + (bwd_stage<H, NT, T>() ? bwd_lds_stage<H, NT, T>() : 0) <= 160 * 1024;
 }
 

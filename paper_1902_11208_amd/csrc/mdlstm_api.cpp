@@ -189,8 +189,6 @@ mdlstm_status prepare(const mdlstm_layer_desc* desc, int32_t ch, int32_t cw, con
     int32_t max_h = 0;
     st = check_rects(n_rects, rects, ch, cw, &max_h);
     if (st != MDLSTM_OK) return st;
-    if (desc->dtype == MDLSTM_BF16 && desc->hidden == 128 && max_h > 48)
-        return fail(MDLSTM_ERR_UNSUPPORTED, "bf16 hidden 128 supports rectangles up to 48 high, got %d", max_h);
     const int64_t cells = (int64_t)ch * cw;
     if (cells > 0 && (!d_x || !d_mask)) return fail(MDLSTM_ERR_INVALID_ARG, "x or mask is NULL");
     if (!d_wx || !d_u || !d_b) return fail(MDLSTM_ERR_INVALID_ARG, "a weight pointer is NULL");

@@ -77,6 +77,7 @@ SMALL = [
     ("bf16_H32", [20, 12], [30, 18], 64, 16, 32, "bf16"),
     ("bf16_H64", [33, 12], [30, 41], 80, 32, 64, "bf16"),
     ("bf16_H128", [48, 10], [30, 60], 128, 64, 128, "bf16"),
+    ("bf16_H128_four_tiles", [64, 17, 3], [21, 40, 9], 96, 8, 128, "bf16"),
 ]
 
 
