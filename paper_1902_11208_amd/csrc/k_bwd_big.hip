@@ -157,10 +157,11 @@ k_dx_big(int64_t n_cells, int C, int N, const T* __restrict__ dZ, const T* __res
 }
 
 // --- dW --------------------------------------------------------------------------
-constexpr int BW_KC = 32;    // cells per step
-constexpr int BW_RB = 128;   // gate rows per workgroup
-constexpr int BW_CB = 128;   // columns per workgroup
-constexpr int BW_TARGET = 512;  // workgroups aimed for
+constexpr int BW_KC = 32;         // cells per step
+constexpr int BW_RB = 320;        // gate rows per workgroup
+constexpr int BW_CB = 160;        // columns per workgroup
+constexpr int BW_THREADS = 512;   // 8 waves: 4 along the rows x 2 along the columns, 80 x 80 each
+constexpr int BW_TARGET = 256;    // workgroups aimed for (one per CU)
 
 struct BigDw {
     int G, NB, rblocks, cblocks, chunks, PP;
@@ -185,135 +186,218 @@ static BigDw big_dw(const LayerGeom& g) {
     return q;
 }
 
-// Workgroup (row block, column block, direction) x chunk. LDS holds the
-// step's operands transposed: sA[row][cell], sB[col][cell] (pitch KC + 8
-// elements). Wave w owns rows 32 w .. 32 w + 31 (two M tiles) and all eight
-// N tiles of the column block. Thread t stages cell t % KC: the 16-byte
-// chunks (t / KC) + 8 j of the cell's dZ rows and of its column operand.
-template <typename T>
-__global__ void __launch_bounds__(256)
+// Workgroup = (row block, column block) of one direction and one chunk of
+// cells. The blocks of a (direction, chunk) read the same dZ rows and column
+// operands, so they are placed on one XCD (workgroups are dealt to the XCDs
+// in turn) to share its L2. Each step stages 32 cells of dZ and of the column
+// operand in LDS transposed (cells contiguous; a thread writes the values of
+// two adjacent cells together), so that an MFMA operand is one 16-byte LDS
+// read; the loads of the next PD steps are in flight meanwhile. The bias
+// gradient is summed from the staged dZ values in registers.
+template <typename T, int PD>
+__global__ void __launch_bounds__(BW_THREADS)
 k_dw_big(int64_t n_cells, int canvas_w, int C, int H, BigDw q, const T* __restrict__ dZ, const T* __restrict__ X,
          const T* __restrict__ Y, const uint8_t* __restrict__ flags, float* __restrict__ part) {
     using B = BigT<T>;
     constexpr int E = B::E;
     constexpr int KC = BW_KC, PIT = KC + 8;
-    constexpr int CPC = BW_RB / E;            // 16-byte chunks per cell row of a block
-    constexpr int NJ = CPC / 8;               // chunks per thread (8 threads per cell)
+    constexpr int CA = BW_RB / E, CBK = BW_CB / E;  // 16-byte chunks per cell: dZ rows, columns
+    constexpr int NP = KC / 2;                      // cell pairs per step
+    constexpr int NITEM = (CA + CBK) * NP;          // staging items (chunk, cell pair)
+    constexpr int NPASS = (NITEM + BW_THREADS - 1) / BW_THREADS;
+    static_assert(BW_THREADS % NP == 0, "a thread keeps its cell pair in every pass");
     __shared__ __attribute__((aligned(16))) T sA[BW_RB][PIT];
     __shared__ __attribute__((aligned(16))) T sB[BW_CB][PIT];
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int g = lane >> 4, i16 = lane & 15;
-    const int rb = blockIdx.x % q.rblocks, cb = (blockIdx.x / q.rblocks) % q.cblocks, d = blockIdx.x / (q.rblocks * q.cblocks);
-    const int chunk = blockIdx.y;
+    const int wr = wave >> 1, wc = wave & 1;
+    const int M = q.rblocks * q.cblocks, L = blockIdx.x;
+    int gi, mem;
+    if ((4 * q.chunks) % 8 == 0) {
+        const int slot = L >> 3;
+        gi = (slot / M) * 8 + (L & 7);
+        mem = slot % M;
+    } else {
+        gi = L / M;
+        mem = L % M;
+    }
+    const int rb = mem % q.rblocks, cb = mem / q.rblocks, d = gi & 3, chunk = gi >> 2;
     const int G = q.G, N = 20 * H;
     const int r0 = rb * BW_RB, c0 = cb * BW_CB;
     const int64_t k_begin = (int64_t)chunk * q.chunk_cells;
     const int64_t k_end = min(n_cells, k_begin + q.chunk_cells);
-    const int lstep = (d & 1) ? 1 : -1;                // left predecessor: cell + lstep
+    const int lstep = (d & 1) ? 1 : -1;                              // left predecessor: cell + lstep
     const int64_t tstep = (d & 2) ? canvas_w : -(int64_t)canvas_w;  // top predecessor
     const uint8_t lbit = (d & 1) ? 4 : 2, tbit = (d & 2) ? 16 : 8;
-
-    const int cs = tid % KC, cq = tid / KC;  // staging: cell slot, chunk phase
-    // source of column chunk k (k = cq + 8 j): 0 X, 1 left, 2 top, 3 none; element offset in its row
-    int ksrc[NJ], koff[NJ];
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-        const int col = c0 + E * (cq + 8 * j);
-        if (col < C) { ksrc[j] = 0; koff[j] = col; }
-        else if (col < C + H) { ksrc[j] = 1; koff[j] = d * H + col - C; }
-        else if (col < C + 2 * H) { ksrc[j] = 2; koff[j] = d * H + col - C - H; }
-        else { ksrc[j] = 3; koff[j] = 0; }
-    }
     const int rlim = min(BW_RB, G - r0);  // rows of this block inside the direction
-    u32x4 va[NJ], vb[NJ];
-    uint32_t vf;
-    auto issue = [&](int64_t kb) {
-        const int64_t p = kb + cs;
-        const bool in = p < k_end;
-        const int64_t pc = in ? p : k_end - 1;
-        vf = in ? flags[pc] : 0u;
-        const int64_t pl = min(max(pc + lstep, (int64_t)0), n_cells - 1);
-        const int64_t pt = min(max(pc + tstep, (int64_t)0), n_cells - 1);
+    const int p2 = 2 * (tid % NP);        // first cell of the thread's pair
+
+    // Items of the thread, pass by pass: source 0 dZ, 1 X, 2 left Y, 3 top Y,
+    // 4 zero columns, 5 idle; element offset in the source row; LDS row.
+    int isrc[NPASS], ioff[NPASS], irow[NPASS];
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int rr = E * (cq + 8 * j);
-            va[j] = *reinterpret_cast<const u32x4*>(dZ + pc * N + d * G + r0 + min(rr, max(rlim - E, 0)));
-            const T* src = ksrc[j] == 0 ? X + pc * C : (ksrc[j] == 1 ? Y + pl * (4 * H) : Y + pt * (4 * H));
-            vb[j] = *reinterpret_cast<const u32x4*>(src + koff[j]);
+    for (int ps = 0; ps < NPASS; ++ps) {
+        const int i = ps * BW_THREADS + tid;
+        if (i < CA * NP) {
+            const int rr = E * (i / NP);
+            isrc[ps] = 0;
+            ioff[ps] = d * G + r0 + min(rr, max(rlim - E, 0));
+            irow[ps] = rr;
+        } else if (i < NITEM) {
+            const int kk = E * ((i - CA * NP) / NP), col = c0 + kk;
+            irow[ps] = kk;
+            if (col < C) { isrc[ps] = 1; ioff[ps] = col; }
+            else if (col < C + H) { isrc[ps] = 2; ioff[ps] = d * H + col - C; }
+            else if (col < C + 2 * H) { isrc[ps] = 3; ioff[ps] = d * H + col - C - H; }
+            else { isrc[ps] = 4; ioff[ps] = 0; }
+        } else {
+            isrc[ps] = 5;
+            ioff[ps] = 0;
+            irow[ps] = 0;
         }
+    }
+    u32x4 va[PD][NPASS][2];
+    uint32_t vf[PD][2];
+    // Loads of the step at cell kb into register set k: the pair's flags and,
+    // per pass, the item's 16-byte chunk of both cells (cells past the
+    // chunk's end read its last cell and get flags 0).
+    auto issue = [&](int64_t kb, int k) {
+        int64_t pc[2], pl[2], pt[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int64_t p = kb + p2 + c;
+            const bool in = p < k_end;
+            pc[c] = in ? p : k_end - 1;
+            vf[k][c] = in ? flags[pc[c]] : 0u;
+            pl[c] = min(max(pc[c] + lstep, (int64_t)0), n_cells - 1);
+            pt[c] = min(max(pc[c] + tstep, (int64_t)0), n_cells - 1);
+        }
+#pragma unroll
+        for (int ps = 0; ps < NPASS; ++ps)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const T* src = isrc[ps] == 0   ? dZ + pc[c] * N
+                               : isrc[ps] == 2 ? Y + pl[c] * (4 * H)
+                               : isrc[ps] == 3 ? Y + pt[c] * (4 * H)
+                                               : X + pc[c] * C;
+                va[k][ps][c] = *reinterpret_cast<const u32x4*>(src + ioff[ps]);
+            }
     };
-    auto commit = [&]() {
-        const bool v = vf & 1, vl = vf & lbit, vt = vf & tbit;
+    // bias partial sums of the thread's dZ items (column block 0 only)
+    float bsum[NPASS][E];
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int rr = E * (cq + 8 * j);
-            const bool oka = v && rr < rlim;
-            const bool okb = v && (ksrc[j] == 0 || (ksrc[j] == 1 && vl) || (ksrc[j] == 2 && vt));
-            const u32x4 a = oka ? va[j] : zero4();
-            const u32x4 b = okb ? vb[j] : zero4();
-            const T* ae = reinterpret_cast<const T*>(&a);
-            const T* be = reinterpret_cast<const T*>(&b);
+    for (int ps = 0; ps < NPASS; ++ps)
 #pragma unroll
-            for (int e = 0; e < E; ++e) {
-                sA[rr + e][cs] = ae[e];
-                sB[rr + e][cs] = be[e];
+        for (int e = 0; e < E; ++e) bsum[ps][e] = 0.0f;
+    const bool do_bias = cb == 0;
+    auto commit = [&](int k) {
+        bool ok[NPASS][2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const uint32_t f = vf[k][c];
+            const bool v = f & 1, vl = f & lbit, vt = f & tbit;
+#pragma unroll
+            for (int ps = 0; ps < NPASS; ++ps)
+                ok[ps][c] = v && ((isrc[ps] == 0 && irow[ps] < rlim) || isrc[ps] == 1 || (isrc[ps] == 2 && vl) ||
+                                  (isrc[ps] == 3 && vt));
+        }
+#pragma unroll
+        for (int ps = 0; ps < NPASS; ++ps) {
+            if (isrc[ps] == 5) continue;
+            const u32x4 a = ok[ps][0] ? va[k][ps][0] : zero4();
+            const u32x4 b = ok[ps][1] ? va[k][ps][1] : zero4();
+            T* dst = isrc[ps] == 0 ? &sA[irow[ps]][p2] : &sB[irow[ps]][p2];
+            if constexpr (std::is_same<T, float>::value) {
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    *reinterpret_cast<uint2*>(dst + e * PIT) = make_uint2(a[e], b[e]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const uint32_t lo = (e & 1) ? a[e >> 1] >> 16 : a[e >> 1] & 0xffffu;
+                    const uint32_t hi = (e & 1) ? b[e >> 1] & 0xffff0000u : b[e >> 1] << 16;
+                    *reinterpret_cast<uint32_t*>(dst + e * PIT) = lo | hi;
+                }
+            }
+            if (do_bias && isrc[ps] == 0) {
+                const T* ae = reinterpret_cast<const T*>(&a);
+                const T* be = reinterpret_cast<const T*>(&b);
+#pragma unroll
+                for (int e = 0; e < E; ++e) bsum[ps][e] += St<T>::ld1(ae + e) + St<T>::ld1(be + e);
             }
         }
     };
 
-    floatx4 acc[2][8];
+    floatx4 acc[5][5];
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < 5; ++m)
 #pragma unroll
-        for (int n = 0; n < 8; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
-    // bias (column block 0 only): thread t sums row t / 2, cells of half t % 2
-    float bsum = 0.0f;
-    const bool do_bias = cb == 0;
+        for (int n = 0; n < 5; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    if (k_begin < k_end) issue(k_begin);
-    for (int64_t kb = k_begin; kb < k_end; kb += KC) {
-        commit();
+    auto step = [&](int64_t kb, int k) {
+        commit(k);
         lds_barrier();
-        issue(kb + KC);  // past the chunk's end the loads re-read its last cell (flags 0)
-        if (do_bias) {
-            const int row = tid >> 1, h = tid & 1;
-#pragma unroll 8
-            for (int c = 0; c < KC / 2; ++c) bsum += St<T>::ld1(&sA[row][h * (KC / 2) + c]);
-        }
-        // MFMA: lane (g, i16) reads row 32 w + 16 m + i16 of sA and column 16 n + i16 of sB,
-        // cells KS-blocks: fp32 cells 16 s + 4 g .. + 3; bf16 cells 8 g .. 8 g + 7
+        issue(kb + PD * KC, k);  // past the chunk's end the loads re-read its last cell (flags 0)
+        // MFMA: lane (g, i16) reads row 80 wr + 16 m + i16 of sA and column
+        // 80 wc + 16 n + i16 of sB at cells KS s + E g .. + E - 1
         constexpr int KS = B::KSTEP;
 #pragma unroll
         for (int s = 0; s < KC / KS; ++s) {
-            u32x4 a[2], b[8];
+            u32x4 a[5], b[5];
 #pragma unroll
-            for (int m = 0; m < 2; ++m) a[m] = *reinterpret_cast<const u32x4*>(&sA[32 * wave + 16 * m + i16][KS * s + E * g]);
+            for (int m = 0; m < 5; ++m)
+                a[m] = *reinterpret_cast<const u32x4*>(&sA[80 * wr + 16 * m + i16][KS * s + E * g]);
 #pragma unroll
-            for (int n = 0; n < 8; ++n) b[n] = *reinterpret_cast<const u32x4*>(&sB[16 * n + i16][KS * s + E * g]);
+            for (int n = 0; n < 5; ++n)
+                b[n] = *reinterpret_cast<const u32x4*>(&sB[80 * wc + 16 * n + i16][KS * s + E * g]);
 #pragma unroll
-            for (int m = 0; m < 2; ++m)
+            for (int m = 0; m < 5; ++m)
 #pragma unroll
-                for (int n = 0; n < 8; ++n) acc[m][n] = mma16<T>(a[m], b[n], acc[m][n]);
+                for (int n = 0; n < 5; ++n) acc[m][n] = mma16<T>(a[m], b[n], acc[m][n]);
         }
         lds_barrier();
+    };
+    if (k_begin < k_end) {
+#pragma unroll
+        for (int k = 0; k < PD; ++k) issue(k_begin + k * KC, k);
+    }
+    for (int64_t kb = k_begin; kb < k_end; kb += PD * KC) {
+        step(kb, 0);
+        if constexpr (PD == 2) {
+            if (kb + KC >= k_end) break;
+            step(kb + KC, 1);
+        }
     }
 
-    // partial [chunk][d][G][PP]: columns then the bias; lane (q, n) holds rows 4 q + r of tile (m, n)
+    // partial [chunk][d][G][PP]: columns then the bias; lane (g, i16) holds rows 4 g + r of tile (m, n)
     float* out = part + ((int64_t)chunk * 4 + d) * (int64_t)G * q.PP;
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < 5; ++m)
 #pragma unroll
-        for (int n = 0; n < 8; ++n)
+        for (int n = 0; n < 5; ++n)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int row = r0 + 32 * wave + 16 * m + 4 * g + r, col = c0 + 16 * n + i16;
+                const int row = r0 + 80 * wr + 16 * m + 4 * g + r, col = c0 + 80 * wc + 16 * n + i16;
                 if (row < G && col < q.NB) out[(int64_t)row * q.PP + col] = acc[m][n][r];
             }
     if (do_bias) {
-        bsum += __shfl_xor(bsum, 1);
-        const int row = r0 + (tid >> 1);
-        if ((tid & 1) == 0 && row < G) out[(int64_t)row * q.PP + q.NB] = bsum;
+        // the NP threads of an item's chunk are NP consecutive lanes
+#pragma unroll
+        for (int ps = 0; ps < NPASS; ++ps)
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+#pragma unroll
+                for (int o = 1; o < NP; o <<= 1) bsum[ps][e] += __shfl_xor(bsum[ps][e], o);
+#pragma unroll
+        for (int ps = 0; ps < NPASS; ++ps) {
+            if (isrc[ps] != 0 || tid % NP != 0) continue;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int rr = irow[ps] + e;
+                if (rr < rlim) out[(int64_t)(r0 + rr) * q.PP + q.NB] = bsum[ps][e];
+            }
+        }
     }
 }
 
@@ -357,25 +441,27 @@ hipError_t launch_bwd_big(const LayerGeom& g, const void* d_dz, const void* d_x,
     const int tb = (int)std::min<int64_t>((nw + 255) / 256, 4096);
     const BigDw q = big_dw(g);
     const dim3 gx((unsigned)(((g.n_cells + 63) / 64 + 3) / 4), (unsigned)((g.c_in + 63) / 64));
-    const dim3 gw((unsigned)(q.rblocks * q.cblocks * 4), (unsigned)q.chunks);
+    const dim3 gw((unsigned)(q.rblocks * q.cblocks * 4 * q.chunks));
     const int64_t total = (int64_t)4 * q.G * q.PP;
     const int rbk = (int)std::min<int64_t>((total + 255) / 256, 4096);
     if (g.dtype == 0) {
         using T = float;
+        constexpr int PD = 1;
         hipLaunchKernelGGL(k_transpose<T>, dim3(tb), dim3(256), 0, s, N, g.c_in, static_cast<const T*>(d_wx),
                            static_cast<T*>(d_wxt));
         hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, static_cast<const T*>(d_dz),
                            static_cast<const T*>(d_wxt), d_flags, static_cast<T*>(d_dx));
-        hipLaunchKernelGGL(k_dw_big<T>, gw, dim3(256), 0, s, g.n_cells, g.canvas_w, g.c_in, g.hidden, q,
+        hipLaunchKernelGGL((k_dw_big<T, PD>), gw, dim3(BW_THREADS), 0, s, g.n_cells, g.canvas_w, g.c_in, g.hidden, q,
                            static_cast<const T*>(d_dz), static_cast<const T*>(d_x), static_cast<const T*>(d_y),
                            d_flags, d_part);
     } else {
         using T = bf16_t;
+        constexpr int PD = 2;
         hipLaunchKernelGGL(k_transpose<T>, dim3(tb), dim3(256), 0, s, N, g.c_in, static_cast<const T*>(d_wx),
                            static_cast<T*>(d_wxt));
         hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, static_cast<const T*>(d_dz),
                            static_cast<const T*>(d_wxt), d_flags, static_cast<T*>(d_dx));
-        hipLaunchKernelGGL(k_dw_big<T>, gw, dim3(256), 0, s, g.n_cells, g.canvas_w, g.c_in, g.hidden, q,
+        hipLaunchKernelGGL((k_dw_big<T, PD>), gw, dim3(BW_THREADS), 0, s, g.n_cells, g.canvas_w, g.c_in, g.hidden, q,
                            static_cast<const T*>(d_dz), static_cast<const T*>(d_x), static_cast<const T*>(d_y),
                            d_flags, d_part);
     }
