@@ -14,11 +14,13 @@ typedef uint16_t bf16_t;  // bfloat16 storage (upper half of an fp32)
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf2f(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
 
+// Round to nearest, ties to even; a NaN stays a (quiet) NaN. Written as a
+// select, so that no conversion becomes a branch.
 __device__ __forceinline__ bf16_t f2bf(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (bf16_t)((u >> 16) | 0x40);  // NaN
-    u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest, ties to even
-    return (bf16_t)(u >> 16);
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t r = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+    const bool nan = (u & 0x7fffffffu) > 0x7f800000u;
+    return (bf16_t)(nan ? ((u >> 16) | 0x40u) : r);
 }
 
 // Storage traits: loads/stores of 4 consecutive elements as fp32.

@@ -634,9 +634,26 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
 // accumulators of one tile only), their pre-activations loaded two tiles
 // ahead; one barrier per diagonal publishes h and c.
 // ---------------------------------------------------------------------------
+// Target of the stores of lanes whose cell is outside the diagonal in the
+// wide-layer kernels: every lane stores on every path, so the number of
+// memory operations in flight is the same on all paths and the compiler waits
+// for exactly the loads it needs (a skipped store would make it wait for
+// everything). 1536 bytes per lane (a cell's gates of one direction, its
+// output and its cell state at the offsets below), shared by workgroups eight
+// apart; the contents are never read.
+constexpr int SINK_LANE = 96;  // 16-byte slots per lane
+__device__ __attribute__((aligned(256))) uint4 g_wave_sink[8 * 64 * SINK_LANE];
+
+template <typename T>
+__device__ __forceinline__ T* wave_sink() {
+    return reinterpret_cast<T*>(&g_wave_sink[((blockIdx.x & 7) * 64 + (threadIdx.x & 63)) * SINK_LANE]);
+}
+
 template <int H, typename T>
 struct FwdBig {
     static constexpr bool on = sizeof(T) == 2 && Geo<H, T>::NW == 8 && Geo<H, T>::WQ == 4;
+    // sink offsets (elements of T) of the output and (bytes 16 past it) the cell state
+    static_assert(5 * H * sizeof(T) + 16 + 4 * sizeof(float) * 4 <= SINK_LANE * 16, "sink row");
 };
 
 template <int H, int NT, typename T>
@@ -763,13 +780,14 @@ __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) 
         *reinterpret_cast<uint2*>(&hbuf[cur][yy + 1][u0]) = pack(hv);
         *reinterpret_cast<float4*>(&cbuf[cur][yy + 1][u0]) = make_float4(cv[0], cv[1], cv[2], cv[3]);
         const int64_t idx = (int64_t)(M.sx * s + yy * M.ky);
-        if (live) {
-            T* zp = zb + idx * (4 * G);
+        T* const sink = wave_sink<T>();
+        T* const zp = live ? zb + idx * (4 * G) : sink;
+        T* const yp = live ? yb + idx * (4 * H) : sink + 5 * H;
+        float* const cp = inr ? cb + idx * (4 * H) : reinterpret_cast<float*>(sink + 5 * H) + 4;
 #pragma unroll
-            for (int t = 0; t < 5; ++t) *reinterpret_cast<uint2*>(zp + t * H) = pack(gv[t]);
-            *reinterpret_cast<uint2*>(yb + idx * (4 * H)) = pack(hv);
-        }
-        if (inr) *reinterpret_cast<float4*>(cb + idx * (4 * H)) = make_float4(cv[0], cv[1], cv[2], cv[3]);
+        for (int t = 0; t < 5; ++t) *reinterpret_cast<uint2*>(zp + t * H) = pack(gv[t]);
+        *reinterpret_cast<uint2*>(yp) = pack(hv);
+        *reinterpret_cast<float4*>(cp) = make_float4(cv[0], cv[1], cv[2], cv[3]);
         if (16 * nt + 16 > yhi) lds_barrier();  // last tile of the diagonal
     };
 
@@ -1234,8 +1252,8 @@ __device__ __forceinline__ void wave_bwd_big(const WaveArgs& a, const int unit) 
         *reinterpret_cast<float4*>(&dct[yy][u0]) = make_float4(ndt[0], ndt[1], ndt[2], ndt[3]);
 #pragma unroll
         for (int t = 0; t < 5; ++t) *reinterpret_cast<uint2*>(&dabuf[yy][t * H + u0]) = pack(da[t]);
-        if (inr) {
-            T* zp = zb + (int64_t)(M.sx * s + yy * M.ky) * (4 * G);
+        {
+            T* const zp = inr ? zb + (int64_t)(M.sx * s + yy * M.ky) * (4 * G) : wave_sink<T>();
 #pragma unroll
             for (int t = 0; t < 5; ++t) *reinterpret_cast<uint2*>(zp + t * H) = pack(da[t]);
         }
@@ -1254,6 +1272,11 @@ __device__ __forceinline__ void wave_bwd_big(const WaveArgs& a, const int unit) 
         *reinterpret_cast<float4*>(&gtop[16 * nt + n16][u0]) = make_float4(at[0], at[1], at[2], at[3]);
     };
 
+    // The inputs of the next tile's phase A are loaded right after the
+    // current one (one register set), so they are in flight across the
+    // barrier and the next segment's MFMAs.
+    In in;
+    load(steps - 1, max(0, steps - R.w) >> 4, in);
     lds_barrier();
     for (int s = steps - 1; s >= 0; --s) {
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
@@ -1262,10 +1285,12 @@ __device__ __forceinline__ void wave_bwd_big(const WaveArgs& a, const int unit) 
         for (int k = 0; k <= NT; ++k) {
             const bool pa = k < NT && k >= t0 && k <= t1;      // A(k) in this segment
             const bool pb = k >= 1 && k - 1 >= t0 && k - 1 <= t1;  // B(k - 1) in this segment
-            In in;
-            if (pa) load(s, k, in);
             if (pb) phase_b(k - 1);
-            if (pa) phase_a(s, k, in);
+            if (pa) {
+                phase_a(s, k, in);
+                if (k < t1) load(s, k + 1, in);
+                else load(max(s - 1, 0), max(0, s - R.w) >> 4, in);  // first tile of the next diagonal
+            }
             if (pa || pb) lds_barrier();
         }
     }
