@@ -629,10 +629,12 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
 // the candidate tile are the wave's sixteen units in order, so its register
 // k is the candidate of unit u0 + k. No value crosses lanes: the cell update
 // follows each tile's MFMAs without a barrier, both neighbours' cell states
-// come from LDS, and pre-activations, gates, outputs and cell states move as
-// 8- and 16-byte vectors. Tiles of a diagonal run one after another (the
-// accumulators of one tile only), their pre-activations loaded two tiles
-// ahead; one barrier per diagonal publishes h and c.
+// come from LDS, and pre-activations arrive as 8-byte vectors. Tiles of a
+// diagonal run one after another (the accumulators of one tile only), their
+// pre-activations loaded two tiles ahead. The diagonal's gates, outputs and
+// cell states are left in LDS and, after a barrier, written back by the whole
+// workgroup as contiguous 16-byte chunks (a lane's own values would be
+// 8-byte pieces of sixteen canvas rows per store).
 // ---------------------------------------------------------------------------
 // Target of the stores of lanes whose cell is outside the diagonal in the
 // wide-layer kernels: every lane stores on every path, so the number of
@@ -660,12 +662,22 @@ template <int H, int NT, typename T>
 __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) {
     using O = Ops<T>;
     using Op = typename O::Op;
-    constexpr int G = 5 * H, KRUN = H / 2, NSTEP = KRUN / O::PER;
+    constexpr int G = 5 * H, KRUN = H / 2, NSTEP = KRUN / O::PER, NTH = 512;
     constexpr int ROWS = NT * 16 + 1;            // row 0: zero row above local row 0
     constexpr int HP = H + 16 / (int)sizeof(T);  // padded LDS row pitches
     constexpr int CP = H + 4;
+    constexpr int GP = G + 16 / (int)sizeof(T);
+    // 16-byte chunks of a cell's outputs: gates, output, cell state
+    constexpr int QZ = G * (int)sizeof(T) / 16, QY = H * (int)sizeof(T) / 16, QC = H * 4 / 16;
+    constexpr int QF = QZ + QY + QC, NPS = NT * 16 * QF / NTH;
+    static_assert(NT * 16 * QF % NTH == 0, "store passes");
     __shared__ __attribute__((aligned(16))) T hbuf[2][ROWS][HP];
-    __shared__ __attribute__((aligned(16))) float cbuf[2][ROWS][CP];
+    // Cell states of the previous diagonal, overwritten row by row by the
+    // current one: the tiles run from the bottom up, so a tile never
+    // overwrites a row that a later tile of the diagonal still reads (a
+    // lane's hidden units are its wave's columns, read before written).
+    __shared__ __attribute__((aligned(16))) float cbuf[ROWS][CP];
+    __shared__ __attribute__((aligned(16))) T gst[NT * 16][GP];  // activated gates of the diagonal
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int q = lane >> 4, n16 = lane & 15;
@@ -681,7 +693,7 @@ __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) 
     if (sb >= se) return;
 
     for (int i = threadIdx.x; i < 2 * ROWS * HP; i += blockDim.x) (&hbuf[0][0][0])[i] = T(0);
-    for (int i = threadIdx.x; i < 2 * ROWS * CP; i += blockDim.x) (&cbuf[0][0][0])[i] = 0.0f;
+    for (int i = threadIdx.x; i < ROWS * CP; i += blockDim.x) (&cbuf[0][0])[i] = 0.0f;
     if (sb > 0) {  // state of diagonal sb - 1 from the previous launch's outputs
         const int pb = (sb & 1) ^ 1;
         for (int i = threadIdx.x; i < NT * 16 * H; i += blockDim.x) {
@@ -689,7 +701,7 @@ __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) 
             if (yy < R.h && xx >= 0 && xx < R.w) {
                 const int64_t p = canvas_index(R, d, yy, xx, a.canvas_w);
                 hbuf[pb][yy + 1][j] = Y[p * (4 * H) + d * H + j];
-                cbuf[pb][yy + 1][j] = Cs[p * (4 * H) + d * H + j];
+                cbuf[yy + 1][j] = Cs[p * (4 * H) + d * H + j];
             }
         }
     }
@@ -705,10 +717,43 @@ __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) 
 
     const DiagMap M(R, d, a.canvas_w);
     const uint8_t* mrow = a.mask + M.c0;
-    // the lane's elements at diagonal index idx = 0 (cell = c0 + idx)
-    T* const zb = Z + M.c0 * (4 * G) + d * G + u0;
-    T* const yb = Y + M.c0 * (4 * H) + d * H + u0;
-    float* const cb = Cs + M.c0 * (4 * H) + d * H + u0;
+    const T* const zb = Z + M.c0 * (4 * G) + d * G + u0;  // the lane's pre-activations at idx = 0
+
+    // Outputs of diagonal s, staged in LDS, written back as contiguous 16-byte
+    // chunks (pass ps, thread t: chunk (ps * 512 + t) % QF of cell row slot
+    // (ps * 512 + t) / QF); every thread stores in every pass (rows outside
+    // the diagonal repeat its nearest cell, which writes the same bytes twice).
+    char* const zd = reinterpret_cast<char*>(Z + d * G) + M.c0 * (4 * G * (int)sizeof(T));
+    char* const yd = reinterpret_cast<char*>(Y + d * H) + M.c0 * (4 * H * (int)sizeof(T));
+    char* const cd = reinterpret_cast<char*>(Cs + d * H) + M.c0 * (16 * H);
+    auto write_back = [&](int s) {
+        const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
+        const int cur = s & 1, sxs = M.sx * s;
+        constexpr int GR = 4;  // passes per LDS round trip (registers)
+        static_assert(NPS % GR == 0, "pass groups");
+#pragma unroll
+        for (int p0 = 0; p0 < NPS; p0 += GR) {
+            u32x4 v[GR];
+#pragma unroll
+            for (int k = 0; k < GR; ++k) {
+                const int i = (p0 + k) * NTH + (int)threadIdx.x, r = i % QF;
+                const int cell = min(max(i / QF, ylo), yhi);
+                const u32x4* src = r < QZ        ? reinterpret_cast<const u32x4*>(&gst[cell][0]) + r
+                                   : r < QZ + QY ? reinterpret_cast<const u32x4*>(&hbuf[cur][cell + 1][0]) + (r - QZ)
+                                                 : reinterpret_cast<const u32x4*>(&cbuf[cell + 1][0]) + (r - QZ - QY);
+                v[k] = *src;
+            }
+#pragma unroll
+            for (int k = 0; k < GR; ++k) {
+                const int i = (p0 + k) * NTH + (int)threadIdx.x, r = i % QF;
+                const int64_t idx = sxs + min(max(i / QF, ylo), yhi) * M.ky;
+                char* dst = r < QZ        ? zd + idx * (4 * G * (int)sizeof(T)) + 16 * r
+                            : r < QZ + QY ? yd + idx * (4 * H * (int)sizeof(T)) + 16 * (r - QZ)
+                                          : cd + idx * (16 * H) + 16 * (r - QZ - QY);
+                *reinterpret_cast<u32x4*>(dst) = v[k];
+            }
+        }
+    };
 
     // Pre-activations (5 gates x 4 units) and mask byte of the lane's cell of
     // tile nt of diagonal s; past the last diagonal, or for rows outside the
@@ -723,15 +768,15 @@ __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) 
         for (int t = 0; t < 5; ++t) zr[t] = *reinterpret_cast<const uint2*>(zp + t * H);
         m = mrow[idx];
     };
-    // Next tile of the walk: the next active tile of the diagonal, else the
-    // first active tile of the next one.
+    // Next tile of the walk: the next active tile up the diagonal, else the
+    // bottom active tile of the next one.
     auto advance = [&](int& s, int& nt) {
-        const int yhi = min(R.h - 1, s);
-        if (16 * (nt + 1) <= yhi) {
-            ++nt;
+        const int ylo = max(0, s - R.w + 1);
+        if (16 * nt > ylo) {
+            --nt;
         } else {
             ++s;
-            nt = max(0, s - R.w + 1) >> 4;
+            nt = min(R.h - 1, s) >> 4;
         }
     };
     auto tile = [&](int s, int nt, const uint2 (&zr)[5], uint32_t m) {
@@ -749,11 +794,10 @@ __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) 
 #pragma unroll
             for (int k = 0; k < 4; ++k) acc[k] = O::mma(Aown[k][ks], b, acc[k]);
         }
-        const float4 cl = *reinterpret_cast<const float4*>(&cbuf[prv][yy + 1][u0]);
-        const float4 ct = *reinterpret_cast<const float4*>(&cbuf[prv][yy][u0]);
+        const float4 cl = *reinterpret_cast<const float4*>(&cbuf[yy + 1][u0]);
+        const float4 ct = *reinterpret_cast<const float4*>(&cbuf[yy][u0]);
         const float clv[4] = {cl.x, cl.y, cl.z, cl.w}, ctv[4] = {ct.x, ct.y, ct.z, ct.w};
-        const bool inr = yy >= ylo && yy <= yhi;
-        const bool live = inr && m != 0;
+        const bool live = yy >= ylo && yy <= yhi && m != 0;
         float gv[5][4], hv[4], cv[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -778,23 +822,20 @@ __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) 
                               (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
         };
         *reinterpret_cast<uint2*>(&hbuf[cur][yy + 1][u0]) = pack(hv);
-        *reinterpret_cast<float4*>(&cbuf[cur][yy + 1][u0]) = make_float4(cv[0], cv[1], cv[2], cv[3]);
-        const int64_t idx = (int64_t)(M.sx * s + yy * M.ky);
-        T* const sink = wave_sink<T>();
-        T* const zp = live ? zb + idx * (4 * G) : sink;
-        T* const yp = live ? yb + idx * (4 * H) : sink + 5 * H;
-        float* const cp = inr ? cb + idx * (4 * H) : reinterpret_cast<float*>(sink + 5 * H) + 4;
+        *reinterpret_cast<float4*>(&cbuf[yy + 1][u0]) = make_float4(cv[0], cv[1], cv[2], cv[3]);
 #pragma unroll
-        for (int t = 0; t < 5; ++t) *reinterpret_cast<uint2*>(zp + t * H) = pack(gv[t]);
-        *reinterpret_cast<uint2*>(yp) = pack(hv);
-        *reinterpret_cast<float4*>(cp) = make_float4(cv[0], cv[1], cv[2], cv[3]);
-        if (16 * nt + 16 > yhi) lds_barrier();  // last tile of the diagonal
+        for (int t = 0; t < 5; ++t) *reinterpret_cast<uint2*>(&gst[yy][t * H + u0]) = pack(gv[t]);
+        if (16 * nt <= ylo) {  // top tile of the diagonal: publish it, write it back
+            lds_barrier();
+            write_back(s);
+            lds_barrier();
+        }
     };
 
     lds_barrier();
     uint2 z0[5], z1[5];
     uint32_t m0, m1;
-    int s = sb, nt = max(0, sb - R.w + 1) >> 4;
+    int s = sb, nt = min(R.h - 1, sb) >> 4;
     int ls = s, lnt = nt;
     load(ls, lnt, z0, m0);
     advance(ls, lnt);
