@@ -636,13 +636,12 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
 // workgroup as contiguous 16-byte chunks (a lane's own values would be
 // 8-byte pieces of sixteen canvas rows per store).
 // ---------------------------------------------------------------------------
-// Target of the stores of lanes whose cell is outside the diagonal in the
-// wide-layer kernels: every lane stores on every path, so the number of
-// memory operations in flight is the same on all paths and the compiler waits
-// for exactly the loads it needs (a skipped store would make it wait for
-// everything). 1536 bytes per lane (a cell's gates of one direction, its
-// output and its cell state at the offsets below), shared by workgroups eight
-// apart; the contents are never read.
+// Target of the gate-gradient stores of lanes whose cell is outside the
+// diagonal in the wide-layer backward: every lane stores on every path, so the
+// number of memory operations in flight is the same on all paths and the
+// compiler waits for exactly the loads it needs (a skipped store would make it
+// wait for everything). 1536 bytes per lane (room for a cell's gate gradients
+// of one direction), shared by workgroups eight apart; never read.
 constexpr int SINK_LANE = 96;  // 16-byte slots per lane
 __device__ __attribute__((aligned(256))) uint4 g_wave_sink[8 * 64 * SINK_LANE];
 
@@ -654,8 +653,6 @@ __device__ __forceinline__ T* wave_sink() {
 template <int H, typename T>
 struct FwdBig {
     static constexpr bool on = sizeof(T) == 2 && Geo<H, T>::NW == 8 && Geo<H, T>::WQ == 4;
-    // sink offsets (elements of T) of the output and (bytes 16 past it) the cell state
-    static_assert(5 * H * sizeof(T) + 16 + 4 * sizeof(float) * 4 <= SINK_LANE * 16, "sink row");
 };
 
 template <int H, int NT, typename T>
@@ -1182,6 +1179,7 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
 template <int H, typename T>
 struct BwdBig {
     static constexpr bool on = sizeof(T) == 2 && Geo<H, T>::NW == 8 && Geo<H, T>::WQ == 4 && 2 * H == 256;
+    static_assert(!on || 5 * H * sizeof(T) <= SINK_LANE * 16, "sink row");
 };
 
 template <int H, int NT, typename T>
