@@ -10,12 +10,14 @@ namespace mdl {
 //  1. Sort keys (height ascending, width descending, original index ascending)
 //     with a bitonic network in LDS: this is the bucketing by height and the
 //     "widest first" candidate order inside each bucket.
-//  2. One lane walks the buckets and fills rows greedily: the first remaining
-//     candidate opens a row; then, while space is left, a binary search finds
-//     the first candidate no wider than the remaining space (widths are sorted
-//     within the bucket), and a path-compressed "next unused" array skips the
-//     candidates already placed. A row closes when nothing fits and is flushed
-//     when its bucket runs empty. Coordinates are assigned as rows are made.
+//  2. One wave walks the buckets and fills rows greedily: the first remaining
+//     candidate opens a row; then, while space is left, the first candidate
+//     no wider than the remaining space (widths are sorted within the bucket)
+//     and from there the first one not yet placed are found, each with one or
+//     two ballots (a 64-way search over the sorted keys; a bit per position,
+//     64 per lane, marks the placed ones). A row closes when nothing fits and
+//     is flushed when its bucket runs empty. Coordinates are assigned as rows
+//     are made.
 // Key layout: [63:42] height, [41:21] (2^21-1-width), [20:0] index.
 // ---------------------------------------------------------------------------
 constexpr int PLACE_THREADS = 1024;
@@ -23,8 +25,7 @@ constexpr int PLACE_THREADS = 1024;
 __global__ void __launch_bounds__(PLACE_THREADS)
 k_pack_place(int n, int npow2, int canvas_w, const int32_t* __restrict__ hw, int32_t* __restrict__ out) {
     extern __shared__ unsigned long long smem_keys[];
-    unsigned long long* keys = smem_keys;                          // npow2
-    int32_t* nxt = reinterpret_cast<int32_t*>(keys + npow2);        // n + 1
+    unsigned long long* keys = smem_keys;  // npow2
     const int tid = threadIdx.x;
     for (int i = tid; i < npow2; i += PLACE_THREADS) {
         unsigned long long k = ~0ull;
@@ -51,78 +52,113 @@ k_pack_place(int n, int npow2, int canvas_w, const int32_t* __restrict__ hw, int
             __syncthreads();
         }
     }
-    for (int i = tid; i <= n; i += PLACE_THREADS) nxt[i] = i;
     __syncthreads();
-    if (tid != 0) return;
+    if (tid >= 64) return;
+    // From here one wave. Lane l holds the "placed" bits of sorted positions
+    // 64 l .. 64 l + 63 (positions past n count as placed); searches over the
+    // sorted keys are 64-way with a ballot per level.
+    const int lane = tid;
+    uint64_t placed = 0;
+    if (64 * lane >= n) placed = ~0ull;
+    else if (n - 64 * lane < 64) placed = ~0ull << (n - 64 * lane);
 
     auto kh = [&](int i) { return (int)(keys[i] >> 42); };
     auto kw = [&](int i) { return (int)((1 << 21) - 1 - (int)((keys[i] >> 21) & ((1ull << 21) - 1))); };
     auto ki = [&](int i) { return (int)(keys[i] & ((1ull << 21) - 1)); };
-    // first unused position >= i (n when none), with path halving
-    auto find = [&](int i) {
-        while (nxt[i] != i) {
-            nxt[i] = nxt[nxt[i]];
-            i = nxt[i];
+    // first position >= from not yet placed (n when none)
+    auto first_free = [&](int from) {
+        uint64_t fr = ~placed;
+        const int wd = from >> 6;
+        if (lane < wd) fr = 0;
+        else if (lane == wd) fr &= ~0ull << (from & 63);
+        const uint64_t has = __ballot(fr != 0);
+        if (has == 0) return n;
+        const int f = __builtin_ctzll(has);
+        const uint32_t lo = __shfl((uint32_t)fr, f), hi = __shfl((uint32_t)(fr >> 32), f);
+        const uint64_t w = ((uint64_t)hi << 32) | lo;
+        return 64 * f + __builtin_ctzll(w);
+    };
+    // first position in [a, b) where pred holds (b when none), pred being
+    // false then true along [a, b): blocks of `stride`, then within one block
+    auto first_true = [&](int a, int b, auto pred) {
+        if (a >= b) return b;
+        const int stride = (b - a + 63) / 64;
+        const int pos = a + lane * stride;
+        const bool tp = pred(min(pos, b - 1));  // every lane reads a position inside [a, b)
+        const uint64_t t = __ballot(pos < b && tp);
+        int lo, hi;
+        if (t & 1ull) return a;
+        if (t) {
+            const int f = __builtin_ctzll(t);
+            lo = a + (f - 1) * stride + 1;
+            hi = a + f * stride;  // pred(hi) holds
+        } else {
+            const int last = (b - 1 - a) / stride;  // last block with a valid start
+            lo = a + last * stride + 1;
+            hi = b;
         }
-        return i;
+        const int p2 = lo + lane;
+        const bool tp2 = pred(min(p2, b - 1));
+        const uint64_t t2 = __ballot(p2 < hi && tp2);
+        return t2 ? lo + __builtin_ctzll(t2) : hi;
+    };
+    auto mark = [&](int p) {
+        if (lane == (p >> 6)) placed |= 1ull << (p & 63);
     };
 
     int y = 0;
     bool first_row = true;
     int b0 = 0;
     while (b0 < n) {
-        int hb = kh(b0);
-        int b1 = b0;
-        while (b1 < n && kh(b1) == hb) ++b1;
-        // the bucket [b0, b1) is filled row by row
+        const int hb = kh(b0);
+        // the bucket [b0, b1) of height hb (heights ascend)
+        const int b1 = first_true(b0 + 1, n, [&](int i) { return kh(i) > hb; });
+        // the bucket is filled row by row
         while (true) {
-            int p = find(b0);
+            const int p = first_free(b0);
             if (p >= b1) break;
             if (!first_row) y += 1;  // separator row
             first_row = false;
             int used = kw(p);
-            int x = 0;
-            int k = ki(p);
-            out[4 * k + 0] = y;
-            out[4 * k + 1] = 0;
-            out[4 * k + 2] = hb;
-            out[4 * k + 3] = used;
-            nxt[p] = p + 1;
-            x = used;
+            if (lane == 0) {
+                const int k = ki(p);
+                out[4 * k + 0] = y;
+                out[4 * k + 1] = 0;
+                out[4 * k + 2] = hb;
+                out[4 * k + 3] = used;
+            }
+            mark(p);
             while (true) {
-                int cap = canvas_w - used - 1;
+                const int cap = canvas_w - used - 1;
                 if (cap < 1) break;
-                // first position in [b0, b1) whose width <= cap (widths descend)
-                int lo = b0, hi = b1;
-                while (lo < hi) {
-                    int mid = (lo + hi) >> 1;
-                    if (kw(mid) <= cap) hi = mid;
-                    else lo = mid + 1;
-                }
-                int q = find(lo);
+                // first candidate no wider than the space left (widths descend
+                // within the bucket), then the first one not yet placed from there
+                const int lo = first_true(b0, b1, [&](int i) { return kw(i) <= cap; });
+                const int q = first_free(lo);
                 if (q >= b1) break;
-                int wq = kw(q);
-                int kq = ki(q);
-                out[4 * kq + 0] = y;
-                out[4 * kq + 1] = x + 1;
-                out[4 * kq + 2] = hb;
-                out[4 * kq + 3] = wq;
-                x += 1 + wq;
+                const int wq = kw(q);
+                if (lane == 0) {
+                    const int kq = ki(q);
+                    out[4 * kq + 0] = y;
+                    out[4 * kq + 1] = used + 1;
+                    out[4 * kq + 2] = hb;
+                    out[4 * kq + 3] = wq;
+                }
                 used += 1 + wq;
-                nxt[q] = q + 1;
+                mark(q);
             }
             y += hb;
         }
         b0 = b1;
     }
-    out[4 * n] = y;
+    if (lane == 0) out[4 * n] = y;
 }
 
 hipError_t launch_pack_place(int n, int canvas_w, const int32_t* d_hw, int32_t* d_out, int32_t*,
                              hipStream_t s) {
     int npow2 = 1;
     while (npow2 < n) npow2 <<= 1;
-    size_t lds = (size_t)npow2 * 8 + (size_t)(n + 1) * 4;
+    size_t lds = (size_t)npow2 * 8;
     hipLaunchKernelGGL(k_pack_place, dim3(1), dim3(PLACE_THREADS), lds, s, n, npow2, canvas_w, d_hw, d_out);
     return hipGetLastError();
 }

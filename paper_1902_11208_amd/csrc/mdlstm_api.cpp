@@ -45,7 +45,7 @@ mdlstm_status device_fail(hipError_t e, const char* where) {
     } while (0)
 
 constexpr int32_t kMaxDim = (1 << 21) - 1;  // largest canvas side / example side
-constexpr int32_t kMaxPackN = 4096;         // placement keys + skip list fit 48 KB of LDS
+constexpr int32_t kMaxPackN = 4096;         // placement keys in LDS; a placed bit per key, 64 per lane
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
