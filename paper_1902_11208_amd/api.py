@@ -77,11 +77,21 @@ def pack_layout(heights, widths, canvas_w: int, device="cuda", stream=None):
     rects = (Rect * max(1, n))()
     ch = ctypes.c_int32(0)
     st = _stream(stream)
-    check(lib().mdlstm_pack_layout(n, hs, ws, int(canvas_w), rects, ctypes.byref(ch), None, 0, _ptr(work),
-                                   work.numel(), st))
-    mask = torch.empty((ch.value, int(canvas_w)), dtype=torch.uint8, device=device)
-    check(lib().mdlstm_pack_layout(n, hs, ws, int(canvas_w), rects, ctypes.byref(ch), _ptr(mask), mask.numel(),
-                                   _ptr(work), work.numel(), st))
+    # One call when the sizes are valid: the mask is allocated for the tallest
+    # possible canvas (every example on its own row, plus separators) and cut
+    # to the placed height. Otherwise the library reports what is wrong.
+    h64 = np.asarray(heights, np.int64).reshape(-1)
+    w64 = np.asarray(widths, np.int64).reshape(-1)
+    max_h = int(np.sum(h64 + 1)) if n else 0
+    if n and h64.min() >= 1 and w64.min() >= 1 and w64.max() <= int(canvas_w) and max_h <= 2 ** 21 - 1:
+        full = torch.empty((max_h, int(canvas_w)), dtype=torch.uint8, device=device)
+        check(lib().mdlstm_pack_layout(n, hs, ws, int(canvas_w), rects, ctypes.byref(ch), _ptr(full), full.numel(),
+                                       _ptr(work), work.numel(), st))
+        mask = full[:ch.value]
+    else:
+        check(lib().mdlstm_pack_layout(n, hs, ws, int(canvas_w), rects, ctypes.byref(ch), None, 0, _ptr(work),
+                                       work.numel(), st))
+        mask = torch.empty((ch.value, int(canvas_w)), dtype=torch.uint8, device=device)
     torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
     return _rects_from(rects, n), ch.value, mask
 
