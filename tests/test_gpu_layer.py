@@ -132,6 +132,28 @@ def test_config2_words_forward_backward(kind):
     assert np.all(gpu["dx_canvas"].cpu().numpy()[m == 0] == 0)
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_output_rows_outside_rectangles_are_zeroed(dt):
+    """The forward writes every output row: zeros outside the rectangles (the
+    buffer holds NaN before the call), finite values inside."""
+    from paper_1902_11208_amd import api
+    from synth import configs
+    import gpu_run
+
+    H, C = (16, 16) if dt == "f32" else (128, 64)
+    wl = configs.custom_workload(64, [7, 12, 3, 16], [30, 9, 41, 22], 64, C, H, dtype=dt)
+    print(f"case: output rows outside rectangles, {dt} H={H}", flush=True)
+    units, ch, mask = api.pack_layout(wl.heights, wl.widths, wl.canvas_w)
+    x = api.pack_data([gpu_run.to_dev(e, wl.dtype) for e in wl.examples()], units, ch, wl.canvas_w)
+    layer = api.MDLSTMLayer(*[gpu_run.to_dev(p, wl.dtype) for p in wl.params()], ch, wl.canvas_w, units, mask)
+    layer.y.fill_(float("nan"))
+    y = layer.forward(x).float().cpu().numpy()
+    m = mask.cpu().numpy()
+    assert (m == 0).any() and (m == 1).any()
+    assert np.all(y[m == 0] == 0)
+    assert np.all(np.isfinite(y[m == 1]))
+
+
 def test_config3_lines_forward_backward():
     # full batch on the GPU; per-example Y and dX checked on a seeded sample of
     # 12 examples (the oracle takes about 2 s per example), weight gradients on
