@@ -1426,10 +1426,10 @@ static hipError_t launch_nt(bool fwd, int nt, int n_units, const WaveArgs& a, hi
     return hipGetLastError();
 }
 
-// Workgroups per CU when units are taken from a queue.
-#ifndef WAVE_GROUPS_PER_CU
-#define WAVE_GROUPS_PER_CU 2
-#endif
+// Workgroups per CU when units are taken from a queue: the forward runs
+// fastest with a unit per CU at a time, the backward (fewer registers, more
+// latency per step) with two.
+constexpr int FWD_GROUPS_PER_CU = 1, BWD_GROUPS_PER_CU = 2;
 
 static hipError_t launch_wave(bool fwd, const LayerGeom& g, int nt, int n_units, WaveArgs a, hipStream_t s) {
     if (n_units == 0) return hipSuccess;
@@ -1439,7 +1439,7 @@ static hipError_t launch_wave(bool fwd, const LayerGeom& g, int nt, int n_units,
         hipError_t e = hipGetDevice(&dev);
         if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
-        const int groups = WAVE_GROUPS_PER_CU * std::max(cus, 1);
+        const int groups = (fwd ? FWD_GROUPS_PER_CU : BWD_GROUPS_PER_CU) * std::max(cus, 1);
         if (n_units > groups) {  // else one workgroup per unit
             n_units = groups;
         } else {
