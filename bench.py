@@ -37,8 +37,8 @@ PEAK_BF16_MFMA_TFLOPS = 2500.0  # dense bf16 matrix
 
 COPY_BYTES = 256 << 20  # plain device copy used to calibrate FETCH_SIZE / WRITE_SIZE
 
-PHASES = [("projection", 0, 1), ("wavefront_fwd", 2, 3), ("wavefront_bwd", 4, 5), ("input_grad", 5, 6),
-          ("weight_grad", 6, 7)]
+PHASES = [("projection", 0, 1), ("zero_invalid", 1, 2), ("wavefront_fwd", 2, 3), ("wavefront_bwd", 4, 5),
+          ("input_grad", 5, 6), ("weight_grad", 6, 7)]
 
 
 def _parse():
@@ -64,9 +64,8 @@ def algorithmic(wl, n_cells: int, unit_cells: int):
     s = 2 if wl.dtype == "bf16" else 4
     cd = 4 * unit_cells
     return {
-        # Z for every cell, and zeros in the output rows of the cells outside the rectangles
-        "projection": (n_cells * (C + 20 * H) * s + 20 * H * (C + 1) * s + (n_cells - unit_cells) * 4 * H * s,
-                       2.0 * n_cells * C * 20 * H),
+        "projection": (n_cells * (C + 20 * H) * s + 20 * H * (C + 1) * s, 2.0 * n_cells * C * 20 * H),
+        "zero_invalid": (0, 0.0),
         "wavefront_fwd": (cd * (10 * H * s + H * s + 4 * H), cd * 20.0 * H * H),
         "wavefront_bwd": (cd * (11 * H * s + 4 * H), cd * 20.0 * H * H),
         "input_grad": (n_cells * (20 * H + C) * s, 2.0 * n_cells * 20 * H * C),

@@ -275,9 +275,8 @@ const char* mdlstm_last_error(void);
  * events[n] (host array of hipEvent_t handles owned by the caller). While set,
  * mdlstm_forward and mdlstm_backward called on this thread record them on
  * their stream at kernel boundaries:
- *   [0] before the projection   [1] after the projection (which also zeroes
- *   the output rows of cells outside the rectangles or masked)  [2] recorded
- *   right after [1]   [3] after the forward wavefront
+ *   [0] before the projection   [1] after the projection   [2] after zeroing
+ *   invalid output rows         [3] after the forward wavefront
  *   [4] before the backward wavefront  [5] after it  [6] after the input
  *   gradient  [7] after the weight gradients.
  * n must be 0 (disable) or 8. The handles must stay valid while set.

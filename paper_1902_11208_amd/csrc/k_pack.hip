@@ -277,4 +277,36 @@ hipError_t launch_gather(int n, void* const* d_ptrs, const int32_t* d_rects, int
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Zero the rows of invalid cells (mask 0 or outside every rectangle) of a
+// [n_cells][width] tensor; width*esize is a multiple of 8 bytes.
+// ---------------------------------------------------------------------------
+// A wave takes 64 cells: each lane reads one cell's mask byte and rect id,
+// then the wave writes the rows of the invalid ones, one row at a time with
+// the lanes along the row.
+__global__ void k_zero_invalid(int64_t n_cells, int row_words, const uint8_t* __restrict__ mask,
+                               const int32_t* __restrict__ rid, uint2* __restrict__ t) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wstride = (int64_t)gridDim.x * (blockDim.x >> 6) * 64;
+    for (int64_t c0 = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 64; c0 < n_cells;
+         c0 += wstride) {
+        const int64_t p = c0 + lane;
+        const bool bad = p < n_cells && (mask[p] == 0 || rid[p] < 0);
+        for (uint64_t bm = __ballot(bad); bm; bm &= bm - 1) {
+            uint2* row = t + (c0 + __builtin_ctzll(bm)) * row_words;
+            for (int k = lane; k < row_words; k += 64) row[k] = make_uint2(0, 0);
+        }
+    }
+}
+
+hipError_t launch_zero_invalid(const LayerGeom& g, int width, const uint8_t* d_mask, const int32_t* d_rid,
+                               void* d_t, hipStream_t s) {
+    int esize = g.dtype == 1 ? 2 : 4;
+    int row_words = width * esize / 8;
+    if (g.n_cells > 0 && row_words > 0)
+        hipLaunchKernelGGL(k_zero_invalid, dim3(fill_blocks(g.n_cells)), dim3(256), 0, s, g.n_cells, row_words,
+                           d_mask, d_rid, reinterpret_cast<uint2*>(d_t));
+    return hipGetLastError();
+}
+
 }  // namespace mdl

@@ -55,8 +55,7 @@ struct PK<bf16_t> {  // 16x16x32 bf16: K step ks, slot g holds k = 32 ks + 8 g +
 template <typename T, int KS>
 __global__ void __launch_bounds__(256)
 k_projection(int64_t n_cells, int64_t n_blocks, int C, int N, int nch, const T* __restrict__ X,
-             const T* __restrict__ Wx, const T* __restrict__ bias, T* __restrict__ Z, const uint8_t* __restrict__ mask,
-             const int32_t* __restrict__ rid, uint2* __restrict__ yz, int yrow_words) {
+             const T* __restrict__ Wx, const T* __restrict__ bias, T* __restrict__ Z) {
     using K = PK<T>;
     using Op = typename K::Op;
     constexpr int RW = K::PERK * KS;  // staged k values per row
@@ -132,27 +131,10 @@ k_projection(int64_t n_cells, int64_t n_blocks, int C, int N, int nch, const T* 
             }
         }
     }
-    // The layer output's rows at cells outside every rectangle or masked are
-    // zeroed here (the wavefront writes only the valid ones): per block a lane
-    // per cell, the wave then clears the invalid rows, each workgroup its
-    // column chunk's share of the row.
-    if (yz) {
-        const int w0 = (int)((int64_t)yrow_words * blockIdx.y / gridDim.y);
-        const int w1 = (int)((int64_t)yrow_words * (blockIdx.y + 1) / gridDim.y);
-        for (int64_t blk = blockIdx.x; blk < n_blocks; blk += gridDim.x) {
-            const int64_t c0 = (blk * 4 + wave) * PCELLS, p = c0 + lane;
-            const bool bad = p < n_cells && (mask[p] == 0 || rid[p] < 0);
-            for (uint64_t bm = __ballot(bad); bm; bm &= bm - 1) {
-                uint2* row = yz + (c0 + __builtin_ctzll(bm)) * yrow_words;
-                for (int k = w0 + lane; k < w1; k += 64) row[k] = make_uint2(0u, 0u);
-            }
-        }
-    }
 }
 
 template <typename T, int KS>
-static hipError_t launch_proj(const LayerGeom& g, const T* X, const T* W, const T* B, T* Z, const uint8_t* mask,
-                              const int32_t* rid, void* y, hipStream_t s) {
+static hipError_t launch_proj(const LayerGeom& g, const T* X, const T* W, const T* B, T* Z, hipStream_t s) {
     constexpr int RW = PK<T>::PERK * KS, P = RW + PK<T>::PAD;
     const int N = 20 * g.hidden;
     // columns per workgroup: as many as the LDS budget holds (a multiple of 16,
@@ -174,14 +156,13 @@ static hipError_t launch_proj(const LayerGeom& g, const T* X, const T* W, const 
     const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(4, 160 * 1024 / lds));
     const int64_t want = std::max<int64_t>(1, (int64_t)per_cu * std::max(cus, 1) / nchunks_col);
     const dim3 grid((unsigned)std::min<int64_t>(blocks, want), (unsigned)nchunks_col), block(256);
-    const int yrow_words = 4 * g.hidden * (int)sizeof(T) / 8;
     hipLaunchKernelGGL((k_projection<T, KS>), grid, block, (size_t)nch * P * sizeof(T), s, g.n_cells, blocks, g.c_in,
-                       N, nch, X, W, B, Z, mask, rid, static_cast<uint2*>(y), yrow_words);
+                       N, nch, X, W, B, Z);
     return hipGetLastError();
 }
 
 hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_wx, const void* d_b, void* d_z,
-                             const uint8_t* d_mask, const int32_t* d_rid, void* d_y, hipStream_t s) {
+                             hipStream_t s) {
     if (g.n_cells == 0) return hipSuccess;
     if (g.dtype == 0) {
         const int ks = (g.c_in + 3) / 4;
@@ -189,13 +170,13 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
         auto W = static_cast<const float*>(d_wx);
         auto B = static_cast<const float*>(d_b);
         auto Z = static_cast<float*>(d_z);
-        if (ks <= 1) return launch_proj<float, 1>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
-        if (ks <= 2) return launch_proj<float, 2>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
-        if (ks <= 4) return launch_proj<float, 4>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
-        if (ks <= 8) return launch_proj<float, 8>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
-        if (ks <= 16) return launch_proj<float, 16>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
-        if (ks <= 32) return launch_proj<float, 32>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
-        if (ks <= 64) return launch_proj<float, 64>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
+        if (ks <= 1) return launch_proj<float, 1>(g, X, W, B, Z, s);
+        if (ks <= 2) return launch_proj<float, 2>(g, X, W, B, Z, s);
+        if (ks <= 4) return launch_proj<float, 4>(g, X, W, B, Z, s);
+        if (ks <= 8) return launch_proj<float, 8>(g, X, W, B, Z, s);
+        if (ks <= 16) return launch_proj<float, 16>(g, X, W, B, Z, s);
+        if (ks <= 32) return launch_proj<float, 32>(g, X, W, B, Z, s);
+        if (ks <= 64) return launch_proj<float, 64>(g, X, W, B, Z, s);
         return hipErrorInvalidValue;
     }
     const int ks = (g.c_in + 31) / 32;
@@ -203,10 +184,10 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
     auto W = static_cast<const bf16_t*>(d_wx);
     auto B = static_cast<const bf16_t*>(d_b);
     auto Z = static_cast<bf16_t*>(d_z);
-    if (ks <= 1) return launch_proj<bf16_t, 1>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
-    if (ks <= 2) return launch_proj<bf16_t, 2>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
-    if (ks <= 4) return launch_proj<bf16_t, 4>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
-    if (ks <= 8) return launch_proj<bf16_t, 8>(g, X, W, B, Z, d_mask, d_rid, d_y, s);
+    if (ks <= 1) return launch_proj<bf16_t, 1>(g, X, W, B, Z, s);
+    if (ks <= 2) return launch_proj<bf16_t, 2>(g, X, W, B, Z, s);
+    if (ks <= 4) return launch_proj<bf16_t, 4>(g, X, W, B, Z, s);
+    if (ks <= 8) return launch_proj<bf16_t, 8>(g, X, W, B, Z, s);
     return hipErrorInvalidValue;
 }
 

@@ -33,11 +33,12 @@ hipError_t launch_gather(int n, void* const* d_ptrs, const int32_t* d_rects, int
                          int esize, const void* d_canvas, int max_h, hipStream_t s);
 
 // --- forward ---------------------------------------------------------------
-// Z[p][20H] = Wx_all[20H][C] x[p] + b_all; also zeroes the rows [4H] of the
-// layer output d_y (storage dtype) at cells outside every rectangle or masked
-// (d_y may be NULL).
+// Z[p][20H] = Wx_all[20H][C] x[p] + b_all.
 hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_wx, const void* d_b,
-                             void* d_z, const uint8_t* d_mask, const int32_t* d_rid, void* d_y, hipStream_t s);
+                             void* d_z, hipStream_t s);
+// Zero the rows of a [n_cells][width] tensor (storage dtype) whose cell is invalid.
+hipError_t launch_zero_invalid(const LayerGeom& g, int width, const uint8_t* d_mask,
+                               const int32_t* d_rid, void* d_t, hipStream_t s);
 // Forward anti-diagonal wavefront over n_units units (rectangle, direction)
 // in the order of d_units. d_queue: two device counters, zero on entry (the
 // workgroups take units from the first, a fixed number per CU, and count

@@ -476,9 +476,10 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
     const int32_t* drects = reinterpret_cast<const int32_t*>(c.ws + c.p.rects);
     float* cs = reinterpret_cast<float*>(c.ws + c.p.c);
     HIP_OR_FAIL(mark(0, s));
-    HIP_OR_FAIL(mdl::launch_projection(c.g, d_x, d_wx, d_b, c.ws + c.p.z, d_mask, rid, d_y, s));
+    HIP_OR_FAIL(mdl::launch_projection(c.g, d_x, d_wx, d_b, c.ws + c.p.z, s));
     HIP_OR_FAIL(mark(1, s));
-    HIP_OR_FAIL(mark(2, s));  // invalid output rows are zeroed by the projection
+    HIP_OR_FAIL(mdl::launch_zero_invalid(c.g, 4 * c.g.hidden, d_mask, rid, d_y, s));
+    HIP_OR_FAIL(mark(2, s));
     if (!stepwise) {
         HIP_OR_FAIL(mdl::launch_wavefront_fwd(c.g, c.nt, 4 * n_rects, units, drects, d_mask, d_u, c.ws + c.p.z, cs,
                                               d_y, reinterpret_cast<unsigned*>(c.ws + c.p.queue), s));
