@@ -97,6 +97,27 @@ def test_small_cases_forward_backward(case):
     _compare(gpu, ref, dt, label=name)
 
 
+def test_wide_layer_unit_queue():
+    """bf16 H = 128 with 520 units: more than the CUs hold at once in both
+    directions, so the forward and backward wide-layer kernels take units
+    from the device queue (and leave it zeroed for the second call)."""
+    import gpu_run
+    import oracle_run
+    from synth.configs import custom_workload
+
+    rng = np.random.default_rng(7)
+    hs = rng.integers(1, 6, 130).tolist()
+    ws = rng.integers(1, 9, 130).tolist()
+    wl = custom_workload(65, hs, ws, 64, 8, 128, "bf16")
+    _say(f"case wide-layer queue: {len(hs)} examples, {4 * len(hs)} units, H=128 bf16")
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    ref = oracle_run.run_layer(xs, params, dys, workers=oracle_run.default_workers())
+    for rep in range(2):
+        gpu = gpu_run.run_layer(xs, params, dys, hs, ws, 64, dtype="bf16")
+        _compare(gpu, ref, "bf16", label=f"wide-layer queue, call {rep}")
+
+
 def test_config1_forward():
     import gpu_run
     import oracle_run
