@@ -276,7 +276,9 @@ const char* mdlstm_last_error(void);
  * mdlstm_forward and mdlstm_backward called on this thread record them on
  * their stream at kernel boundaries:
  *   [0] before the projection   [1] after the projection   [2] after zeroing
- *   invalid output rows         [3] after the forward wavefront
+ *   invalid output rows (the persistent forward wavefront zeroes them itself
+ *   when the batch has at least a unit per CU; then [2] follows [1] directly)
+ *   [3] after the forward wavefront
  *   [4] before the backward wavefront  [5] after it  [6] after the input
  *   gradient  [7] after the weight gradients.
  * n must be 0 (disable) or 8. The handles must stay valid while set.

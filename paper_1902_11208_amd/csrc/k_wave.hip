@@ -175,6 +175,11 @@ struct WaveArgs {
     int s0, s1;            // forward: local diagonals [s0, s1) of every unit
     unsigned* queue;       // next unit to take (zeroed before the launch), or NULL: unit = block
     int n_units;
+    // forward: when rid is set, the output rows [yrow_words x 8 bytes] of the
+    // cells outside every rectangle or masked are zeroed before the units run
+    const int32_t* rid;    // [n_cells] rectangle id, -1 outside every rectangle
+    int64_t n_cells;
+    int yrow_words;
 };
 
 template <int NT, int WQ, typename T>
@@ -248,6 +253,7 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
     for (int i = threadIdx.x; i < 2 * ROWS * HP; i += blockDim.x) (&hbuf[0][0][0])[i] = T(0);
     for (int i = threadIdx.x; i < 2 * ROWS * (H + 2); i += blockDim.x) (&cbuf[0][0][0])[i] = 0.0f;
     if (sb > 0) {
+        lds_barrier();  // every zero written before the read-back fills the same rows
         const int pb = (sb & 1) ^ 1;  // buffer of diagonal sb - 1
         for (int i = threadIdx.x; i < NT * 16 * H; i += blockDim.x) {
             const int yy = i / H, j = i - yy * H, xx = sb - 1 - yy;
@@ -692,6 +698,7 @@ __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) 
     for (int i = threadIdx.x; i < 2 * ROWS * HP; i += blockDim.x) (&hbuf[0][0][0])[i] = T(0);
     for (int i = threadIdx.x; i < ROWS * CP; i += blockDim.x) (&cbuf[0][0])[i] = 0.0f;
     if (sb > 0) {  // state of diagonal sb - 1 from the previous launch's outputs
+        lds_barrier();  // every zero written before the read-back fills the same rows
         const int pb = (sb & 1) ^ 1;
         for (int i = threadIdx.x; i < NT * 16 * H; i += blockDim.x) {
             const int yy = i / H, j = i - yy * H, xx = sb - 1 - yy;
@@ -1344,8 +1351,31 @@ __device__ __forceinline__ void wave_bwd_big(const WaveArgs& a, const int unit) 
 // Forward loads run one step ahead with one workgroup per unit, two steps
 // ahead when several workgroups per CU take units from the queue (the load
 // latency grows while every CU streams to and from memory).
+// Output rows of the invalid cells (outside every rectangle, or masked) set
+// to zero, a wave per 64 cells over the grid: each lane reads one cell's mask
+// byte and rect id, then the wave clears the rows of the invalid ones with the
+// lanes along the row. Done before any unit starts; the units write the rows
+// of the valid cells.
+__device__ __forceinline__ void zero_invalid_rows(const WaveArgs& a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+    uint2* const y = static_cast<uint2*>(a.y);
+    for (int64_t c0 = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 64; c0 < a.n_cells;
+         c0 += waves * 64) {
+        const int64_t p = c0 + lane;
+        const bool bad = p < a.n_cells && (a.mask[p] == 0 || a.rid[p] < 0);
+        for (uint64_t bm = __ballot(bad); bm; bm &= bm - 1) {
+            uint2* row = y + (c0 + __builtin_ctzll(bm)) * a.yrow_words;
+            for (int k = lane; k < a.yrow_words; k += 64) row[k] = make_uint2(0u, 0u);
+        }
+    }
+}
+
 template <int H, int NT, typename T, bool FWD, bool QUEUE>
 __device__ __forceinline__ void run_units(const WaveArgs& a) {
+    if constexpr (FWD) {
+        if (a.rid) zero_invalid_rows(a);
+    }
     if constexpr (!QUEUE) {
         if constexpr (FWD && FwdBig<H, T>::on) wave_fwd_big<H, NT, T>(a, a.units[blockIdx.x]);
         else if (FWD) wave_fwd_unit<H, NT, T, 1>(a, a.units[blockIdx.x]);
@@ -1465,17 +1495,31 @@ static hipError_t launch_wave(bool fwd, const LayerGeom& g, int nt, int n_units,
 }
 
 hipError_t launch_wavefront_fwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
-                                const int32_t* d_rects, const uint8_t* d_mask, const void* d_u, void* d_z,
-                                float* d_c, void* d_y, unsigned* d_queue, hipStream_t s) {
-    WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w, 0, INT_MAX, d_queue, n_units};
+                                const int32_t* d_rects, const uint8_t* d_mask, const int32_t* d_rid, const void* d_u,
+                                void* d_z, float* d_c, void* d_y, unsigned* d_queue, hipStream_t s) {
+    const int yrow_words = 4 * g.hidden * (g.dtype == 1 ? 2 : 4) / 8;
+    // the launch's own workgroups zero the invalid rows when there are enough
+    // of them to cover the canvas quickly (at least one per CU); else a
+    // separate kernel does
+    int dev = 0, cus = 256;
+    if (d_rid && (hipGetDevice(&dev) != hipSuccess ||
+                  hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess))
+        return hipErrorInvalidDevice;
+    if (d_rid && n_units < cus) {
+        const hipError_t e = launch_zero_invalid(g, 4 * g.hidden, d_mask, d_rid, d_y, s);
+        if (e != hipSuccess) return e;
+        d_rid = nullptr;
+    }
+    WaveArgs a{d_units,  d_rects, d_mask, d_u,   d_z,       d_c,       d_y,       nullptr, g.canvas_w, 0,
+               INT_MAX, d_queue, n_units, d_rid, g.n_cells, yrow_words};
     return launch_wave(true, g, nt, n_units, a, s);
 }
 
 hipError_t launch_wavefront_bwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u, const void* d_dy,
                                 void* d_z, const float* d_c, unsigned* d_queue, hipStream_t s) {
-    WaveArgs a{d_units,  d_rects, d_mask, d_u,     d_z,     const_cast<float*>(d_c), nullptr, d_dy, g.canvas_w, 0,
-               INT_MAX, d_queue, n_units};
+    WaveArgs a{d_units, d_rects, d_mask,  d_u,     d_z,     const_cast<float*>(d_c), nullptr, d_dy, g.canvas_w, 0,
+               INT_MAX, d_queue, n_units, nullptr, 0,       0};
     return launch_wave(false, g, nt, n_units, a, s);
 }
 
@@ -1521,7 +1565,8 @@ hipError_t build_wavefront_fwd_graph(const LayerGeom& g, int nt, int n_units, in
     if (e != hipSuccess) return e;
     hipGraphNode_t prev = nullptr;
     for (int st = 0; st < max_steps && e == hipSuccess; ++st) {
-        WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w, st, st + 1, nullptr, n_units};
+        WaveArgs a{d_units, d_rects, d_mask, d_u, d_z, d_c, d_y, nullptr, g.canvas_w, st, st + 1, nullptr, n_units,
+                   nullptr, 0,       0};
         void* params[] = {&a};
         hipKernelNodeParams p{};
         p.func = const_cast<void*>(fn);

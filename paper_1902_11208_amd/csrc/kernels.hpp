@@ -42,10 +42,12 @@ hipError_t launch_zero_invalid(const LayerGeom& g, int width, const uint8_t* d_m
 // Forward anti-diagonal wavefront over n_units units (rectangle, direction)
 // in the order of d_units. d_queue: two device counters, zero on entry (the
 // workgroups take units from the first, a fixed number per CU, and count
-// themselves out on the second; the last one out zeroes both again).
+// themselves out on the second; the last one out zeroes both again). With
+// d_rid set, the output rows of cells outside every rectangle or masked are
+// zeroed first.
 hipError_t launch_wavefront_fwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
-                                const int32_t* d_rects, const uint8_t* d_mask, const void* d_u,
-                                void* d_z, float* d_c, void* d_y, unsigned* d_queue, hipStream_t s);
+                                const int32_t* d_rects, const uint8_t* d_mask, const int32_t* d_rid,
+                                const void* d_u, void* d_z, float* d_c, void* d_y, unsigned* d_queue, hipStream_t s);
 
 // The forward wavefront as one launch per local diagonal (diagonal s of every
 // unit in launch s), recorded as a chain of max_steps kernel nodes into an

@@ -478,11 +478,12 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
     HIP_OR_FAIL(mark(0, s));
     HIP_OR_FAIL(mdl::launch_projection(c.g, d_x, d_wx, d_b, c.ws + c.p.z, s));
     HIP_OR_FAIL(mark(1, s));
-    HIP_OR_FAIL(mdl::launch_zero_invalid(c.g, 4 * c.g.hidden, d_mask, rid, d_y, s));
+    if (stepwise || n_rects == 0) HIP_OR_FAIL(mdl::launch_zero_invalid(c.g, 4 * c.g.hidden, d_mask, rid, d_y, s));
     HIP_OR_FAIL(mark(2, s));
     if (!stepwise) {
-        HIP_OR_FAIL(mdl::launch_wavefront_fwd(c.g, c.nt, 4 * n_rects, units, drects, d_mask, d_u, c.ws + c.p.z, cs,
-                                              d_y, reinterpret_cast<unsigned*>(c.ws + c.p.queue), s));
+        // the persistent launch also zeroes the output rows of the invalid cells
+        HIP_OR_FAIL(mdl::launch_wavefront_fwd(c.g, c.nt, 4 * n_rects, units, drects, d_mask, rid, d_u, c.ws + c.p.z,
+                                              cs, d_y, reinterpret_cast<unsigned*>(c.ws + c.p.queue), s));
     } else if (n_rects > 0) {
         int32_t max_steps = 0;
         for (int32_t k = 0; k < n_rects; ++k) max_steps = std::max(max_steps, rects[k].h + rects[k].w - 1);

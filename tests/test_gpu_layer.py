@@ -153,17 +153,24 @@ def test_config2_words_forward_backward(kind):
     assert np.all(gpu["dx_canvas"].cpu().numpy()[m == 0] == 0)
 
 
-@pytest.mark.parametrize("dt", ["f32", "bf16"])
-def test_output_rows_outside_rectangles_are_zeroed(dt):
+@pytest.mark.parametrize("case", ["f32", "bf16", "f32_many"])
+def test_output_rows_outside_rectangles_are_zeroed(case):
     """The forward writes every output row: zeros outside the rectangles (the
-    buffer holds NaN before the call), finite values inside."""
+    buffer holds NaN before the call), finite values inside. With few units a
+    separate kernel zeroes the rows; with a unit per CU or more (f32_many,
+    320 units) the forward wavefront's own workgroups do."""
     from paper_1902_11208_amd import api
     from synth import configs
     import gpu_run
 
+    dt = "bf16" if case == "bf16" else "f32"
     H, C = (16, 16) if dt == "f32" else (128, 64)
-    wl = configs.custom_workload(64, [7, 12, 3, 16], [30, 9, 41, 22], 64, C, H, dtype=dt)
-    print(f"case: output rows outside rectangles, {dt} H={H}", flush=True)
+    if case == "f32_many":
+        rng = np.random.default_rng(11)
+        wl = configs.custom_workload(66, rng.integers(2, 9, 80).tolist(), rng.integers(2, 13, 80).tolist(), 96, C, H)
+    else:
+        wl = configs.custom_workload(64, [7, 12, 3, 16], [30, 9, 41, 22], 64, C, H, dtype=dt)
+    print(f"case: output rows outside rectangles, {case} H={H}, {4 * wl.n} units", flush=True)
     units, ch, mask = api.pack_layout(wl.heights, wl.widths, wl.canvas_w)
     x = api.pack_data([gpu_run.to_dev(e, wl.dtype) for e in wl.examples()], units, ch, wl.canvas_w)
     layer = api.MDLSTMLayer(*[gpu_run.to_dev(p, wl.dtype) for p in wl.params()], ch, wl.canvas_w, units, mask)
