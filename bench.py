@@ -54,19 +54,23 @@ def _parse():
     return ap.parse_args()
 
 
-def algorithmic(wl, n_cells: int, unit_cells: int):
+def algorithmic(wl, n_cells: int, unit_cells: int, n_units: int = 0, cus: int = 256):
     """Algorithmic bytes and flops per launch of each kernel.
 
     unit_cells: cells covered by the scheduling rectangles (x4 directions below).
     n_cells: canvas cells (the dense GEMMs run over the whole canvas).
+    n_units: units of the forward wavefront; with at least one per CU it also
+    writes the zero output rows of the cells outside the rectangles.
     """
     H, C = wl.hidden, wl.c_in
     s = 2 if wl.dtype == "bf16" else 4
     cd = 4 * unit_cells
+    zero = (n_cells - unit_cells) * 4 * H * s
+    in_wave = n_units >= cus
     return {
         "projection": (n_cells * (C + 20 * H) * s + 20 * H * (C + 1) * s, 2.0 * n_cells * C * 20 * H),
-        "zero_invalid": (0, 0.0),
-        "wavefront_fwd": (cd * (10 * H * s + H * s + 4 * H), cd * 20.0 * H * H),
+        "zero_invalid": (0 if in_wave else zero, 0.0),
+        "wavefront_fwd": (cd * (10 * H * s + H * s + 4 * H) + (zero if in_wave else 0), cd * 20.0 * H * H),
         "wavefront_bwd": (cd * (11 * H * s + 4 * H), cd * 20.0 * H * H),
         "input_grad": (n_cells * (20 * H + C) * s, 2.0 * n_cells * 20 * H * C),
         "weight_grad": (n_cells * (20 * H + C + 8 * H) * s, 2.0 * n_cells * 20 * H * (C + 2 * H + 1)),
@@ -409,7 +413,10 @@ def measured_traffic(kernel: str, workload: str):
 
 def _rooflines(wl, packed, phase):
     """Per-phase rates, the dominant kernel's HBM roofline and the projection's MFMA fraction."""
-    alg = algorithmic(wl, packed.n_cells, packed.unit_cells)
+    import torch
+
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    alg = algorithmic(wl, packed.n_cells, packed.unit_cells, 4 * len(wl.heights), cus)
     phases_out = {}
     for name, t in phase.items():
         by, fl = alg[name]
