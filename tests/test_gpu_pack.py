@@ -28,6 +28,14 @@ def _cases():
         out.append((f"random{i}", rng.integers(1, 9, n), rng.integers(1, cw + 1, n), cw))
     out.append(("single", np.array([3]), np.array([7]), 7))
     out.append(("ties", np.array([2, 2, 2, 2, 2]), np.array([3, 3, 3, 3, 3]), 7))
+    # the placement keeps a bit per sorted example, 64 per lane of one wave:
+    # word boundaries and the largest packing call (4096 examples), with many
+    # height buckets and with a single one
+    rng = np.random.default_rng(3)
+    out.append(("n64", rng.integers(1, 4, 64), rng.integers(1, 51, 64), 50))
+    out.append(("n65", rng.integers(1, 4, 65), rng.integers(1, 51, 65), 50))
+    out.append(("max_n_buckets", rng.integers(1, 41, 4096), rng.integers(1, 65, 4096), 512))
+    out.append(("max_n_one_bucket", np.full(4096, 5), rng.integers(1, 65, 4096), 1024))
     return out
 
 
