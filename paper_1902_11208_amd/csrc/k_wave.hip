@@ -182,6 +182,16 @@ struct WaveArgs {
     int yrow_words;
 };
 
+// Waves of a forward unit in groups of NW, one group per 16-row tile, when
+// the workgroup stays within 1024 threads and the registers allow (fp32 up
+// to H = 32): the tiles of a diagonal then run side by side on their own
+// waves instead of one after another on the same ones.
+template <int H, int NT, typename T>
+struct TileGroups {
+    static constexpr int NG =
+        (std::is_same<T, float>::value && H <= 32 && NT >= 2 && 64 * Geo<H, T>::NW * NT <= 1024) ? NT : 1;
+};
+
 template <int NT, int WQ, typename T>
 struct FPre {
     T z[NT][WQ][5];
@@ -211,7 +221,9 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
     using Op = typename O::Op;
     using Q = OutQ<H, T>;
     constexpr int NW = Gm::NW, WQ = Gm::WQ, G = Gm::G, KRUN = Gm::KRUN, NSTEP = Gm::NSTEP;
-    constexpr int SPL = Gm::SPL, GSTEP = Gm::GSTEP, NTH = 64 * NW;
+    // tile groups: NG groups of NW waves, group tg owning tiles tg, tg + NG, ...
+    constexpr int NG = TileGroups<H, NT, T>::NG, TPG = NT / NG;
+    constexpr int SPL = Gm::SPL, GSTEP = Gm::GSTEP, NTH = 64 * NW * NG;
     constexpr int ROWS = NT * 16 + 1;             // row 0: zero row above local row 0
     constexpr int HP = H + 16 / (int)sizeof(T);   // padded LDS row pitch (elements)
     // Staged: the pre-activations of the next diagonal are loaded as contiguous
@@ -234,7 +246,9 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
     // writes (rows below 16 NT are read)
     __shared__ uint32_t mst[STAGE ? 2 : 1][STAGE ? NTH : 1];
 
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int tg = NG == 1 ? 0 : (int)(threadIdx.x >> 6) / NW;     // tile group
+    const int w = NG == 1 ? (int)(threadIdx.x >> 6) : (int)(threadIdx.x >> 6) % NW;  // wave in the group
     const int q = lane >> 4, n16 = lane & 15;
     const int gt = w / SPL, sp = w % SPL;  // candidate tile and reduction slice of this wave
     const int d = unit & 3;
@@ -279,13 +293,14 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
         const bool ok = j < H;
         load_slot<T, GSTEP>(U + (int64_t)(4 * H + (ok ? j : 0)) * 2 * H + q * KRUN + sp * GSTEP * O::PER, 1, ok, Ag);
     }
-    float cprev[NT][WQ];  // c_L: the lane's cell state of the previous diagonal
+    float cprev[TPG][WQ];  // c_L: the lane's cell state of the previous diagonal
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int lt = 0; lt < TPG; ++lt)
 #pragma unroll
         for (int wq = 0; wq < WQ; ++wq) {
+            const int nt = tg + NG * lt;
             const int yy = 16 * nt + n16, j = 4 * (w * WQ + wq) + q, xx = sb - 1 - yy;
-            cprev[nt][wq] = sb > 0 && yy < R.h && xx >= 0 && xx < R.w
+            cprev[lt][wq] = sb > 0 && yy < R.h && xx >= 0 && xx < R.w
                                 ? Cs[canvas_index(R, d, yy, xx, a.canvas_w) * (4 * H) + d * H + j]
                                 : 0.0f;
         }
@@ -328,25 +343,26 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
     // diagonal's active range) so their number is the same on every path,
     // which lets the compiler wait for exactly these loads one step later;
     // `live` says whether they are used.
-    auto fetch = [&](int s, FPre<NT, WQ, T>& b) {
+    auto fetch = [&](int s, FPre<TPG, WQ, T>& b) {
         const int sc = min(s, steps - 1);
         const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
         const int sxs = M.sx * sc;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int lt = 0; lt < TPG; ++lt) {
+            const int nt = tg + NG * lt;
             const int yy = 16 * nt + n16;
-            b.live[nt] = s < steps && yy >= ylo && yy <= yhi;
+            b.live[lt] = s < steps && yy >= ylo && yy <= yhi;
             const int idx = sxs + min(max(yy, ylo), yhi) * M.ky;
-            b.m[nt] = mrow[idx];
+            b.m[lt] = mrow[idx];
             if constexpr (!STAGE) {
                 const int64_t p = M.c0 + idx;
-                b.p[nt] = p;
+                b.p[lt] = p;
                 const T* zp = Z + p * (4 * G) + d * G;
 #pragma unroll
                 for (int wq = 0; wq < WQ; ++wq) {
                     const int j = 4 * (w * WQ + wq) + q;
 #pragma unroll
-                    for (int t = 0; t < 5; ++t) b.z[nt][wq][t] = zp[t * H + j];
+                    for (int t = 0; t < 5; ++t) b.z[lt][wq][t] = zp[t * H + j];
                 }
             }
         }
@@ -429,11 +445,12 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
     // in one block with the memory work issued behind them; otherwise they
     // are skipped.
     constexpr bool SKIP = !STAGE;
-    auto mma = [&](int s, floatx4 (&acc)[NT][WQ], floatx4 (&ag)[NT]) {
+    auto mma = [&](int s, floatx4 (&acc)[TPG][WQ], floatx4 (&ag)[TPG]) {
         const int prv = (s & 1) ^ 1;
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int lt = 0; lt < TPG; ++lt) {
+            const int nt = tg + NG * lt;
             if (SKIP && (16 * nt > yhi || 16 * nt + 15 < ylo)) continue;  // uniform over the workgroup
             const int yy = 16 * nt + n16;
             const T* brow = (q < 2) ? &hbuf[prv][yy + 1][q * KRUN] : &hbuf[prv][yy][(q - 2) * KRUN];
@@ -442,64 +459,67 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
             for (int ks = 0; ks < NSTEP; ++ks) bop[ks] = O::lds(brow + ks * O::PER);
 #pragma unroll
             for (int ks = 0; ks < GSTEP; ++ks) bg[ks] = O::lds(brow + (sp * GSTEP + ks) * O::PER);
-            ag[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+            ag[lt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int ks = 0; ks < GSTEP; ++ks) ag[nt] = O::mma(Ag[ks], bg[ks], ag[nt]);
+            for (int ks = 0; ks < GSTEP; ++ks) ag[lt] = O::mma(Ag[ks], bg[ks], ag[lt]);
 #pragma unroll
-            for (int wq = 0; wq < WQ; ++wq) acc[nt][wq] = floatx4{0.f, 0.f, 0.f, 0.f};
+            for (int wq = 0; wq < WQ; ++wq) acc[lt][wq] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < NSTEP; ++ks)
 #pragma unroll
-                for (int wq = 0; wq < WQ; ++wq) acc[nt][wq] = O::mma(Aown[wq][ks], bop[ks], acc[nt][wq]);
+                for (int wq = 0; wq < WQ; ++wq) acc[lt][wq] = O::mma(Aown[wq][ks], bop[ks], acc[lt][wq]);
         }
     };
     // The candidate slices go to LDS for the cell phase to sum.
-    auto partials = [&](int s, const floatx4 (&ag)[NT]) {
+    auto partials = [&](int s, const floatx4 (&ag)[TPG]) {
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
         const int j0 = 16 * gt + 4 * q;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int lt = 0; lt < TPG; ++lt) {
+            const int nt = tg + NG * lt;
             if (SKIP && (16 * nt > yhi || 16 * nt + 15 < ylo)) continue;
             const int yy = 16 * nt + n16;
             if (j0 < H) {
-                *reinterpret_cast<float2*>(&gpart[sp][yy][j0]) = make_float2(ag[nt][0], ag[nt][1]);
-                *reinterpret_cast<float2*>(&gpart[sp][yy][j0 + 2]) = make_float2(ag[nt][2], ag[nt][3]);
+                *reinterpret_cast<float2*>(&gpart[sp][yy][j0]) = make_float2(ag[lt][0], ag[lt][1]);
+                *reinterpret_cast<float2*>(&gpart[sp][yy][j0 + 2]) = make_float2(ag[lt][2], ag[lt][3]);
             }
         }
     };
     // Inputs of the cell updates of step s that are ready before its
     // contraction: the pre-activations and the top neighbours' cell states.
-    auto pre_read = [&](int s, const FPre<NT, WQ, T>& b, float (&zv)[NT][WQ][5], float (&ct)[NT][WQ],
-                        uint32_t (&mk)[NT]) {
+    auto pre_read = [&](int s, const FPre<TPG, WQ, T>& b, float (&zv)[TPG][WQ][5], float (&ct)[TPG][WQ],
+                        uint32_t (&mk)[TPG]) {
         const int prv = (s & 1) ^ 1;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int lt = 0; lt < TPG; ++lt) {
+            const int nt = tg + NG * lt;
             const int yy = 16 * nt + n16;
             if constexpr (STAGE)
-                mk[nt] = mst[s & 1][yy];
+                mk[lt] = mst[s & 1][yy];
             else
-                mk[nt] = b.m[nt];
+                mk[lt] = b.m[lt];
 #pragma unroll
             for (int wq = 0; wq < WQ; ++wq) {
                 const int j = 4 * (w * WQ + wq) + q;
 #pragma unroll
                 for (int t = 0; t < 5; ++t) {
                     if constexpr (STAGE)
-                        zv[nt][wq][t] = ld1f<T>(reinterpret_cast<const T*>(&zst[s & 1][yy * PZ]) + t * H + j);
+                        zv[lt][wq][t] = ld1f<T>(reinterpret_cast<const T*>(&zst[s & 1][yy * PZ]) + t * H + j);
                     else
-                        zv[nt][wq][t] = ld1f<T>(&b.z[nt][wq][t]);
+                        zv[lt][wq][t] = ld1f<T>(&b.z[lt][wq][t]);
                 }
-                ct[nt][wq] = cbuf[prv][yy][j];
+                ct[lt][wq] = cbuf[prv][yy][j];
             }
         }
     };
     // Cell updates: the lane owns (cell 16 nt + n16, hidden unit 4 (w WQ + wq) + q).
-    auto update = [&](int s, const FPre<NT, WQ, T>& b, const floatx4 (&acc)[NT][WQ], const float (&zv0)[NT][WQ][5],
-                      const float (&ct)[NT][WQ], const uint32_t (&mk)[NT]) {
+    auto update = [&](int s, const FPre<TPG, WQ, T>& b, const floatx4 (&acc)[TPG][WQ], const float (&zv0)[TPG][WQ][5],
+                      const float (&ct)[TPG][WQ], const uint32_t (&mk)[TPG]) {
         const int cur = s & 1, prv = cur ^ 1;
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int lt = 0; lt < TPG; ++lt) {
+            const int nt = tg + NG * lt;
             if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;
             const int yy = 16 * nt + n16;
 #pragma unroll
@@ -507,18 +527,18 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
                 const int j = 4 * (w * WQ + wq) + q;
                 float cn = 0.0f, hn = 0.0f;
                 if (yy >= ylo && yy <= yhi) {
-                    const float* zv = zv0[nt][wq];
+                    const float* zv = zv0[lt][wq];
                     float gs = 0.0f;
 #pragma unroll
                     for (int k = 0; k < SPL; ++k) gs += gpart[k][yy][j];
-                    const float gi = sigm_fast(acc[nt][wq][0] + zv[0]);
-                    const float gfl = sigm_fast(acc[nt][wq][1] + zv[1]);
-                    const float gft = sigm_fast(acc[nt][wq][2] + zv[2]);
-                    const float go = sigm_fast(acc[nt][wq][3] + zv[3]);
+                    const float gi = sigm_fast(acc[lt][wq][0] + zv[0]);
+                    const float gfl = sigm_fast(acc[lt][wq][1] + zv[1]);
+                    const float gft = sigm_fast(acc[lt][wq][2] + zv[2]);
+                    const float go = sigm_fast(acc[lt][wq][3] + zv[3]);
                     const float gg = tanh_fast(gs + zv[4]);
-                    cn = gi * gg + gfl * cprev[nt][wq] + gft * ct[nt][wq];
+                    cn = gi * gg + gfl * cprev[lt][wq] + gft * ct[lt][wq];
                     hn = go * tanh_fast(cn);
-                    if (!mk[nt]) {
+                    if (!mk[lt]) {
                         cn = 0.0f;
                         hn = 0.0f;
                     }
@@ -532,8 +552,8 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
                         oz[5 * H + j] = from_f<T>(hn);
                         reinterpret_cast<float*>(&ostage[yy][Q::QZ + Q::QY])[j] = cn;
                     } else {
-                        const int64_t p = b.p[nt];
-                        if (mk[nt]) {
+                        const int64_t p = b.p[lt];
+                        if (mk[lt]) {
                             T* zp = Z + p * (4 * G) + d * G + j;
                             zp[0 * H] = from_f<T>(gi);
                             zp[1 * H] = from_f<T>(gfl);
@@ -545,16 +565,16 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
                         Cs[p * (4 * H) + d * H + j] = cn;
                     }
                 }
-                cprev[nt][wq] = cn;
+                cprev[lt][wq] = cn;
                 hbuf[cur][yy + 1][j] = from_f<T>(hn);
                 cbuf[cur][yy + 1][j] = cn;
             }
         }
     };
-    auto compute = [&](int s, const FPre<NT, WQ, T>& b) {
-        floatx4 acc[NT][WQ], ag[NT];
-        float zv[NT][WQ][5], ct[NT][WQ];
-        uint32_t mk[NT];
+    auto compute = [&](int s, const FPre<TPG, WQ, T>& b) {
+        floatx4 acc[TPG][WQ], ag[TPG];
+        float zv[TPG][WQ][5], ct[TPG][WQ];
+        uint32_t mk[TPG];
         pre_read(s, b, zv, ct, mk);
         mma(s, acc, ag);
         partials(s, ag);
@@ -564,7 +584,7 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
     };
 
     lds_barrier();
-    FPre<NT, WQ, T> b0, b1;
+    FPre<TPG, WQ, T> b0, b1;
     if constexpr (STAGE) {
         // Step s: the MFMAs first, then the LDS reads that the previous step
         // made ready (the outputs of step s - 1 to write back, the
@@ -577,12 +597,12 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
         // latency when the whole chip streams to and from memory.
         auto step = [&](int s, int k, auto with_flush) {
             constexpr bool WF = decltype(with_flush)::value;
-            floatx4 acc[NT][WQ], ag[NT];
+            floatx4 acc[TPG][WQ], ag[TPG];
             mma(s, acc, ag);
             u32x4 fv[NITF > 0 ? NITF : 1];
             if constexpr (WF) flush_read(s - 1, fv);
-            float zv[NT][WQ][5], ct[NT][WQ];
-            uint32_t mk[NT];
+            float zv[TPG][WQ][5], ct[TPG][WQ];
+            uint32_t mk[TPG];
             pre_read(s, b0, zv, ct, mk);
             stage_in(s + 1, k);
             fetch_z(s + 1 + PFD, k);
@@ -606,7 +626,7 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
         }
         if (s < se) step(s, 0, std::true_type{});
         flush(se - 1);
-    } else if constexpr (Prefetch2<T>::template on<NT, WQ>()) {
+    } else if constexpr (Prefetch2<T>::template on<TPG, WQ>()) {
         fetch(sb, b0);
         int s = sb;
         for (; s + 1 < se; s += 2) {
@@ -1408,7 +1428,7 @@ __device__ __forceinline__ void run_units(const WaveArgs& a) {
 }
 
 template <int H, int NT, typename T, bool QUEUE>
-__global__ void __launch_bounds__((64 * Geo<H, T>::NW))
+__global__ void __launch_bounds__((64 * Geo<H, T>::NW * TileGroups<H, NT, T>::NG))
 k_wave_fwd(WaveArgs a) {
     run_units<H, NT, T, true, QUEUE>(a);
 }
@@ -1433,12 +1453,12 @@ constexpr bool bwd_fits() {
 
 template <int H, int NT, typename T>
 static void launch_unit(bool fwd, int n_groups, const WaveArgs& a, hipStream_t s) {
-    const dim3 grid(n_groups), block(64 * Geo<H, T>::NW);
+    const dim3 grid(n_groups), block(64 * Geo<H, T>::NW), fblock(64 * Geo<H, T>::NW * TileGroups<H, NT, T>::NG);
     if (a.queue) {
-        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, true>), grid, block, 0, s, a);
+        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, true>), grid, fblock, 0, s, a);
         else if constexpr (bwd_fits<H, NT, T>()) hipLaunchKernelGGL((k_wave_bwd<H, NT, T, true>), grid, block, 0, s, a);
     } else {
-        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, false>), grid, block, 0, s, a);
+        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, false>), grid, fblock, 0, s, a);
         else if constexpr (bwd_fits<H, NT, T>()) hipLaunchKernelGGL((k_wave_bwd<H, NT, T, false>), grid, block, 0, s, a);
     }
 }
@@ -1526,12 +1546,12 @@ hipError_t launch_wavefront_bwd(const LayerGeom& g, int nt, int n_units, const i
 // Forward kernel of a shape and its workgroup size, for graph nodes.
 template <int H, typename T>
 static bool fwd_kernel(int nt, const void** fn, int* threads) {
-    *threads = 64 * Geo<H, T>::NW;
+    constexpr int w64 = 64 * Geo<H, T>::NW;
     switch (nt) {
-        case 1: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 1, T, false>); return true;
-        case 2: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 2, T, false>); return true;
-        case 3: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 3, T, false>); return true;
-        case 4: *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 4, T, false>); return true;
+        case 1: *threads = w64 * TileGroups<H, 1, T>::NG; *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 1, T, false>); return true;
+        case 2: *threads = w64 * TileGroups<H, 2, T>::NG; *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 2, T, false>); return true;
+        case 3: *threads = w64 * TileGroups<H, 3, T>::NG; *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 3, T, false>); return true;
+        case 4: *threads = w64 * TileGroups<H, 4, T>::NG; *fn = reinterpret_cast<const void*>(&k_wave_fwd<H, 4, T, false>); return true;
         default: return false;
     }
 }
