@@ -124,6 +124,16 @@ struct OutQ {
     static_assert(QZ * 16 == 5 * H * (int)sizeof(T) && QY * 16 == H * (int)sizeof(T), "chunking");
 };
 
+// Waves of a unit (forward and backward) in groups of NW, one group per
+// 16-row tile, when the workgroup stays within 1024 threads and the registers
+// allow (fp32 up to H = 32): the tiles of a diagonal then run side by side on
+// their own waves instead of one after another on the same ones.
+template <int H, int NT, typename T>
+struct TileGroups {
+    static constexpr int NG =
+        (std::is_same<T, float>::value && H <= 32 && NT >= 2 && 64 * Geo<H, T>::NW * NT <= 1024) ? NT : 1;
+};
+
 // LDS bytes of the forward kernel without and with staging of its inputs
 // (two diagonals of pre-activations) and outputs (one diagonal).
 template <int H, int NT, typename T>
@@ -148,7 +158,7 @@ constexpr size_t bwd_lds_base() {
 }
 template <int H, int NT, typename T>
 constexpr size_t bwd_lds_stage() {
-    constexpr size_t nth = 64 * Geo<H, T>::NW;
+    constexpr size_t nth = 64 * Geo<H, T>::NW * TileGroups<H, NT, T>::NG;
     return 2 * ((NT * 16 * (OutQ<H, T>::QF + 1) + nth - 1) / nth * nth) * 16;
 }
 template <int H, int NT, typename T>
@@ -180,16 +190,6 @@ struct WaveArgs {
     const int32_t* rid;    // [n_cells] rectangle id, -1 outside every rectangle
     int64_t n_cells;
     int yrow_words;
-};
-
-// Waves of a forward unit in groups of NW, one group per 16-row tile, when
-// the workgroup stays within 1024 threads and the registers allow (fp32 up
-// to H = 32): the tiles of a diagonal then run side by side on their own
-// waves instead of one after another on the same ones.
-template <int H, int NT, typename T>
-struct TileGroups {
-    static constexpr int NG =
-        (std::is_same<T, float>::value && H <= 32 && NT >= 2 && 64 * Geo<H, T>::NW * NT <= 1024) ? NT : 1;
 };
 
 template <int NT, int WQ, typename T>
@@ -892,7 +892,9 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
     using O = Ops<T>;
     using Op = typename O::Op;
     using Q = OutQ<H, T>;
-    constexpr int WQ = Gm::WQ, G = Gm::G, KRUNB = Gm::KRUNB, NTH = 64 * Gm::NW;
+    // tile groups as in the forward: group tg owns tiles tg, tg + NG, ...
+    constexpr int NG = TileGroups<H, NT, T>::NG, TPG = NT / NG;
+    constexpr int WQ = Gm::WQ, G = Gm::G, KRUNB = Gm::KRUNB, NTH = 64 * Gm::NW * NG;
     constexpr int TPW = Gm::TPW, SPLB = Gm::SPLB, BSTEP = Gm::BSTEP;
     constexpr int GP = G + 16 / (int)sizeof(T);
     // Staged: the gates, upstream gradients and cell states of a diagonal are
@@ -912,7 +914,9 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
     __shared__ __attribute__((aligned(16))) float dct[NT * 16 + 2][H + 2];
     __shared__ __attribute__((aligned(16))) u32x4 ist[STAGE ? 2 : 1][NSL];
 
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int tg = NG == 1 ? 0 : (int)(threadIdx.x >> 6) / Gm::NW;
+    const int w = NG == 1 ? (int)(threadIdx.x >> 6) : (int)(threadIdx.x >> 6) % Gm::NW;
     const int q = lane >> 4, n16 = lane & 15;
     const int mt0 = (w / SPLB) * TPW, sb = w % SPLB;  // output tiles and reduction slice of this wave
     const int d = unit & 3;
@@ -936,11 +940,11 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
         const bool ok = k < 2 * H;
         load_slot<T, BSTEP>(U + (int64_t)(q * KRUNB + sb * BSTEP * O::PER) * 2 * H + (ok ? k : 0), 2 * H, ok, A[tt]);
     }
-    float dcl[NT][WQ], dcn[NT][WQ];
+    float dcl[TPG][WQ], dcn[TPG][WQ];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int lt = 0; lt < TPG; ++lt)
 #pragma unroll
-        for (int wq = 0; wq < WQ; ++wq) dcl[nt][wq] = dcn[nt][wq] = 0.0f;
+        for (int wq = 0; wq < WQ; ++wq) dcl[lt][wq] = dcn[lt][wq] = 0.0f;
     __builtin_amdgcn_s_waitcnt(0);  // U operands in registers before the step loop
 
     // Cells of diagonal s, their mask bytes and (unstaged) the lane's inputs,
@@ -948,20 +952,20 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
     // predecessors outside the rectangle read the cell itself and are zeroed
     // on use.
     const DiagMap M(R, d, a.canvas_w);
-    auto fetch = [&](int s, BPre<NT, WQ, T>& b) {
+    auto fetch = [&](int s, BPre<TPG, WQ, T>& b) {
         const int sc = max(s, 0);
         const int ylo = max(0, sc - R.w + 1), yhi = min(R.h - 1, sc);
         const int64_t base = M.base(sc);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            const int yy = 16 * nt + n16;
-            b.live[nt] = s >= 0 && yy >= ylo && yy <= yhi;
+        for (int lt = 0; lt < TPG; ++lt) {
+            const int yy = 16 * (tg + NG * lt) + n16;
+            b.live[lt] = s >= 0 && yy >= ylo && yy <= yhi;
             const int yc = min(max(yy, ylo), yhi), xc = sc - yc;
             const int64_t p = M.at(base, yc);
-            b.p[nt] = p;
-            b.m[nt] = a.mask[p];
-            b.hasl[nt] = xc > 0;
-            b.hast[nt] = yc > 0;
+            b.p[lt] = p;
+            b.m[lt] = a.mask[p];
+            b.hasl[lt] = xc > 0;
+            b.hast[lt] = yc > 0;
             if constexpr (!STAGE) {
                 const int64_t pl = xc > 0 ? canvas_index(R, d, yc, xc - 1, a.canvas_w) : p;
                 const int64_t pt = yc > 0 ? canvas_index(R, d, yc - 1, xc, a.canvas_w) : p;
@@ -970,11 +974,11 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
                     const int j = 4 * (w * WQ + wq) + q;
                     const T* zp = Z + p * (4 * G) + d * G + j;
 #pragma unroll
-                    for (int t = 0; t < 5; ++t) b.g[nt][wq][t] = zp[t * H];
-                    b.dy[nt][wq] = DY[p * (4 * H) + d * H + j];
-                    b.c[nt][wq] = Cs[p * (4 * H) + d * H + j];
-                    b.cl[nt][wq] = Cs[pl * (4 * H) + d * H + j];
-                    b.ct[nt][wq] = Cs[pt * (4 * H) + d * H + j];
+                    for (int t = 0; t < 5; ++t) b.g[lt][wq][t] = zp[t * H];
+                    b.dy[lt][wq] = DY[p * (4 * H) + d * H + j];
+                    b.c[lt][wq] = Cs[p * (4 * H) + d * H + j];
+                    b.cl[lt][wq] = Cs[pl * (4 * H) + d * H + j];
+                    b.ct[lt][wq] = Cs[pt * (4 * H) + d * H + j];
                 }
             }
         }
@@ -1031,11 +1035,12 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
         dchunk[it] = i - dcell[it] * Q::QZ;
     }
     char* const Zd = reinterpret_cast<char*>(Z + d * G);
-    auto compute = [&](int s, const BPre<NT, WQ, T>& b) {
+    auto compute = [&](int s, const BPre<TPG, WQ, T>& b) {
         const int ylo = max(0, s - R.w + 1), yhi = min(R.h - 1, s);
         // Phase A: gate-gradient update of this lane's (cell, hidden unit) pairs.
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int lt = 0; lt < TPG; ++lt) {
+            const int nt = tg + NG * lt;
             if (16 * nt > yhi || 16 * nt + 15 < ylo) continue;
             const int yy = 16 * nt + n16;
 #pragma unroll
@@ -1043,7 +1048,7 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
                 const int j = 4 * (w * WQ + wq) + q;
                 float da[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
                 float ndl = 0.0f, ndt = 0.0f;
-                if (b.live[nt] && b.m[nt]) {
+                if (b.live[lt] && b.m[lt]) {
                     float g[5], dyv, cv, cL, cT;
                     if constexpr (STAGE) {
                         const T* row = reinterpret_cast<const T*>(&ist[s & 1][yy * PB]);
@@ -1052,15 +1057,15 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
                         dyv = ld1f<T>(row + 5 * H + j);
                         cv = reinterpret_cast<const float*>(&ist[s & 1][yy * PB + CC])[j];
                         const u32x4* prv = &ist[(s - 1) & 1][0];
-                        cL = b.hasl[nt] ? reinterpret_cast<const float*>(prv + yy * PB + CC)[j] : 0.0f;
-                        cT = b.hast[nt] ? reinterpret_cast<const float*>(prv + max(yy - 1, 0) * PB + CC)[j] : 0.0f;
+                        cL = b.hasl[lt] ? reinterpret_cast<const float*>(prv + yy * PB + CC)[j] : 0.0f;
+                        cT = b.hast[lt] ? reinterpret_cast<const float*>(prv + max(yy - 1, 0) * PB + CC)[j] : 0.0f;
                     } else {
 #pragma unroll
-                        for (int t = 0; t < 5; ++t) g[t] = ld1f<T>(&b.g[nt][wq][t]);
-                        dyv = ld1f<T>(&b.dy[nt][wq]);
-                        cv = b.c[nt][wq];
-                        cL = b.hasl[nt] ? b.cl[nt][wq] : 0.0f;
-                        cT = b.hast[nt] ? b.ct[nt][wq] : 0.0f;
+                        for (int t = 0; t < 5; ++t) g[t] = ld1f<T>(&b.g[lt][wq][t]);
+                        dyv = ld1f<T>(&b.dy[lt][wq]);
+                        cv = b.c[lt][wq];
+                        cL = b.hasl[lt] ? b.cl[lt][wq] : 0.0f;
+                        cT = b.hast[lt] ? b.ct[lt][wq] : 0.0f;
                     }
                     const float gi = g[0], gfl = g[1], gft = g[2], go = g[3], gg = g[4];
                     float gl = 0.0f, gtv = 0.0f;
@@ -1071,7 +1076,7 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
                     }
                     const float dh = dyv + gl + gtv;
                     const float tc = tanh_fast(cv);
-                    const float dc = dcl[nt][wq] + dct[yy + 1][j] + dh * go * (1.0f - tc * tc);
+                    const float dc = dcl[lt][wq] + dct[yy + 1][j] + dh * go * (1.0f - tc * tc);
                     da[0] = dc * gg * gi * (1.0f - gi);
                     da[1] = dc * cL * gfl * (1.0f - gfl);
                     da[2] = dc * cT * gft * (1.0f - gft);
@@ -1082,8 +1087,8 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
                 }
 #pragma unroll
                 for (int t = 0; t < 5; ++t) dabuf[yy][t * H + j] = from_f<T>(da[t]);
-                dcl[nt][wq] = ndl;
-                dcn[nt][wq] = ndt;
+                dcl[lt][wq] = ndl;
+                dcn[lt][wq] = ndt;
             }
         }
         lds_barrier();
@@ -1091,9 +1096,10 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
         // predecessors, on MFMA; issued first so that the memory work below
         // runs behind it. Staged, tiles outside the diagonal are computed too
         // (their results are not used), which keeps the MFMAs in one block.
-        floatx4 acc[NT][TPW];
+        floatx4 acc[TPG][TPW];
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int lt = 0; lt < TPG; ++lt) {
+            const int nt = tg + NG * lt;
             if (!STAGE && (16 * nt > yhi || 16 * nt + 15 < ylo)) continue;
             const int yy = 16 * nt + n16;
             const T* brow = &dabuf[yy][q * KRUNB + sb * BSTEP * O::PER];
@@ -1102,9 +1108,9 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
             for (int ks = 0; ks < BSTEP; ++ks) bop[ks] = O::lds(brow + ks * O::PER);
 #pragma unroll
             for (int tt = 0; tt < TPW; ++tt) {
-                acc[nt][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
+                acc[lt][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ks = 0; ks < BSTEP; ++ks) acc[nt][tt] = O::mma(A[tt][ks], bop[ks], acc[nt][tt]);
+                for (int ks = 0; ks < BSTEP; ++ks) acc[lt][tt] = O::mma(A[tt][ks], bop[ks], acc[lt][tt]);
             }
         }
         // The rows of dabuf are the gate gradients of the diagonal's cells:
@@ -1135,23 +1141,24 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
         // the unread last rows), so the MFMA results are read in the same
         // straight-line block that produced them.
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int lt = 0; lt < TPG; ++lt) {
+            const int nt = tg + NG * lt;
             const bool act = !(16 * nt > yhi || 16 * nt + 15 < ylo);
             const int yy = act ? 16 * nt + n16 : NT * 16 + 1;
 #pragma unroll
             for (int tt = 0; tt < TPW; ++tt) {
                 const int k0 = 16 * (mt0 + tt) + 4 * q;
                 float* gp = (act && k0 < 2 * H) ? &gbuf[sb][yy][k0] : &gbuf[sb][NT * 16 + 1][0];
-                *reinterpret_cast<float2*>(gp) = make_float2(acc[nt][tt][0], acc[nt][tt][1]);
-                *reinterpret_cast<float2*>(gp + 2) = make_float2(acc[nt][tt][2], acc[nt][tt][3]);
+                *reinterpret_cast<float2*>(gp) = make_float2(acc[lt][tt][0], acc[lt][tt][1]);
+                *reinterpret_cast<float2*>(gp + 2) = make_float2(acc[lt][tt][2], acc[lt][tt][3]);
             }
 #pragma unroll
-            for (int wq = 0; wq < WQ; ++wq) dct[yy][act ? 4 * (w * WQ + wq) + q : 0] = dcn[nt][wq];
+            for (int wq = 0; wq < WQ; ++wq) dct[yy][act ? 4 * (w * WQ + wq) + q : 0] = dcn[lt][wq];
         }
         lds_barrier();
     };
 
-    BPre<NT, WQ, T> b0, b1;
+    BPre<TPG, WQ, T> b0, b1;
     if constexpr (STAGE) {
         // Before step s: rows of diagonals s and s - 1 in LDS, rows of s - 2
         // loading, cells of s in registers.
@@ -1162,7 +1169,7 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
         fetch_rows(steps - 3);
         fetch(steps - 1, b0);
         lds_barrier();
-        auto step = [&](int s, const BPre<NT, WQ, T>& cur, BPre<NT, WQ, T>& nxt) {
+        auto step = [&](int s, const BPre<TPG, WQ, T>& cur, BPre<TPG, WQ, T>& nxt) {
             fetch(s - 1, nxt);
             compute(s, cur);
         };
@@ -1170,7 +1177,7 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
             step(s, b0, b1);
             if (s - 1 >= 0) step(s - 1, b1, b0);
         }
-    } else if constexpr (Prefetch2<T>::template on<NT, WQ>()) {
+    } else if constexpr (Prefetch2<T>::template on<TPG, WQ>()) {
         lds_barrier();
         fetch(steps - 1, b0);
         int s = steps - 1;
@@ -1434,7 +1441,7 @@ k_wave_fwd(WaveArgs a) {
 }
 
 template <int H, int NT, typename T, bool QUEUE>
-__global__ void __launch_bounds__((64 * Geo<H, T>::NW))
+__global__ void __launch_bounds__((64 * Geo<H, T>::NW * TileGroups<H, NT, T>::NG))
 k_wave_bwd(WaveArgs a) {
     run_units<H, NT, T, false, QUEUE>(a);
 }
@@ -1453,12 +1460,12 @@ constexpr bool bwd_fits() {
 
 template <int H, int NT, typename T>
 static void launch_unit(bool fwd, int n_groups, const WaveArgs& a, hipStream_t s) {
-    const dim3 grid(n_groups), block(64 * Geo<H, T>::NW), fblock(64 * Geo<H, T>::NW * TileGroups<H, NT, T>::NG);
+    const dim3 grid(n_groups), block(64 * Geo<H, T>::NW * TileGroups<H, NT, T>::NG);
     if (a.queue) {
-        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, true>), grid, fblock, 0, s, a);
+        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, true>), grid, block, 0, s, a);
         else if constexpr (bwd_fits<H, NT, T>()) hipLaunchKernelGGL((k_wave_bwd<H, NT, T, true>), grid, block, 0, s, a);
     } else {
-        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, false>), grid, fblock, 0, s, a);
+        if (fwd) hipLaunchKernelGGL((k_wave_fwd<H, NT, T, false>), grid, block, 0, s, a);
         else if constexpr (bwd_fits<H, NT, T>()) hipLaunchKernelGGL((k_wave_bwd<H, NT, T, false>), grid, block, 0, s, a);
     }
 }
