@@ -55,7 +55,7 @@ def _parse():
 
 
 def algorithmic(wl, n_cells: int, unit_cells: int, n_units: int = 0, cus: int = 256):
-    """Algorithmic bytes and flops per launch of each kernel (see DESIGN.md).
+    """Algorithmic bytes and flops per launch of each kernel.
 
     unit_cells: cells covered by the scheduling rectangles (x4 directions below).
     n_cells: canvas cells (the dense GEMMs run over the whole canvas).
@@ -292,8 +292,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} (WORLD_SIZE {world}) is not supported; the layer has "
-              "no multi-GPU path in this build (examples would be split across GPUs with an all-reduce of the "
-              "weight gradients, see DESIGN.md)", file=sys.stderr)
+              "no multi-GPU path (examples would be split across GPUs with an all-reduce of the weight "
+              "gradients)", file=sys.stderr)
         sys.exit(2)
     import torch
 
