@@ -34,7 +34,11 @@ struct PK<float> {  // 16x16x4 f32: K step ks, slot g holds k = g*KS + ks
     static __device__ __forceinline__ Op lds(const float* p) { return *p; }
     static __device__ __forceinline__ Op gload(const float* row, int k, int C) { return k < C ? row[k] : 0.0f; }
     static __device__ __forceinline__ floatx4 mma(Op a, Op b, floatx4 c) { return mfma_f32(a, b, c); }
-    static __device__ __forceinline__ void st4(float* p, floatx4 v) { St<float>::st4(p, v); }
+    // non-temporal: Z is far larger than the caches and is next read by the
+    // wavefront; streaming it past them measured faster for the whole step
+    static __device__ __forceinline__ void st4(float* p, floatx4 v) {
+        __builtin_nontemporal_store(v, reinterpret_cast<floatx4*>(p));
+    }
 };
 template <>
 struct PK<bf16_t> {  // 16x16x32 bf16: K step ks, slot g holds k = 32 ks + 8 g + e

@@ -1133,8 +1133,10 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
                 stage_in(s - 2);
                 fetch_rows(s - 3);
             }
+            // non-temporal: the gate gradients are read again only by the
+            // gradient GEMMs after the whole wavefront
 #pragma unroll
-            for (int it = 0; it < NITF; ++it) *reinterpret_cast<u32x4*>(dst[it]) = v[it];
+            for (int it = 0; it < NITF; ++it) __builtin_nontemporal_store(v[it], reinterpret_cast<u32x4*>(dst[it]));
         }
         // The products and the dc of the top predecessors go to LDS without
         // branches (tiles outside the diagonal and padding columns write to
