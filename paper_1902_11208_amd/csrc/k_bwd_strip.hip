@@ -70,6 +70,11 @@ template <>
 struct V4<float> {
     using R = float4;
     static __device__ __forceinline__ R load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+    // non-temporal load, for data read once (keeps the re-read Y rows cached)
+    static __device__ __forceinline__ R ldnt(const float* p) {
+        const floatx4 v = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(p));
+        return make_float4(v[0], v[1], v[2], v[3]);
+    }
     static __device__ __forceinline__ float4 f(R v) { return v; }
     static __device__ __forceinline__ void store(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
 };
@@ -77,6 +82,10 @@ template <>
 struct V4<bf16_t> {
     using R = uint2;
     static __device__ __forceinline__ R load(const bf16_t* p) { return *reinterpret_cast<const uint2*>(p); }
+    static __device__ __forceinline__ R ldnt(const bf16_t* p) {
+        const uint64_t v = __builtin_nontemporal_load(reinterpret_cast<const uint64_t*>(p));
+        return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+    }
     static __device__ __forceinline__ float4 f(R v) {
         return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
                            __uint_as_float(v.y & 0xffff0000u));
@@ -187,7 +196,7 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
         for (int k = 0; k < PZ * (parts & 1); ++k) {
             const int e = min(tid + k * NTH, NZ - 1);
             const int c = (4 * e) / N, n = 4 * e - c * N;
-            vz[k] = L4::load(dZ + (p0 + min(c, len - 1)) * N + n);
+            vz[k] = L4::ldnt(dZ + (p0 + min(c, len - 1)) * N + n);
         }
 #pragma unroll
         for (int k = 0; k < PY * ((parts >> 1) & 1); ++k) {
