@@ -51,7 +51,12 @@ struct PK<bf16_t> {  // 16x16x32 bf16: K step ks, slot g holds k = 32 ks + 8 g +
         return as_bf16x8(k < C ? *reinterpret_cast<const uint4*>(row + k) : make_uint4(0, 0, 0, 0));
     }
     static __device__ __forceinline__ floatx4 mma(Op a, Op b, floatx4 c) { return mfma_bf16(a, b, c); }
-    static __device__ __forceinline__ void st4(bf16_t* p, floatx4 v) { St<bf16_t>::st4(p, v); }
+    // non-temporal, as for fp32: four bf16 values as one 8-byte store
+    static __device__ __forceinline__ void st4(bf16_t* p, floatx4 v) {
+        const uint64_t lo = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+        const uint64_t hi = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+        __builtin_nontemporal_store(lo | (hi << 32), reinterpret_cast<uint64_t*>(p));
+    }
 };
 
 }  // namespace
