@@ -45,7 +45,9 @@ struct StripCfg {
     static constexpr int CXT = (C + 15) / 16;         // dX channel tiles
     static constexpr int WPD = H >= 32 ? 2 : 1;       // waves per direction
     static constexpr int RTW = (RT + WPD - 1) / WPD;  // gate-row tiles per wave
-    static constexpr int TC = H >= 32 ? 16 : 32;      // cells per strip
+    // cells per strip: 16 where the registers need it (H >= 32) or where two
+    // workgroups then fit on a CU (H = 16 with 16 input channels), else 32
+    static constexpr int TC = (H >= 32 || (H == 16 && C >= 16)) ? 16 : 32;
     static constexpr int THREADS = 256 * WPD;
     static constexpr int ZP = N + 4;                  // LDS pitch of dZ rows (4 mod 16: the cells read by one MFMA hit distinct banks)
     static constexpr int YP = 4 * H + 4;              // LDS pitch of Y rows
@@ -53,10 +55,11 @@ struct StripCfg {
     static constexpr int SY = 3 * (TC + 2) * YP, SDX = 4 * TC * XP;
     static constexpr int HW = TC + 2;                 // halo block width
     // The next strip's loads are prefetched into registers where the dW tiles
-    // leave room; those shapes use over 256 registers per lane (one
-    // workgroup per CU), the others run two workgroups per CU.
+    // leave room (H <= 16). With 32-cell strips at H = 16 that takes over 256
+    // registers per lane (one workgroup per CU); the 16-cell strips of H = 16
+    // with 16 input channels and the other shapes run two workgroups per CU.
     static constexpr bool PREFETCH = H <= 16;
-    static constexpr int WGS = H == 16 ? 256 : 512;
+    static constexpr int WGS = (H == 16 && TC == 32) ? 256 : 512;
     // register budget of the H = 32 shapes: dW steps unrolled by two, dX
     // operands read five blocks at a time
     static constexpr int DW_UNROLL = H >= 32 ? 2 : TC / 4;
@@ -483,7 +486,14 @@ k_strip_reduce(int C, int H, int RT, int PP, int CT, int nwg, const float* __res
     X(float, 4, 4) X(float, 4, 8) X(float, 8, 8) X(float, 16, 8) X(float, 16, 16) X(float, 32, 16) \
     X(float, 32, 32) X(bf16_t, 32, 16) X(bf16_t, 32, 32)
 
-static int strip_tc(int hidden) { return hidden >= 32 ? 16 : 32; }
+static int strip_tc(const LayerGeom& g) {
+    int tc = 0;
+#define MDL_STRIP_TC(T, H, C) \
+    if (!tc && (g.dtype == 1) == std::is_same<T, bf16_t>::value && g.hidden == H && g.c_in == C) tc = StripCfg<H, C>::TC;
+    MDL_STRIP_SHAPES(MDL_STRIP_TC)
+#undef MDL_STRIP_TC
+    return tc > 0 ? tc : 32;
+}
 
 bool strip_supported(const LayerGeom& g) {
 #define MDL_STRIP_MATCH(T, H, C) \
@@ -494,7 +504,7 @@ bool strip_supported(const LayerGeom& g) {
 }
 
 static int strip_wgs(const LayerGeom& g) {
-    const int tc = strip_tc(g.hidden);
+    const int tc = strip_tc(g);
     const int64_t strips = (int64_t)g.canvas_h * ((g.canvas_w + tc - 1) / tc);
     int wgs = 0;
 #define MDL_STRIP_WGS(T, H, C) \
@@ -514,7 +524,7 @@ size_t strip_partial_bytes(const LayerGeom& g) {
 hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y, const void* d_wx,
                             const uint8_t* d_mask, const int32_t* d_rid, void* d_dx, float* d_part, float* d_dwx,
                             float* d_du, float* d_db, hipStream_t s) {
-    const int tc = strip_tc(g.hidden);
+    const int tc = strip_tc(g);
     const int segs = (g.canvas_w + tc - 1) / tc;
     const int n_strips = g.canvas_h * segs;
     const int nwg = strip_wgs(g);

@@ -70,6 +70,7 @@ SMALL = [
     ("H4_ragged", [3, 5, 2, 1], [4, 7, 9, 1], 16, 4, 4, "f32"),
     ("H8_two_tiles", [17, 5, 1], [20, 3, 30], 32, 8, 8, "f32"),
     ("H16_tall_narrow", [40, 9, 16], [5, 40, 16], 64, 16, 16, "f32"),
+    ("H16_c16_ragged_strips", [7, 12, 3, 1], [23, 9, 30, 2], 50, 16, 16, "f32"),
     ("H16_two_tiles_c8", [32, 20, 17, 3], [30, 50, 9, 12], 128, 8, 16, "f32"),
     ("H32_c16", [16, 9, 5], [40, 25, 60], 96, 16, 32, "f32"),
     ("H32_three_tiles", [40, 33, 2], [37, 50, 3], 96, 32, 32, "f32"),
