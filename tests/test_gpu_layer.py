@@ -71,6 +71,7 @@ SMALL = [
     ("H8_two_tiles", [17, 5, 1], [20, 3, 30], 32, 8, 8, "f32"),
     ("H16_tall_narrow", [40, 9, 16], [5, 40, 16], 64, 16, 16, "f32"),
     ("H16_c16_ragged_strips", [7, 12, 3, 1], [23, 9, 30, 2], 50, 16, 16, "f32"),
+    ("H16_four_tiles", [64, 50, 7], [12, 20, 33], 72, 8, 16, "f32"),
     ("H16_two_tiles_c8", [32, 20, 17, 3], [30, 50, 9, 12], 128, 8, 16, "f32"),
     ("H32_c16", [16, 9, 5], [40, 25, 60], 96, 16, 32, "f32"),
     ("H32_three_tiles", [40, 33, 2], [37, 50, 3], 96, 32, 32, "f32"),
@@ -117,6 +118,31 @@ def test_wide_layer_unit_queue():
     for rep in range(2):
         gpu = gpu_run.run_layer(xs, params, dys, hs, ws, 64, dtype="bf16")
         _compare(gpu, ref, "bf16", label=f"wide-layer queue, call {rep}")
+
+
+@pytest.mark.parametrize("case", ["H32_two_tiles", "H16_four_tiles"])
+def test_tile_groups_unit_queue(case):
+    """fp32 units of two or four 16-row tiles, one wave group per tile, with
+    at least one unit per CU so that both wavefronts take units from the
+    device queue (two calls: the queue is left zeroed)."""
+    import gpu_run
+    import oracle_run
+    from synth.configs import custom_workload
+
+    rng = np.random.default_rng(11)
+    if case == "H32_two_tiles":
+        n, hs, ws, c_in, H = 72, rng.integers(17, 33, 72), rng.integers(2, 11, 72), 16, 32
+    else:
+        n, hs, ws, c_in, H = 64, rng.integers(49, 65, 64), rng.integers(2, 7, 64), 16, 16
+    hs, ws = hs.tolist(), ws.tolist()
+    wl = custom_workload(66 if H == 32 else 67, hs, ws, 64, c_in, H, "f32")
+    _say(f"case tile-group queue {case}: {n} examples, {4 * n} units, H={H} fp32")
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    ref = oracle_run.run_layer(xs, params, dys, workers=oracle_run.default_workers())
+    for rep in range(2):
+        gpu = gpu_run.run_layer(xs, params, dys, hs, ws, 64, dtype="f32")
+        _compare(gpu, ref, "f32", label=f"tile-group queue {case}, call {rep}")
 
 
 def test_config1_forward():
