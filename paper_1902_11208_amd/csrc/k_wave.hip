@@ -1419,8 +1419,10 @@ __device__ __forceinline__ void run_units(const WaveArgs& a) {
         lds_barrier();
         const int k = slot;
         if (k >= a.n_units) break;
+        // forward: two steps of prefetch, except where tile groups at H >= 32
+        // leave too few registers (1024 threads) and one step measured faster
         if constexpr (FWD && FwdBig<H, T>::on) wave_fwd_big<H, NT, T>(a, a.units[k]);
-        else if (FWD) wave_fwd_unit<H, NT, T, 2>(a, a.units[k]);
+        else if (FWD) wave_fwd_unit<H, NT, T, (TileGroups<H, NT, T>::NG > 1 && H >= 32) ? 1 : 2>(a, a.units[k]);
         else if constexpr (BwdBig<H, T>::on) wave_bwd_big<H, NT, T>(a, a.units[k]);
         else wave_bwd_unit<H, NT, T>(a, a.units[k]);
     }
