@@ -22,7 +22,9 @@ thread_local std::string g_last_error;
 thread_local hipEvent_t g_phase_events[8];
 thread_local bool g_phase_on = false;
 
-hipError_t mark(int i, hipStream_t s) { return g_phase_on ? hipEventRecord(g_phase_events[i], s) : hipSuccess; }
+hipError_t mark(int i, hipStream_t s) {
+    return g_phase_on && g_phase_events[i] ? hipEventRecord(g_phase_events[i], s) : hipSuccess;
+}
 
 mdlstm_status fail(mdlstm_status st, const char* fmt, ...) {
     char buf[512];
@@ -285,10 +287,7 @@ mdlstm_status mdlstm_set_phase_events(int32_t n, void* const* events) {
         return MDLSTM_OK;
     }
     if (n != 8 || !events) return fail(MDLSTM_ERR_INVALID_ARG, "phase events: n must be 0 or 8");
-    for (int i = 0; i < 8; ++i) {
-        if (!events[i]) return fail(MDLSTM_ERR_INVALID_ARG, "phase event %d is NULL", i);
-        g_phase_events[i] = reinterpret_cast<hipEvent_t>(events[i]);
-    }
+    for (int i = 0; i < 8; ++i) g_phase_events[i] = reinterpret_cast<hipEvent_t>(events[i]);  // NULL: not recorded
     g_phase_on = true;
     return MDLSTM_OK;
 }

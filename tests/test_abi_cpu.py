@@ -56,6 +56,16 @@ def test_pack_layout_errors(built_lib):
     assert st == 0 and ch == 0
 
 
+def test_phase_events_argument_checks(built_lib):
+    """n must be 0 or 8 and the array present; NULL entries are allowed (not
+    recorded). Setting and clearing touch no device."""
+    L = _lib().lib()
+    assert L.mdlstm_set_phase_events(3, (ctypes.c_void_p * 8)()) == 1
+    assert L.mdlstm_set_phase_events(8, None) == 1
+    assert L.mdlstm_set_phase_events(8, (ctypes.c_void_p * 8)()) == 0
+    assert L.mdlstm_set_phase_events(0, None) == 0
+
+
 def _fwd(desc, ch, cw, rects, ws_bytes=None):
     L = _lib()
     arr = (L.Rect * max(1, len(rects)))(*[L.Rect(*r) for r in rects])
