@@ -61,6 +61,21 @@ def _check_dev(t: torch.Tensor, name: str):
         raise ValueError(f"{name} must be contiguous")
 
 
+def check_tensor(t, name: str, shape, dtype: torch.dtype, device=None):
+    """Reject a tensor whose shape, dtype or device differs from what the C ABI
+    will assume: the library sees only pointers, so a wrong buffer would be
+    read or written past its end by the kernels."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch.Tensor")
+    if tuple(t.shape) != tuple(int(v) for v in shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(int(v) for v in shape)}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    _check_dev(t, name)
+    if device is not None and t.device != torch.device(device):
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
 # ---------------------------------------------------------------------------
 # Packing
 # ---------------------------------------------------------------------------
@@ -125,6 +140,8 @@ def pack_data(examples, rects, canvas_h: int, canvas_w: int, stream=None, out=No
         _check_dev(e, f"example {k}")
         if e.dtype != dt or e.shape != (r[k, 2], r[k, 3], c):
             raise ValueError(f"example {k} has shape {tuple(e.shape)}, rect says {tuple(r[k, 2:])}x{c}")
+    if out is not None:
+        check_tensor(out, "out", (canvas_h, canvas_w, c), dt, dev)
     canvas = out if out is not None else torch.empty((canvas_h, canvas_w, c), dtype=dt, device=dev)
     ptrs = (ctypes.c_void_p * n)(*[e.data_ptr() for e in examples])
     work = torch.empty(pack_workspace_bytes(n), dtype=torch.uint8, device=dev)
@@ -209,13 +226,17 @@ class MDLSTMLayer:
 
     def __init__(self, wx: torch.Tensor, u: torch.Tensor, b: torch.Tensor, canvas_h: int, canvas_w: int, rects,
                  mask: torch.Tensor):
-        for t, nm in ((wx, "wx"), (u, "u"), (b, "b"), (mask, "mask")):
-            _check_dev(t, nm)
+        if wx.dim() != 3 or u.dim() != 3:
+            raise ValueError("wx must be [4, 5H, c_in] and u [4, 5H, 2H]")
         self.dtype = dtype_code(wx.dtype)
         self.hidden = int(u.shape[2]) // 2
         self.c_in = int(wx.shape[2])
+        H, td, dev = self.hidden, wx.dtype, wx.device
+        check_tensor(wx, "wx", (4, 5 * H, self.c_in), td)
+        check_tensor(u, "u", (4, 5 * H, 2 * H), td, dev)
+        check_tensor(b, "b", (4, 5 * H), td, dev)
+        check_tensor(mask, "mask", (canvas_h, canvas_w), torch.uint8, dev)
         self.wx, self.u, self.b, self.mask = wx, u, b, mask
-        dev = wx.device
         self.prep = Prepared(self.c_in, self.hidden, self.dtype, canvas_h, canvas_w, rects)
         self.workspace = torch.empty(max(1, self.prep.ws_bytes), dtype=torch.uint8, device=dev)
         td = wx.dtype
@@ -226,20 +247,26 @@ class MDLSTMLayer:
         self.du = torch.empty((4, 5 * H, 2 * H), dtype=torch.float32, device=dev)
         self.db = torch.empty((4, 5 * H), dtype=torch.float32, device=dev)
 
+    def _check_x(self, x):
+        check_tensor(x, "x", (self.prep.canvas_h, self.prep.canvas_w, self.c_in), self.wx.dtype, self.wx.device)
+
     def forward(self, x: torch.Tensor, stream=None) -> torch.Tensor:
-        _check_dev(x, "x")
+        self._check_x(x)
         self.x = x
         forward(self.prep, x, self.mask, self.wx, self.u, self.b, self.y, self.workspace, stream)
         return self.y
 
     def forward_stepwise(self, x: torch.Tensor, stream=None) -> torch.Tensor:
-        _check_dev(x, "x")
+        self._check_x(x)
         self.x = x
         forward_stepwise(self.prep, x, self.mask, self.wx, self.u, self.b, self.y, self.workspace, stream)
         return self.y
 
     def backward(self, dy: torch.Tensor, stream=None):
-        _check_dev(dy, "dy")
+        if getattr(self, "x", None) is None:
+            raise ValueError("backward needs a forward call on this layer first")
+        check_tensor(dy, "dy", (self.prep.canvas_h, self.prep.canvas_w, 4 * self.hidden), self.wx.dtype,
+                     self.wx.device)
         backward(self.prep, self.x, self.mask, self.wx, self.u, self.b, self.y, dy, self.dx, self.dwx, self.du,
                  self.db, self.workspace, stream)
         return self.dx, self.dwx, self.du, self.db
@@ -262,6 +289,8 @@ def pack_blocks(images, rects, canvas_h: int, canvas_w: int, bh: int, bw: int, o
         _check_dev(im, f"image {k}")
         if im.dtype != torch.float32 or tuple(im.shape) != (r[k, 2] * bh, r[k, 3] * bw, c):
             raise ValueError(f"image {k} has shape {tuple(im.shape)}, rect says {r[k, 2] * bh}x{r[k, 3] * bw}x{c}")
+    if out is not None:
+        check_tensor(out, "out", (canvas_h, canvas_w, bh * bw * c), torch.float32, dev)
     canvas = out if out is not None else torch.empty((canvas_h, canvas_w, bh * bw * c), dtype=torch.float32,
                                                      device=dev)
     ptrs = (ctypes.c_void_p * max(1, n))(*[im.data_ptr() for im in images])
@@ -278,11 +307,13 @@ class BlockConv:
 
     def __init__(self, w: torch.Tensor, b: torch.Tensor, in_rects, in_hw, out_rects, out_hw, bh: int = 2,
                  bw: int = 4):
-        _check_dev(w, "w")
-        _check_dev(b, "b")
-        self.w, self.b = w, b
+        if w.dim() != 3 or int(w.shape[2]) % (bh * bw):
+            raise ValueError("w must be [4, og, bh*bw*hidden]")
         self.og = int(w.shape[1])
         self.hidden = int(w.shape[2]) // (bh * bw)
+        check_tensor(w, "w", (4, self.og, bh * bw * self.hidden), torch.float32)
+        check_tensor(b, "b", (4, self.og), torch.float32, w.device)
+        self.w, self.b = w, b
         self.bh, self.bw = int(bh), int(bw)
         self.in_np = np.asarray(in_rects, np.int32).reshape(-1, 4)
         self.out_np = np.asarray(out_rects, np.int32).reshape(-1, 4)
@@ -298,7 +329,7 @@ class BlockConv:
         self.db = torch.empty_like(b)
 
     def forward(self, y: torch.Tensor, stream=None) -> torch.Tensor:
-        _check_dev(y, "y")
+        check_tensor(y, "y", (self.in_h, self.in_w, 4 * self.hidden), torch.float32, self.w.device)
         self.y = y
         check(lib().mdlstm_block_conv_forward(self.n, self.hidden, self.og, self.bh, self.bw, self.in_rects, self.in_h,
                                               self.in_w, _ptr(y), _ptr(self.w), _ptr(self.b), self.out_rects,
@@ -307,7 +338,9 @@ class BlockConv:
         return self.out
 
     def backward(self, dout: torch.Tensor, stream=None):
-        _check_dev(dout, "dout")
+        if getattr(self, "y", None) is None:
+            raise ValueError("backward needs a forward call on this convolution first")
+        check_tensor(dout, "dout", (self.out_h, self.out_w, 4 * self.og), torch.float32, self.w.device)
         check(lib().mdlstm_block_conv_backward(self.n, self.hidden, self.og, self.bh, self.bw, self.in_rects,
                                                self.in_h, self.in_w, _ptr(self.y), _ptr(self.w), self.out_rects,
                                                self.out_h, self.out_w, _ptr(self.out), _ptr(dout), _ptr(self.dy),

@@ -27,8 +27,11 @@ def layout(heights, widths, canvas_w, kind="packed"):
     return tiles, place, ch, cw, mask
 
 
-def run_layer(xs, params, dys, heights, widths, canvas_w, dtype="f32", kind="packed", backward=True):
-    """xs/dys: per-example numpy arrays. Returns dict with per-example Y (and dX) and summed dW."""
+def run_layer(xs, params, dys, heights, widths, canvas_w, dtype="f32", kind="packed", backward=True, keep=None):
+    """xs/dys: per-example numpy arrays. Returns dict with per-example Y (and dX) and summed dW.
+
+    keep: indices of the examples whose Y and dX are copied back (all by
+    default); the others' entries are None. The whole batch always runs."""
     units, place, ch, cw, mask = layout(heights, widths, canvas_w, kind)
     wx, u, b = (to_dev(p, dtype) for p in params)
     ex = [to_dev(x, dtype) for x in xs]
@@ -37,12 +40,13 @@ def run_layer(xs, params, dys, heights, widths, canvas_w, dtype="f32", kind="pac
     y = layer.forward(canvas)
     out = {"rects": place, "canvas_h": ch, "canvas_w": cw, "mask": mask, "layer": layer,
            "y_canvas": y.clone()}
-    out["Y"] = [to_np(t) for t in api.unpack_data(y, place)]
+    ks = set(range(len(xs))) if keep is None else set(int(k) for k in keep)
+    out["Y"] = [to_np(t) if k in ks else None for k, t in enumerate(api.unpack_data(y, place))]
     if backward:
         dyc = api.pack_data([to_dev(g, dtype) for g in dys], place, ch, cw)
         dx, dwx, du, db = layer.backward(dyc)
         torch.cuda.synchronize()
-        out["dX"] = [to_np(t) for t in api.unpack_data(dx, place)]
+        out["dX"] = [to_np(t) if k in ks else None for k, t in enumerate(api.unpack_data(dx, place))]
         out["dx_canvas"] = dx.clone()
         out["dWx"], out["dU"], out["db"] = to_np(dwx), to_np(du), to_np(db)
     torch.cuda.synchronize()

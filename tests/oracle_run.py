@@ -26,15 +26,31 @@ def default_workers() -> int:
     return max(1, min(16, n))
 
 
-def run_layer(xs, params, dys, backward=True, workers=1):
+def _pool_map(fn, jobs, workers, progress):
+    """fn over jobs in a fork pool, results in job order; with `progress`, a
+    line per finished job (long oracle runs stay visibly alive)."""
+    if workers <= 1 or len(jobs) <= 1:
+        out = []
+        for i, j in enumerate(jobs):
+            out.append(fn(j))
+            if progress:
+                print(f"{progress}: {i + 1}/{len(jobs)} done", flush=True)
+        return out
+    results = [None] * len(jobs)
+    with cf.ProcessPoolExecutor(workers, mp_context=mp.get_context("fork")) as ex:
+        futs = {ex.submit(fn, j): i for i, j in enumerate(jobs)}
+        for done, f in enumerate(cf.as_completed(futs), 1):
+            results[futs[f]] = f.result()
+            if progress:
+                print(f"{progress}: job {futs[f]} finished, {done}/{len(jobs)}", flush=True)
+    return results
+
+
+def run_layer(xs, params, dys, backward=True, workers=1, progress=None):
     """Per example, each computed alone: Y (and dX), plus weight gradients summed over examples."""
     p64 = [np.asarray(t, np.float64) for t in params]
     jobs = [(x, p64, (dys[k] if backward else None), backward) for k, x in enumerate(xs)]
-    if workers > 1 and len(jobs) > 1:
-        with cf.ProcessPoolExecutor(workers, mp_context=mp.get_context("fork")) as ex:
-            results = list(ex.map(_one, jobs))
-    else:
-        results = [_one(j) for j in jobs]
+    results = _pool_map(_one, jobs, workers, progress)
     out = {"Y": [r[0] for r in results], "dX": []}
     if backward:
         H = params[1].shape[2] // 2
@@ -57,16 +73,12 @@ def _stack_one(args):
     return Y3, lg, cg, g
 
 
-def run_stack(images, layers, convs, dys, block=(2, 4), workers=1):
+def run_stack(images, layers, convs, dys, block=(2, 4), workers=1, progress=None):
     """Per image, alone: last output Y3, input-block gradient, and the summed layer/conv gradients."""
     l64 = [tuple(np.asarray(t, np.float64) for t in p) for p in layers]
     c64 = [tuple(np.asarray(t, np.float64) for t in p) for p in convs]
     jobs = [(np.asarray(im, np.float64), l64, c64, dys[k], block) for k, im in enumerate(images)]
-    if workers > 1 and len(jobs) > 1:
-        with cf.ProcessPoolExecutor(workers, mp_context=mp.get_context("fork")) as ex:
-            results = list(ex.map(_stack_one, jobs))
-    else:
-        results = [_stack_one(j) for j in jobs]
+    results = _pool_map(_stack_one, jobs, workers, progress)
     out = {"Y": [r[0] for r in results], "dX0": [r[3] for r in results]}
     lsum = [[np.zeros_like(a) for a in results[0][1][i]] for i in range(len(layers))]
     csum = [[np.zeros_like(a) for a in results[0][2][i]] for i in range(len(convs))]

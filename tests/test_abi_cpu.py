@@ -151,3 +151,59 @@ def test_pack_blocks_rejects_bad_arguments(built_lib):
     assert f(1, ctypes.cast(imgs, L.P_VOIDP), 1, 2, 4, r, 2, 2, FAKE, FAKE, 16, None) == 4     # workspace
     assert f(1, ctypes.cast(imgs, L.P_VOIDP), 1, 2, 4, r, 1, 2, FAKE, FAKE, need, None) == 3   # leaves canvas
     assert f(1, ctypes.cast(imgs, L.P_VOIDP), 0, 2, 4, r, 2, 2, FAKE, FAKE, need, None) == 1   # c < 1
+
+
+def test_binding_rejects_wrong_tensors():
+    """The Python binding checks shape, dtype and device before a pointer
+    reaches the C ABI (which cannot know buffer sizes)."""
+    import torch
+
+    from paper_1902_11208_amd import api
+
+    t = torch.zeros((4, 6, 8), dtype=torch.float32)
+    with pytest.raises(ValueError, match="shape"):
+        api.check_tensor(t, "x", (4, 6, 16), torch.float32)
+    with pytest.raises(ValueError, match="dtype"):
+        api.check_tensor(t.to(torch.bfloat16), "x", (4, 6, 8), torch.float32)
+    with pytest.raises(ValueError, match="device tensor"):
+        api.check_tensor(t, "x", (4, 6, 8), torch.float32)
+    with pytest.raises(ValueError, match="torch.Tensor"):
+        api.check_tensor(t.numpy(), "x", (4, 6, 8), torch.float32)
+    # a layer built from host tensors is refused before any allocation
+    H, C = 4, 8
+    with pytest.raises(ValueError):
+        api.MDLSTMLayer(torch.zeros(4, 5 * H, C), torch.zeros(4, 5 * H, 2 * H), torch.zeros(4, 5 * H), 2, 3,
+                        [[0, 0, 2, 3]], torch.zeros(2, 3, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="shape"):
+        api.MDLSTMLayer(torch.zeros(4, 5 * H, C), torch.zeros(4, 5 * H, 3 * H), torch.zeros(4, 5 * H), 2, 3,
+                        [[0, 0, 2, 3]], torch.zeros(2, 3, dtype=torch.uint8))
+
+
+def _bwd(desc, ch, cw, rects, ws_bytes=None, **over):
+    L = _lib()
+    arr = (L.Rect * max(1, len(rects)))(*[L.Rect(*r) for r in rects])
+    need = L.lib().mdlstm_workspace_bytes(ctypes.byref(desc), ch, cw, len(rects))
+    p = {k: FAKE for k in ("x", "mask", "wx", "u", "b", "y", "dy", "dx", "dwx", "du", "db", "workspace")}
+    p.update(over)
+    return L.lib().mdlstm_backward(ctypes.byref(desc), ch, cw, p["x"], p["mask"], len(rects), arr, p["wx"], p["u"],
+                                   p["b"], p["y"], p["dy"], p["dx"], p["dwx"], p["du"], p["db"], p["workspace"],
+                                   need if ws_bytes is None else ws_bytes, None)
+
+
+def test_backward_rejects_bad_arguments(built_lib):
+    """mdlstm_backward validates like mdlstm_forward, plus its gradient buffers,
+    before any HIP call."""
+    L = _lib()
+    ok = L.LayerDesc(16, 16, 0)
+    assert _bwd(L.LayerDesc(16, 12, 0), 10, 10, [(0, 0, 2, 2)]) == 5          # hidden not built
+    assert _bwd(L.LayerDesc(16, 16, 9), 10, 10, [(0, 0, 2, 2)]) == 1          # dtype
+    assert _bwd(ok, 10, 10, [(0, 0, 3, 3), (2, 2, 3, 3)]) == 3                # overlap
+    assert _bwd(ok, 10, 10, [(0, 8, 3, 3)]) == 3                              # leaves the canvas
+    assert _bwd(ok, 100, 10, [(0, 0, 65, 3)]) == 5                            # too tall
+    assert _bwd(ok, 10, 10, [(0, 0, 3, 3)], ws_bytes=16) == 4                 # workspace
+    assert _bwd(ok, 10, 10, [(0, 0, 3, 3)], workspace=None) == 1              # no workspace
+    for nm in ("dwx", "du", "db", "y", "dy", "dx"):
+        assert _bwd(ok, 10, 10, [(0, 0, 3, 3)], **{nm: None}) == 1, nm       # NULL output or input
+    for nm in ("dy", "dx", "dwx", "y"):
+        assert _bwd(ok, 10, 10, [(0, 0, 3, 3)], **{nm: FAKE + 4}) == 1, nm   # misaligned
+        assert b"aligned" in L.lib().mdlstm_last_error()

@@ -9,9 +9,9 @@ the pre-activations to 8 significant bits).
 These workloads centre the forget-gate biases at -1, which keeps the plain
 cell's state bounded. With forget gates summing to about 1 the state grows
 without bound along long scans (Section III), |c| reaching 1e5 on 600-wide
-lines; there no fp32 evaluation tracks float64 to 1e-5 (a float32 NumPy
-evaluation of the same definition is 1.8e-4 off in dX), and
-test_exploding_state_regime checks the documented looser bounds instead.
+lines; there no fp32 evaluation tracks float64 to 1e-5 in every norm (a
+float32 NumPy evaluation of the same definition is 1.8e-4 off in dX), and
+test_exploding_state_regime holds the bounds that floor allows.
 """
 import sys
 
@@ -123,20 +123,24 @@ def test_wide_layer_unit_queue():
 @pytest.mark.parametrize("case", ["H32_two_tiles", "H16_four_tiles"])
 def test_tile_groups_unit_queue(case):
     """fp32 units of two or four 16-row tiles, one wave group per tile, with
-    at least one unit per CU so that both wavefronts take units from the
-    device queue (two calls: the queue is left zeroed)."""
+    more units than the forward (one workgroup per CU) and the backward (two
+    per CU) keep resident, so both wavefronts take units from the device
+    queue; two calls, since the last workgroup leaves the queue zeroed."""
     import gpu_run
     import oracle_run
     from synth.configs import custom_workload
 
     rng = np.random.default_rng(11)
+    n = 136  # 544 units: above 2 x 256 CUs
     if case == "H32_two_tiles":
-        n, hs, ws, c_in, H = 72, rng.integers(17, 33, 72), rng.integers(2, 11, 72), 16, 32
+        hs, ws, c_in, H = rng.integers(17, 33, n), rng.integers(2, 11, n), 16, 32
     else:
-        n, hs, ws, c_in, H = 64, rng.integers(49, 65, 64), rng.integers(2, 7, 64), 16, 16
+        hs, ws, c_in, H = rng.integers(49, 65, n), rng.integers(2, 7, n), 16, 16
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    assert 4 * n > 2 * cus, "the case must exceed what two workgroups per CU hold"
     hs, ws = hs.tolist(), ws.tolist()
     wl = custom_workload(66 if H == 32 else 67, hs, ws, 64, c_in, H, "f32")
-    _say(f"case tile-group queue {case}: {n} examples, {4 * n} units, H={H} fp32")
+    _say(f"case tile-group queue {case}: {n} examples, {4 * n} units, H={H} fp32, {cus} CUs")
     xs, params = wl.examples(), wl.params()
     dys = [wl.dy(k) for k in range(wl.n)]
     ref = oracle_run.run_layer(xs, params, dys, workers=oracle_run.default_workers())
@@ -210,55 +214,67 @@ def test_output_rows_outside_rectangles_are_zeroed(case):
 
 
 def test_config3_lines_forward_backward():
-    # full batch on the GPU; per-example Y and dX checked on a seeded sample of
-    # 12 examples (the oracle takes about 2 s per example), weight gradients on
-    # a second GPU run packing just that sample
+    """The line batch (64 x h32, widths 200-600, C_in 32, H 32) in one GPU
+    run: every example's Y and dX, and the full-batch dWx/dU/db of that same
+    run, against the oracle computing each example alone."""
     import gpu_run
     import oracle_run
     from synth import configs
 
     wl = configs.workload(3)
-    _say(f"config 3: n={wl.n} H={wl.hidden} C={wl.c_in}")
+    _say(f"config 3: n={wl.n} H={wl.hidden} C={wl.c_in}, full batch")
     xs, params = wl.examples(), wl.params()
     dys = [wl.dy(k) for k in range(wl.n)]
     gpu = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w)
-    pick = sorted(np.random.default_rng(3).choice(wl.n, size=12, replace=False).tolist())
-    pick = sorted(set(pick) | {int(np.argmax(wl.widths)), int(np.argmin(wl.widths))})
-    ref = oracle_run.run_layer([xs[k] for k in pick], params, [dys[k] for k in pick],
-                               workers=oracle_run.default_workers())
-    sub = {"Y": [gpu["Y"][k] for k in pick], "dX": [gpu["dX"][k] for k in pick]}
-    _compare(sub, ref, "f32", backward=False, label="config3 sample Y")
-    _compare({"Y": sub["dX"]}, {"Y": ref["dX"]}, "f32", backward=False, label="config3 sample dX")
-    gsub = gpu_run.run_layer([xs[k] for k in pick], params, [dys[k] for k in pick], wl.heights[pick],
-                             wl.widths[pick], wl.canvas_w)
-    _compare(gsub, ref, "f32", label="config3 sample packed alone")
+    ref = oracle_run.run_layer(xs, params, dys, workers=oracle_run.default_workers(), progress="config 3 oracle")
+    _compare(gpu, ref, "f32", label="config3 full batch")
+
+
+def _bf16_stress_golden(wl):
+    """Full-batch weight gradients of the bf16 stress batch, written by
+    tests/golden/make_bf16_stress_grads.py (the float64 oracle, about an hour
+    of core time), with the digest of the inputs they were computed from."""
+    import os
+
+    sys.path.insert(0, os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden"))
+    from make_bf16_stress_grads import OUT, input_digest
+
+    if not os.path.exists(OUT):
+        pytest.fail(f"{OUT} is missing: run tests/golden/make_bf16_stress_grads.py")
+    g = np.load(OUT, allow_pickle=False)
+    assert str(g["inputs_sha256"]) == input_digest(wl), "the stored gradients were computed from other inputs"
+    return {k: np.asarray(g[k], np.float64) for k in ("dWx", "dU", "db")}
 
 
 def test_config5_bf16_forward_backward():
-    # the bf16 stress batch (128 x h48, widths 300-1200, C_in 64, H 128) at full
-    # size on the GPU; the oracle (float64 on the bf16-representable inputs)
-    # takes 15-60 s per example, so Y and dX are checked on the narrowest
-    # example and one of about 600 columns, weight gradients on a second GPU
-    # run that packs just those two
+    """The bf16 stress batch (128 x h48, widths 300-1200, C_in 64, H 128) in
+    one GPU run: the full-batch dWx/dU/db against the stored oracle result,
+    and Y and dX of 16 examples (the widest, whose 1247-diagonal scans are the
+    longest bf16 chains, the narrowest and 14 seeded picks) against the oracle
+    computing each alone, on the host's cores."""
     import gpu_run
     import oracle_run
     from synth import configs
 
     wl = configs.workload(5)
-    _say(f"config 5: n={wl.n} H={wl.hidden} C={wl.c_in} bf16, full batch")
+    golden = _bf16_stress_golden(wl)
+    pick = np.random.default_rng(5).choice(wl.n, size=14, replace=False).tolist()
+    pick = sorted(set(pick) | {int(np.argmax(wl.widths)), int(np.argmin(wl.widths))})
+    while len(pick) < 16:  # the seeded draw may hit the widest or narrowest
+        pick = sorted(set(pick) | {int(np.setdiff1d(np.arange(wl.n), pick)[0])})
+    _say(f"config 5: n={wl.n} H={wl.hidden} C={wl.c_in} bf16, full batch; Y/dX of examples {pick} "
+         f"(widths {wl.widths[pick].tolist()})")
     xs, params = wl.examples(), wl.params()
     dys = [wl.dy(k) for k in range(wl.n)]
-    gpu = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w, dtype="bf16")
-    pick = sorted({int(np.argmin(wl.widths)), int(np.argmin(np.abs(wl.widths - 600)))})
-    _say(f"config 5: oracle on examples {pick} (widths {wl.widths[pick].tolist()})")
-    ref = oracle_run.run_layer([xs[k] for k in pick], params, [dys[k] for k in pick],
-                               workers=oracle_run.default_workers())
+    gpu = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w, dtype="bf16", keep=pick)
+    del xs
+    _compare({"Y": [], "dWx": gpu["dWx"], "dU": gpu["dU"], "db": gpu["db"], "dX": []},
+             {"Y": [], "dX": [], **golden}, "bf16", label="config5 full-batch weight gradients")
+    ref = oracle_run.run_layer(wl.examples(pick), params, [wl.dy(k) for k in pick],
+                               workers=oracle_run.default_workers(), progress="config 5 oracle")
     sub = {"Y": [gpu["Y"][k] for k in pick], "dX": [gpu["dX"][k] for k in pick]}
-    _compare(sub, ref, "bf16", backward=False, label="config5 sample Y")
-    _compare({"Y": sub["dX"]}, {"Y": ref["dX"]}, "bf16", backward=False, label="config5 sample dX")
-    gsub = gpu_run.run_layer([xs[k] for k in pick], params, [dys[k] for k in pick], wl.heights[pick],
-                             wl.widths[pick], wl.canvas_w, dtype="bf16")
-    _compare(gsub, ref, "bf16", label="config5 sample packed alone")
+    _compare(sub, ref, "bf16", backward=False, label="config5 sampled Y")
+    _compare({"Y": sub["dX"]}, {"Y": ref["dX"]}, "bf16", backward=False, label="config5 sampled dX")
 
 
 def test_masked_holes_and_touching_rectangles():
@@ -337,10 +353,12 @@ def test_placement_invariance_and_determinism():
 
 
 def test_exploding_state_regime():
-    # forget-gate biases U(-0.1, 0.1): the state grows to |c| ~ 1e5 over these
-    # lines. Y still matches to 1e-5 (L2); in the gradients the fp32 floor of
-    # the problem itself is ~2e-4 (a float32 NumPy evaluation of the same
-    # definition), so they are held to 1e-3 L2 here.
+    """Forget-gate biases U(-0.1, 0.1): the forget gates sum to about 1 and the
+    state grows to |c| ~ 1e5 over these lines (Section III). The bounds come
+    from the float32 floor of the problem itself, measured with a float32
+    NumPy evaluation of the same definition: 5.8e-5 max-norm on Y of a 32 x 600
+    line, 1.8e-4 L2 on the gradients of a 49 x 70 example. Held here: Y to
+    1e-5 in L2 and 1e-4 in max-norm, dX and the weight gradients to 2e-4 in L2."""
     import gpu_run
     import oracle_run
     from conftest import rel_err, rel_max
@@ -353,15 +371,14 @@ def test_exploding_state_regime():
     gpu = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w)
     ref = oracle_run.run_layer(xs, params, dys, workers=oracle_run.default_workers())
     for k in range(wl.n):
-        e = rel_err(gpu["Y"][k], ref["Y"][k])
-        _say(f"  example {k}: Y L2 {e:.1e} max {rel_max(gpu['Y'][k], ref['Y'][k]):.1e}, "
-             f"dX L2 {rel_err(gpu['dX'][k], ref['dX'][k]):.1e}")
-        assert e <= 1e-5
-        assert rel_err(gpu["dX"][k], ref["dX"][k]) <= 1e-3
+        e, m = rel_err(gpu["Y"][k], ref["Y"][k]), rel_max(gpu["Y"][k], ref["Y"][k])
+        ex = rel_err(gpu["dX"][k], ref["dX"][k])
+        _say(f"  example {k}: Y L2 {e:.1e} max {m:.1e}, dX L2 {ex:.1e}")
+        assert e <= 1e-5 and m <= 1e-4 and ex <= 2e-4
     for nm in ("dWx", "dU", "db"):
         e = rel_err(gpu[nm], ref[nm])
         _say(f"  {nm}: L2 {e:.1e}")
-        assert e <= 1e-3
+        assert e <= 2e-4
 
 
 @pytest.mark.parametrize("case", ["H16_words", "H32_tall", "bf16_H64", "bf16_H128"])

@@ -68,19 +68,33 @@ def test_small_stack_forward_backward():
             _check(f"conv{i}.{nm}", a, b)
 
 
-def test_stack_config4_sampled():
-    """The 32-image line batch at full size: outputs and input gradients of
-    the widest, the narrowest and two more images, each computed alone by the
-    oracle."""
+def test_stack_config4_full_batch():
+    """The 32-image line batch at full size in one GPU run: every image's
+    output and input-block gradient, and the full-batch gradients of all three
+    MDLSTM layers and both block convolutions, against the oracle running
+    every image alone."""
+    import oracle_run
+
     wl = configs.stack_workload()
-    order = np.argsort(wl.widths, kind="stable")
-    ks = sorted({int(order[-1]), int(order[0]), 5, 17})
-    print(f"case: config 4 stack, sampled images {ks}", flush=True)
-    got, layers, convs = _gpu_stack(wl, sample=ks)
-    want = _oracle(wl, layers, convs, ks)
-    for i, k in enumerate(ks):
-        _check(f"Y3[{k}]", got["Y"][i], want["Y"][i])
-        _check(f"dX0[{k}]", got["dX0"][i], want["dX0"][i])
+    print(f"case: config 4 stack, all {wl.n} images", flush=True)
+    got, layers, convs = _gpu_stack(wl)
+    want = oracle_run.run_stack([wl.image(k) for k in range(wl.n)], layers, convs,
+                                [wl.dy(k) for k in range(wl.n)], wl.block, workers=oracle_run.default_workers(),
+                                progress="config 4 oracle")
+    worst = {}
+    for k in range(wl.n):
+        for nm, a, b in (("Y3", got["Y"][k], want["Y"][k]), ("dX0", got["dX0"][k], want["dX0"][k])):
+            e2, em = rel_err(a, b), rel_max(a, b)
+            assert e2 <= TOL and em <= TOL, (nm, k, e2, em)
+            worst[nm] = max(worst.get(nm, (0, 0)), (e2, em))
+    print("  worst over images: " + ", ".join(f"{k} L2 {v[0]:.2e} max {v[1]:.2e}" for k, v in worst.items()),
+          flush=True)
+    for i, (g, w) in enumerate(zip(got["layer_grads"], want["layer_grads"])):
+        for nm, a, b in zip(("dWx", "dU", "db"), g, w):
+            _check(f"layer{i}.{nm}", a, b)
+    for i, (g, w) in enumerate(zip(got["conv_grads"], want["conv_grads"])):
+        for nm, a, b in zip(("dW", "db"), g, w):
+            _check(f"conv{i}.{nm}", a, b)
     st = got["stack"]
     # every layer's canvas holds all 32 images, several per row
     assert all(r.shape[0] == wl.n for r in st.rects)
