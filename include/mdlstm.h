@@ -26,8 +26,10 @@
  *     the kernels.
  *   - Pointers named d_* are DEVICE memory of the current HIP device; all
  *     other pointers are HOST memory. The caller owns every buffer; the library
- *     allocates no memory of its own and keeps no pointer after returning
- *     (workspace addresses serve as lookup keys only, never dereferenced).
+ *     allocates no memory of its own (its one static device array, the scratch
+ *     of mdlstm_pack_layout_noalloc, is described there) and keeps no pointer
+ *     after returning (workspace addresses serve as lookup keys only, never
+ *     dereferenced).
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream). Work
  *     is enqueued on it asynchronously unless stated otherwise.
  *   - Every argument is validated on the host before any HIP call; on error
@@ -103,6 +105,28 @@ mdlstm_status mdlstm_pack_layout(int32_t n, const int32_t* heights, const int32_
                                  int32_t canvas_w, mdlstm_rect* rects, int32_t* canvas_h,
                                  uint8_t* d_mask, size_t mask_bytes,
                                  void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* Most examples one mdlstm_pack_layout_noalloc call places. */
+#define MDLSTM_NOALLOC_MAX_N 4096
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * placement and mask as mdlstm_pack_layout, with the same arguments, results
+ * (bit for bit) and errors, but no workspace argument. Its device scratch (the
+ * uploaded sizes and the placement, 4 * (6n + 1) bytes) lives in a static
+ * array of MDLSTM_NOALLOC_MAX_N * 24 + 4 bytes that each GPU the library runs
+ * on holds until the process ends; the call allocates neither device nor heap
+ * memory (host staging is a per-thread static buffer).
+ * n > MDLSTM_NOALLOC_MAX_N is refused with UNSUPPORTED before any HIP call.
+ * Every call on one GPU shares that GPU's array, and the mask kernel reads it
+ * after the call returns: calls that overlap on one GPU (other threads, or
+ * another stream before this call's mask kernel has run) race. Nothing in the
+ * array needs to start at zero: every call writes what it reads.
+ */
+mdlstm_status mdlstm_pack_layout_noalloc(int32_t n, const int32_t* heights, const int32_t* widths,
+                                         int32_t canvas_w, mdlstm_rect* rects, int32_t* canvas_h,
+                                         uint8_t* d_mask, size_t mask_bytes, void* stream);
 
 /*
  * Last-minute batch padding layout (Section VI-B): every example padded to the

@@ -31,6 +31,7 @@ P_VOIDP = ctypes.POINTER(c_void)
 SIGNATURES = {
     "mdlstm_pack_workspace_bytes": (c_size, [c_i32]),
     "mdlstm_pack_layout": (c_i32, [c_i32, P_I32, P_I32, c_i32, P_RECT, P_I32, c_void, c_size, c_void, c_size, c_void]),
+    "mdlstm_pack_layout_noalloc": (c_i32, [c_i32, P_I32, P_I32, c_i32, P_RECT, P_I32, c_void, c_size, c_void]),
     "mdlstm_pad_layout": (c_i32, [c_i32, P_I32, P_I32, P_RECT, P_RECT, P_I32, P_I32, c_void, c_size, c_void, c_size,
                                   c_void]),
     "mdlstm_pack_data": (c_i32, [c_i32, P_VOIDP, P_RECT, c_i32, c_i32, c_i32, c_i32, c_void, c_void, c_size, c_void]),

@@ -111,6 +111,25 @@ def pack_layout(heights, widths, canvas_w: int, device="cuda", stream=None):
     return _rects_from(rects, n), ch.value, mask
 
 
+def pack_layout_noalloc(heights, widths, canvas_w: int, mask=None, stream=None):
+    """Placement and mask through the allocation-free entry point: the caller
+    owns the mask buffer (uint8, at least canvas_h x canvas_w cells, row-major
+    from its start; None computes the placement only) and the library uses its
+    static device scratch. Returns (rects int32 [n, 4], canvas_h)."""
+    n = len(np.asarray(heights).reshape(-1))
+    hs, ws = _i32_array(heights), _i32_array(widths)
+    if mask is not None:
+        if mask.dtype != torch.uint8:
+            raise ValueError(f"mask has dtype {mask.dtype}, expected torch.uint8")
+        _check_dev(mask, "mask")
+    rects = (Rect * max(1, n))()
+    ch = ctypes.c_int32(0)
+    s = stream if stream is not None else torch.cuda.current_stream()
+    check(lib().mdlstm_pack_layout_noalloc(n, hs, ws, int(canvas_w), rects, ctypes.byref(ch), _ptr(mask),
+                                           0 if mask is None else mask.numel(), _stream(s)))
+    return _rects_from(rects, n), ch.value
+
+
 def pad_layout(heights, widths, device="cuda", stream=None):
     """Last-minute batch padding layout. Returns (tiles, place, canvas_h, canvas_w, mask)."""
     n = len(np.asarray(heights).reshape(-1))

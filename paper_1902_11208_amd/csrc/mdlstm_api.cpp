@@ -275,6 +275,92 @@ size_t pack_ws_bytes(int32_t n) {
     return align_up(nn * 8) + align_up(nn * 16) + align_up((6 * nn + 1) * 4);
 }
 
+// Size checks shared by the two placement entry points (no HIP call).
+mdlstm_status check_pack_sizes(int32_t n, const int32_t* heights, const int32_t* widths, int32_t canvas_w,
+                               mdlstm_rect* rects, int32_t* canvas_h) {
+    if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n is negative");
+    if (n > kMaxPackN) return fail(MDLSTM_ERR_UNSUPPORTED, "at most %d examples per packing call", kMaxPackN);
+    if (!canvas_h) return fail(MDLSTM_ERR_INVALID_ARG, "canvas_h is NULL");
+    if (n > 0 && (!heights || !widths || !rects)) return fail(MDLSTM_ERR_INVALID_ARG, "size or rect array is NULL");
+    if (canvas_w < 1 || canvas_w > kMaxDim) return fail(MDLSTM_ERR_INVALID_ARG, "canvas width %d out of range", canvas_w);
+    for (int32_t k = 0; k < n; ++k) {
+        if (heights[k] < 1 || widths[k] < 1 || heights[k] > kMaxDim || widths[k] > kMaxDim)
+            return fail(MDLSTM_ERR_INVALID_ARG, "example %d has size %dx%d", k, heights[k], widths[k]);
+        if (widths[k] > canvas_w)
+            return fail(MDLSTM_ERR_TOO_WIDE, "example %d is %d wide; the canvas is %d", k, widths[k], canvas_w);
+    }
+    // total canvas height must stay addressable
+    int64_t hsum = 0;
+    for (int32_t k = 0; k < n; ++k) hsum += (int64_t)heights[k] + 1;
+    if (hsum > kMaxDim) return fail(MDLSTM_ERR_UNSUPPORTED, "packed canvas could exceed %d rows", kMaxDim);
+    if (n == 0) *canvas_h = 0;
+    return MDLSTM_OK;
+}
+
+// Placement kernel, then (with d_mask) the mask. d_hw: 2n device int32 (the
+// sizes, uploaded here); d_out: 4n + 1 device int32 (the placement, then the
+// canvas height), read again by the mask kernel; host: 6n + 1 host int32 of
+// staging. Waits for the placement (rects and canvas_h are host outputs); the
+// mask kernel stays queued on s.
+mdlstm_status place_and_mask(int32_t n, const int32_t* heights, const int32_t* widths, int32_t canvas_w,
+                             mdlstm_rect* rects, int32_t* canvas_h, uint8_t* d_mask, size_t mask_bytes,
+                             int32_t* d_hw, int32_t* d_out, int32_t* host, hipStream_t s) {
+    const size_t nn = (size_t)n;
+    std::copy(heights, heights + n, host);
+    std::copy(widths, widths + n, host + nn);
+    HIP_OR_FAIL(hipMemcpyAsync(d_hw, host, 2 * nn * 4, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(mdl::launch_pack_place(n, canvas_w, d_hw, d_out, nullptr, s));
+    int32_t* res = host + 2 * nn;
+    HIP_OR_FAIL(hipMemcpyAsync(res, d_out, (4 * nn + 1) * 4, hipMemcpyDeviceToHost, s));
+    HIP_OR_FAIL(hipStreamSynchronize(s));
+    for (size_t k = 0; k < nn; ++k) {
+        rects[k].y0 = res[4 * k];
+        rects[k].x0 = res[4 * k + 1];
+        rects[k].h = res[4 * k + 2];
+        rects[k].w = res[4 * k + 3];
+    }
+    *canvas_h = res[4 * nn];
+    if (d_mask) {
+        const size_t need = (size_t)(*canvas_h) * (size_t)canvas_w;
+        if (mask_bytes < need)
+            return fail(MDLSTM_ERR_WORKSPACE, "mask of %zu bytes, %zu needed", mask_bytes, need);
+        HIP_OR_FAIL(mdl::launch_mask(n, d_out, *canvas_h, canvas_w, d_mask, s));
+    }
+    return MDLSTM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of the allocation-free placement (mdlstm_pack_layout_noalloc): the
+// sizes (2n words) and the placement (4n + 1 words) of at most
+// MDLSTM_NOALLOC_MAX_N examples in a file-scope device array, which every GPU
+// holds its own copy of. Host code never passes the array's name to a kernel
+// or a copy (on the host it is only a stand-in for the symbol): the device
+// address comes from hipGetSymbolAddress, taken once per device with that
+// device current on the first call there, and kept per device.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchWords = 6 * (size_t)MDLSTM_NOALLOC_MAX_N + 1;
+static_assert(MDLSTM_NOALLOC_MAX_N <= kMaxPackN, "the allocation-free placement shares the placement kernel");
+static __device__ __align__(256) int32_t scratch[kScratchWords];
+
+constexpr int kMaxDevices = 256;
+std::mutex g_scratch_mu;
+int32_t* g_scratch_ptr[kMaxDevices] = {};
+
+mdlstm_status scratch_for_current_device(int32_t** out) {
+    int dev = -1;
+    HIP_OR_FAIL(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(MDLSTM_ERR_DEVICE, "device index %d out of range", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        HIP_OR_FAIL(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return fail(MDLSTM_ERR_DEVICE, "hipGetSymbolAddress returned no address for the scratch array");
+        g_scratch_ptr[dev] = static_cast<int32_t*>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return MDLSTM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -297,56 +383,33 @@ size_t mdlstm_pack_workspace_bytes(int32_t n) { return pack_ws_bytes(n); }
 mdlstm_status mdlstm_pack_layout(int32_t n, const int32_t* heights, const int32_t* widths, int32_t canvas_w,
                                  mdlstm_rect* rects, int32_t* canvas_h, uint8_t* d_mask, size_t mask_bytes,
                                  void* d_workspace, size_t workspace_bytes, void* stream) {
-    if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n is negative");
-    if (n > kMaxPackN) return fail(MDLSTM_ERR_UNSUPPORTED, "at most %d examples per packing call", kMaxPackN);
-    if (!canvas_h) return fail(MDLSTM_ERR_INVALID_ARG, "canvas_h is NULL");
-    if (n > 0 && (!heights || !widths || !rects)) return fail(MDLSTM_ERR_INVALID_ARG, "size or rect array is NULL");
-    if (canvas_w < 1 || canvas_w > kMaxDim) return fail(MDLSTM_ERR_INVALID_ARG, "canvas width %d out of range", canvas_w);
-    for (int32_t k = 0; k < n; ++k) {
-        if (heights[k] < 1 || widths[k] < 1 || heights[k] > kMaxDim || widths[k] > kMaxDim)
-            return fail(MDLSTM_ERR_INVALID_ARG, "example %d has size %dx%d", k, heights[k], widths[k]);
-        if (widths[k] > canvas_w)
-            return fail(MDLSTM_ERR_TOO_WIDE, "example %d is %d wide; the canvas is %d", k, widths[k], canvas_w);
-    }
-    if (n == 0) {
-        *canvas_h = 0;
-        return MDLSTM_OK;
-    }
+    mdlstm_status st = check_pack_sizes(n, heights, widths, canvas_w, rects, canvas_h);
+    if (st != MDLSTM_OK || n == 0) return st;
     if (!d_workspace || workspace_bytes < pack_ws_bytes(n))
         return fail(MDLSTM_ERR_WORKSPACE, "packing workspace of %zu bytes, %zu needed", workspace_bytes,
                     pack_ws_bytes(n));
-    // total canvas height must stay addressable
-    int64_t hsum = 0;
-    for (int32_t k = 0; k < n; ++k) hsum += (int64_t)heights[k] + 1;
-    if (hsum > kMaxDim) return fail(MDLSTM_ERR_UNSUPPORTED, "packed canvas could exceed %d rows", kMaxDim);
-
-    hipStream_t s = as_stream(stream);
-    char* ws = static_cast<char*>(d_workspace);
     const size_t nn = (size_t)n;
-    int32_t* d_hw = reinterpret_cast<int32_t*>(ws + align_up(nn * 8) + align_up(nn * 16));
-    int32_t* d_out = d_hw + 2 * nn;
-    std::vector<int32_t> hw(2 * nn);
-    std::copy(heights, heights + n, hw.begin());
-    std::copy(widths, widths + n, hw.begin() + n);
-    HIP_OR_FAIL(hipMemcpyAsync(d_hw, hw.data(), 2 * nn * 4, hipMemcpyHostToDevice, s));
-    HIP_OR_FAIL(mdl::launch_pack_place(n, canvas_w, d_hw, d_out, nullptr, s));
-    std::vector<int32_t> res(4 * nn + 1);
-    HIP_OR_FAIL(hipMemcpyAsync(res.data(), d_out, (4 * nn + 1) * 4, hipMemcpyDeviceToHost, s));
-    HIP_OR_FAIL(hipStreamSynchronize(s));
-    for (size_t k = 0; k < nn; ++k) {
-        rects[k].y0 = res[4 * k];
-        rects[k].x0 = res[4 * k + 1];
-        rects[k].h = res[4 * k + 2];
-        rects[k].w = res[4 * k + 3];
-    }
-    *canvas_h = res[4 * nn];
-    if (d_mask) {
-        const size_t need = (size_t)(*canvas_h) * (size_t)canvas_w;
-        if (mask_bytes < need)
-            return fail(MDLSTM_ERR_WORKSPACE, "mask of %zu bytes, %zu needed", mask_bytes, need);
-        HIP_OR_FAIL(mdl::launch_mask(n, d_out, *canvas_h, canvas_w, d_mask, s));
-    }
-    return MDLSTM_OK;
+    int32_t* d_hw = reinterpret_cast<int32_t*>(static_cast<char*>(d_workspace) + align_up(nn * 8) + align_up(nn * 16));
+    std::vector<int32_t> host(6 * nn + 1);
+    return place_and_mask(n, heights, widths, canvas_w, rects, canvas_h, d_mask, mask_bytes, d_hw, d_hw + 2 * nn,
+                          host.data(), as_stream(stream));
+}
+
+mdlstm_status mdlstm_pack_layout_noalloc(int32_t n, const int32_t* heights, const int32_t* widths,
+                                         int32_t canvas_w, mdlstm_rect* rects, int32_t* canvas_h, uint8_t* d_mask,
+                                         size_t mask_bytes, void* stream) {
+    mdlstm_status st = check_pack_sizes(n, heights, widths, canvas_w, rects, canvas_h);
+    if (st != MDLSTM_OK || n == 0) return st;
+    if (n > MDLSTM_NOALLOC_MAX_N)
+        return fail(MDLSTM_ERR_UNSUPPORTED, "at most %d examples per allocation-free packing call",
+                    MDLSTM_NOALLOC_MAX_N);
+    int32_t* d_scratch = nullptr;
+    st = scratch_for_current_device(&d_scratch);
+    if (st != MDLSTM_OK) return st;
+    // host staging without heap allocation: one buffer per calling thread
+    static thread_local int32_t host[kScratchWords];
+    return place_and_mask(n, heights, widths, canvas_w, rects, canvas_h, d_mask, mask_bytes, d_scratch,
+                          d_scratch + 2 * (size_t)n, host, as_stream(stream));
 }
 
 mdlstm_status mdlstm_pad_layout(int32_t n, const int32_t* heights, const int32_t* widths, mdlstm_rect* tiles,

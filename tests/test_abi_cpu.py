@@ -207,3 +207,24 @@ def test_backward_rejects_bad_arguments(built_lib):
     for nm in ("dy", "dx", "dwx", "y"):
         assert _bwd(ok, 10, 10, [(0, 0, 3, 3)], **{nm: FAKE + 4}) == 1, nm   # misaligned
         assert b"aligned" in L.lib().mdlstm_last_error()
+
+
+def test_pack_layout_noalloc_errors(built_lib):
+    """The allocation-free placement validates like mdlstm_pack_layout and
+    refuses more than MDLSTM_NOALLOC_MAX_N examples, all before any HIP call."""
+    L = _lib()
+    f = L.lib().mdlstm_pack_layout_noalloc
+
+    def call(n, hs, ws, cw):
+        rects = (L.Rect * max(1, n))()
+        ch = ctypes.c_int32(-1)
+        st = f(n, (ctypes.c_int32 * max(1, n))(*hs), (ctypes.c_int32 * max(1, n))(*ws), cw, rects,
+               ctypes.byref(ch), None, 0, None)
+        return st, ch.value
+
+    assert call(-1, [], [], 10)[0] == 1
+    assert call(2, [2, 2], [5, 11], 10)[0] == 2                    # TOO_WIDE
+    assert call(1, [0], [3], 10)[0] == 1                           # INVALID_ARG
+    assert call(4097, [1] * 4097, [1] * 4097, 10)[0] == 5          # above the static scratch
+    assert b"4096" in L.lib().mdlstm_last_error()
+    assert call(0, [], [], 10) == (0, 0)
