@@ -231,6 +231,14 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
                               void* d_workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * 1 if mdlstm_backward computes the input and weight gradients of this layer
+ * shape in one kernel (reading the gate gradients once), 0 if in two (input
+ * gradient, then weight gradients), -1 for a descriptor mdlstm_backward
+ * refuses. Host-only; for profilers that attribute time to the kernels.
+ */
+int32_t mdlstm_gradients_fused(const mdlstm_layer_desc* desc);
+
+/*
  * Stack glue (Section V-B, Fig. 1): a multi-layer network keeps every layer
  * on a packed canvas. Between two MDLSTM layers a block-strided convolution
  * (stride equal to its bh x bw kernel, so blocks never overlap) with tanh maps
@@ -304,7 +312,10 @@ const char* mdlstm_last_error(void);
  *   when the batch has at least a unit per CU; then [2] follows [1] directly)
  *   [3] after the forward wavefront
  *   [4] before the backward wavefront  [5] after it  [6] after the input
- *   gradient  [7] after the weight gradients.
+ *   gradient  [7] after the weight gradients. Where one kernel computes both
+ *   gradients (fp32 (hidden, c_in) in {(4, 4), (4, 8), (8, 8), (16, 8), (16, 16),
+ *   (32, 16), (32, 32)}, bf16 (32, 16) and (32, 32)) [6] is recorded
+ *   right after [5] and [6]..[7] spans the fused kernel.
  * n must be 0 (disable) or 8; a NULL entry is not recorded (each record
  * costs the stream a few microseconds, so a caller timing whole steps records
  * only the boundaries it needs). The handles must stay valid while set.

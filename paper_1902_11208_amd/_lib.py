@@ -45,6 +45,7 @@ SIGNATURES = {
     "mdlstm_backward": (c_i32, [P_DESC, c_i32, c_i32, c_void, c_void, c_i32, P_RECT, c_void, c_void, c_void, c_void,
                                 c_void, c_void, c_void, c_void, c_void, c_void, c_size, c_void]),
     "mdlstm_last_error": (c_char_p, []),
+    "mdlstm_gradients_fused": (c_i32, [P_DESC]),
     "mdlstm_set_phase_events": (c_i32, [c_i32, P_VOIDP]),
     "mdlstm_blocks_workspace_bytes": (c_size, [c_i32, c_i32, c_i32]),
     "mdlstm_pack_blocks": (c_i32, [c_i32, P_VOIDP, c_i32, c_i32, c_i32, P_RECT, c_i32, c_i32, c_void, c_void, c_size,

@@ -201,6 +201,15 @@ def workspace_bytes(c_in: int, hidden: int, dtype: int, canvas_h: int, canvas_w:
     return int(lib().mdlstm_workspace_bytes(ctypes.byref(d), canvas_h, canvas_w, n_rects))
 
 
+def gradients_fused(c_in: int, hidden: int, dtype: int) -> bool:
+    """Whether one kernel computes both the input and the weight gradients."""
+    d = layer_desc(c_in, hidden, dtype)
+    r = int(lib().mdlstm_gradients_fused(ctypes.byref(d)))
+    if r < 0:
+        raise ValueError(f"layer c_in={c_in} hidden={hidden} dtype={dtype} is not supported")
+    return bool(r)
+
+
 class Prepared:
     """Host-side argument bundle for one canvas layout, reused across calls."""
 

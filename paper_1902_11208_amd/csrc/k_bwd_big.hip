@@ -430,37 +430,48 @@ size_t big_partial_bytes(const LayerGeom& g) {
     return (size_t)q.chunks * 4 * q.G * q.PP * sizeof(float);
 }
 
-hipError_t launch_bwd_big(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y, const void* d_wx,
-                          const uint8_t* d_mask, const int32_t* d_rid, void* d_dx, uint8_t* d_flags, void* d_wxt,
-                          float* d_part, float* d_dwx, float* d_du, float* d_db, hipStream_t s) {
+hipError_t launch_bwd_big_dx(const LayerGeom& g, const void* d_dz, const void* d_wx, const uint8_t* d_mask,
+                             const int32_t* d_rid, void* d_dx, uint8_t* d_flags, void* d_wxt, hipStream_t s) {
     if (g.n_cells == 0) return hipSuccess;
     const int N = 20 * g.hidden;
     int fb = (int)std::min<int64_t>((g.n_cells + 255) / 256, 4096);
     hipLaunchKernelGGL(k_cell_flags, dim3(fb), dim3(256), 0, s, g.canvas_h, g.canvas_w, d_mask, d_rid, d_flags);
     const int64_t nw = (int64_t)N * g.c_in;
     const int tb = (int)std::min<int64_t>((nw + 255) / 256, 4096);
-    const BigDw q = big_dw(g);
     const dim3 gx((unsigned)(((g.n_cells + 63) / 64 + 3) / 4), (unsigned)((g.c_in + 63) / 64));
+    if (g.dtype == 0) {
+        using T = float;
+        hipLaunchKernelGGL(k_transpose<T>, dim3(tb), dim3(256), 0, s, N, g.c_in, static_cast<const T*>(d_wx),
+                           static_cast<T*>(d_wxt));
+        hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, static_cast<const T*>(d_dz),
+                           static_cast<const T*>(d_wxt), d_flags, static_cast<T*>(d_dx));
+    } else {
+        using T = bf16_t;
+        hipLaunchKernelGGL(k_transpose<T>, dim3(tb), dim3(256), 0, s, N, g.c_in, static_cast<const T*>(d_wx),
+                           static_cast<T*>(d_wxt));
+        hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, static_cast<const T*>(d_dz),
+                           static_cast<const T*>(d_wxt), d_flags, static_cast<T*>(d_dx));
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_big_dw(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y,
+                             const uint8_t* d_flags, float* d_part, float* d_dwx, float* d_du, float* d_db,
+                             hipStream_t s) {
+    if (g.n_cells == 0) return hipSuccess;
+    const BigDw q = big_dw(g);
     const dim3 gw((unsigned)(q.rblocks * q.cblocks * 4 * q.chunks));
     const int64_t total = (int64_t)4 * q.G * q.PP;
     const int rbk = (int)std::min<int64_t>((total + 255) / 256, 4096);
     if (g.dtype == 0) {
         using T = float;
         constexpr int PD = 1;
-        hipLaunchKernelGGL(k_transpose<T>, dim3(tb), dim3(256), 0, s, N, g.c_in, static_cast<const T*>(d_wx),
-                           static_cast<T*>(d_wxt));
-        hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, static_cast<const T*>(d_dz),
-                           static_cast<const T*>(d_wxt), d_flags, static_cast<T*>(d_dx));
         hipLaunchKernelGGL((k_dw_big<T, PD>), gw, dim3(BW_THREADS), 0, s, g.n_cells, g.canvas_w, g.c_in, g.hidden, q,
                            static_cast<const T*>(d_dz), static_cast<const T*>(d_x), static_cast<const T*>(d_y),
                            d_flags, d_part);
     } else {
         using T = bf16_t;
         constexpr int PD = 2;
-        hipLaunchKernelGGL(k_transpose<T>, dim3(tb), dim3(256), 0, s, N, g.c_in, static_cast<const T*>(d_wx),
-                           static_cast<T*>(d_wxt));
-        hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, static_cast<const T*>(d_dz),
-                           static_cast<const T*>(d_wxt), d_flags, static_cast<T*>(d_dx));
         hipLaunchKernelGGL((k_dw_big<T, PD>), gw, dim3(BW_THREADS), 0, s, g.n_cells, g.canvas_w, g.c_in, g.hidden, q,
                            static_cast<const T*>(d_dz), static_cast<const T*>(d_x), static_cast<const T*>(d_y),
                            d_flags, d_part);

@@ -60,16 +60,19 @@ hipError_t build_wavefront_fwd_graph(const LayerGeom& g, int nt, int n_units, in
 hipError_t launch_wavefront_bwd(const LayerGeom& g, int nt, int n_units, const int32_t* d_units,
                                 const int32_t* d_rects, const uint8_t* d_mask, const void* d_u,
                                 const void* d_dy, void* d_z, const float* d_c, unsigned* d_queue, hipStream_t s);
-// Input and weight gradients as tiled MFMA products (any built shape): a
-// validity byte per cell (d_flags, n_cells bytes), Wx_all transposed
-// (d_wxt), the input gradient, and the weight gradients from chunk partials
-// (d_part) summed in a fixed order.
+// Input and weight gradients as tiled MFMA products (any built shape), in
+// two launches: first a validity byte per cell (d_flags, n_cells bytes),
+// Wx_all transposed (d_wxt) and the input gradient; then the weight
+// gradients from chunk partials (d_part) summed in a fixed order (it reads
+// the validity bytes of the first).
 size_t big_flags_bytes(const LayerGeom& g);
 size_t big_wxt_bytes(const LayerGeom& g);
 size_t big_partial_bytes(const LayerGeom& g);
-hipError_t launch_bwd_big(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y, const void* d_wx,
-                          const uint8_t* d_mask, const int32_t* d_rid, void* d_dx, uint8_t* d_flags, void* d_wxt,
-                          float* d_part, float* d_dwx, float* d_du, float* d_db, hipStream_t s);
+hipError_t launch_bwd_big_dx(const LayerGeom& g, const void* d_dz, const void* d_wx, const uint8_t* d_mask,
+                             const int32_t* d_rid, void* d_dx, uint8_t* d_flags, void* d_wxt, hipStream_t s);
+hipError_t launch_bwd_big_dw(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y,
+                             const uint8_t* d_flags, float* d_part, float* d_dwx, float* d_du, float* d_db,
+                             hipStream_t s);
 // Input and weight gradients together, staged through LDS by canvas-row
 // strips (hidden sizes up to 32 and c_in + 2H + 1 <= 128).
 bool strip_supported(const LayerGeom& g);

@@ -509,6 +509,11 @@ size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, i
     return plan(desc, canvas_h, canvas_w, n_rects).total;
 }
 
+int32_t mdlstm_gradients_fused(const mdlstm_layer_desc* desc) {
+    if (check_desc(desc) != MDLSTM_OK) return -1;
+    return mdl::strip_supported(geom(desc, 1, 1)) ? 1 : 0;
+}
+
 namespace {
 
 // The per-diagonal graph of the last mdlstm_forward_stepwise call on this
@@ -623,13 +628,15 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
         HIP_OR_FAIL(mdl::launch_bwd_strip(c.g, c.ws + c.p.z, d_x, d_y, d_wx, d_mask, rid, d_dx,
                                           reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
     } else {
-        // tiled products (phase boundary 6 coincides with 5)
-        HIP_OR_FAIL(mark(6, s));
+        // tiled products: the input gradient (boundary 6), then the weight gradients
         if (c.g.n_cells > 0) {
-            HIP_OR_FAIL(mdl::launch_bwd_big(c.g, c.ws + c.p.z, d_x, d_y, d_wx, d_mask, rid, d_dx,
-                                            reinterpret_cast<uint8_t*>(c.ws + c.p.flags), c.ws + c.p.wxt,
-                                            reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
+            uint8_t* flags = reinterpret_cast<uint8_t*>(c.ws + c.p.flags);
+            HIP_OR_FAIL(mdl::launch_bwd_big_dx(c.g, c.ws + c.p.z, d_wx, d_mask, rid, d_dx, flags, c.ws + c.p.wxt, s));
+            HIP_OR_FAIL(mark(6, s));
+            HIP_OR_FAIL(mdl::launch_bwd_big_dw(c.g, c.ws + c.p.z, d_x, d_y, flags,
+                                               reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
         } else {
+            HIP_OR_FAIL(mark(6, s));
             HIP_OR_FAIL(mdl::launch_zero_f32(d_dwx, (int64_t)4 * 5 * c.g.hidden * c.g.c_in, s));
             HIP_OR_FAIL(mdl::launch_zero_f32(d_du, (int64_t)4 * 5 * c.g.hidden * 2 * c.g.hidden, s));
             HIP_OR_FAIL(mdl::launch_zero_f32(d_db, (int64_t)4 * 5 * c.g.hidden, s));

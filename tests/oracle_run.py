@@ -26,9 +26,21 @@ def default_workers() -> int:
     return max(1, min(16, n))
 
 
+_LIMITS = None
+
+
+def single_threaded_blas():
+    """Hold NumPy's BLAS to one thread in this process (pool workers each use one core)."""
+    global _LIMITS
+    from threadpoolctl import threadpool_limits
+
+    _LIMITS = threadpool_limits(limits=1)
+
+
 def _pool_map(fn, jobs, workers, progress):
-    """fn over jobs in a fork pool, results in job order; with `progress`, a
-    line per finished job (long oracle runs stay visibly alive)."""
+    """fn over jobs in a fork pool (one BLAS thread per worker), results in job
+    order; with `progress`, a line per finished job (long oracle runs stay
+    visibly alive)."""
     if workers <= 1 or len(jobs) <= 1:
         out = []
         for i, j in enumerate(jobs):
@@ -37,7 +49,7 @@ def _pool_map(fn, jobs, workers, progress):
                 print(f"{progress}: {i + 1}/{len(jobs)} done", flush=True)
         return out
     results = [None] * len(jobs)
-    with cf.ProcessPoolExecutor(workers, mp_context=mp.get_context("fork")) as ex:
+    with cf.ProcessPoolExecutor(workers, mp_context=mp.get_context("fork"), initializer=single_threaded_blas) as ex:
         futs = {ex.submit(fn, j): i for i, j in enumerate(jobs)}
         for done, f in enumerate(cf.as_completed(futs), 1):
             results[futs[f]] = f.result()

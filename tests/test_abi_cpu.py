@@ -228,3 +228,12 @@ def test_pack_layout_noalloc_errors(built_lib):
     assert call(4097, [1] * 4097, [1] * 4097, 10)[0] == 5          # above the static scratch
     assert b"4096" in L.lib().mdlstm_last_error()
     assert call(0, [], [], 10) == (0, 0)
+
+
+def test_gradients_fused_query(built_lib):
+    L = _lib()
+    f = L.lib().mdlstm_gradients_fused
+    assert f(ctypes.byref(L.LayerDesc(32, 32, 0))) == 1    # lines: one kernel
+    assert f(ctypes.byref(L.LayerDesc(64, 128, 1))) == 0   # bf16 H 128: two kernels
+    assert f(ctypes.byref(L.LayerDesc(16, 12, 0))) == -1   # not built
+    assert f(None) == -1
