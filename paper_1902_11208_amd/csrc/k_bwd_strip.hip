@@ -440,6 +440,262 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
     }
 }
 
+// ---------------------------------------------------------------------------
+// fp32 storage at H = 32: the same computation, with every strip's dZ, X and
+// Y block copied by direct global-to-LDS loads (no registers) into one of two
+// buffer sets, the next strip's copy in flight while the current one is
+// computed. The accumulators of the dW tiles fill the register file at this
+// width, so staging through registers leaves no room to load ahead.
+//
+// LDS layouts (floats): dZ [TC][20H] with its 16-byte chunks permuted within
+// each aligned group of sixteen by the cell index (chunk j of cell c sits at
+// j ^ (c & 15)), so that the dX operand reads of sixteen cells hit distinct
+// banks; Y [3][TC + 2][4H] (rows above, same, below; one halo cell each
+// side); X [TC][C_in]; the validity ids (rectangle id of a valid cell, -1
+// for an invalid one, computed once per call) of the halo, [3][TC + 2]. A
+// wave's load instruction fills 1 KB of LDS (256 bytes for the ids), lane l
+// slot l, so each lane fetches the element its slot holds.
+// ---------------------------------------------------------------------------
+template <int H, int C>
+struct DmaCfg {
+    static constexpr int TC = 16, HW = TC + 2, N = 20 * H, G = 5 * H;
+    static constexpr int NW = 8, THREADS = 64 * NW;
+    static constexpr int ZCH = TC * N / 4, YCH = 3 * HW * H, XCH = TC * C / 4;  // 16-byte chunks per strip
+    static constexpr int ZI = ZCH / 64, YI = YCH / 64, XI = XCH / 64;           // wave load instructions
+    static_assert(ZCH % 64 == 0 && YCH % 64 == 0 && XCH % 64 == 0, "whole 1 KB load instructions");
+    static_assert((N / 4) % 16 == 0, "dZ rows hold whole chunk groups of sixteen");
+    static_assert(H == 32 && C % 16 == 0, "laid out for H = 32");
+};
+
+__device__ __forceinline__ int zswz(int cell, int f) {  // LDS float index of dZ element f of a strip cell
+    return (((f >> 2) ^ (cell & 15)) << 2) | (f & 3);
+}
+
+template <int H, int C>
+__global__ void __launch_bounds__((DmaCfg<H, C>::THREADS))
+k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float* __restrict__ dZ,
+                const float* __restrict__ X, const float* __restrict__ Y, const float* __restrict__ Wx,
+                const int32_t* __restrict__ vid, float* __restrict__ dX, float* __restrict__ part) {
+    using Cf = StripCfg<H, C>;
+    using Dc = DmaCfg<H, C>;
+    constexpr int TC = Dc::TC, HW = Dc::HW, N = Dc::N, G = Dc::G, NW = Dc::NW, NTH = Dc::THREADS;
+    constexpr int RTW = Cf::RTW, WPD = Cf::WPD, CT = Cf::CT, CXT = Cf::CXT, XP = Cf::XP;
+    static_assert(TC == Cf::TC && NTH == Cf::THREADS, "same strips and waves as the staged kernel");
+    static_assert(4 * TC * XP <= 3 * HW * 4 * H, "dX partials fit in a buffer's Y rows");
+    __shared__ __attribute__((aligned(16))) float zA[TC * N], zB[TC * N];
+    __shared__ __attribute__((aligned(16))) float yA[3 * HW * 4 * H], yB[3 * HW * 4 * H];
+    __shared__ __attribute__((aligned(16))) float xA[TC * C], xB[TC * C];
+    __shared__ __attribute__((aligned(16))) int32_t vA[64], vB[64];
+    static_assert(3 * HW <= 64, "the halo's ids fill one 256-byte load instruction");
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int g = lane >> 4, i16 = lane & 15;
+    const int d = wave / WPD, rslice = wave % WPD;
+    const int rt0 = rslice * RTW;
+
+    floatx4 acc[RTW][CT];
+#pragma unroll
+    for (int a = 0; a < RTW; ++a)
+#pragma unroll
+        for (int b = 0; b < CT; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float dbp[RTW];
+#pragma unroll
+    for (int a = 0; a < RTW; ++a) dbp[a] = 0.0f;
+    // dX A operand Wx_d^T in registers, as in the staged kernel
+    constexpr int CXW = (CXT + WPD - 1) / WPD, KBL = G / 16;
+    float wa[CXW][KBL][4];
+#pragma unroll
+    for (int cc = 0; cc < CXW; ++cc) {
+        const int ch = (rslice + cc * WPD) * 16 + i16;
+#pragma unroll
+        for (int m = 0; m < KBL; ++m)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                wa[cc][m][j] = ch < C ? Wx[((int64_t)d * G + 16 * m + 4 * g + j) * C + ch] : 0.0f;
+    }
+    // with the operand loads complete here, the waits the compiler places in
+    // the strip loop need not cover them (which would make the dX products
+    // wait for the next strip's copies as well)
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+
+    auto strip_pos = [&](int strip, int& cy, int& cx0, int& len, int64_t& p0) {
+        cy = strip / segs;
+        cx0 = (strip - cy * segs) * TC;
+        len = min(TC, canvas_w - cx0);
+        p0 = (int64_t)cy * canvas_w + cx0;
+    };
+    // direct loads of a strip into one buffer set; every lane reads a valid
+    // address (cells past the row's end repeat its last cell, halo cells
+    // outside the canvas the nearest one; both are marked invalid once staged)
+    auto copy_in = [&](int strip, float* zb, float* yb, float* xb, int32_t* vb) __attribute__((always_inline)) {
+        int cy, cx0, len;
+        int64_t p0;
+        strip_pos(strip, cy, cx0, len, p0);
+        for (int q = wave; q < Dc::ZI; q += NW) {
+            const int s = q * 64 + lane, cell = s / (N / 4), pos = s - cell * (N / 4);
+            const float* src = dZ + (p0 + min(cell, len - 1)) * N + 4 * (pos ^ (cell & 15));
+            __builtin_amdgcn_global_load_lds(src, zb + q * 256, 16, 0, 0);
+        }
+        for (int q = wave; q < Dc::YI; q += NW) {
+            const int s = q * 64 + lane, row = s / (HW * H), rem = s - row * (HW * H);
+            const int c = rem / H, k = rem - c * H;
+            const int yy = min(max(cy + row - 1, 0), canvas_h - 1), xx = min(max(cx0 + c - 1, 0), canvas_w - 1);
+            __builtin_amdgcn_global_load_lds(Y + ((int64_t)yy * canvas_w + xx) * (4 * H) + 4 * k, yb + q * 256, 16,
+                                             0, 0);
+        }
+        for (int q = wave; q < Dc::XI; q += NW) {
+            const int s = q * 64 + lane, cell = s / (C / 4), k = s - cell * (C / 4);
+            __builtin_amdgcn_global_load_lds(X + (p0 + min(cell, len - 1)) * C + 4 * k, xb + q * 256, 16, 0, 0);
+        }
+        if (wave == NW - 1) {
+            const int e = min(lane, 3 * HW - 1), row = e / HW, c = e - row * HW;
+            const int yy = min(max(cy + row - 1, 0), canvas_h - 1), xx = min(max(cx0 + c - 1, 0), canvas_w - 1);
+            __builtin_amdgcn_global_load_lds(vid + (int64_t)yy * canvas_w + xx, vb, 4, 0, 0);
+        }
+    };
+
+    auto process = [&](int strip, float* zb, float* yb, float* xb, int32_t* vb, float* zn, float* yn, float* xn,
+                       int32_t* vn) __attribute__((always_inline)) {
+        int cy, cx0, len;
+        int64_t p0;
+        strip_pos(strip, cy, cx0, len, p0);
+        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's copies into zb, yb, xb, vb have landed
+        lds_barrier();
+        // validity folded into the staged data (as in the staged kernel): a
+        // cell is valid with a nonnegative id, a predecessor counts when it is
+        // on the canvas and has the cell's id
+        auto inside = [&](int row, int k) {
+            const int yy = cy + row - 1, xx = cx0 + k - 1;
+            return yy >= 0 && yy < canvas_h && xx >= 0 && xx < canvas_w;
+        };
+        bool cv = false;
+        if (lane < TC) cv = lane < len && vb[HW + lane + 1] >= 0;
+        const uint64_t bad = ~__ballot(cv) & ((1ull << TC) - 1);
+        for (uint64_t bm = bad; bm; bm &= bm - 1) {
+            const int c = __builtin_ctzll(bm);
+            for (int e = tid; e < N / 4; e += NTH) st_f4(&zb[c * N + 4 * e], make_float4(0.f, 0.f, 0.f, 0.f));
+            if (tid < C / 4) st_f4(&xb[c * C + 4 * tid], make_float4(0.f, 0.f, 0.f, 0.f));
+        }
+        for (int e = tid; e < 8 * TC; e += NTH) {
+            const int c = e % TC, lt = (e / TC) & 1, dd = e / (2 * TC);
+            const int row = lt ? ((dd & 2) ? 2 : 0) : 1;
+            const int k = lt ? c + 1 : ((dd & 1) ? c + 2 : c);
+            if (!(inside(row, k) && vb[row * HW + k] == vb[HW + c + 1])) {
+#pragma unroll
+                for (int j = 0; j < H; j += 4)
+                    st_f4(&yb[(row * HW + k) * (4 * H) + dd * H + j], make_float4(0.f, 0.f, 0.f, 0.f));
+            }
+        }
+        const int next = strip + (int)gridDim.x;
+        lds_barrier();
+        if (next < n_strips) copy_in(next, zn, yn, xn, vn);  // the other buffers: free since the last barrier
+
+        // dW (K = the strip's cells, four per MFMA step, slot g = cell 16 (ks / 4) + 4 g + ks % 4)
+#pragma unroll 2
+        for (int ks = 0; ks < TC / 4; ++ks) {
+            const int c = 16 * (ks >> 2) + 4 * g + (ks & 3);
+            const int lc = (d & 1) ? c + 2 : c;
+            const int trow = (d & 2) ? 2 : 0;
+            float av[RTW], bv[CT];
+#pragma unroll
+            for (int a = 0; a < RTW; ++a) av[a] = zb[c * N + zswz(c, d * G + (rt0 + a) * 16 + i16)];
+#pragma unroll
+            for (int b = 0; b < CT; ++b) {
+                if (b < C / 16) bv[b] = xb[c * C + b * 16 + i16];
+                else if (b < (C + H) / 16) bv[b] = yb[(HW + lc) * (4 * H) + d * H + (b - C / 16) * 16 + i16];
+                else bv[b] = yb[(trow * HW + c + 1) * (4 * H) + d * H + (b - (C + H) / 16) * 16 + i16];
+            }
+#pragma unroll
+            for (int a = 0; a < RTW; ++a) {
+                dbp[a] += av[a];
+#pragma unroll
+                for (int b = 0; b < CT; ++b) acc[a][b] = mfma_f32(av[a], bv[b], acc[a][b]);
+            }
+        }
+        // dX partial of direction d
+        floatx4 axs[CXW];
+#pragma unroll
+        for (int cc = 0; cc < CXW; ++cc) {
+            floatx4 ax = floatx4{0.f, 0.f, 0.f, 0.f};
+            if (rslice + cc * WPD < CXT) {
+                constexpr int DXB = 5;
+#pragma unroll
+                for (int m0 = 0; m0 < KBL; m0 += DXB) {
+                    float4 bz[DXB];
+#pragma unroll
+                    for (int m = 0; m < DXB; ++m)
+                        if (m0 + m < KBL)
+                            bz[m] = *reinterpret_cast<const float4*>(
+                                &zb[i16 * N + zswz(i16, d * G + 16 * (m0 + m) + 4 * g)]);
+#pragma unroll
+                    for (int m = 0; m < DXB; ++m) {
+                        if (m0 + m < KBL) {
+                            ax = mfma_f32(wa[cc][m0 + m][0], bz[m].x, ax);
+                            ax = mfma_f32(wa[cc][m0 + m][1], bz[m].y, ax);
+                            ax = mfma_f32(wa[cc][m0 + m][2], bz[m].z, ax);
+                            ax = mfma_f32(wa[cc][m0 + m][3], bz[m].w, ax);
+                        }
+                    }
+                }
+            }
+            axs[cc] = ax;
+        }
+        lds_barrier();  // every wave is done reading this buffer's Y rows
+        auto sdx = reinterpret_cast<float(*)[TC][XP]>(yb);
+#pragma unroll
+        for (int cc = 0; cc < CXW; ++cc) {
+            const int ct = rslice + cc * WPD;
+            if (ct < CXT) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) sdx[d][i16][ct * 16 + 4 * g + r] = axs[cc][r];
+            }
+        }
+        lds_barrier();
+        constexpr int NXS = TC * C / 4, PXS = (NXS + NTH - 1) / NTH;
+#pragma unroll
+        for (int k = 0; k < PXS; ++k) {
+            const int e = min(tid + k * NTH, NXS - 1);
+            const int c = min(e / (C / 4), len - 1), k4 = 4 * (e - (e / (C / 4)) * (C / 4));
+            const float4 a0 = *reinterpret_cast<const float4*>(&sdx[0][c][k4]);
+            const float4 a1 = *reinterpret_cast<const float4*>(&sdx[1][c][k4]);
+            const float4 a2 = *reinterpret_cast<const float4*>(&sdx[2][c][k4]);
+            const float4 a3 = *reinterpret_cast<const float4*>(&sdx[3][c][k4]);
+            *reinterpret_cast<float4*>(dX + (p0 + c) * C + k4) =
+                make_float4(((a0.x + a1.x) + a2.x) + a3.x, ((a0.y + a1.y) + a2.y) + a3.y,
+                            ((a0.z + a1.z) + a2.z) + a3.z, ((a0.w + a1.w) + a2.w) + a3.w);
+        }
+    };
+
+    int strip = blockIdx.x;
+    if (strip < n_strips) copy_in(strip, zA, yA, xA, vA);
+    while (strip < n_strips) {
+        process(strip, zA, yA, xA, vA, zB, yB, xB, vB);
+        strip += gridDim.x;
+        if (strip >= n_strips) break;
+        process(strip, zB, yB, xB, vB, zA, yA, xA, vA);
+        strip += gridDim.x;
+    }
+
+    float* out = part + ((int64_t)blockIdx.x * 4 + d) * (Cf::RT * 16) * Cf::PP;
+#pragma unroll
+    for (int a = 0; a < RTW; ++a) {
+        if (rt0 + a >= Cf::RT) continue;
+#pragma unroll
+        for (int b = 0; b < CT; ++b)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                out[(int64_t)((rt0 + a) * 16 + 4 * g + r) * Cf::PP + b * 16 + i16] = acc[a][b][r];
+    }
+#pragma unroll
+    for (int a = 0; a < RTW; ++a) {
+        float sb = dbp[a];
+        sb += __shfl_xor(sb, 16);
+        sb += __shfl_xor(sb, 32);
+        if (g == 0 && rt0 + a < Cf::RT) out[(int64_t)((rt0 + a) * 16 + i16) * Cf::PP + CT * 16] = sb;
+    }
+}
+
 // Fixed-order sum over workgroup partials. A block takes 64 consecutive
 // outputs; its four thread groups sum every fourth workgroup each (loads
 // batched), and the four sums are added in a fixed order.
@@ -521,9 +777,40 @@ size_t strip_partial_bytes(const LayerGeom& g) {
     return (size_t)strip_wgs(g) * 4 * RT * 16 * strip_pp(g) * sizeof(float);
 }
 
+// Validity id of every canvas cell: its rectangle id where the cell is
+// inside a rectangle and unmasked, else -1.
+__global__ void k_valid_ids(int64_t n_cells, const uint8_t* __restrict__ mask, const int32_t* __restrict__ rid,
+                            int32_t* __restrict__ vid) {
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n_cells; p += (int64_t)gridDim.x * blockDim.x)
+        vid[p] = (mask[p] && rid[p] >= 0) ? rid[p] : -1;
+}
+
+// fp32 storage at H = 32 takes the direct-to-LDS kernel, the other shapes
+// the register-staged one.
+template <typename T, int H, int C>
+static void launch_strip_shape(const LayerGeom& g, int nwg, int n_strips, int segs, const void* d_dz, const void* d_x,
+                               const void* d_y, const void* d_wx, const uint8_t* d_mask, const int32_t* d_rid,
+                               int32_t* d_vid, void* d_dx, float* d_part, hipStream_t s) {
+    if constexpr (std::is_same<T, float>::value && H == 32) {
+        const int vb = (int)std::min<int64_t>((g.n_cells + 255) / 256, 4096);
+        hipLaunchKernelGGL(k_valid_ids, dim3(vb), dim3(256), 0, s, g.n_cells, d_mask, d_rid, d_vid);
+        hipLaunchKernelGGL((k_bwd_strip_dma<H, C>), dim3(nwg), dim3(DmaCfg<H, C>::THREADS), 0, s, g.canvas_h,
+                           g.canvas_w, n_strips, segs, static_cast<const float*>(d_dz), static_cast<const float*>(d_x),
+                           static_cast<const float*>(d_y), static_cast<const float*>(d_wx), d_vid,
+                           static_cast<float*>(d_dx), d_part);
+    } else {
+        hipLaunchKernelGGL((k_bwd_strip<T, H, C>), dim3(nwg), dim3(StripCfg<H, C>::THREADS), 0, s, g.canvas_h,
+                           g.canvas_w, n_strips, segs, static_cast<const T*>(d_dz), static_cast<const T*>(d_x),
+                           static_cast<const T*>(d_y), static_cast<const T*>(d_wx), d_mask, d_rid,
+                           static_cast<T*>(d_dx), d_part);
+    }
+}
+
+size_t strip_vid_bytes(const LayerGeom& g) { return (size_t)(g.n_cells > 0 ? g.n_cells : 1) * 4; }
+
 hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y, const void* d_wx,
-                            const uint8_t* d_mask, const int32_t* d_rid, void* d_dx, float* d_part, float* d_dwx,
-                            float* d_du, float* d_db, hipStream_t s) {
+                            const uint8_t* d_mask, const int32_t* d_rid, int32_t* d_vid, void* d_dx, float* d_part,
+                            float* d_dwx, float* d_du, float* d_db, hipStream_t s) {
     const int tc = strip_tc(g);
     const int segs = (g.canvas_w + tc - 1) / tc;
     const int n_strips = g.canvas_h * segs;
@@ -532,10 +819,8 @@ hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_
     bool ok = false;
 #define MDL_STRIP_LAUNCH(T, H, C)                                                                                  \
     if (!ok && (g.dtype == 1) == std::is_same<T, bf16_t>::value && g.hidden == H && g.c_in == C) {                 \
-        hipLaunchKernelGGL((k_bwd_strip<T, H, C>), dim3(nwg), dim3(StripCfg<H, C>::THREADS), 0, s, g.canvas_h,     \
-                           g.canvas_w, n_strips, segs, static_cast<const T*>(d_dz), static_cast<const T*>(d_x),    \
-                           static_cast<const T*>(d_y), static_cast<const T*>(d_wx), d_mask, d_rid,                 \
-                           static_cast<T*>(d_dx), d_part);                                                         \
+        launch_strip_shape<T, H, C>(g, nwg, n_strips, segs, d_dz, d_x, d_y, d_wx, d_mask, d_rid, d_vid, d_dx,      \
+                                    d_part, s);                                                                    \
         ok = true;                                                                                                 \
     }
     MDL_STRIP_SHAPES(MDL_STRIP_LAUNCH)

@@ -74,12 +74,14 @@ hipError_t launch_bwd_big_dw(const LayerGeom& g, const void* d_dz, const void* d
                              const uint8_t* d_flags, float* d_part, float* d_dwx, float* d_du, float* d_db,
                              hipStream_t s);
 // Input and weight gradients together, staged through LDS by canvas-row
-// strips (hidden sizes up to 32 and c_in + 2H + 1 <= 128).
+// strips (the shapes strip_supported lists). d_vid: strip_vid_bytes of
+// workspace for a validity id per cell.
 bool strip_supported(const LayerGeom& g);
 size_t strip_partial_bytes(const LayerGeom& g);
+size_t strip_vid_bytes(const LayerGeom& g);
 hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y,
-                            const void* d_wx, const uint8_t* d_mask, const int32_t* d_rid, void* d_dx,
-                            float* d_part, float* d_dwx, float* d_du, float* d_db, hipStream_t s);
+                            const void* d_wx, const uint8_t* d_mask, const int32_t* d_rid, int32_t* d_vid,
+                            void* d_dx, float* d_part, float* d_dwx, float* d_du, float* d_db, hipStream_t s);
 
 // --- stack glue (block reshape, grouped block convolution) -----------------
 // d_blk_off[n + 1]: first block of each example (prefix sum of out_h*out_w).

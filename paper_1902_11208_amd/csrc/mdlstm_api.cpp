@@ -114,8 +114,8 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
     p.part = off;
     const bool strip = mdl::strip_supported(g);
     off += align_up(strip ? mdl::strip_partial_bytes(g) : mdl::big_partial_bytes(g));
-    p.flags = off;  // the tiled gradient path only
-    off += strip ? 0 : align_up(mdl::big_flags_bytes(g));
+    p.flags = off;  // tiled gradient path: a validity byte per cell; strip path: a validity id per cell
+    off += align_up(strip ? mdl::strip_vid_bytes(g) : mdl::big_flags_bytes(g));
     p.wxt = off;
     off += strip ? 0 : align_up(mdl::big_wxt_bytes(g));
     p.queue = off;  // unit queue: next unit, workgroups done
@@ -625,7 +625,8 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
     if (c.g.n_cells > 0 && mdl::strip_supported(c.g)) {
         // input and weight gradients in one pass (phase boundary 6 coincides with 5)
         HIP_OR_FAIL(mark(6, s));
-        HIP_OR_FAIL(mdl::launch_bwd_strip(c.g, c.ws + c.p.z, d_x, d_y, d_wx, d_mask, rid, d_dx,
+        HIP_OR_FAIL(mdl::launch_bwd_strip(c.g, c.ws + c.p.z, d_x, d_y, d_wx, d_mask, rid,
+                                          reinterpret_cast<int32_t*>(c.ws + c.p.flags), d_dx,
                                           reinterpret_cast<float*>(c.ws + c.p.part), d_dwx, d_du, d_db, s));
     } else {
         // tiled products: the input gradient (boundary 6), then the weight gradients
