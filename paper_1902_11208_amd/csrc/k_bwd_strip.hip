@@ -59,7 +59,9 @@ struct StripCfg {
     // registers per lane (one workgroup per CU); the 16-cell strips of H = 16
     // with 16 input channels and the other shapes run two workgroups per CU.
     static constexpr bool PREFETCH = H <= 16;
-    static constexpr int WGS = (H == 16 && TC == 32) ? 256 : 512;
+    // workgroups launched: one round of resident workgroups (H = 32 holds
+    // one per CU: its registers, and LDS in the direct-to-LDS kernel)
+    static constexpr int WGS = (H == 16 && TC == 32) || H >= 32 ? 256 : 512;
     // register budget of the H = 32 shapes: dW steps unrolled by two, dX
     // operands read five blocks at a time
     static constexpr int DW_UNROLL = H >= 32 ? 2 : TC / 4;
@@ -571,7 +573,8 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
         };
         bool cv = false;
         if (lane < TC) cv = lane < len && vb[HW + lane + 1] >= 0;
-        const uint64_t bad = ~__ballot(cv) & ((1ull << TC) - 1);
+        const uint64_t good = __ballot(cv);  // the same in every wave
+        const uint64_t bad = ~good & ((1ull << TC) - 1);
         for (uint64_t bm = bad; bm; bm &= bm - 1) {
             const int c = __builtin_ctzll(bm);
             for (int e = tid; e < N / 4; e += NTH) st_f4(&zb[c * N + 4 * e], make_float4(0.f, 0.f, 0.f, 0.f));
@@ -591,9 +594,11 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
         lds_barrier();
         if (next < n_strips) copy_in(next, zn, yn, xn, vn);  // the other buffers: free since the last barrier
 
-        // dW (K = the strip's cells, four per MFMA step, slot g = cell 16 (ks / 4) + 4 g + ks % 4)
+        // dW (K = the strip's cells, four per MFMA step, slot g = cell 16 (ks / 4) + 4 g + ks % 4);
+        // a strip without a valid cell (separator rows, row slack) adds
+        // nothing and its dX is zero
 #pragma unroll 2
-        for (int ks = 0; ks < TC / 4; ++ks) {
+        for (int ks = 0; ks < (good ? TC / 4 : 0); ++ks) {
             const int c = 16 * (ks >> 2) + 4 * g + (ks & 3);
             const int lc = (d & 1) ? c + 2 : c;
             const int trow = (d & 2) ? 2 : 0;
@@ -618,7 +623,7 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
 #pragma unroll
         for (int cc = 0; cc < CXW; ++cc) {
             floatx4 ax = floatx4{0.f, 0.f, 0.f, 0.f};
-            if (rslice + cc * WPD < CXT) {
+            if (good && rslice + cc * WPD < CXT) {
                 constexpr int DXB = 5;
 #pragma unroll
                 for (int m0 = 0; m0 < KBL; m0 += DXB) {
