@@ -11,6 +11,8 @@ Plain, slow, float64 NumPy definitions of what the GPU path computes:
   predecessors).
 * ``oracle.stack``  — the three-layer stack with block-strided convolutions
   and tensor-list chunking (Section V-B).
+* ``oracle.head``   — the output layer shared by the four directions with the
+  collapse of the rows (Section II), and the CTC loss with its gradient.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package. The product path (the HIP library and
@@ -19,5 +21,8 @@ here imports the product path.
 
 Parity unpinned: the block-convolution grouping convention of the three-layer
 stack (one group per direction, outputs concatenated) is a reading, checked
-only against its own definition and finite differences.
+only against its own definition and finite differences; so is the output
+layer's collapse of the rows (a sum over the rows and the four directions),
+while the CTC loss itself is pinned by hand-worked cases, brute force over
+every frame path and PyTorch's float64 CTC loss.
 """

@@ -18,7 +18,11 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-TAG_SIZES, TAG_INPUT, TAG_PARAMS, TAG_DY = 0, 1, 2, 3
+TAG_SIZES, TAG_INPUT, TAG_PARAMS, TAG_DY, TAG_LABELS = 0, 1, 2, 3, 4
+
+# classes of the output layer: the CTC blank (class 0) and 79 symbols, close to
+# the character set of the handwriting the paper trains on
+HEAD_CLASSES = 80
 
 
 def _rng(cid: int, tag: int, index: int = 0) -> np.random.Generator:
@@ -99,6 +103,22 @@ class Workload:
             b.append(bd)
         return (_store(np.stack(wx), self.dtype), _store(np.stack(u), self.dtype),
                 _store(np.stack(b), self.dtype))
+
+    def label(self, k: int, classes: int = HEAD_CLASSES) -> np.ndarray:
+        """Target sequence of example k for the CTC loss: length U{1..max(1, w // 4)}
+        (short enough for every frame path to exist, repeats included), classes
+        U{1..classes-1} (0 is the blank). int32."""
+        w = int(self.widths[k])
+        rng = _rng(self.cid, TAG_LABELS, k)
+        n = int(rng.integers(1, max(1, w // 4), endpoint=True))
+        return rng.integers(1, classes, n, endpoint=False).astype(np.int32)
+
+    def head_params(self, classes: int = HEAD_CLASSES):
+        """Output layer shared by the directions: W [classes][H], b [classes], U(-0.1, 0.1), float32."""
+        rng = _rng(self.cid, TAG_PARAMS, 1)
+        W = rng.uniform(-0.1, 0.1, (classes, self.hidden))
+        b = rng.uniform(-0.1, 0.1, (classes,))
+        return _store(W, "f32"), _store(b, "f32")
 
     def dy(self, k: int) -> np.ndarray:
         """Upstream gradient of example k, [h, w, 4H] float32, N(0,1)."""
