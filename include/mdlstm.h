@@ -299,6 +299,76 @@ mdlstm_status mdlstm_block_conv_backward(int32_t n, int32_t hidden, int32_t og, 
                                          float* d_dw, float* d_db, void* d_workspace, size_t workspace_bytes,
                                          void* stream);
 
+/*
+ * Output layer and CTC loss (Section II, Overview: the model ends in a
+ * fully-connected layer shared across the four directions and is trained with
+ * connectionist temporal classification; Section V-B: that layer is the 1 x 1
+ * case of the block-strided layers, so it runs on the packed canvas).
+ *
+ * For example i at rects[i] = (y0, x0, h, w) of the last MDLSTM layer's output
+ * canvas d_y [canvas_h][canvas_w][4*hidden] (channel d*hidden + j), frame
+ * t = 0 .. w - 1 is canvas column x0 + t and
+ *   logits[off_i + t][k] = sum_{y < h} sum_{d < 4} (W h_d(y0 + y, x0 + t) + b)[k]
+ * with the shared W [classes][hidden], b [classes]: the layer applied to every
+ * cell of every direction, summed over the directions and the example's rows.
+ * off_i = w_0 + ... + w_{i-1}: frames are stored example after example, in
+ * the order of rects. Class 0 is the CTC blank. All tensors are fp32.
+ * Built: hidden a multiple of 4 in [4, 64], 2 <= classes <= 128.
+ */
+typedef struct {
+    int32_t hidden;
+    int32_t classes;
+} mdlstm_head_desc;
+
+/* Workspace of the head calls for these examples: with label_lens NULL, what
+ * mdlstm_head_forward and mdlstm_head_backward need; with the label lengths,
+ * what mdlstm_ctc_loss needs as well (one workspace serves all three). */
+size_t mdlstm_head_workspace_bytes(const mdlstm_head_desc* desc, int32_t n, const mdlstm_rect* rects,
+                                   const int32_t* label_lens);
+
+/*
+ * logits (out, device) [frames][classes] as above, frames = sum of rects[i].w.
+ * rects (host): inside the canvas and pairwise disjoint (BAD_LAYOUT). The
+ * per-frame sums over rows and directions stay in the workspace for
+ * mdlstm_head_backward, which must follow before the workspace is reused for
+ * another forward call. Asynchronous on `stream`.
+ */
+mdlstm_status mdlstm_head_forward(const mdlstm_head_desc* desc, int32_t canvas_h, int32_t canvas_w,
+                                  const float* d_y, int32_t n, const mdlstm_rect* rects,
+                                  const float* d_w, const float* d_b, float* d_logits,
+                                  void* d_workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * CTC loss (Graves et al. 2006) of every example and its gradient with respect
+ * to the logits, computed in double precision.
+ * label_lens[n], labels (host): example i's target sequence is the next
+ * label_lens[i] entries of labels, each a class in [1, classes); at most 960
+ * labels per example (UNSUPPORTED), and the sequence must fit its frames:
+ * label_lens[i] + (number of adjacent repeats) <= rects[i].w (INVALID_ARG
+ * otherwise, as no frame path would exist).
+ * d_losses (out) [n]: -ln p(label_i | frames of example i).
+ * d_dlogits (out) [frames][classes]: gradient of sum_i loss_i.
+ * The workspace must hold mdlstm_head_workspace_bytes with the label lengths.
+ * Asynchronous on `stream`.
+ */
+mdlstm_status mdlstm_ctc_loss(const mdlstm_head_desc* desc, int32_t n, const mdlstm_rect* rects,
+                              const int32_t* label_lens, const int32_t* labels, const float* d_logits,
+                              float* d_losses, float* d_dlogits, void* d_workspace, size_t workspace_bytes,
+                              void* stream);
+
+/*
+ * Gradients of sum(logits * dlogits) after mdlstm_head_forward on the same
+ * workspace: d_dy (out) [canvas_h][canvas_w][4*hidden] holds W^T dlogits[off_i
+ * + t] at every row of example i's column x0 + t, in every direction, and zero
+ * outside the rectangles (the upstream gradient of the MDLSTM layer's
+ * backward); d_dw [classes][hidden] and d_db [classes] (out) are OVERWRITTEN,
+ * summed over all frames in a fixed order. Asynchronous on `stream`.
+ */
+mdlstm_status mdlstm_head_backward(const mdlstm_head_desc* desc, int32_t canvas_h, int32_t canvas_w, int32_t n,
+                                   const mdlstm_rect* rects, const float* d_w, const float* d_dlogits,
+                                   float* d_dy, float* d_dw, float* d_db,
+                                   void* d_workspace, size_t workspace_bytes, void* stream);
+
 /* Message for the last non-OK status returned on the calling thread. */
 const char* mdlstm_last_error(void);
 

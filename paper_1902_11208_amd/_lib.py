@@ -23,9 +23,14 @@ class LayerDesc(ctypes.Structure):
     _fields_ = [("c_in", c_i32), ("hidden", c_i32), ("dtype", c_i32)]
 
 
+class HeadDesc(ctypes.Structure):
+    _fields_ = [("hidden", c_i32), ("classes", c_i32)]
+
+
 P_I32 = ctypes.POINTER(c_i32)
 P_RECT = ctypes.POINTER(Rect)
 P_DESC = ctypes.POINTER(LayerDesc)
+P_HEAD = ctypes.POINTER(HeadDesc)
 P_VOIDP = ctypes.POINTER(c_void)
 
 SIGNATURES = {
@@ -44,6 +49,12 @@ SIGNATURES = {
                                         c_void, c_void, c_size, c_void]),
     "mdlstm_backward": (c_i32, [P_DESC, c_i32, c_i32, c_void, c_void, c_i32, P_RECT, c_void, c_void, c_void, c_void,
                                 c_void, c_void, c_void, c_void, c_void, c_void, c_size, c_void]),
+    "mdlstm_head_workspace_bytes": (c_size, [P_HEAD, c_i32, P_RECT, P_I32]),
+    "mdlstm_head_forward": (c_i32, [P_HEAD, c_i32, c_i32, c_void, c_i32, P_RECT, c_void, c_void, c_void, c_void,
+                                    c_size, c_void]),
+    "mdlstm_ctc_loss": (c_i32, [P_HEAD, c_i32, P_RECT, P_I32, P_I32, c_void, c_void, c_void, c_void, c_size, c_void]),
+    "mdlstm_head_backward": (c_i32, [P_HEAD, c_i32, c_i32, c_i32, P_RECT, c_void, c_void, c_void, c_void, c_void,
+                                     c_void, c_size, c_void]),
     "mdlstm_last_error": (c_char_p, []),
     "mdlstm_gradients_fused": (c_i32, [P_DESC]),
     "mdlstm_set_phase_events": (c_i32, [c_i32, P_VOIDP]),

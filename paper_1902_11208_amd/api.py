@@ -375,3 +375,68 @@ class BlockConv:
                                                _ptr(self.dw), _ptr(self.db), _ptr(self.work), self.work.numel(),
                                                _stream(stream)))
         return self.dy, self.dw, self.db
+
+
+# ---------------------------------------------------------------------------
+# Output layer shared by the directions, row collapse, CTC loss
+# ---------------------------------------------------------------------------
+class Head:
+    """The shared fully-connected output layer over a packed canvas (frames =
+    canvas columns of each example, rows and directions summed) and the CTC
+    loss of every example. fp32; the workspace is sized for `labels`."""
+
+    def __init__(self, w: torch.Tensor, b: torch.Tensor, rects, canvas_hw, labels):
+        from ._lib import HeadDesc
+
+        if w.dim() != 2:
+            raise ValueError("w must be [classes, hidden]")
+        self.classes, self.hidden = int(w.shape[0]), int(w.shape[1])
+        check_tensor(w, "w", (self.classes, self.hidden), torch.float32)
+        check_tensor(b, "b", (self.classes,), torch.float32, w.device)
+        self.w, self.b = w, b
+        self.desc = HeadDesc(self.hidden, self.classes)
+        self.rects_np = np.asarray(rects, np.int32).reshape(-1, 4)
+        self.n = int(self.rects_np.shape[0])
+        self.rects = _rect_array(self.rects_np)
+        self.canvas_h, self.canvas_w = (int(v) for v in canvas_hw)
+        labels = [np.asarray(l, np.int32).reshape(-1) for l in labels]
+        if len(labels) != self.n:
+            raise ValueError(f"{len(labels)} label sequences for {self.n} examples")
+        self.label_lens = _i32_array([l.size for l in labels])
+        self.labels = _i32_array(np.concatenate(labels) if labels else np.zeros(0, np.int32))
+        self.frames = int(self.rects_np[:, 3].sum()) if self.n else 0
+        nbytes = int(lib().mdlstm_head_workspace_bytes(ctypes.byref(self.desc), self.n, self.rects, self.label_lens))
+        dev = w.device
+        self.workspace = torch.empty(max(1, nbytes), dtype=torch.uint8, device=dev)
+        self.logits = torch.empty((max(1, self.frames), self.classes), dtype=torch.float32, device=dev)
+        self.dlogits = torch.empty_like(self.logits)
+        self.losses = torch.empty(max(1, self.n), dtype=torch.float32, device=dev)
+        self.dy = torch.empty((self.canvas_h, self.canvas_w, 4 * self.hidden), dtype=torch.float32, device=dev)
+        self.dw = torch.empty_like(w)
+        self.db = torch.empty_like(b)
+
+    def forward(self, y: torch.Tensor, stream=None) -> torch.Tensor:
+        """Logits [frames, classes] of the layer's output canvas y."""
+        check_tensor(y, "y", (self.canvas_h, self.canvas_w, 4 * self.hidden), torch.float32, self.w.device)
+        check(lib().mdlstm_head_forward(ctypes.byref(self.desc), self.canvas_h, self.canvas_w, _ptr(y), self.n,
+                                        self.rects, _ptr(self.w), _ptr(self.b), _ptr(self.logits),
+                                        _ptr(self.workspace), self.workspace.numel(), _stream(stream)))
+        return self.logits[:self.frames]
+
+    def ctc(self, logits=None, stream=None):
+        """(losses [n], dlogits [frames, classes]) of the CTC loss."""
+        z = self.logits if logits is None else logits
+        check_tensor(z, "logits", tuple(self.logits.shape), torch.float32, self.w.device)
+        check(lib().mdlstm_ctc_loss(ctypes.byref(self.desc), self.n, self.rects, self.label_lens, self.labels,
+                                    _ptr(z), _ptr(self.losses), _ptr(self.dlogits), _ptr(self.workspace),
+                                    self.workspace.numel(), _stream(stream)))
+        return self.losses[:self.n], self.dlogits[:self.frames]
+
+    def backward(self, dlogits=None, stream=None):
+        """(dy canvas, dw, db) from the gradient of the logits (default: the CTC gradient)."""
+        g = self.dlogits if dlogits is None else dlogits
+        check_tensor(g, "dlogits", tuple(self.dlogits.shape), torch.float32, self.w.device)
+        check(lib().mdlstm_head_backward(ctypes.byref(self.desc), self.canvas_h, self.canvas_w, self.n, self.rects,
+                                         _ptr(self.w), _ptr(g), _ptr(self.dy), _ptr(self.dw), _ptr(self.db),
+                                         _ptr(self.workspace), self.workspace.numel(), _stream(stream)))
+        return self.dy, self.dw, self.db

@@ -112,4 +112,46 @@ hipError_t launch_block_conv(bool fwd, const ConvArgs& a, hipStream_t s);
 // Fill n floats with zero.
 hipError_t launch_zero_f32(float* d, int64_t n, hipStream_t s);
 
+// --- output layer shared by the directions, row collapse, CTC loss ---------
+struct HeadArgs {
+    int H, K, canvas_w;
+    int n_tiles;                 // tiles of head_tile_frames() frames
+    int frames;                  // frames of all examples
+    const float* y;              // forward: the last layer's output canvas [canvas][4H]
+    const int32_t* rects;        // [n][4] example rectangles on that canvas
+    const int32_t* frame_off;    // [n + 1] first frame of each example
+    const int32_t* tiles;        // [n_tiles][2] (example, first frame)
+    const float* w;              // [K][H]
+    const float* b;              // [K]
+    float* logits;               // forward output [frames][K]
+    float* S;                    // column sums [frames][H + 4], forward output, backward input
+    const float* dlogits;        // backward input [frames][K]
+    float* dy;                   // backward output canvas [canvas][4H]
+    float* part;                 // backward: weight-gradient partials
+    float* dw;                   // backward output [K][H]
+    float* db;                   // backward output [K]
+};
+struct CtcArgs {
+    int n, K, max_labels;
+    const int32_t* frame_off;    // [n + 1]
+    const int32_t* lab_off;      // [n + 1]
+    const int32_t* labels;       // concatenated labels
+    const int64_t* a_off;        // [n] first double of each example's alpha table
+    const float* logits;         // [frames][K]
+    double* lp;                  // workspace [frames][K]
+    double* alpha;               // workspace
+    float* losses;               // [n]
+    float* dlogits;              // [frames][K]
+};
+int head_tile_frames();
+int head_dw_chunk_frames();
+size_t head_fwd_lds(int H, int K);
+size_t head_bwd_lds(int H, int K);
+size_t head_dw_lds(int H, int K);
+size_t ctc_lds(int max_labels, int K);
+hipError_t launch_head_fwd(const HeadArgs& a, hipStream_t s);
+hipError_t launch_ctc(const CtcArgs& a, hipStream_t s);
+// zeroes the dy canvas (canvas_floats floats), then writes the rectangles
+hipError_t launch_head_bwd(const HeadArgs& a, int64_t canvas_floats, hipStream_t s);
+
 }  // namespace mdl

@@ -648,6 +648,285 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
 }
 
 // ---------------------------------------------------------------------------
+// Output layer shared by the directions, row collapse, CTC loss.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr int32_t kMaxHeadClasses = 128;
+constexpr int32_t kMaxLabel = 960;  // labels per example (LDS of the CTC kernel)
+
+mdlstm_status check_head_desc(const mdlstm_head_desc* d) {
+    if (!d) return fail(MDLSTM_ERR_INVALID_ARG, "head desc is NULL");
+    if (d->hidden < 4 || d->hidden > 64 || d->hidden % 4)
+        return fail(MDLSTM_ERR_UNSUPPORTED, "head hidden size %d: a multiple of 4 in [4, 64] is built", d->hidden);
+    if (d->classes < 2 || d->classes > kMaxHeadClasses)
+        return fail(MDLSTM_ERR_UNSUPPORTED, "head classes %d: 2 to %d are built", d->classes, kMaxHeadClasses);
+    return MDLSTM_OK;
+}
+
+// Workspace sections. The first part (tiles .. weight-gradient partials)
+// serves the layer's forward and backward; the second (labels .. alpha) the
+// CTC loss.
+struct HeadPlan {
+    int64_t frames = 0, alpha_doubles = 0;
+    int32_t n_tiles = 0, chunks = 0, labels = 0, max_label = 0;
+    size_t tiles, rects, frame_off, S, part, part1_end, lab_off, lab, a_off, lp, alpha, total;
+};
+
+HeadPlan head_plan(const mdlstm_head_desc* d, int32_t n, const mdlstm_rect* rects, const int32_t* label_lens) {
+    HeadPlan p;
+    const int hc = mdl::head_tile_frames();
+    for (int32_t i = 0; i < n; ++i) {
+        p.frames += rects[i].w;
+        p.n_tiles += (rects[i].w + hc - 1) / hc;
+        if (label_lens) {
+            p.labels += label_lens[i];
+            p.max_label = std::max(p.max_label, label_lens[i]);
+            p.alpha_doubles += (int64_t)rects[i].w * (2 * label_lens[i] + 1);
+        }
+    }
+    const int dwf = mdl::head_dw_chunk_frames();
+    p.chunks = (int32_t)((p.frames + dwf - 1) / dwf);
+    const size_t nn = (size_t)(n > 0 ? n : 1);
+    size_t off = 0;
+    p.tiles = off;
+    off += align_up((size_t)std::max(p.n_tiles, 1) * 8);
+    p.rects = off;
+    off += align_up(nn * 16);
+    p.frame_off = off;
+    off += align_up((nn + 1) * 4);
+    p.S = off;
+    off += align_up((size_t)std::max<int64_t>(p.frames, 1) * (d->hidden + 4) * 4);
+    p.part = off;
+    off += align_up((size_t)std::max(p.chunks, 1) * d->classes * (d->hidden + 1) * 4);
+    p.part1_end = off;
+    p.lab_off = off;
+    off += align_up((nn + 1) * 4);
+    p.lab = off;
+    off += align_up((size_t)std::max(p.labels, 1) * 4);
+    p.a_off = off;
+    off += align_up(nn * 8);
+    p.lp = off;
+    off += align_up((size_t)std::max<int64_t>(p.frames, 1) * d->classes * 8);
+    p.alpha = off;
+    off += align_up((size_t)std::max<int64_t>(p.alpha_doubles, 1) * 8);
+    p.total = off;
+    return p;
+}
+
+// Validation shared by the three calls (rectangles inside the canvas and
+// disjoint when a canvas is given; the frames of all examples addressable).
+mdlstm_status check_head_rects(int32_t n, const mdlstm_rect* rects, int32_t ch, int32_t cw) {
+    if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n is negative");
+    if (n > 0 && !rects) return fail(MDLSTM_ERR_INVALID_ARG, "rects is NULL");
+    int64_t frames = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        if (rects[i].h < 1 || rects[i].w < 1)
+            return fail(MDLSTM_ERR_BAD_LAYOUT, "rect %d has size %dx%d", i, rects[i].h, rects[i].w);
+        frames += rects[i].w;
+    }
+    if (frames > (int64_t)INT32_MAX / 256) return fail(MDLSTM_ERR_UNSUPPORTED, "%lld frames", (long long)frames);
+    if (ch >= 0) {
+        if (ch > kMaxDim || cw < 0 || cw > kMaxDim) return fail(MDLSTM_ERR_INVALID_ARG, "canvas %dx%d out of range", ch, cw);
+        int32_t mh = 0;
+        return check_rects(n, rects, ch, cw, &mh, kMaxDim);
+    }
+    return MDLSTM_OK;
+}
+
+// The small host-computed tables of the first workspace part, staged in one copy.
+mdlstm_status stage_head_tables(const HeadPlan& p, int32_t n, const mdlstm_rect* rects, char* ws, hipStream_t s) {
+    std::vector<unsigned char> host(p.S - p.tiles, 0);
+    int32_t* tiles = reinterpret_cast<int32_t*>(host.data() + (p.tiles - p.tiles));
+    int32_t* fo = reinterpret_cast<int32_t*>(host.data() + (p.frame_off - p.tiles));
+    const int hc = mdl::head_tile_frames();
+    int32_t t = 0, f = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        fo[i] = f;
+        f += rects[i].w;
+        for (int32_t c = 0; c < rects[i].w; c += hc) {
+            tiles[2 * t] = i;
+            tiles[2 * t + 1] = c;
+            ++t;
+        }
+    }
+    fo[n] = f;
+    if (n > 0) std::memcpy(host.data() + (p.rects - p.tiles), rects, (size_t)n * 16);
+    HIP_OR_FAIL(hipMemcpyAsync(ws + p.tiles, host.data(), host.size(), hipMemcpyHostToDevice, s));
+    return MDLSTM_OK;
+}
+
+}  // namespace
+
+size_t mdlstm_head_workspace_bytes(const mdlstm_head_desc* desc, int32_t n, const mdlstm_rect* rects,
+                                   const int32_t* label_lens) {
+    if (!desc || desc->hidden < 1 || desc->classes < 1 || n < 0 || (n > 0 && !rects)) return 0;
+    const HeadPlan p = head_plan(desc, n, rects, label_lens);
+    return label_lens ? p.total : p.part1_end;
+}
+
+mdlstm_status mdlstm_head_forward(const mdlstm_head_desc* desc, int32_t canvas_h, int32_t canvas_w, const float* d_y,
+                                  int32_t n, const mdlstm_rect* rects, const float* d_w, const float* d_b,
+                                  float* d_logits, void* d_workspace, size_t workspace_bytes, void* stream) {
+    mdlstm_status st = check_head_desc(desc);
+    if (st != MDLSTM_OK) return st;
+    if (canvas_h < 0) return fail(MDLSTM_ERR_INVALID_ARG, "canvas_h is negative");
+    st = check_head_rects(n, rects, canvas_h, canvas_w);
+    if (st != MDLSTM_OK) return st;
+    if (n > 0 && (!d_y || !d_w || !d_b || !d_logits)) return fail(MDLSTM_ERR_INVALID_ARG, "a device pointer is NULL");
+    if (misaligned(d_y) || misaligned(d_w) || misaligned(d_workspace))
+        return fail(MDLSTM_ERR_INVALID_ARG, "y, w and workspace must be 16-byte aligned");
+    const HeadPlan p = head_plan(desc, n, rects, nullptr);
+    if (!d_workspace || workspace_bytes < p.part1_end)
+        return fail(MDLSTM_ERR_WORKSPACE, "head workspace of %zu bytes, %zu needed", workspace_bytes, p.part1_end);
+    if (n == 0) return MDLSTM_OK;
+    hipStream_t s = as_stream(stream);
+    char* ws = static_cast<char*>(d_workspace);
+    st = stage_head_tables(p, n, rects, ws, s);
+    if (st != MDLSTM_OK) return st;
+    mdl::HeadArgs a{};
+    a.H = desc->hidden;
+    a.K = desc->classes;
+    a.canvas_w = canvas_w;
+    a.n_tiles = p.n_tiles;
+    a.frames = (int)p.frames;
+    a.y = d_y;
+    a.rects = reinterpret_cast<const int32_t*>(ws + p.rects);
+    a.frame_off = reinterpret_cast<const int32_t*>(ws + p.frame_off);
+    a.tiles = reinterpret_cast<const int32_t*>(ws + p.tiles);
+    a.w = d_w;
+    a.b = d_b;
+    a.logits = d_logits;
+    a.S = reinterpret_cast<float*>(ws + p.S);
+    HIP_OR_FAIL(mdl::launch_head_fwd(a, s));
+    return MDLSTM_OK;
+}
+
+mdlstm_status mdlstm_ctc_loss(const mdlstm_head_desc* desc, int32_t n, const mdlstm_rect* rects,
+                              const int32_t* label_lens, const int32_t* labels, const float* d_logits,
+                              float* d_losses, float* d_dlogits, void* d_workspace, size_t workspace_bytes,
+                              void* stream) {
+    mdlstm_status st = check_head_desc(desc);
+    if (st != MDLSTM_OK) return st;
+    st = check_head_rects(n, rects, -1, -1);
+    if (st != MDLSTM_OK) return st;
+    if (n > 0 && !label_lens) return fail(MDLSTM_ERR_INVALID_ARG, "label_lens is NULL");
+    int64_t total = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        if (label_lens[i] < 0 || label_lens[i] > kMaxLabel)
+            return fail(MDLSTM_ERR_UNSUPPORTED, "example %d: %d labels; 0 to %d are supported", i, label_lens[i],
+                        kMaxLabel);
+        total += label_lens[i];
+    }
+    if (total > 0 && !labels) return fail(MDLSTM_ERR_INVALID_ARG, "labels is NULL");
+    int64_t o = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t repeats = 0;
+        for (int32_t j = 0; j < label_lens[i]; ++j) {
+            const int32_t c = labels[o + j];
+            if (c < 1 || c >= desc->classes)
+                return fail(MDLSTM_ERR_INVALID_ARG, "example %d label %d is class %d; 1 to %d are labels (0 is the blank)",
+                            i, j, c, desc->classes - 1);
+            if (j > 0 && c == labels[o + j - 1]) ++repeats;
+        }
+        if ((int64_t)label_lens[i] + repeats > rects[i].w)
+            return fail(MDLSTM_ERR_INVALID_ARG, "example %d: %d labels (%d repeats) cannot be aligned to %d frames", i,
+                        label_lens[i], repeats, rects[i].w);
+        o += label_lens[i];
+    }
+    if (n > 0 && (!d_logits || !d_losses || !d_dlogits)) return fail(MDLSTM_ERR_INVALID_ARG, "a device pointer is NULL");
+    if (misaligned(d_workspace)) return fail(MDLSTM_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    const HeadPlan p = head_plan(desc, n, rects, label_lens);
+    if (!d_workspace || workspace_bytes < p.total)
+        return fail(MDLSTM_ERR_WORKSPACE, "CTC workspace of %zu bytes, %zu needed", workspace_bytes, p.total);
+    if (n == 0) return MDLSTM_OK;
+    hipStream_t s = as_stream(stream);
+    char* ws = static_cast<char*>(d_workspace);
+    // frame offsets (first part) and the label tables (second part)
+    std::vector<int32_t> fo((size_t)n + 1);
+    int32_t f = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        fo[i] = f;
+        f += rects[i].w;
+    }
+    fo[n] = f;
+    std::vector<unsigned char> host(p.lp - p.lab_off, 0);
+    int32_t* lo = reinterpret_cast<int32_t*>(host.data());
+    int64_t* ao = reinterpret_cast<int64_t*>(host.data() + (p.a_off - p.lab_off));
+    int32_t l = 0;
+    int64_t a = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        lo[i] = l;
+        l += label_lens[i];
+        ao[i] = a;
+        a += (int64_t)rects[i].w * (2 * label_lens[i] + 1);
+    }
+    lo[n] = l;
+    if (total > 0) std::memcpy(host.data() + (p.lab - p.lab_off), labels, (size_t)total * 4);
+    HIP_OR_FAIL(hipMemcpyAsync(ws + p.frame_off, fo.data(), fo.size() * 4, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(hipMemcpyAsync(ws + p.lab_off, host.data(), host.size(), hipMemcpyHostToDevice, s));
+    mdl::CtcArgs c{};
+    c.n = n;
+    c.K = desc->classes;
+    c.max_labels = p.max_label;
+    c.frame_off = reinterpret_cast<const int32_t*>(ws + p.frame_off);
+    c.lab_off = reinterpret_cast<const int32_t*>(ws + p.lab_off);
+    c.labels = reinterpret_cast<const int32_t*>(ws + p.lab);
+    c.a_off = reinterpret_cast<const int64_t*>(ws + p.a_off);
+    c.logits = d_logits;
+    c.lp = reinterpret_cast<double*>(ws + p.lp);
+    c.alpha = reinterpret_cast<double*>(ws + p.alpha);
+    c.losses = d_losses;
+    c.dlogits = d_dlogits;
+    HIP_OR_FAIL(mdl::launch_ctc(c, s));
+    return MDLSTM_OK;
+}
+
+mdlstm_status mdlstm_head_backward(const mdlstm_head_desc* desc, int32_t canvas_h, int32_t canvas_w, int32_t n,
+                                   const mdlstm_rect* rects, const float* d_w, const float* d_dlogits, float* d_dy,
+                                   float* d_dw, float* d_db, void* d_workspace, size_t workspace_bytes,
+                                   void* stream) {
+    mdlstm_status st = check_head_desc(desc);
+    if (st != MDLSTM_OK) return st;
+    if (canvas_h < 0) return fail(MDLSTM_ERR_INVALID_ARG, "canvas_h is negative");
+    st = check_head_rects(n, rects, canvas_h, canvas_w);
+    if (st != MDLSTM_OK) return st;
+    if (!d_dw || !d_db) return fail(MDLSTM_ERR_INVALID_ARG, "a weight-gradient pointer is NULL");
+    const int64_t canvas_floats = (int64_t)canvas_h * canvas_w * 4 * desc->hidden;
+    if (canvas_floats > 0 && !d_dy) return fail(MDLSTM_ERR_INVALID_ARG, "dy is NULL");
+    if (n > 0 && (!d_w || !d_dlogits)) return fail(MDLSTM_ERR_INVALID_ARG, "w or dlogits is NULL");
+    if (misaligned(d_dy) || misaligned(d_w) || misaligned(d_workspace))
+        return fail(MDLSTM_ERR_INVALID_ARG, "dy, w and workspace must be 16-byte aligned");
+    const HeadPlan p = head_plan(desc, n, rects, nullptr);
+    if (!d_workspace || workspace_bytes < p.part1_end)
+        return fail(MDLSTM_ERR_WORKSPACE, "head workspace of %zu bytes, %zu needed", workspace_bytes, p.part1_end);
+    hipStream_t s = as_stream(stream);
+    char* ws = static_cast<char*>(d_workspace);
+    if (n > 0) {
+        st = stage_head_tables(p, n, rects, ws, s);
+        if (st != MDLSTM_OK) return st;
+    }
+    mdl::HeadArgs a{};
+    a.H = desc->hidden;
+    a.K = desc->classes;
+    a.canvas_w = canvas_w;
+    a.n_tiles = p.n_tiles;
+    a.frames = (int)p.frames;
+    a.rects = reinterpret_cast<const int32_t*>(ws + p.rects);
+    a.frame_off = reinterpret_cast<const int32_t*>(ws + p.frame_off);
+    a.tiles = reinterpret_cast<const int32_t*>(ws + p.tiles);
+    a.w = d_w;
+    a.S = reinterpret_cast<float*>(ws + p.S);
+    a.dlogits = d_dlogits;
+    a.dy = d_dy;
+    a.part = reinterpret_cast<float*>(ws + p.part);
+    a.dw = d_dw;
+    a.db = d_db;
+    HIP_OR_FAIL(mdl::launch_head_bwd(a, canvas_floats, s));
+    return MDLSTM_OK;
+}
+
+// ---------------------------------------------------------------------------
 // Stack glue: block reshape and grouped block convolution between layers.
 // ---------------------------------------------------------------------------
 namespace {

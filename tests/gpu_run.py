@@ -51,3 +51,29 @@ def run_layer(xs, params, dys, heights, widths, canvas_w, dtype="f32", kind="pac
         out["dWx"], out["dU"], out["db"] = to_np(dwx), to_np(du), to_np(db)
     torch.cuda.synchronize()
     return out
+
+
+def run_training_step(xs, params, head_params, labels, heights, widths, canvas_w, keep=None):
+    """MDLSTM layer forward, shared output layer, CTC loss, head backward and
+    layer backward on one packed canvas, all through the C ABI."""
+    units, place, ch, cw, mask = layout(heights, widths, canvas_w)
+    wx, u, b = (to_dev(p, "f32") for p in params)
+    canvas = api.pack_data([to_dev(x, "f32") for x in xs], place, ch, cw)
+    layer = api.MDLSTMLayer(wx, u, b, ch, cw, units, mask)
+    hw, hb = (to_dev(p, "f32") for p in head_params)
+    head = api.Head(hw, hb, place, (ch, cw), labels)
+    y = layer.forward(canvas)
+    logits = head.forward(y)
+    losses, dlogits = head.ctc()
+    dy, dwfc, dbfc = head.backward()
+    dx, dwx, du, db = layer.backward(dy)
+    torch.cuda.synchronize()
+    off = np.concatenate([[0], np.cumsum(np.asarray(widths, np.int64))])
+    ks = set(range(len(xs))) if keep is None else set(int(k) for k in keep)
+    lg, dl = to_np(logits), to_np(dlogits)
+    out = {"loss": to_np(losses), "rects": place, "dy_canvas": dy.clone(), "mask": mask, "head": head,
+           "logits": [lg[off[k]:off[k + 1]] if k in ks else None for k in range(len(xs))],
+           "dlogits": [dl[off[k]:off[k + 1]] if k in ks else None for k in range(len(xs))],
+           "dX": [to_np(t) if k in ks else None for k, t in enumerate(api.unpack_data(dx, place))],
+           "dWfc": to_np(dwfc), "dbfc": to_np(dbfc), "dWx": to_np(dwx), "dU": to_np(du), "db": to_np(db)}
+    return out

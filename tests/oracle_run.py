@@ -101,3 +101,33 @@ def run_stack(images, layers, convs, dys, block=(2, 4), workers=1, progress=None
             csum[i] = [a + b for a, b in zip(csum[i], cg[i])]
     out["layer_grads"], out["conv_grads"] = lsum, csum
     return out
+
+
+def _step_one(args):
+    from oracle import head
+
+    x, p64, w64, b64, label = args
+    Y, cache = mdlstm.layer_forward(x, *p64)
+    loss, dY, dW, db, logits, dlogits = head.head_loss_forward_backward(Y, w64, b64, label)
+    g = mdlstm.layer_backward(cache, dY, *p64)
+    return loss, logits, dlogits, dW, db, g
+
+
+def run_training_step(xs, params, head_params, labels, workers=1, progress=None):
+    """One training step per example, each alone: MDLSTM layer, the shared
+    output layer with the row collapse, CTC loss, and back. Returns losses,
+    logits, dlogits and dX per example, and every weight gradient summed."""
+    p64 = [np.asarray(t, np.float64) for t in params]
+    w64, b64 = (np.asarray(t, np.float64) for t in head_params)
+    jobs = [(x, p64, w64, b64, labels[k]) for k, x in enumerate(xs)]
+    results = _pool_map(_step_one, jobs, workers, progress)
+    out = {"loss": np.array([r[0] for r in results]), "logits": [r[1] for r in results],
+           "dlogits": [r[2] for r in results], "dX": [r[5][0] for r in results]}
+    out["dWfc"] = sum(r[3] for r in results)
+    out["dbfc"] = sum(r[4] for r in results)
+    for i, nm in enumerate(("dWx", "dU", "db")):
+        acc = np.zeros_like(results[0][5][i + 1])
+        for r in results:
+            acc = acc + r[5][i + 1]
+        out[nm] = acc
+    return out

@@ -237,3 +237,42 @@ def test_gradients_fused_query(built_lib):
     assert f(ctypes.byref(L.LayerDesc(64, 128, 1))) == 0   # bf16 H 128: two kernels
     assert f(ctypes.byref(L.LayerDesc(16, 12, 0))) == -1   # not built
     assert f(None) == -1
+
+
+def test_head_calls_reject_bad_arguments(built_lib):
+    """The output-layer and CTC calls validate sizes, rectangles and labels on
+    the host before any HIP call."""
+    L = _lib()
+    lib = L.lib()
+    ok = L.HeadDesc(8, 6)
+    rects = (L.Rect * 2)(L.Rect(0, 0, 3, 5), L.Rect(0, 6, 2, 4))
+    lens = (ctypes.c_int32 * 2)(2, 1)
+    need = lib.mdlstm_head_workspace_bytes(ctypes.byref(ok), 2, rects, lens)
+    assert need > lib.mdlstm_head_workspace_bytes(ctypes.byref(ok), 2, rects, None) > 0
+
+    def fwd(desc, ch=4, cw=12, r=rects, ws=need):
+        return lib.mdlstm_head_forward(ctypes.byref(desc), ch, cw, FAKE, 2, r, FAKE, FAKE, FAKE, FAKE, ws, None)
+
+    assert fwd(L.HeadDesc(6, 6)) == 5            # hidden not a multiple of 4
+    assert fwd(L.HeadDesc(8, 300)) == 5          # too many classes
+    assert fwd(ok, ch=2) == 3                    # a rectangle leaves the canvas
+    assert fwd(ok, r=(L.Rect * 2)(L.Rect(0, 0, 3, 5), L.Rect(0, 4, 2, 4))) == 3  # overlap
+    assert fwd(ok, ws=16) == 4                   # workspace
+
+    def ctc(lens_, labs, ws=need):
+        ll = (ctypes.c_int32 * 2)(*lens_)
+        lb = (ctypes.c_int32 * max(1, len(labs)))(*labs)
+        return lib.mdlstm_ctc_loss(ctypes.byref(ok), 2, rects, ll, lb, FAKE, FAKE, FAKE, FAKE, ws, None)
+
+    assert ctc([2, 1], [1, 0, 3]) == 1           # a label is the blank
+    assert ctc([2, 1], [1, 6, 3]) == 1           # a label past the classes
+    assert ctc([5, 1], [2, 2, 2, 1, 1, 3]) == 1  # 5 labels + 3 repeats > 5 frames
+    assert b"aligned" in lib.mdlstm_last_error()
+    assert ctc([1000, 1], [1] * 1001) == 5       # above the labels per example
+    assert ctc([2, 1], [1, 2, 3], ws=need - 256) == 4
+
+    def bwd(ws=need, dw=FAKE):
+        return lib.mdlstm_head_backward(ctypes.byref(ok), 4, 12, 2, rects, FAKE, FAKE, FAKE, dw, FAKE, FAKE, ws, None)
+
+    assert bwd(dw=None) == 1
+    assert bwd(ws=16) == 4
