@@ -19,6 +19,18 @@ A predecessor that lies outside the example or is masked out hands over
 zeros (Section V: binary masking blocks the hidden and memory state of
 invalid predecessors); a masked cell outputs h = c = 0.
 
+Memory-state matrices (Appendix A: besides the five matrices per predecessor
+hidden state, three per predecessor memory state S1 = c_L and S2 = c_T, whose
+products are summed with the hidden-state ones). Reading: both memory states
+feed the same three gates, the input gate and the two forget gates (the gates
+that decide what enters and what stays in the new state), through full
+H x H matrices:
+
+    a[i, f_L, f_T] += V [c_L ; c_T]           (V: 3H x 2H, per direction)
+
+The output gate and the cell candidate take no memory state. Passing no V
+(the default) is the plain cell above; V = 0 gives the same values.
+
 Four directions (Section III): one MDLSTM per scan origin, outputs stacked
 along channels as [Y_0 | Y_1 | Y_2 | Y_3]. Direction 0 scans from the
 top-left (L = (y, x-1), T = (y-1, x)), 1 from the top-right (L = (y, x+1),
@@ -65,8 +77,9 @@ def _flip(a, d: int):
 # Scalar form: per-cell loop, explicit predecessor offsets per direction.
 # ----------------------------------------------------------------------------
 
-def layer_forward_scalar(x, wx, u, b, valid=None):
-    """x [h, w, C]; wx [4, 5H, C]; u [4, 5H, 2H]; b [4, 5H] -> Y [h, w, 4H]."""
+def layer_forward_scalar(x, wx, u, b, valid=None, v=None):
+    """x [h, w, C]; wx [4, 5H, C]; u [4, 5H, 2H]; b [4, 5H]; optional memory-state
+    matrices v [4, 3H, 2H] -> Y [h, w, 4H]."""
     x = np.asarray(x, np.float64)
     h, w, _ = x.shape
     H = u.shape[2] // 2
@@ -76,6 +89,7 @@ def layer_forward_scalar(x, wx, u, b, valid=None):
     for d in range(4):
         sy, sx = _steps(d)
         W, U, B = (np.asarray(t[d], np.float64) for t in (wx, u, b))
+        V = None if v is None else np.asarray(v[d], np.float64)
         hh = np.zeros((h, w, H))
         cc = np.zeros((h, w, H))
         for yy in (range(h) if sy == 1 else range(h - 1, -1, -1)):
@@ -86,6 +100,8 @@ def layer_forward_scalar(x, wx, u, b, valid=None):
                 hL, cL = (hh[yy, lx], cc[yy, lx]) if 0 <= lx < w else (zero, zero)
                 hT, cT = (hh[ty, xx], cc[ty, xx]) if 0 <= ty < h else (zero, zero)
                 a = W @ x[yy, xx] + B + U @ np.concatenate([hL, hT])
+                if V is not None:
+                    a[0:3 * H] += V @ np.concatenate([cL, cT])
                 ig = sigmoid(a[0:H])
                 fL = sigmoid(a[H:2 * H])
                 fT = sigmoid(a[2 * H:3 * H])
@@ -102,8 +118,9 @@ def layer_forward_scalar(x, wx, u, b, valid=None):
 # Diagonal form in direction 0's frame.
 # ----------------------------------------------------------------------------
 
-def scan_forward(z, valid, U):
-    """Direction-0 scan. z [h, w, 5H] = Wx x + b; valid [h, w] bool; U [5H, 2H].
+def scan_forward(z, valid, U, V=None):
+    """Direction-0 scan. z [h, w, 5H] = Wx x + b; valid [h, w] bool; U [5H, 2H];
+    V [3H, 2H] memory-state matrices or None.
 
     Returns a cache dict with h, c, activated gates, and the predecessor
     states actually used (zeros where the predecessor is outside or invalid).
@@ -124,6 +141,8 @@ def scan_forward(z, valid, U):
         hl, ht = hs[y + 1, x], hs[y, x + 1]
         cl, ct = cs[y + 1, x], cs[y, x + 1]
         a = z[y, x] + np.concatenate([hl, ht], axis=1) @ U.T
+        if V is not None:
+            a[:, 0:3 * H] += np.concatenate([cl, ct], axis=1) @ V.T
         ig = sigmoid(a[:, 0:H])
         fL = sigmoid(a[:, H:2 * H])
         fT = sigmoid(a[:, 2 * H:3 * H])
@@ -140,9 +159,11 @@ def scan_forward(z, valid, U):
             "hL": hL, "hT": hT, "cL": cL, "cT": cT, "valid": valid}
 
 
-def scan_backward(cache, dh_out, U):
+def scan_backward(cache, dh_out, U, V=None):
     """Reverse-diagonal backward of ``scan_forward``. Returns dz [h, w, 5H]
-    (gradient of the pre-activations) for upstream gradient dh_out [h, w, H]."""
+    (gradient of the pre-activations) for upstream gradient dh_out [h, w, H].
+    With memory-state matrices V, a predecessor's state also receives
+    V^T da[i, f_L, f_T] (its c_L or c_T half)."""
     gates, c_all, valid = cache["gates"], cache["c"], cache["valid"]
     h, w, _, H = gates.shape
     # accumulators for gradient arriving from successors, with one sink row
@@ -167,15 +188,17 @@ def scan_backward(cache, dh_out, U):
         ], axis=1)
         dz[y, x] = da
         back = da @ U
+        backc = da[:, 0:3 * H] @ V if V is not None else np.zeros((len(y), 2 * H))
         dh_acc[y + 1, x] += back[:, :H]      # to the left predecessor (y, x-1)
-        dc_acc[y + 1, x] += dc * fL
+        dc_acc[y + 1, x] += dc * fL + backc[:, :H]
         dh_acc[y, x + 1] += back[:, H:]      # to the top predecessor (y-1, x)
-        dc_acc[y, x + 1] += dc * fT
+        dc_acc[y, x + 1] += dc * fT + backc[:, H:]
     return dz
 
 
-def layer_forward(x, wx, u, b, valid=None):
-    """Four-direction layer on one example. Returns (Y [h, w, 4H], cache)."""
+def layer_forward(x, wx, u, b, valid=None, v=None):
+    """Four-direction layer on one example (memory-state matrices v [4, 3H, 2H]
+    optional). Returns (Y [h, w, 4H], cache)."""
     x = np.asarray(x, np.float64)
     h, w, _ = x.shape
     H = u.shape[2] // 2
@@ -184,15 +207,17 @@ def layer_forward(x, wx, u, b, valid=None):
     caches = []
     for d in range(4):
         W, U, B = (np.asarray(t[d], np.float64) for t in (wx, u, b))
+        V = None if v is None else np.asarray(v[d], np.float64)
         z = _flip(x, d) @ W.T + B
-        cd = scan_forward(z, _flip(valid, d), U)
+        cd = scan_forward(z, _flip(valid, d), U, V)
         Y[:, :, d * H:(d + 1) * H] = _flip(cd["h"], d)
         caches.append(cd)
     return Y, {"x": x, "dirs": caches, "H": H}
 
 
-def layer_backward(cache, dY, wx, u, b):
-    """Gradients of sum(Y * dY) for ``layer_forward``: (dX, dWx, dU, db), all float64.
+def layer_backward(cache, dY, wx, u, b, v=None):
+    """Gradients of sum(Y * dY) for ``layer_forward``: (dX, dWx, dU, db), all
+    float64, and dV as a fifth entry when memory-state matrices v were used.
     Weight gradients are sums over every cell (not means)."""
     x = cache["x"]
     H = cache["H"]
@@ -201,16 +226,23 @@ def layer_backward(cache, dY, wx, u, b):
     dWx = np.zeros((4, 5 * H, x.shape[2]))
     dU = np.zeros((4, 5 * H, 2 * H))
     db = np.zeros((4, 5 * H))
+    dV = None if v is None else np.zeros((4, 3 * H, 2 * H))
     for d in range(4):
         cd = cache["dirs"][d]
         U = np.asarray(u[d], np.float64)
-        dz = scan_backward(cd, _flip(dY[:, :, d * H:(d + 1) * H], d), U)
+        V = None if v is None else np.asarray(v[d], np.float64)
+        dz = scan_backward(cd, _flip(dY[:, :, d * H:(d + 1) * H], d), U, V)
         xf = _flip(x, d)
         dWx[d] = np.einsum("ywr,ywk->rk", dz, xf)
         db[d] = dz.sum(axis=(0, 1))
         hcat = np.concatenate([cd["hL"], cd["hT"]], axis=2)
         dU[d] = np.einsum("ywr,ywk->rk", dz, hcat)
+        if V is not None:
+            ccat = np.concatenate([cd["cL"], cd["cT"]], axis=2)
+            dV[d] = np.einsum("ywr,ywk->rk", dz[:, :, 0:3 * H], ccat)
         dX += _flip(dz @ np.asarray(wx[d], np.float64), d)
+    if v is not None:
+        return dX, dWx, dU, db, dV
     return dX, dWx, dU, db
 
 
@@ -240,8 +272,10 @@ def canvas_scan_forward(canvas_x, mask, params):
 def units_forward(canvas_x, mask, rects, params):
     """Canvas forward with scheduling rectangles: the recurrence restarts at
     every rectangle edge and at every masked cell; cells outside every
-    rectangle output zero. Returns (Y [H_c, W_c, 4H], caches)."""
-    wx, u, b = params
+    rectangle output zero. params: (wx, u, b) or (wx, u, b, v).
+    Returns (Y [H_c, W_c, 4H], caches)."""
+    wx, u, b = params[:3]
+    v = params[3] if len(params) > 3 else None
     canvas_x = np.asarray(canvas_x, np.float64)
     Hc, Wc, _ = canvas_x.shape
     H = u.shape[2] // 2
@@ -250,16 +284,17 @@ def units_forward(canvas_x, mask, rects, params):
     caches = []
     for y0, x0, h, w in np.asarray(rects).reshape(-1, 4):
         win = (slice(y0, y0 + h), slice(x0, x0 + w))
-        Yr, cr = layer_forward(canvas_x[win], wx, u, b, valid=mask[win])
+        Yr, cr = layer_forward(canvas_x[win], wx, u, b, valid=mask[win], v=v)
         Y[win] = Yr
         caches.append(cr)
     return Y, caches
 
 
 def units_backward(canvas_x, mask, rects, params, caches, dY):
-    """Backward of ``units_forward``: (dX canvas, dWx, dU, db); dY is ignored
-    where the mask is 0 or outside every rectangle."""
-    wx, u, b = params
+    """Backward of ``units_forward``: (dX canvas, dWx, dU, db[, dV]); dY is
+    ignored where the mask is 0 or outside every rectangle."""
+    wx, u, b = params[:3]
+    v = params[3] if len(params) > 3 else None
     canvas_x = np.asarray(canvas_x, np.float64)
     H = u.shape[2] // 2
     mask = np.asarray(mask, bool)
@@ -268,12 +303,18 @@ def units_backward(canvas_x, mask, rects, params, caches, dY):
     dWx = np.zeros((4, 5 * H, canvas_x.shape[2]))
     dU = np.zeros((4, 5 * H, 2 * H))
     db = np.zeros((4, 5 * H))
+    dV = None if v is None else np.zeros((4, 3 * H, 2 * H))
     for (y0, x0, h, w), cr in zip(np.asarray(rects).reshape(-1, 4), caches):
         win = (slice(y0, y0 + h), slice(x0, x0 + w))
         g = dY[win] * mask[win][:, :, None]
-        a, bw, cu, cb = layer_backward(cr, g, wx, u, b)
+        grads = layer_backward(cr, g, wx, u, b, v)
+        a, bw, cu, cb = grads[:4]
         dX[win] = a * mask[win][:, :, None]
         dWx += bw
         dU += cu
         db += cb
+        if v is not None:
+            dV += grads[4]
+    if v is not None:
+        return dX, dWx, dU, db, dV
     return dX, dWx, dU, db
