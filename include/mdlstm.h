@@ -67,11 +67,24 @@ typedef struct {
 
 /* One MDLSTM layer. Supported: F32 with hidden in {4, 8, 16, 32, 64};
  * BF16 with hidden in {32, 64, 128}; c_in a multiple of 4 (F32) or 8 (BF16),
- * 4 <= c_in <= 256. */
+ * 4 <= c_in <= 256.
+ *
+ * memory_states = 1 adds the memory-state matrices of Appendix A (three per
+ * predecessor memory state S1 = c_L and S2 = c_T, next to the five per
+ * predecessor hidden state). Reading: both states feed the input gate and the
+ * two forget gates through V_d (3H x 2H, rows i, f_L, f_T; columns c_L, c_T):
+ *     a = Wx_d x + b_d + U_d [h_L ; h_T] + [V_d [c_L ; c_T] ; 0 ; 0]
+ * The recurrent weight argument then holds U [4][5H][2H] immediately followed
+ * by V [4][3H][2H] (one buffer), and the backward writes dU followed by dV the
+ * same way. Built for F32 with hidden 16 or 32 (UNSUPPORTED otherwise); the
+ * per-diagonal schedule (mdlstm_forward_stepwise) is not built for it.
+ * 0 (or a descriptor initialised with its first three fields) is the plain
+ * cell. */
 typedef struct {
     int32_t c_in;
     int32_t hidden;
-    int32_t dtype; /* mdlstm_dtype */
+    int32_t dtype;         /* mdlstm_dtype */
+    int32_t memory_states; /* 0 or 1 */
 } mdlstm_layer_desc;
 
 /* Largest rectangle height the wavefront kernels accept. */

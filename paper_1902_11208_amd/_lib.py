@@ -20,7 +20,7 @@ class Rect(ctypes.Structure):
 
 
 class LayerDesc(ctypes.Structure):
-    _fields_ = [("c_in", c_i32), ("hidden", c_i32), ("dtype", c_i32)]
+    _fields_ = [("c_in", c_i32), ("hidden", c_i32), ("dtype", c_i32), ("memory_states", c_i32)]
 
 
 class HeadDesc(ctypes.Structure):

@@ -192,8 +192,8 @@ def unpack_data(canvas: torch.Tensor, rects, stream=None):
 # ---------------------------------------------------------------------------
 # Layer
 # ---------------------------------------------------------------------------
-def layer_desc(c_in: int, hidden: int, dtype: int) -> LayerDesc:
-    return LayerDesc(int(c_in), int(hidden), int(dtype))
+def layer_desc(c_in: int, hidden: int, dtype: int, memory_states: int = 0) -> LayerDesc:
+    return LayerDesc(int(c_in), int(hidden), int(dtype), int(memory_states))
 
 
 def workspace_bytes(c_in: int, hidden: int, dtype: int, canvas_h: int, canvas_w: int, n_rects: int) -> int:
@@ -213,8 +213,8 @@ def gradients_fused(c_in: int, hidden: int, dtype: int) -> bool:
 class Prepared:
     """Host-side argument bundle for one canvas layout, reused across calls."""
 
-    def __init__(self, c_in: int, hidden: int, dtype: int, canvas_h: int, canvas_w: int, rects):
-        self.desc = layer_desc(c_in, hidden, dtype)
+    def __init__(self, c_in: int, hidden: int, dtype: int, canvas_h: int, canvas_w: int, rects, memory_states=0):
+        self.desc = layer_desc(c_in, hidden, dtype, memory_states)
         self.canvas_h, self.canvas_w = int(canvas_h), int(canvas_w)
         self.rects_np = np.asarray(rects, np.int32).reshape(-1, 4)
         self.n_rects = int(self.rects_np.shape[0])
@@ -250,10 +250,12 @@ class MDLSTMLayer:
     """Four-direction MDLSTM layer over a canvas with a fixed layout.
 
     Owns the workspace and the output/gradient buffers for that layout.
+    v [4, 3H, 2H] (optional, fp32): memory-state matrices feeding the input and
+    forget gates; the backward then also fills self.dv.
     """
 
     def __init__(self, wx: torch.Tensor, u: torch.Tensor, b: torch.Tensor, canvas_h: int, canvas_w: int, rects,
-                 mask: torch.Tensor):
+                 mask: torch.Tensor, v: torch.Tensor = None):
         if wx.dim() != 3 or u.dim() != 3:
             raise ValueError("wx must be [4, 5H, c_in] and u [4, 5H, 2H]")
         self.dtype = dtype_code(wx.dtype)
@@ -264,15 +266,20 @@ class MDLSTMLayer:
         check_tensor(u, "u", (4, 5 * H, 2 * H), td, dev)
         check_tensor(b, "b", (4, 5 * H), td, dev)
         check_tensor(mask, "mask", (canvas_h, canvas_w), torch.uint8, dev)
+        self.memory = v is not None
+        if self.memory:
+            check_tensor(v, "v", (4, 3 * H, 2 * H), td, dev)
+            u = torch.cat([u.reshape(-1), v.reshape(-1)])  # U then V, one buffer
         self.wx, self.u, self.b, self.mask = wx, u, b, mask
-        self.prep = Prepared(self.c_in, self.hidden, self.dtype, canvas_h, canvas_w, rects)
+        self.prep = Prepared(self.c_in, self.hidden, self.dtype, canvas_h, canvas_w, rects, int(self.memory))
         self.workspace = torch.empty(max(1, self.prep.ws_bytes), dtype=torch.uint8, device=dev)
-        td = wx.dtype
-        H = self.hidden
         self.y = torch.empty((canvas_h, canvas_w, 4 * H), dtype=td, device=dev)
         self.dx = torch.empty((canvas_h, canvas_w, self.c_in), dtype=td, device=dev)
         self.dwx = torch.empty((4, 5 * H, self.c_in), dtype=torch.float32, device=dev)
-        self.du = torch.empty((4, 5 * H, 2 * H), dtype=torch.float32, device=dev)
+        nu, nv = 4 * 5 * H * 2 * H, (4 * 3 * H * 2 * H if self.memory else 0)
+        self._dgrad = torch.empty(nu + nv, dtype=torch.float32, device=dev)
+        self.du = self._dgrad[:nu].view(4, 5 * H, 2 * H)
+        self.dv = self._dgrad[nu:].view(4, 3 * H, 2 * H) if self.memory else None
         self.db = torch.empty((4, 5 * H), dtype=torch.float32, device=dev)
 
     def _check_x(self, x):
@@ -295,8 +302,10 @@ class MDLSTMLayer:
             raise ValueError("backward needs a forward call on this layer first")
         check_tensor(dy, "dy", (self.prep.canvas_h, self.prep.canvas_w, 4 * self.hidden), self.wx.dtype,
                      self.wx.device)
-        backward(self.prep, self.x, self.mask, self.wx, self.u, self.b, self.y, dy, self.dx, self.dwx, self.du,
+        backward(self.prep, self.x, self.mask, self.wx, self.u, self.b, self.y, dy, self.dx, self.dwx, self._dgrad,
                  self.db, self.workspace, stream)
+        if self.memory:
+            return self.dx, self.dwx, self.du, self.db, self.dv
         return self.dx, self.dwx, self.du, self.db
 
 

@@ -112,6 +112,26 @@ hipError_t launch_block_conv(bool fwd, const ConvArgs& a, hipStream_t s);
 // Fill n floats with zero.
 hipError_t launch_zero_f32(float* d, int64_t n, hipStream_t s);
 
+// --- layer with memory-state matrices (fp32, H = 16 or 32) -----------------
+struct MemArgs {
+    const int32_t* units;   // unit order (4 * rect + direction), one workgroup each
+    const int32_t* rects;   // [n_rects][4]
+    const uint8_t* mask;
+    const float* u;         // [4][5H][2H]
+    const float* v;         // [4][3H][2H]
+    float* z;               // pre-activations -> activated gates (forward) -> gate gradients (backward)
+    float* c;               // cell states [cells][4H]
+    float* y;               // forward output [cells][4H]
+    const float* dy;        // backward input [cells][4H]
+    int canvas_w;
+    float* dvpart;          // backward: [units][3H][2H] partials
+};
+bool mem_supported(const LayerGeom& g);
+size_t mem_partial_bytes(const LayerGeom& g, int n_units);
+hipError_t launch_wavefront_mem(bool fwd, const LayerGeom& g, int n_units, const MemArgs& a, hipStream_t s);
+hipError_t launch_dv_reduce(const LayerGeom& g, int n_units, const int32_t* d_units, const float* d_part, float* d_dv,
+                            hipStream_t s);
+
 // --- output layer shared by the directions, row collapse, CTC loss ---------
 struct HeadArgs {
     int H, K, canvas_w;

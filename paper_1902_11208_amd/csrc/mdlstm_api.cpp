@@ -64,6 +64,10 @@ mdlstm_status check_desc(const mdlstm_layer_desc* d) {
     if (d->dtype != MDLSTM_F32 && d->dtype != MDLSTM_BF16)
         return fail(MDLSTM_ERR_INVALID_ARG, "dtype %d is not MDLSTM_F32 or MDLSTM_BF16", d->dtype);
     if (d->c_in < 1 || d->hidden < 1) return fail(MDLSTM_ERR_INVALID_ARG, "c_in and hidden must be positive");
+    if (d->memory_states != 0 && d->memory_states != 1)
+        return fail(MDLSTM_ERR_INVALID_ARG, "memory_states %d is not 0 or 1", d->memory_states);
+    if (d->memory_states && (d->dtype != MDLSTM_F32 || (d->hidden != 16 && d->hidden != 32)))
+        return fail(MDLSTM_ERR_UNSUPPORTED, "memory-state matrices are built for F32 with hidden 16 or 32");
     if (d->dtype == MDLSTM_F32) {
         const int h = d->hidden;
         if (!(h == 4 || h == 8 || h == 16 || h == 32 || h == 64))
@@ -81,7 +85,7 @@ mdlstm_status check_desc(const mdlstm_layer_desc* d) {
 }
 
 struct Plan {
-    size_t z, c, rid, rects, units, part, flags, wxt, queue, total;
+    size_t z, c, rid, rects, units, part, flags, wxt, dvpart, queue, total;
 };
 
 mdl::LayerGeom geom(const mdlstm_layer_desc* d, int32_t ch, int32_t cw) {
@@ -118,6 +122,8 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
     off += align_up(strip ? mdl::strip_vid_bytes(g) : mdl::big_flags_bytes(g));
     p.wxt = off;
     off += strip ? 0 : align_up(mdl::big_wxt_bytes(g));
+    p.dvpart = off;  // memory-state matrices: a dV partial per unit
+    off += d->memory_states ? align_up(mdl::mem_partial_bytes(g, 4 * (nr > 0 ? nr : 1))) : 0;
     p.queue = off;  // unit queue: next unit, workgroups done
     off += align_up(8);
     p.total = off;
@@ -178,6 +184,7 @@ struct Common {
     mdl::LayerGeom g;
     Plan p;
     int nt;
+    int memory;
     char* ws;
 };
 
@@ -202,6 +209,7 @@ mdlstm_status prepare(const mdlstm_layer_desc* desc, int32_t ch, int32_t cw, con
         return fail(MDLSTM_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, p.total);
     out->g = geom(desc, ch, cw);
     out->p = p;
+    out->memory = desc->memory_states;
     out->nt = (max_h + 15) / 16;
     if (out->nt < 1) out->nt = 1;
     out->ws = static_cast<char*>(d_workspace);
@@ -211,10 +219,10 @@ mdlstm_status prepare(const mdlstm_layer_desc* desc, int32_t ch, int32_t cw, con
 // Identity of what a workspace holds after layout staging: the layer shape,
 // canvas and rectangles (with a hash of the rectangle list).
 struct StagedKey {
-    int32_t c_in = 0, hidden = 0, dtype = 0, canvas_h = 0, canvas_w = 0, n_rects = -1, device = -1;
+    int32_t c_in = 0, hidden = 0, dtype = 0, memory = 0, canvas_h = 0, canvas_w = 0, n_rects = -1, device = -1;
     uint64_t hash = 0;
     bool operator==(const StagedKey& o) const {
-        return c_in == o.c_in && hidden == o.hidden && dtype == o.dtype && canvas_h == o.canvas_h &&
+        return c_in == o.c_in && hidden == o.hidden && dtype == o.dtype && memory == o.memory && canvas_h == o.canvas_h &&
                canvas_w == o.canvas_w && n_rects == o.n_rects && device == o.device && hash == o.hash;
     }
 };
@@ -224,6 +232,7 @@ StagedKey staged_key(const Common& c, int32_t n_rects, const mdlstm_rect* rects)
     k.c_in = c.g.c_in;
     k.hidden = c.g.hidden;
     k.dtype = c.g.dtype;
+    k.memory = c.memory;
     k.canvas_h = c.g.canvas_h;
     k.canvas_w = c.g.canvas_w;
     k.n_rects = n_rects;
@@ -542,12 +551,21 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
     const int32_t* units = reinterpret_cast<const int32_t*>(c.ws + c.p.units);
     const int32_t* drects = reinterpret_cast<const int32_t*>(c.ws + c.p.rects);
     float* cs = reinterpret_cast<float*>(c.ws + c.p.c);
+    if (desc->memory_states && stepwise)
+        return fail(MDLSTM_ERR_UNSUPPORTED, "the per-diagonal schedule is not built with memory-state matrices");
     HIP_OR_FAIL(mark(0, s));
     HIP_OR_FAIL(mdl::launch_projection(c.g, d_x, d_wx, d_b, c.ws + c.p.z, s));
     HIP_OR_FAIL(mark(1, s));
-    if (stepwise || n_rects == 0) HIP_OR_FAIL(mdl::launch_zero_invalid(c.g, 4 * c.g.hidden, d_mask, rid, d_y, s));
+    if (stepwise || n_rects == 0 || desc->memory_states)
+        HIP_OR_FAIL(mdl::launch_zero_invalid(c.g, 4 * c.g.hidden, d_mask, rid, d_y, s));
     HIP_OR_FAIL(mark(2, s));
-    if (!stepwise) {
+    if (desc->memory_states) {
+        const int64_t nu = 4 * (int64_t)c.g.hidden * 5 * 2 * c.g.hidden;  // floats of U before V
+        mdl::MemArgs m{units, drects, d_mask, static_cast<const float*>(d_u), static_cast<const float*>(d_u) + nu,
+                       reinterpret_cast<float*>(c.ws + c.p.z), cs, static_cast<float*>(d_y), nullptr, canvas_w,
+                       nullptr};
+        HIP_OR_FAIL(mdl::launch_wavefront_mem(true, c.g, 4 * n_rects, m, s));
+    } else if (!stepwise) {
         // the persistent launch also zeroes the output rows of the invalid cells
         HIP_OR_FAIL(mdl::launch_wavefront_fwd(c.g, c.nt, 4 * n_rects, units, drects, d_mask, rid, d_u, c.ws + c.p.z,
                                               cs, d_y, reinterpret_cast<unsigned*>(c.ws + c.p.queue), s));
@@ -614,12 +632,26 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
     if (st != MDLSTM_OK) return st;
     const int32_t* rid = reinterpret_cast<const int32_t*>(c.ws + c.p.rid);
     HIP_OR_FAIL(mark(4, s));
-    if (c.g.n_cells > 0) {
+    if (c.g.n_cells > 0 && desc->memory_states) {
+        const int64_t nu = 4 * (int64_t)c.g.hidden * 5 * 2 * c.g.hidden;  // floats of U (and dU) before V (dV)
+        const int32_t* units = reinterpret_cast<const int32_t*>(c.ws + c.p.units);
+        float* part = reinterpret_cast<float*>(c.ws + c.p.dvpart);
+        mdl::MemArgs m{units, reinterpret_cast<const int32_t*>(c.ws + c.p.rects), d_mask,
+                       static_cast<const float*>(d_u), static_cast<const float*>(d_u) + nu,
+                       reinterpret_cast<float*>(c.ws + c.p.z), reinterpret_cast<float*>(c.ws + c.p.c), nullptr,
+                       static_cast<const float*>(d_dy), canvas_w, part};
+        HIP_OR_FAIL(mdl::launch_wavefront_mem(false, c.g, 4 * n_rects, m, s));
+        if (n_rects > 0) HIP_OR_FAIL(mdl::launch_dv_reduce(c.g, 4 * n_rects, units, part, d_du + nu, s));
+        else HIP_OR_FAIL(mdl::launch_zero_f32(d_du + nu, 4 * (int64_t)c.g.hidden * 3 * 2 * c.g.hidden, s));
+    } else if (c.g.n_cells > 0) {
         HIP_OR_FAIL(mdl::launch_wavefront_bwd(c.g, c.nt, 4 * n_rects,
                                               reinterpret_cast<const int32_t*>(c.ws + c.p.units),
                                               reinterpret_cast<const int32_t*>(c.ws + c.p.rects), d_mask, d_u, d_dy,
                                               c.ws + c.p.z, reinterpret_cast<const float*>(c.ws + c.p.c),
                                               reinterpret_cast<unsigned*>(c.ws + c.p.queue), s));
+    } else if (desc->memory_states) {
+        const int64_t nu = 4 * (int64_t)c.g.hidden * 5 * 2 * c.g.hidden;
+        HIP_OR_FAIL(mdl::launch_zero_f32(d_du + nu, 4 * (int64_t)c.g.hidden * 3 * 2 * c.g.hidden, s));
     }
     HIP_OR_FAIL(mark(5, s));
     if (c.g.n_cells > 0 && mdl::strip_supported(c.g)) {

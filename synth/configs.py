@@ -104,6 +104,12 @@ class Workload:
         return (_store(np.stack(wx), self.dtype), _store(np.stack(u), self.dtype),
                 _store(np.stack(b), self.dtype))
 
+    def memory_params(self) -> np.ndarray:
+        """Memory-state matrices V [4][3H][2H] (rows i, f_L, f_T; columns c_L,
+        c_T), U(-0.1, 0.1), in the storage dtype."""
+        rng = _rng(self.cid, TAG_PARAMS, 2)
+        return _store(rng.uniform(-0.1, 0.1, (4, 3 * self.hidden, 2 * self.hidden)), self.dtype)
+
     def label(self, k: int, classes: int = HEAD_CLASSES) -> np.ndarray:
         """Target sequence of example k for the CTC loss: length U{1..max(1, w // 4)}
         (short enough for every frame path to exist, repeats included), classes

@@ -29,14 +29,16 @@ def layout(heights, widths, canvas_w, kind="packed"):
 
 def run_layer(xs, params, dys, heights, widths, canvas_w, dtype="f32", kind="packed", backward=True, keep=None):
     """xs/dys: per-example numpy arrays. Returns dict with per-example Y (and dX) and summed dW.
+    params: (wx, u, b) or (wx, u, b, v) with memory-state matrices.
 
     keep: indices of the examples whose Y and dX are copied back (all by
     default); the others' entries are None. The whole batch always runs."""
     units, place, ch, cw, mask = layout(heights, widths, canvas_w, kind)
-    wx, u, b = (to_dev(p, dtype) for p in params)
+    wx, u, b = (to_dev(p, dtype) for p in params[:3])
+    v = to_dev(params[3], dtype) if len(params) > 3 else None
     ex = [to_dev(x, dtype) for x in xs]
     canvas = api.pack_data(ex, place, ch, cw)
-    layer = api.MDLSTMLayer(wx, u, b, ch, cw, units, mask)
+    layer = api.MDLSTMLayer(wx, u, b, ch, cw, units, mask, v=v)
     y = layer.forward(canvas)
     out = {"rects": place, "canvas_h": ch, "canvas_w": cw, "mask": mask, "layer": layer,
            "y_canvas": y.clone()}
@@ -44,7 +46,10 @@ def run_layer(xs, params, dys, heights, widths, canvas_w, dtype="f32", kind="pac
     out["Y"] = [to_np(t) if k in ks else None for k, t in enumerate(api.unpack_data(y, place))]
     if backward:
         dyc = api.pack_data([to_dev(g, dtype) for g in dys], place, ch, cw)
-        dx, dwx, du, db = layer.backward(dyc)
+        grads = layer.backward(dyc)
+        dx, dwx, du, db = grads[:4]
+        if v is not None:
+            out["dV"] = to_np(grads[4])
         torch.cuda.synchronize()
         out["dX"] = [to_np(t) if k in ks else None for k, t in enumerate(api.unpack_data(dx, place))]
         out["dx_canvas"] = dx.clone()

@@ -12,10 +12,11 @@ from oracle import mdlstm
 
 def _one(args):
     x, p64, dy, backward = args
-    Y, cache = mdlstm.layer_forward(x, *p64)
+    v = p64[3] if len(p64) > 3 else None
+    Y, cache = mdlstm.layer_forward(x, *p64[:3], v=v)
     if not backward:
         return Y, None
-    return Y, mdlstm.layer_backward(cache, dy, *p64)
+    return Y, mdlstm.layer_backward(cache, dy, *p64[:3], v=v)
 
 
 def default_workers() -> int:
@@ -59,7 +60,9 @@ def _pool_map(fn, jobs, workers, progress):
 
 
 def run_layer(xs, params, dys, backward=True, workers=1, progress=None):
-    """Per example, each computed alone: Y (and dX), plus weight gradients summed over examples."""
+    """Per example, each computed alone: Y (and dX), plus weight gradients summed
+    over examples. params: (wx, u, b), or (wx, u, b, v) with memory-state
+    matrices (then dV is summed too)."""
     p64 = [np.asarray(t, np.float64) for t in params]
     jobs = [(x, p64, (dys[k] if backward else None), backward) for k, x in enumerate(xs)]
     results = _pool_map(_one, jobs, workers, progress)
@@ -68,11 +71,14 @@ def run_layer(xs, params, dys, backward=True, workers=1, progress=None):
         H = params[1].shape[2] // 2
         C = params[0].shape[2]
         acc = [np.zeros((4, 5 * H, C)), np.zeros((4, 5 * H, 2 * H)), np.zeros((4, 5 * H))]
+        if len(params) > 3:
+            acc.append(np.zeros((4, 3 * H, 2 * H)))
         for _, g in results:
-            dX, dWx, dU, db = g
-            out["dX"].append(dX)
-            acc = [a + b for a, b in zip(acc, (dWx, dU, db))]
-        out["dWx"], out["dU"], out["db"] = acc
+            out["dX"].append(g[0])
+            acc = [a + b for a, b in zip(acc, g[1:])]
+        out["dWx"], out["dU"], out["db"] = acc[:3]
+        if len(params) > 3:
+            out["dV"] = acc[3]
     return out
 
 
