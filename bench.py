@@ -515,6 +515,69 @@ def measure_gpu(cid: int, steps: int, warmup: int, padded: bool, stepwise: bool)
     return res
 
 
+def measure_head(steps: int, warmup: int):
+    """The shared output layer, row collapse and CTC loss on the word batch's
+    packed canvas (80 classes, synthetic labels): head forward, CTC loss and
+    gradient, head backward, each timed with events on the stream."""
+    import torch
+
+    from paper_1902_11208_amd import api
+    from synth import configs
+
+    wl = configs.workload(2)
+    rects, ch, _ = api.pack_layout(wl.heights, wl.widths, wl.canvas_w)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2)
+    y = torch.randn((ch, wl.canvas_w, 4 * wl.hidden), device="cuda", generator=g) * 0.3
+    W, b = (torch.from_numpy(t).cuda() for t in wl.head_params())
+    labels = [wl.label(k) for k in range(wl.n)]
+    hd = api.Head(W, b, rects, (ch, wl.canvas_w), labels)
+    for _ in range(warmup):
+        hd.forward(y)
+        hd.ctc()
+        hd.backward()
+    evs = [_events(torch, 4) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e in evs:
+        e[0].record()
+        hd.forward(y)
+        e[1].record()
+        hd.ctc()
+        e[2].record()
+        hd.backward()
+        e[3].record()
+    torch.cuda.synchronize()
+    ms = {n: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
+          for i, n in enumerate(("head_forward", "ctc", "head_backward"))}
+    H, K = wl.hidden, W.shape[0]
+    U, F = wl.useful_cells, int(np.sum(wl.widths))
+    S = sum(2 * len(l) + 1 for l in labels)
+    TS = int(sum(int(w) * (2 * len(l) + 1) for w, l in zip(wl.widths, labels)))
+    # cost model: the forward reads the examples' cells once and writes the
+    # logits; CTC reads the logits and writes their gradient (its forward and
+    # backward variables, T x S doubles each way, stay in the caches when they
+    # can); the backward writes the layer's upstream gradient over the examples
+    alg = {"head_forward": (U * 4 * H * 4 + F * K * 4, U * 4 * H + 2.0 * F * K * H),
+           "ctc": (2 * F * K * 4 + 2 * TS * 8, 30.0 * TS + 10.0 * F * K),
+           "head_backward": (U * 4 * H * 4 + F * K * 4 + F * (H + 4) * 4, 2.0 * F * K * H + 2.0 * F * K * (H + 1))}
+    dom = max(ms, key=lambda k: ms[k])
+    by, fl = alg[dom]
+    gbs = by / (ms[dom] * 1e-3) / 1e9
+    out = {"workload": "word batch (256 x h16, H 16) output layer shared by the directions, row collapse, CTC loss "
+                       f"with {K} classes and synthetic labels",
+           "frames": F, "label_states": S, "ms_per_step": round(sum(ms.values()), 4),
+           "phases": phase_rates(ms, alg, "f32", "head"),
+           "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None, "kernel": dom,
+                        "ms": round(ms[dom], 4), "bytes_per_launch": int(by), "flops_per_launch": int(fl),
+                        "note": "the CTC recursion walks the frames in order; its floor is the longest "
+                                "example's frames times a step's latency, not bandwidth"
+                        if dom == "ctc" else None}}
+    print(f"[bench] output layer + CTC on the word batch: {out['ms_per_step']:.3f} ms "
+          f"({', '.join(f'{k} {v:.3f}' for k, v in ms.items())})", file=sys.stderr, flush=True)
+    return out
+
+
 def measured_traffic(kernel: str, cid: int):
     """HBM bytes per launch of `kernel` on workload `cid` from the committed
     hardware-counter summary, or None when there is none or the kernel source
@@ -702,6 +765,8 @@ def main():
         if k in h:
             out[k] = h[k]
     out["configs"] = {str(cid): res[cid] for cid in cids[1:]}
+    if not args.no_nested:
+        out["head_ctc"] = measure_head(min(args.steps, 10), args.warmup)
     out["paper_context"] = PAPER_CONTEXT
     out["host"] = host
     if args.copy_calibration:
