@@ -454,8 +454,13 @@ def measure_gpu(cid: int, steps: int, warmup: int, padded: bool, stepwise: bool)
         name, dtype = wl.name, ("bf16" if wl.dtype == "bf16" else "f32")
         RunCls = Run
     print(f"[bench] workload {cid}: {name}, {wl.n} examples", file=sys.stderr, flush=True)
+    import torch
+
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats()
     run = RunCls(wl, "packed")
     ms, wall_ms, phase, per_step, dom = run.time(steps, warmup)
+    peak_mb = torch.cuda.max_memory_allocated() / 2**20
     if cid == 4:
         useful = 4 * run.unit_cells
         alg = stack_algorithmic(wl, run)
@@ -490,6 +495,9 @@ def measure_gpu(cid: int, steps: int, warmup: int, padded: bool, stepwise: bool)
         "roofline": roof, "projection": proj, "phases": phases_out,
         "layout_ms": round(run.layout_ms, 3), "scatter_ms": round(run.scatter_ms, 3),
         "value_with_layout": useful / ((ms + run.layout_ms + run.scatter_ms) * 1e-3),
+        # device memory held at most by the packed run (inputs, weights, outputs,
+        # gradients, workspace), the quantity the paper's Table IV reports per GPU
+        "peak_memory_MB": round(peak_mb, 1),
     }
     res.update(extra)
     if stepwise and cid != 4:
@@ -499,18 +507,20 @@ def measure_gpu(cid: int, steps: int, warmup: int, padded: bool, stepwise: bool)
               flush=True)
     del run
     if padded:
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
         pr = RunCls(wl, "padded")
         pms, _, pphase, pper, _ = pr.time(max(3, steps // 2), warmup)
+        ppeak = torch.cuda.max_memory_allocated() / 2**20
         res["padded"] = {"ms_per_step": round(pms, 4), "median_ms": round(float(np.median(pper)), 4),
                          "value": useful / (pms * 1e-3), "canvas_cells": pr.n_cells, "unit_cells": pr.unit_cells,
                          "speedup_packed_vs_padded": round(pms / ms, 3),
                          "padded_over_useful_cells": round(pr.unit_cells * 4 / useful, 3),
                          "layout_ms": round(pr.layout_ms + pr.scatter_ms, 3),
+                         "peak_memory_MB": round(ppeak, 1),
                          "phases_ms": {k: round(v, 4) for k, v in pphase.items()}}
         print(f"[bench] workload {cid} padded: {pms:.3f} ms/step", file=sys.stderr, flush=True)
         del pr
-    import torch
-
     torch.cuda.empty_cache()
     return res
 
@@ -761,7 +771,7 @@ def main():
     }
     for k in ("padded", "projection", "phases", "design_bytes", "layers", "wavefront_fwd_stepwise_graph_ms",
               "critical_path_diagonals", "median_ms", "min_ms", "layout_ms", "scatter_ms", "value_with_layout",
-              "wall_ms_per_step"):
+              "wall_ms_per_step", "peak_memory_MB"):
         if k in h:
             out[k] = h[k]
     out["configs"] = {str(cid): res[cid] for cid in cids[1:]}
