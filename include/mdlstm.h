@@ -53,7 +53,9 @@ typedef enum {
     MDLSTM_ERR_BAD_LAYOUT = 3,  /* rectangles overlap or leave the canvas       */
     MDLSTM_ERR_WORKSPACE = 4,   /* workspace or output buffer too small         */
     MDLSTM_ERR_UNSUPPORTED = 5, /* hidden size / dtype / rectangle height not built */
-    MDLSTM_ERR_DEVICE = 6       /* a HIP call failed; message has the HIP string */
+    MDLSTM_ERR_DEVICE = 6,      /* a HIP call failed; message has the HIP string */
+    MDLSTM_ERR_NUMERIC = 7      /* non-finite outputs, reported only when the
+                                   environment sets MDLSTM_CHECK_FINITE=1 (see mdlstm_forward) */
 } mdlstm_status;
 
 /* Storage type of x, y, weights, dx and the saved gates. Accumulation and the
@@ -195,7 +197,10 @@ size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, i
  * d_y (out): [canvas_h][canvas_w][4H], channel d*H + j; 0 at invalid cells.
  * d_workspace: mdlstm_workspace_bytes(...) bytes; keeps the gates and the cell
  *   state for mdlstm_backward, so it must not be modified in between.
- * Asynchronous on `stream`.
+ * Asynchronous on `stream`. Debug mode: with MDLSTM_CHECK_FINITE=1 in the
+ * environment the call also counts the non-finite values of y and of the
+ * cell state (the plain cell's state can grow without bound, Section III),
+ * waits for the count, and returns MDLSTM_ERR_NUMERIC when it is not zero.
  */
 mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
                              const void* d_x, const uint8_t* d_mask,

@@ -68,7 +68,8 @@ SIGNATURES = {
                                            c_void]),
 }
 
-STATUS = {0: "OK", 1: "INVALID_ARG", 2: "TOO_WIDE", 3: "BAD_LAYOUT", 4: "WORKSPACE", 5: "UNSUPPORTED", 6: "DEVICE"}
+STATUS = {0: "OK", 1: "INVALID_ARG", 2: "TOO_WIDE", 3: "BAD_LAYOUT", 4: "WORKSPACE", 5: "UNSUPPORTED", 6: "DEVICE",
+          7: "NUMERIC"}
 
 
 class MdlstmError(RuntimeError):

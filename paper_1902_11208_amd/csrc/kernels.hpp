@@ -36,6 +36,9 @@ hipError_t launch_gather(int n, void* const* d_ptrs, const int32_t* d_rects, int
 // Z[p][20H] = Wx_all[20H][C] x[p] + b_all.
 hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_wx, const void* d_b,
                              void* d_z, hipStream_t s);
+// Count the non-finite values of n elements (dtype 0 fp32, 1 bf16) into
+// *d_count (added to; the caller zeroes it).
+hipError_t launch_count_nonfinite(const void* d, int64_t n, int dtype, unsigned long long* d_count, hipStream_t s);
 // Zero the rows of a [n_cells][width] tensor (storage dtype) whose cell is invalid.
 hipError_t launch_zero_invalid(const LayerGeom& g, int width, const uint8_t* d_mask,
                                const int32_t* d_rid, void* d_t, hipStream_t s);

@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -56,6 +57,13 @@ bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) !=
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Debug mode of the forward pass: MDLSTM_CHECK_FINITE=1 in the environment
+// (read at every call, so a process can switch it on and off).
+bool check_finite_requested() {
+    const char* v = std::getenv("MDLSTM_CHECK_FINITE");
+    return v && v[0] == '1' && v[1] == 0;
+}
+
 // ---------------------------------------------------------------------------
 // Layer descriptor and workspace plan.
 // ---------------------------------------------------------------------------
@@ -85,7 +93,7 @@ mdlstm_status check_desc(const mdlstm_layer_desc* d) {
 }
 
 struct Plan {
-    size_t z, c, rid, rects, units, part, flags, wxt, dvpart, queue, total;
+    size_t z, c, rid, rects, units, part, flags, wxt, dvpart, queue, check, total;
 };
 
 mdl::LayerGeom geom(const mdlstm_layer_desc* d, int32_t ch, int32_t cw) {
@@ -125,6 +133,8 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
     p.dvpart = off;  // memory-state matrices: a dV partial per unit
     off += d->memory_states ? align_up(mdl::mem_partial_bytes(g, 4 * (nr > 0 ? nr : 1))) : 0;
     p.queue = off;  // unit queue: next unit, workgroups done
+    off += align_up(8);
+    p.check = off;  // non-finite count of the debug mode
     off += align_up(8);
     p.total = off;
     return p;
@@ -592,6 +602,16 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
         HIP_OR_FAIL(hipGraphLaunch(cache->exec, s));
     }
     HIP_OR_FAIL(mark(3, s));
+    if (check_finite_requested()) {
+        unsigned long long* cnt = reinterpret_cast<unsigned long long*>(c.ws + c.p.check);
+        HIP_OR_FAIL(mdl::launch_zero_f32(reinterpret_cast<float*>(cnt), 2, s));
+        HIP_OR_FAIL(mdl::launch_count_nonfinite(d_y, c.g.n_cells * 4 * c.g.hidden, c.g.dtype, cnt, s));
+        HIP_OR_FAIL(mdl::launch_count_nonfinite(cs, c.g.n_cells * 4 * c.g.hidden, 0, cnt, s));
+        unsigned long long h = 0;
+        HIP_OR_FAIL(hipMemcpyAsync(&h, cnt, sizeof(h), hipMemcpyDeviceToHost, s));
+        HIP_OR_FAIL(hipStreamSynchronize(s));
+        if (h) return fail(MDLSTM_ERR_NUMERIC, "%llu non-finite values in the output and cell state", h);
+    }
     return MDLSTM_OK;
 }
 

@@ -413,3 +413,37 @@ def test_stepwise_forward_matches_persistent(case):
     # the saved gates and cell states are the same too: identical gradients
     for g, r in zip(b.backward(dy), ref_grads):
         assert torch.equal(g, r)
+
+
+def test_check_finite_debug_mode():
+    """MDLSTM_CHECK_FINITE=1 makes the forward pass count non-finite outputs
+    and cell states and report them (MDLSTM_ERR_NUMERIC). Forget gates
+    saturated at exactly 1 (bias 40) make the plain cell's state the binomial
+    path count of Section III's instability, past the fp32 range on a
+    64 x 250 example; bounded parameters pass."""
+    import os
+
+    import gpu_run
+    from paper_1902_11208_amd import MdlstmError, api
+    from synth.configs import custom_workload
+
+    def forward(wl):
+        units, place, ch, cw, mask = gpu_run.layout(wl.heights, wl.widths, wl.canvas_w, "packed")
+        x = api.pack_data([gpu_run.to_dev(e, "f32") for e in wl.examples()], place, ch, cw)
+        layer = api.MDLSTMLayer(*[gpu_run.to_dev(p, "f32") for p in wl.params()], ch, cw, units, mask)
+        y = layer.forward(x)
+        torch.cuda.synchronize()
+        return y
+
+    bad = custom_workload(71, [64, 5], [250, 30], 256, 8, 16, forget_bias=40.0)
+    good = custom_workload(72, [64, 5], [250, 30], 256, 8, 16)
+    _say("case: non-finite check, forget gates at 1 on a 64 x 250 example")
+    forward(bad)  # not checked: completes
+    os.environ["MDLSTM_CHECK_FINITE"] = "1"
+    try:
+        with pytest.raises(MdlstmError) as err:
+            forward(bad)
+        assert err.value.code == "NUMERIC" and "non-finite" in str(err.value)
+        forward(good)
+    finally:
+        del os.environ["MDLSTM_CHECK_FINITE"]
