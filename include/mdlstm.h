@@ -92,6 +92,9 @@ typedef struct {
 /* Largest rectangle height the wavefront kernels accept. */
 #define MDLSTM_MAX_RECT_H 64
 
+/* Most rectangles (examples) one call takes (UNSUPPORTED beyond). */
+#define MDLSTM_MAX_RECTS (1 << 24)
+
 /* Device workspace needed by mdlstm_pack_layout / mdlstm_pack_data /
  * mdlstm_unpack_data for n examples. */
 size_t mdlstm_pack_workspace_bytes(int32_t n);
@@ -174,7 +177,9 @@ mdlstm_status mdlstm_unpack_data(int32_t n, void* const* d_examples, const mdlst
                                  const void* d_canvas, void* d_workspace, size_t workspace_bytes,
                                  void* stream);
 
-/* Device workspace needed by mdlstm_forward followed by mdlstm_backward. */
+/* Device workspace needed by mdlstm_forward followed by mdlstm_backward; 0
+ * when the descriptor is invalid or not built, or the canvas or the number of
+ * rectangles is out of range (mdlstm_last_error says which). */
 size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
                               int32_t n_rects);
 
@@ -199,7 +204,8 @@ size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, i
  *   state for mdlstm_backward, so it must not be modified in between.
  * Asynchronous on `stream`. Debug mode: with MDLSTM_CHECK_FINITE=1 in the
  * environment the call also counts the non-finite values of y and of the
- * cell state (the plain cell's state can grow without bound, Section III),
+ * cell state at the cells whose mask byte is set (the plain cell's state can
+ * grow without bound, Section III),
  * waits for the count, and returns MDLSTM_ERR_NUMERIC when it is not zero.
  */
 mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
@@ -340,7 +346,9 @@ typedef struct {
 
 /* Workspace of the head calls for these examples: with label_lens NULL, what
  * mdlstm_head_forward and mdlstm_head_backward need; with the label lengths,
- * what mdlstm_ctc_loss needs as well (one workspace serves all three). */
+ * what mdlstm_ctc_loss needs as well (one workspace serves all three). 0 when
+ * the descriptor, a rectangle or a label length (0 to min(960, the example's
+ * width)) is invalid. */
 size_t mdlstm_head_workspace_bytes(const mdlstm_head_desc* desc, int32_t n, const mdlstm_rect* rects,
                                    const int32_t* label_lens);
 

@@ -180,7 +180,7 @@ static BigDw big_dw(const LayerGeom& g) {
     const int64_t by_size = std::max<int64_t>(1, g.n_cells / (16 * BW_KC));  // at least 16 steps per chunk
     ch = std::max<int64_t>(1, std::min(ch, by_size));
     q.chunk_cells = (g.n_cells + ch - 1) / ch;
-    q.chunk_cells = (q.chunk_cells + BW_KC - 1) / BW_KC * BW_KC;
+    q.chunk_cells = std::max<int64_t>(BW_KC, (q.chunk_cells + BW_KC - 1) / BW_KC * BW_KC);  // an empty canvas: one chunk
     q.chunks = (int)((g.n_cells + q.chunk_cells - 1) / q.chunk_cells);
     if (q.chunks < 1) q.chunks = 1;
     return q;

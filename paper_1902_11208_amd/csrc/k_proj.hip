@@ -200,12 +200,16 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
     return hipErrorInvalidValue;
 }
 
-// Non-finite count (debug mode of the forward pass): a wave adds its lanes'
-// count with one atomic.
+// Number of NaN and infinite values among the rows of the cells whose mask
+// byte is set (row values per cell each), added to *count: a wave reduction
+// and one atomic per wave.
 template <typename T>
-__global__ void k_count_nonfinite(const T* __restrict__ p, int64_t n, unsigned long long* __restrict__ count) {
+__global__ void k_count_nonfinite(const T* __restrict__ p, int64_t n_cells, int row, const uint8_t* __restrict__ mask,
+                                  unsigned long long* __restrict__ count) {
     unsigned local = 0;
+    const int64_t n = n_cells * row;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        if (!mask[i / row]) continue;
         const float v = St<T>::ld1(p + i);
         local += (v - v) != 0.0f ? 1u : 0u;  // NaN or +-inf
     }
@@ -213,15 +217,16 @@ __global__ void k_count_nonfinite(const T* __restrict__ p, int64_t n, unsigned l
     if ((threadIdx.x & 63) == 0 && local) atomicAdd(count, (unsigned long long)local);
 }
 
-hipError_t launch_count_nonfinite(const void* d, int64_t n, int dtype, unsigned long long* d_count, hipStream_t s) {
-    if (n <= 0) return hipSuccess;
-    const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
+hipError_t launch_count_nonfinite(const void* d, int64_t n_cells, int row, const uint8_t* d_mask, int dtype,
+                                  unsigned long long* d_count, hipStream_t s) {
+    if (n_cells <= 0 || row <= 0) return hipSuccess;
+    const int blocks = (int)std::min<int64_t>((n_cells * row + 255) / 256, 4096);
     if (dtype == 0)
-        hipLaunchKernelGGL(k_count_nonfinite<float>, dim3(blocks), dim3(256), 0, s, static_cast<const float*>(d), n,
-                           d_count);
+        hipLaunchKernelGGL(k_count_nonfinite<float>, dim3(blocks), dim3(256), 0, s, static_cast<const float*>(d),
+                           n_cells, row, d_mask, d_count);
     else
-        hipLaunchKernelGGL(k_count_nonfinite<bf16_t>, dim3(blocks), dim3(256), 0, s, static_cast<const bf16_t*>(d), n,
-                           d_count);
+        hipLaunchKernelGGL(k_count_nonfinite<bf16_t>, dim3(blocks), dim3(256), 0, s, static_cast<const bf16_t*>(d),
+                           n_cells, row, d_mask, d_count);
     return hipGetLastError();
 }
 

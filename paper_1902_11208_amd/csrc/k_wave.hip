@@ -52,6 +52,34 @@ struct Ops<bf16_t> {  // 16x16x32 bf16 MFMA: eight consecutive values per slot a
 template <typename T>
 __device__ __forceinline__ float ld1f(const T* p) { return St<T>::ld1(p); }
 
+// N consecutive operands from LDS; fp32 runs of a multiple of four (two)
+// values as 16-byte (8-byte) reads, which the row pitches and run offsets of
+// the callers keep aligned. With row pitches of 4 mod 32 banks, the lanes of
+// a 16-byte read that the LDS serves together fall on distinct bank quads.
+template <typename T, int N>
+__device__ __forceinline__ void lds_run(const T* p, typename Ops<T>::Op (&v)[N]) {
+    if constexpr (std::is_same<T, float>::value && N % 4 == 0) {
+#pragma unroll
+        for (int k = 0; k < N / 4; ++k) {
+            const float4 f = *reinterpret_cast<const float4*>(p + 4 * k);
+            v[4 * k] = f.x;
+            v[4 * k + 1] = f.y;
+            v[4 * k + 2] = f.z;
+            v[4 * k + 3] = f.w;
+        }
+    } else if constexpr (std::is_same<T, float>::value && N % 2 == 0) {
+#pragma unroll
+        for (int k = 0; k < N / 2; ++k) {
+            const float2 f = *reinterpret_cast<const float2*>(p + 2 * k);
+            v[2 * k] = f.x;
+            v[2 * k + 1] = f.y;
+        }
+    } else {
+#pragma unroll
+        for (int ks = 0; ks < N; ++ks) v[ks] = Ops<T>::lds(p + ks * Ops<T>::PER);
+    }
+}
+
 template <typename T>
 __device__ __forceinline__ T from_f(float v);
 template <>
@@ -455,10 +483,8 @@ __device__ __forceinline__ void wave_fwd_unit(const WaveArgs& a, const int unit)
             const int yy = 16 * nt + n16;
             const T* brow = (q < 2) ? &hbuf[prv][yy + 1][q * KRUN] : &hbuf[prv][yy][(q - 2) * KRUN];
             Op bop[NSTEP], bg[GSTEP];
-#pragma unroll
-            for (int ks = 0; ks < NSTEP; ++ks) bop[ks] = O::lds(brow + ks * O::PER);
-#pragma unroll
-            for (int ks = 0; ks < GSTEP; ++ks) bg[ks] = O::lds(brow + (sp * GSTEP + ks) * O::PER);
+            lds_run<T, NSTEP>(brow, bop);
+            lds_run<T, GSTEP>(brow + sp * GSTEP * O::PER, bg);
             ag[lt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < GSTEP; ++ks) ag[lt] = O::mma(Ag[ks], bg[ks], ag[lt]);
@@ -1104,8 +1130,7 @@ __device__ __forceinline__ void wave_bwd_unit(const WaveArgs& a, const int unit)
             const int yy = 16 * nt + n16;
             const T* brow = &dabuf[yy][q * KRUNB + sb * BSTEP * O::PER];
             Op bop[BSTEP];
-#pragma unroll
-            for (int ks = 0; ks < BSTEP; ++ks) bop[ks] = O::lds(brow + ks * O::PER);
+            lds_run<T, BSTEP>(brow, bop);
 #pragma unroll
             for (int tt = 0; tt < TPW; ++tt) {
                 acc[lt][tt] = floatx4{0.f, 0.f, 0.f, 0.f};

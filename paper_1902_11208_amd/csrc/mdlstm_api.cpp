@@ -49,6 +49,7 @@ mdlstm_status device_fail(hipError_t e, const char* where) {
 
 constexpr int32_t kMaxDim = (1 << 21) - 1;  // largest canvas side / example side
 constexpr int32_t kMaxPackN = 4096;         // placement keys in LDS; a placed bit per key, 64 per lane
+constexpr int32_t kMaxRects = MDLSTM_MAX_RECTS;  // rectangles per call (unit ids 4k + d stay within int32)
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -148,6 +149,7 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
 mdlstm_status check_rects(int32_t n, const mdlstm_rect* r, int32_t ch, int32_t cw, int32_t* max_h,
                           int32_t limit_h = MDLSTM_MAX_RECT_H) {
     if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n_rects is negative");
+    if (n > kMaxRects) return fail(MDLSTM_ERR_UNSUPPORTED, "%d rectangles; at most %d per call", n, kMaxRects);
     if (n > 0 && !r) return fail(MDLSTM_ERR_INVALID_ARG, "rects is NULL");
     int32_t mh = 0;
     for (int32_t k = 0; k < n; ++k) {
@@ -523,8 +525,12 @@ mdlstm_status mdlstm_unpack_data(int32_t n, void* const* d_examples, const mdlst
 }
 
 size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, int32_t n_rects) {
-    if (!desc || canvas_h < 0 || canvas_w < 0 || n_rects < 0) return 0;
-    if (desc->hidden < 1 || desc->c_in < 1) return 0;
+    if (check_desc(desc) != MDLSTM_OK) return 0;
+    if (canvas_h < 0 || canvas_w < 0 || canvas_h > kMaxDim || canvas_w > kMaxDim || n_rects < 0 ||
+        n_rects > kMaxRects) {
+        fail(MDLSTM_ERR_INVALID_ARG, "canvas %dx%d or %d rectangles out of range", canvas_h, canvas_w, n_rects);
+        return 0;
+    }
     return plan(desc, canvas_h, canvas_w, n_rects).total;
 }
 
@@ -605,8 +611,10 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
     if (check_finite_requested()) {
         unsigned long long* cnt = reinterpret_cast<unsigned long long*>(c.ws + c.p.check);
         HIP_OR_FAIL(mdl::launch_zero_f32(reinterpret_cast<float*>(cnt), 2, s));
-        HIP_OR_FAIL(mdl::launch_count_nonfinite(d_y, c.g.n_cells * 4 * c.g.hidden, c.g.dtype, cnt, s));
-        HIP_OR_FAIL(mdl::launch_count_nonfinite(cs, c.g.n_cells * 4 * c.g.hidden, 0, cnt, s));
+        // the cell state outside the examples' cells is not defined: count
+        // over the cells whose mask byte is set
+        HIP_OR_FAIL(mdl::launch_count_nonfinite(d_y, c.g.n_cells, 4 * c.g.hidden, d_mask, c.g.dtype, cnt, s));
+        HIP_OR_FAIL(mdl::launch_count_nonfinite(cs, c.g.n_cells, 4 * c.g.hidden, d_mask, 0, cnt, s));
         unsigned long long h = 0;
         HIP_OR_FAIL(hipMemcpyAsync(&h, cnt, sizeof(h), hipMemcpyDeviceToHost, s));
         HIP_OR_FAIL(hipStreamSynchronize(s));
@@ -770,6 +778,7 @@ HeadPlan head_plan(const mdlstm_head_desc* d, int32_t n, const mdlstm_rect* rect
 // disjoint when a canvas is given; the frames of all examples addressable).
 mdlstm_status check_head_rects(int32_t n, const mdlstm_rect* rects, int32_t ch, int32_t cw) {
     if (n < 0) return fail(MDLSTM_ERR_INVALID_ARG, "n is negative");
+    if (n > kMaxRects) return fail(MDLSTM_ERR_UNSUPPORTED, "%d examples; at most %d per call", n, kMaxRects);
     if (n > 0 && !rects) return fail(MDLSTM_ERR_INVALID_ARG, "rects is NULL");
     int64_t frames = 0;
     for (int32_t i = 0; i < n; ++i) {
@@ -812,7 +821,12 @@ mdlstm_status stage_head_tables(const HeadPlan& p, int32_t n, const mdlstm_rect*
 
 size_t mdlstm_head_workspace_bytes(const mdlstm_head_desc* desc, int32_t n, const mdlstm_rect* rects,
                                    const int32_t* label_lens) {
-    if (!desc || desc->hidden < 1 || desc->classes < 1 || n < 0 || (n > 0 && !rects)) return 0;
+    if (check_head_desc(desc) != MDLSTM_OK || check_head_rects(n, rects, -1, -1) != MDLSTM_OK) return 0;
+    for (int32_t i = 0; label_lens && i < n; ++i)
+        if (label_lens[i] < 0 || label_lens[i] > kMaxLabel || label_lens[i] > rects[i].w) {
+            fail(MDLSTM_ERR_INVALID_ARG, "example %d: %d labels for %d frames", i, label_lens[i], rects[i].w);
+            return 0;
+        }
     const HeadPlan p = head_plan(desc, n, rects, label_lens);
     return label_lens ? p.total : p.part1_end;
 }
@@ -985,10 +999,13 @@ namespace {
 
 constexpr int kMaxConvChunks = 512;
 
+constexpr int32_t kMaxConvWidth = 1 << 12;  // hidden and og beyond any built shape
+
 size_t blocks_ws_bytes(int32_t n, int32_t hidden, int32_t og) {
     const size_t nn = n > 0 ? (size_t)n : 1;
     size_t b = align_up(nn * 8) + 2 * align_up(nn * 16) + align_up((nn + 1) * 4);
-    if (hidden > 0 && og > 0) b += align_up((size_t)kMaxConvChunks * (4 * og * 8 * hidden + 4 * og) * 4);
+    if (hidden > 0 && og > 0)
+        b += align_up((size_t)kMaxConvChunks * ((size_t)4 * og * 8 * hidden + (size_t)4 * og) * 4);
     return b;
 }
 
@@ -1091,7 +1108,7 @@ mdlstm_status conv_stage(int32_t n, const mdlstm_rect* in_rects, const mdlstm_re
 }  // namespace
 
 size_t mdlstm_blocks_workspace_bytes(int32_t n, int32_t hidden, int32_t og) {
-    if (n < 0 || hidden < 0 || og < 0) return 0;
+    if (n < 0 || hidden < 0 || og < 0 || n > kMaxRects || hidden > kMaxConvWidth || og > kMaxConvWidth) return 0;
     return blocks_ws_bytes(n, hidden, og);
 }
 

@@ -102,6 +102,13 @@ def test_workspace_bytes_scale():
     assert a > 100 * 100 * (20 * 16 + 4 * 16) * 4
     assert b > a
     assert L.lib().mdlstm_workspace_bytes(None, 1, 1, 1) == 0
+    # an empty canvas still has a (small) workspace; unsupported shapes and
+    # out-of-range canvases report 0 instead of a size
+    assert L.lib().mdlstm_workspace_bytes(ctypes.byref(L.LayerDesc(64, 128, 1)), 0, 0, 0) > 0
+    assert L.lib().mdlstm_workspace_bytes(ctypes.byref(L.LayerDesc(16, 12, 0)), 10, 10, 1) == 0
+    assert L.lib().mdlstm_workspace_bytes(ctypes.byref(L.LayerDesc(16, 1 << 20, 0)), 10, 10, 1) == 0
+    assert L.lib().mdlstm_workspace_bytes(ctypes.byref(d), 1 << 22, 10, 1) == 0
+    assert L.lib().mdlstm_workspace_bytes(ctypes.byref(d), 10, 10, (1 << 24) + 1) == 0
 
 
 @pytest.mark.parametrize("which", ["x", "wx", "workspace", "y"])
