@@ -207,6 +207,12 @@ size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, i
  * cell state at the cells whose mask byte is set (the plain cell's state can
  * grow without bound, Section III),
  * waits for the count, and returns MDLSTM_ERR_NUMERIC when it is not zero.
+ * Debug mode: with MDLSTM_POISON_WORKSPACE=1 in the environment,
+ * mdlstm_forward, mdlstm_backward and the head calls first fill the
+ * floating-point workspace sections they write before reading (gates, cell
+ * states, partial sums; all bits set, NaN in every storage type) so that a
+ * read of a value the call did not write shows as NaN in the results; index
+ * sections are not touched. Results are identical with and without it.
  */
 mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
                              const void* d_x, const uint8_t* d_mask,

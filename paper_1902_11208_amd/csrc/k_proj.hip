@@ -200,6 +200,19 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
     return hipErrorInvalidValue;
 }
 
+// Fill of n 32-bit words with one pattern (the poisoned-workspace debug mode).
+__global__ void k_fill_u32(uint32_t* __restrict__ d, int64_t n, uint32_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        d[i] = v;
+}
+
+hipError_t launch_fill_u32(void* d, int64_t n_words, uint32_t v, hipStream_t s) {
+    if (n_words <= 0) return hipSuccess;
+    const int blocks = (int)std::min<int64_t>((n_words + 255) / 256, 4096);
+    hipLaunchKernelGGL(k_fill_u32, dim3(blocks), dim3(256), 0, s, static_cast<uint32_t*>(d), n_words, v);
+    return hipGetLastError();
+}
+
 // Number of NaN and infinite values among the rows of the cells whose mask
 // byte is set (row values per cell each), added to *count: a wave reduction
 // and one atomic per wave.

@@ -38,6 +38,7 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
                              void* d_z, hipStream_t s);
 // Count the non-finite values of n elements (dtype 0 fp32, 1 bf16) into
 // *d_count (added to; the caller zeroes it).
+hipError_t launch_fill_u32(void* d, int64_t n_words, uint32_t v, hipStream_t s);
 hipError_t launch_count_nonfinite(const void* d, int64_t n_cells, int row, const uint8_t* d_mask, int dtype,
                                   unsigned long long* d_count, hipStream_t s);
 // Zero the rows of a [n_cells][width] tensor (storage dtype) whose cell is invalid.

@@ -65,6 +65,21 @@ bool check_finite_requested() {
     return v && v[0] == '1' && v[1] == 0;
 }
 
+// Debug mode: MDLSTM_POISON_WORKSPACE=1 fills the floating-point sections of
+// a workspace that a call writes before it reads them with NaN (all bits
+// set: NaN as fp32, bf16 and fp64) at the start of the call, so that a read
+// of anything the call has not written shows in its results. Index and
+// offset sections are left alone.
+bool poison_requested() {
+    const char* v = std::getenv("MDLSTM_POISON_WORKSPACE");
+    return v && v[0] == '1' && v[1] == 0;
+}
+
+mdlstm_status poison(char* ws, size_t from, size_t to, hipStream_t s) {
+    if (to > from) HIP_OR_FAIL(mdl::launch_fill_u32(ws + from, (int64_t)((to - from) / 4), 0xffffffffu, s));
+    return MDLSTM_OK;
+}
+
 // ---------------------------------------------------------------------------
 // Layer descriptor and workspace plan.
 // ---------------------------------------------------------------------------
@@ -561,6 +576,12 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
     if (misaligned(d_y)) return fail(MDLSTM_ERR_INVALID_ARG, "y must be 16-byte aligned");
     if (c.g.n_cells == 0) return MDLSTM_OK;
     hipStream_t s = as_stream(stream);
+    if (poison_requested()) {
+        // gates and cell states, and the gradient scratch the backward writes
+        if ((st = poison(c.ws, c.p.z, c.p.rid, s)) != MDLSTM_OK) return st;
+        if ((st = poison(c.ws, c.p.part, c.p.flags, s)) != MDLSTM_OK) return st;
+        if ((st = poison(c.ws, c.p.wxt, c.p.queue, s)) != MDLSTM_OK) return st;
+    }
     st = stage_layout(c, n_rects, rects, false, s);
     if (st != MDLSTM_OK) return st;
     const int32_t* rid = reinterpret_cast<const int32_t*>(c.ws + c.p.rid);
@@ -658,6 +679,12 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
     hipStream_t s = as_stream(stream);
     st = stage_layout(c, n_rects, rects, true, s);
     if (st != MDLSTM_OK) return st;
+    if (poison_requested() && c.g.n_cells > 0) {
+        // the gradient scratch (partials, transposed Wx, dV partials); the
+        // gates and cell states are the forward's
+        if ((st = poison(c.ws, c.p.part, c.p.flags, s)) != MDLSTM_OK) return st;
+        if ((st = poison(c.ws, c.p.wxt, c.p.queue, s)) != MDLSTM_OK) return st;
+    }
     const int32_t* rid = reinterpret_cast<const int32_t*>(c.ws + c.p.rid);
     HIP_OR_FAIL(mark(4, s));
     if (c.g.n_cells > 0 && desc->memory_states) {
@@ -848,6 +875,7 @@ mdlstm_status mdlstm_head_forward(const mdlstm_head_desc* desc, int32_t canvas_h
     if (n == 0) return MDLSTM_OK;
     hipStream_t s = as_stream(stream);
     char* ws = static_cast<char*>(d_workspace);
+    if (poison_requested() && (st = poison(ws, p.S, p.part1_end, s)) != MDLSTM_OK) return st;  // column sums, partials
     st = stage_head_tables(p, n, rects, ws, s);
     if (st != MDLSTM_OK) return st;
     mdl::HeadArgs a{};
@@ -908,6 +936,7 @@ mdlstm_status mdlstm_ctc_loss(const mdlstm_head_desc* desc, int32_t n, const mdl
     if (n == 0) return MDLSTM_OK;
     hipStream_t s = as_stream(stream);
     char* ws = static_cast<char*>(d_workspace);
+    if (poison_requested() && (st = poison(ws, p.lp, p.total, s)) != MDLSTM_OK) return st;  // log-probabilities, alpha
     // frame offsets (first part) and the label tables (second part)
     std::vector<int32_t> fo((size_t)n + 1);
     int32_t f = 0;
@@ -968,6 +997,8 @@ mdlstm_status mdlstm_head_backward(const mdlstm_head_desc* desc, int32_t canvas_
         return fail(MDLSTM_ERR_WORKSPACE, "head workspace of %zu bytes, %zu needed", workspace_bytes, p.part1_end);
     hipStream_t s = as_stream(stream);
     char* ws = static_cast<char*>(d_workspace);
+    // the weight-gradient partials (the column sums are the forward's)
+    if (poison_requested() && n > 0 && (st = poison(ws, p.part, p.part1_end, s)) != MDLSTM_OK) return st;
     if (n > 0) {
         st = stage_head_tables(p, n, rects, ws, s);
         if (st != MDLSTM_OK) return st;
