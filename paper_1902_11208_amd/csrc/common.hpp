@@ -14,14 +14,18 @@ typedef uint16_t bf16_t;  // bfloat16 storage (upper half of an fp32)
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf2f(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
 
-// Round to nearest, ties to even; a NaN stays a (quiet) NaN. Written as a
-// select, so that no conversion becomes a branch.
-__device__ __forceinline__ bf16_t f2bf(float f) {
-    const uint32_t u = __float_as_uint(f);
-    const uint32_t r = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-    const bool nan = (u & 0x7fffffffu) > 0x7f800000u;
-    return (bf16_t)(nan ? ((u >> 16) | 0x40u) : r);
+// Two fp32 values to packed bf16 (lo in the low half): round to nearest,
+// ties to even, a NaN stays a (quiet) NaN; one hardware conversion
+// (v_cvt_pk_bf16_f32) for the pair.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+    const bf16x2 b = __builtin_convertvector(floatx2{lo, hi}, bf16x2);
+    uint32_t r;
+    __builtin_memcpy(&r, &b, 4);
+    return r;
 }
+__device__ __forceinline__ bf16_t f2bf(float f) { return (bf16_t)(f2bf2(f, 0.0f) & 0xffffu); }
 
 // Storage traits: loads/stores of 4 consecutive elements as fp32.
 template <typename T>
@@ -49,8 +53,8 @@ struct St<bf16_t> {
     }
     static __device__ __forceinline__ void st4(bf16_t* p, floatx4 v) {
         uint2 o;
-        o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-        o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+        o.x = f2bf2(v[0], v[1]);
+        o.y = f2bf2(v[2], v[3]);
         *reinterpret_cast<uint2*>(p) = o;
     }
     static __device__ __forceinline__ float ld1(const bf16_t* p) { return bf2f(*p); }

@@ -53,8 +53,8 @@ struct PK<bf16_t> {  // 16x16x32 bf16: K step ks, slot g holds k = 32 ks + 8 g +
     static __device__ __forceinline__ floatx4 mma(Op a, Op b, floatx4 c) { return mfma_bf16(a, b, c); }
     // non-temporal, as for fp32: four bf16 values as one 8-byte store
     static __device__ __forceinline__ void st4(bf16_t* p, floatx4 v) {
-        const uint64_t lo = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-        const uint64_t hi = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+        const uint64_t lo = f2bf2(v[0], v[1]);
+        const uint64_t hi = f2bf2(v[2], v[3]);
         __builtin_nontemporal_store(lo | (hi << 32), reinterpret_cast<uint64_t*>(p));
     }
 };

@@ -868,8 +868,7 @@ __device__ __forceinline__ void wave_fwd_big(const WaveArgs& a, const int unit) 
             hv[k] = live ? hn : 0.0f;
         }
         auto pack = [](const float (&v)[4]) {
-            return make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
-                              (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+            return make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
         };
         *reinterpret_cast<uint2*>(&hbuf[cur][yy + 1][u0]) = pack(hv);
         *reinterpret_cast<float4*>(&cbuf[yy + 1][u0]) = make_float4(cv[0], cv[1], cv[2], cv[3]);
@@ -1315,8 +1314,7 @@ __device__ __forceinline__ void wave_bwd_big(const WaveArgs& a, const int unit) 
         return __uint_as_float((k & 1) ? (wd & 0xffff0000u) : (wd << 16));
     };
     auto pack = [](const float (&v)[4]) {
-        return make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
-                          (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+        return make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
     };
     // Phase A of tile nt: gate gradients of the lane's four units.
     auto phase_a = [&](int s, int nt, const In& in) {
