@@ -12,14 +12,26 @@
 // every direction, summed over the directions and the rows. Class 0 is the
 // CTC blank.
 //
-// CTC (Graves et al. 2006), one workgroup per example, in double precision:
-// log-softmax per frame; the forward variables alpha_t(s) over the extended
-// label l' (blanks around and between the labels, S = 2L + 1 states) frame by
-// frame; log p = logsumexp(alpha_{T-1}(S-1), alpha_{T-1}(S-2)); then the
-// backward variables beta_t(s) frame by frame from the last, and at each frame
-// the gradient of -ln p with respect to the scores,
-//   dlogits[t][k] = softmax_t(k) - sum_{s: l'_s = k} exp(alpha_t(s) + beta_t(s) - lp_t(k) - log p),
-// summed in ascending s (blanks by a fixed-order wave reduction).
+// CTC (Graves et al. 2006) in double precision, with the rescaled forward
+// and backward variables of that paper (each frame's variables divided by
+// their sum, the logarithms of the sums accumulated), over the extended label
+// l' (blanks around and between the labels, S = 2L + 1 states):
+//   1. softmax y_t of every frame (one wave per frame, all frames at once);
+//   2. per example, one wave runs the forward variables
+//        a_t(s) = (a_{t-1}(s) + a_{t-1}(s-1) [+ a_{t-1}(s-2)]) y_t(l'_s),
+//      the skip allowed where l'_s is a label different from l'_{s-2}, and
+//      -ln p = -(sum_t ln C_t + ln(a_{T-1}(S-1) + a_{T-1}(S-2))), C_t the
+//      sum of frame t's unscaled variables; a second wave runs the backward
+//      variables without the current frame's output,
+//        b_{t-1}(s) = b_t(s) y_t(l'_s) + b_t(s+1) y_t(l'_{s+1}) [+ b_t(s+2) y_t(l'_{s+2})];
+//      both store every frame's rescaled variables;
+//   3. per frame, the state posteriors g_t(s) = a_t(s) b_t(s) / sum_s a_t(s) b_t(s)
+//      give the gradient of -ln p with respect to the logits,
+//        dlogits[t][k] = y_t(k) - sum_{s: l'_s = k} g_t(s),
+//      summed in ascending s (the blank's states by a fixed-order wave
+//      reduction).
+// The rescaling keeps every variable in range without a logarithm or an
+// exponential on the sequential path.
 #include <math.h>
 
 #include <algorithm>
@@ -123,120 +135,269 @@ k_head_fwd(int H, int K, int canvas_w, const float* __restrict__ Y, const int32_
     }
 }
 
-// CTC loss and gradient of one example per workgroup (see the file comment).
-// lab_off[i] / frame_off[i]: first label / frame of example i; a_off[i]: first
-// double of its alpha table [T][S]; lp: log-softmax workspace [frames][K].
-__global__ void __launch_bounds__(HT)
-k_ctc(int K, const int32_t* __restrict__ frame_off, const int32_t* __restrict__ lab_off,
-      const int32_t* __restrict__ labels, const int64_t* __restrict__ a_off, const float* __restrict__ logits,
-      double* __restrict__ lp_ws, double* __restrict__ alpha_ws, float* __restrict__ losses,
-      float* __restrict__ dlogits) {
-    extern __shared__ __attribute__((aligned(16))) double csm[];
-    const int ex = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// CTC step 1: softmax of frame f (one wave per frame), y [frames][K].
+__global__ void __launch_bounds__(256)
+k_ctc_softmax(int64_t frames, int K, const float* __restrict__ logits, double* __restrict__ y) {
+    const int lane = threadIdx.x & 63;
+    const int64_t f = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (f >= frames) return;
+    const float* z = logits + f * K;
+    double m = -INFINITY;
+    for (int k = lane; k < K; k += 64) m = fmax(m, (double)z[k]);
+    m = wave_max(m);
+    double se = 0.0;
+    for (int k = lane; k < K; k += 64) se += exp((double)z[k] - m);
+    const double inv = 1.0 / wave_sum(se);
+    for (int k = lane; k < K; k += 64) y[f * K + k] = exp((double)z[k] - m) * inv;
+}
+
+// A nonnegative number as a double mantissa (0, or in [0.5, 1)) and an int
+// exponent: the CTC variables span far more than the double range (states
+// behind and ahead of the bulk of the probability), so each keeps its own
+// exponent and no frame needs rescaling.
+constexpr int XNEG = -(1 << 30);  // exponent of zero
+struct Xd {
+    double m;
+    int e;
+};
+__device__ __forceinline__ Xd xnorm(double v, int e) {
+    int d;
+    const double m = frexp(v, &d);
+    return m == 0.0 ? Xd{0.0, XNEG} : Xd{m, e + d};
+}
+// a + b + c (c only with `with_c`), aligned to the largest exponent
+__device__ __forceinline__ Xd xsum3(Xd a, Xd b, Xd c, bool with_c) {
+    int E = max(a.e, b.e);
+    if (with_c) E = max(E, c.e);
+    double v = ldexp(a.m, a.e - E) + ldexp(b.m, b.e - E);
+    if (with_c) v += ldexp(c.m, c.e - E);
+    return xnorm(v, E);
+}
+__device__ __forceinline__ Xd xshfl_up(Xd v, int d) { return Xd{__shfl_up(v.m, d), __shfl_up(v.e, d)}; }
+__device__ __forceinline__ Xd xshfl_down(Xd v, int d) { return Xd{__shfl_down(v.m, d), __shfl_down(v.e, d)}; }
+
+// CTC step 2: wave 0 the forward variables, wave 1 the backward ones, of
+// example blockIdx.x; lane l owns states l*NM .. l*NM + NM - 1 and stores
+// them for every frame into rows of 64 NM entries (mantissas am / bm
+// [frames][64 NM], exponents ae / be). Frame rows of y are loaded D frames
+// ahead; every frame issues the same loads and stores, so the waits are for
+// exactly those loads.
+template <int NM, int D>
+__global__ void __launch_bounds__(128)
+k_ctc_scan(int K, const int32_t* __restrict__ frame_off, const int32_t* __restrict__ lab_off,
+           const int32_t* __restrict__ labels, const double* __restrict__ y, double* __restrict__ am,
+           int32_t* __restrict__ ae, double* __restrict__ bm, int32_t* __restrict__ be, float* __restrict__ losses) {
+    constexpr int RS = 64 * NM;
+    __shared__ double ys[2][2][2 * 64];  // per wave: y rows by frame parity (K <= 128)
+    __shared__ double finm[RS];          // the forward variables of the last frame
+    __shared__ int fine[RS];
+    const int ex = blockIdx.x, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int f0 = frame_off[ex], T = frame_off[ex + 1] - f0;
-    const int L = lab_off[ex + 1] - lab_off[ex], S = 2 * L + 1;
-    double* A0 = csm;        // [S]
-    double* A1 = A0 + S;     // [S]
-    double* G = A1 + S;      // [S]
-    __shared__ double s_logp;
-    int32_t* lab = reinterpret_cast<int32_t*>(G + S);  // [S]
-    int32_t* nxt = lab + S;                              // [S]
-    int32_t* first = nxt + S;                            // [K]
-    const int32_t* lb = labels + lab_off[ex];
-    for (int s = tid; s < S; s += HT) lab[s] = (s & 1) ? lb[s >> 1] : 0;
-    for (int k = tid; k < K; k += HT) first[k] = -1;
-    __syncthreads();
-    if (tid == 0) {  // occurrence lists of the labels (the odd states), ascending s
-        for (int s = S - 2; s >= 1; s -= 2) {
-            nxt[s] = first[lab[s]];
-            first[lab[s]] = s;
-        }
+    const int lo = lab_off[ex], L = lab_off[ex + 1] - lo, S = 2 * L + 1;
+    // the lane's states: class, valid, skip into s (from s - 2), skip out of s (into s + 2)
+    int cls[NM];
+    uint32_t vm = 0, skin = 0, skout = 0;
+#pragma unroll
+    for (int i = 0; i < NM; ++i) {
+        const int st = lane * NM + i;
+        const bool v = st < S;
+        const bool lab = v && (st & 1);
+        cls[i] = lab ? labels[lo + (st >> 1)] : 0;
+        vm |= (uint32_t)v << i;
+        if (lab && st >= 3 && cls[i] != labels[lo + (st >> 1) - 1]) skin |= 1u << i;
+        if (lab && st + 2 < S && labels[lo + (st >> 1) + 1] != cls[i]) skout |= 1u << i;
     }
-    // log-softmax of every frame, one wave per frame
-    double* lp = lp_ws + (int64_t)f0 * K;
-    for (int t = wave; t < T; t += HT / 64) {
-        const float* z = logits + (int64_t)(f0 + t) * K;
-        double m = -INFINITY;
-        for (int k = lane; k < K; k += 64) m = fmax(m, (double)z[k]);
-        m = wave_max(m);
-        double se = 0.0;
-        for (int k = lane; k < K; k += 64) se += exp((double)z[k] - m);
-        se = wave_sum(se);
-        const double ls = m + log(se);
-        for (int k = lane; k < K; k += 64) lp[(int64_t)t * K + k] = (double)z[k] - ls;
-    }
-    __syncthreads();  // lp (global, this workgroup's) and the lists are complete
-    double* al = alpha_ws + a_off[ex];
-    auto skip_ok = [&](int s) { return s >= 2 && (s & 1) && lab[s] != lab[s - 2]; };
-    // alpha
-    for (int s = tid; s < S; s += HT) {
-        const double v = s < 2 ? lp[lab[s]] : -INFINITY;
-        A0[s] = v;
-        al[s] = v;
-    }
-    __syncthreads();
-    double* ap = A0;
-    double* ac = A1;
-    for (int t = 1; t < T; ++t) {
-        const double* lpt = lp + (int64_t)t * K;
-        for (int s = tid; s < S; s += HT) {
-            const double a = ap[s], b1 = s >= 1 ? ap[s - 1] : -INFINITY;
-            const double v = (skip_ok(s) ? lse3(a, b1, ap[s - 2]) : lse2(a, b1)) + lpt[lab[s]];
-            ac[s] = v;
-            al[(int64_t)t * S + s] = v;
-        }
-        __syncthreads();
-        double* tmp = ap;
-        ap = ac;
-        ac = tmp;
-    }
-    if (tid == 0) {
-        s_logp = S > 1 ? lse2(ap[S - 1], ap[S - 2]) : ap[0];
-        losses[ex] = (float)(-s_logp);
-    }
-    __syncthreads();
-    const double logp = s_logp;
-    // beta and the gradient, from the last frame back
-    double* bc = ac;  // beta of frame t
-    double* bp = ap;  // beta of frame t - 1 (free: alpha is in global memory)
-    {
-        const double* lpt = lp + (int64_t)(T - 1) * K;
-        for (int s = tid; s < S; s += HT) bc[s] = s >= S - 2 ? lpt[lab[s]] : -INFINITY;
-    }
-    __syncthreads();
-    for (int t = T - 1; t >= 0; --t) {
-        const double* lpt = lp + (int64_t)t * K;
-        for (int s = tid; s < S; s += HT) {
-            const double v = al[(int64_t)t * S + s] + bc[s] - lpt[lab[s]] - logp;
-            G[s] = v == -INFINITY ? 0.0 : exp(v);
-        }
-        __syncthreads();
-        float* dz = dlogits + (int64_t)(f0 + t) * K;
-        if (wave == 0) {  // the blank: the even states, a fixed-order reduction
-            double o = 0.0;
-            for (int s = 2 * lane; s < S; s += 128) o += G[s];
-            o = wave_sum(o);
-            if (lane == 0) dz[0] = (float)(exp(lpt[0]) - o);
-        } else {
-            for (int k = 1 + (tid - 64); k < K; k += HT - 64) {
-                double o = 0.0;
-                for (int s = first[k]; s >= 0; s = nxt[s]) o += G[s];
-                dz[k] = (float)(exp(lpt[k]) - o);
+    const double* yb = y + (int64_t)f0 * K;
+    const int k0 = min(lane, K - 1), k1 = min(lane + 64, K - 1);  // the lane's y columns (clamped)
+    double* yl0 = ys[wave][0];
+    double* yl1 = ys[wave][1];
+    const Xd zero{0.0, XNEG};
+    Xd v[NM];
+    double r0[D], r1[D];
+    if (wave == 0) {
+        double* ambase = am + (int64_t)f0 * RS + lane * NM;
+        int32_t* aebase = ae + (int64_t)f0 * RS + lane * NM;
+        auto store = [&](int t) {
+#pragma unroll
+            for (int i = 0; i < NM; ++i) {
+                ambase[(int64_t)t * RS + i] = v[i].m;
+                aebase[(int64_t)t * RS + i] = v[i].e;
             }
+        };
+        // frame 0: the first blank and the first label
+        yl0[lane] = yb[k0];
+        yl0[lane + 64] = yb[k1];
+#pragma unroll
+        for (int i = 0; i < NM; ++i) {
+            const int st = lane * NM + i;
+            v[i] = ((vm >> i) & 1) && st < 2 ? xnorm(yl0[cls[i]], 0) : zero;
         }
-        if (t > 0) {
-            const double* lpp = lp + (int64_t)(t - 1) * K;
-            for (int s = tid; s < S; s += HT) {
-                const double a = bc[s], b1 = s + 1 < S ? bc[s + 1] : -INFINITY;
-                const bool sk = s + 2 < S && (s & 1) && lab[s] != lab[s + 2];
-                bp[s] = (sk ? lse3(a, b1, bc[s + 2]) : lse2(a, b1)) + lpp[lab[s]];
+        store(0);
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            const int t = min(1 + j, T - 1);
+            r0[j] = yb[(int64_t)t * K + k0];
+            r1[j] = yb[(int64_t)t * K + k1];
+        }
+        auto step = [&](int t, int j) {
+            double* yl = (t & 1) ? yl1 : yl0;
+            yl[lane] = r0[j];
+            yl[lane + 64] = r1[j];
+            const int tn = min(t + D, T - 1);
+            r0[j] = yb[(int64_t)tn * K + k0];
+            r1[j] = yb[(int64_t)tn * K + k1];
+            Xd p1 = xshfl_up(v[NM - 1], 1);
+            Xd p2 = NM >= 2 ? xshfl_up(v[NM >= 2 ? NM - 2 : 0], 1) : xshfl_up(v[NM - 1], 2);
+            if (lane < 1) p1 = zero;
+            if (lane < (NM >= 2 ? 1 : 2)) p2 = zero;
+            Xd n[NM];
+#pragma unroll
+            for (int i = 0; i < NM; ++i) {
+                const Xd m1 = i >= 1 ? v[i - 1] : p1;
+                const Xd m2 = i >= 2 ? v[i - 2] : (i == 1 ? p1 : p2);
+                const Xd x = xsum3(v[i], m1, m2, (skin >> i) & 1);
+                n[i] = ((vm >> i) & 1) ? xnorm(x.m * yl[cls[i]], x.e) : zero;
             }
+#pragma unroll
+            for (int i = 0; i < NM; ++i) v[i] = n[i];
+            store(t);
+        };
+        // whole rounds of D frames (the same loads and stores in each, so the
+        // waits stay exact), then the remaining frames
+        int tb = 1;
+        for (; tb + D <= T; tb += D) {
+#pragma unroll
+            for (int j = 0; j < D; ++j) step(tb + j, j);
         }
-        __syncthreads();
-        double* tmp = bc;
-        bc = bp;
-        bp = tmp;
+#pragma unroll
+        for (int j = 0; j < D; ++j)
+            if (tb + j < T) step(tb + j, j);
+        // -ln p from the last frame's variables at S - 1 and S - 2
+#pragma unroll
+        for (int i = 0; i < NM; ++i) {
+            finm[lane * NM + i] = v[i].m;
+            fine[lane * NM + i] = v[i].e;
+        }
+        if (lane == 0) {
+            const Xd a1{finm[S - 1], fine[S - 1]};
+            const Xd a2 = S >= 2 ? Xd{finm[S - 2], fine[S - 2]} : zero;
+            const Xd p = xsum3(a1, a2, zero, false);
+            losses[ex] = (float)(-(log(p.m) + p.e * 0.69314718055994530942));
+        }
+    } else {
+        double* bmbase = bm + (int64_t)f0 * RS + lane * NM;
+        int32_t* bebase = be + (int64_t)f0 * RS + lane * NM;
+        auto store = [&](int t) {
+#pragma unroll
+            for (int i = 0; i < NM; ++i) {
+                bmbase[(int64_t)t * RS + i] = v[i].m;
+                bebase[(int64_t)t * RS + i] = v[i].e;
+            }
+        };
+        // frame T - 1: 1 at the final blank and the last label
+#pragma unroll
+        for (int i = 0; i < NM; ++i) {
+            const int st = lane * NM + i;
+            v[i] = ((vm >> i) & 1) && st >= S - 2 ? Xd{0.5, 1} : zero;
+        }
+        store(T - 1);
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            const int t = max(T - 1 - j, 0);
+            r0[j] = yb[(int64_t)t * K + k0];
+            r1[j] = yb[(int64_t)t * K + k1];
+        }
+        // step t -> t - 1 uses y_t
+        auto step = [&](int t, int j) {
+            double* yl = (t & 1) ? yl1 : yl0;
+            yl[lane] = r0[j];
+            yl[lane + 64] = r1[j];
+            const int tn = max(t - D, 0);
+            r0[j] = yb[(int64_t)tn * K + k0];
+            r1[j] = yb[(int64_t)tn * K + k1];
+            Xd e[NM];
+#pragma unroll
+            for (int i = 0; i < NM; ++i) e[i] = xnorm(v[i].m * yl[cls[i]], v[i].e);
+            Xd q1 = xshfl_down(e[0], 1);
+            Xd q2 = NM >= 2 ? xshfl_down(e[NM >= 2 ? 1 : 0], 1) : xshfl_down(e[0], 2);
+            if (lane >= 63) q1 = zero;
+            if (lane >= (NM >= 2 ? 63 : 62)) q2 = zero;
+#pragma unroll
+            for (int i = 0; i < NM; ++i) {
+                const Xd u1 = i + 1 < NM ? e[i + 1] : q1;
+                const Xd u2 = i + 2 < NM ? e[i + 2] : (i + 1 < NM ? q1 : q2);
+                v[i] = ((vm >> i) & 1) ? xsum3(e[i], u1, u2, (skout >> i) & 1) : zero;
+            }
+            store(t - 1);
+        };
+        int tb = T - 1;
+        for (; tb - D + 1 >= 1; tb -= D) {
+#pragma unroll
+            for (int j = 0; j < D; ++j) step(tb - j, j);
+        }
+#pragma unroll
+        for (int j = 0; j < D; ++j)
+            if (tb - j >= 1) step(tb - j, j);
     }
+}
+
+// CTC step 3: the gradient of frame f (one wave per frame): state posteriors
+// from the stored variables (products aligned to the largest exponent of the
+// frame), per-class sums in ascending state order (the labels through occ:
+// bit 30 marks a class's first occurrence in the example, bits 0-29 the next
+// occurrence or all ones), dlogits = y - sums.
+__global__ void __launch_bounds__(256)
+k_ctc_grad(int n, int64_t frames, int K, int RS, const int32_t* __restrict__ frame_off,
+           const int32_t* __restrict__ lab_off, const int32_t* __restrict__ labels, const int32_t* __restrict__ occ,
+           const double* __restrict__ y, const double* __restrict__ am, const int32_t* __restrict__ ae,
+           const double* __restrict__ bm, const int32_t* __restrict__ be, float* __restrict__ dlogits) {
+    extern __shared__ __attribute__((aligned(16))) double gsm[];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int64_t f = (int64_t)blockIdx.x * 4 + wave;
+    if (f >= frames) return;
+    double* g = gsm + (int64_t)wave * (RS + 128);  // posteriors of the frame's states
+    double* dl = g + RS;                           // the frame's gradient row
+    // example of frame f: the last i with frame_off[i] <= f
+    int lo_i = 0, hi_i = n - 1;
+    while (lo_i < hi_i) {
+        const int mid = (lo_i + hi_i + 1) >> 1;
+        if (frame_off[mid] <= f) lo_i = mid;
+        else hi_i = mid - 1;
+    }
+    const int ex = lo_i;
+    const int lo = lab_off[ex], L = lab_off[ex + 1] - lo, S = 2 * L + 1;
+    const int64_t r = f * RS;
+    int emax = XNEG;
+    for (int st = lane; st < S; st += 64)
+        if (am[r + st] != 0.0 && bm[r + st] != 0.0) emax = max(emax, ae[r + st] + be[r + st]);
+    for (int o = 32; o > 0; o >>= 1) emax = max(emax, __shfl_xor(emax, o));
+    double z = 0.0, zb = 0.0;  // all states, blank states (fixed order: lane's states ascending, then the butterfly)
+    for (int st = lane; st < S; st += 64) {
+        const double pm = am[r + st] * bm[r + st];
+        const double x = pm == 0.0 ? 0.0 : ldexp(pm, ae[r + st] + be[r + st] - emax);
+        g[st] = x;
+        z += x;
+        if (!(st & 1)) zb += x;
+    }
+    z = wave_sum(z);
+    zb = wave_sum(zb);
+    const double inv = 1.0 / z;
+    const double* yr = y + f * K;
+    for (int k = lane; k < K; k += 64) dl[k] = yr[k];
+    if (lane == 0) dl[0] = yr[0] - zb * inv;
+    for (int j = lane; j < L; j += 64) {
+        const int o = occ[lo + j];
+        if (!(o & (1 << 30))) continue;  // not the first occurrence of its class
+        double sum = 0.0;
+        for (int q = j; q >= 0;) {
+            sum += g[2 * q + 1];
+            const int nx = occ[lo + q] & 0x3fffffff;
+            q = nx == 0x3fffffff ? -1 : nx;
+        }
+        const int k = labels[lo + j];
+        dl[k] = yr[k] - sum * inv;
+    }
+    for (int k = lane; k < K; k += 64) dlogits[f * K + k] = (float)dl[k];
 }
 
 // Backward, input gradient: every row of frame t's column, in every
@@ -325,9 +486,11 @@ int head_dw_chunk_frames() { return DWF; }
 size_t head_fwd_lds(int H, int K) { return (size_t)(K * H + HC * H) * 4; }
 size_t head_bwd_lds(int H, int K) { return (size_t)(K * H + HC * H) * 4; }
 size_t head_dw_lds(int H, int K) { return (size_t)(DWF * K + DWF * (H + 4)) * 4; }
-size_t ctc_lds(int max_labels, int K) {
+int ctc_states_per_lane(int max_labels) {
     const int S = 2 * max_labels + 1;
-    return (size_t)3 * S * 8 + (size_t)(2 * S + K) * 4;
+    int nm = 1;
+    while (64 * nm < S) nm *= 2;
+    return nm;
 }
 
 hipError_t launch_head_fwd(const HeadArgs& a, hipStream_t s) {
@@ -337,10 +500,29 @@ hipError_t launch_head_fwd(const HeadArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int NM>
+static void launch_scan(const CtcArgs& a, hipStream_t s) {
+    constexpr int D = NM <= 4 ? 8 : (NM <= 8 ? 4 : 2);  // frames of y loaded ahead
+    hipLaunchKernelGGL((k_ctc_scan<NM, D>), dim3(a.n), dim3(128), 0, s, a.K, a.frame_off, a.lab_off, a.labels, a.y,
+                       a.am, a.ae, a.bm, a.be, a.losses);
+}
+
 hipError_t launch_ctc(const CtcArgs& a, hipStream_t s) {
-    if (a.n == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_ctc, dim3(a.n), dim3(HT), ctc_lds(a.max_labels, a.K), s, a.K, a.frame_off, a.lab_off,
-                       a.labels, a.a_off, a.logits, a.lp, a.alpha, a.losses, a.dlogits);
+    if (a.n == 0 || a.frames == 0) return hipSuccess;
+    const unsigned fb = (unsigned)((a.frames + 3) / 4);
+    hipLaunchKernelGGL(k_ctc_softmax, dim3(fb), dim3(256), 0, s, a.frames, a.K, a.logits, a.y);
+    switch (a.nm) {
+        case 1: launch_scan<1>(a, s); break;
+        case 2: launch_scan<2>(a, s); break;
+        case 4: launch_scan<4>(a, s); break;
+        case 8: launch_scan<8>(a, s); break;
+        case 16: launch_scan<16>(a, s); break;
+        case 32: launch_scan<32>(a, s); break;
+        default: return hipErrorInvalidValue;
+    }
+    const int rs = 64 * a.nm;
+    hipLaunchKernelGGL(k_ctc_grad, dim3(fb), dim3(256), (size_t)4 * (rs + 128) * 8, s, a.n, a.frames, a.K, rs,
+                       a.frame_off, a.lab_off, a.labels, a.occ, a.y, a.am, a.ae, a.bm, a.be, a.dlogits);
     return hipGetLastError();
 }
 

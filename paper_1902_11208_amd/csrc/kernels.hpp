@@ -157,14 +157,18 @@ struct HeadArgs {
     float* db;                   // backward output [K]
 };
 struct CtcArgs {
-    int n, K, max_labels;
+    int n, K, nm;                // examples, classes, states per lane of the scan (a power of two, 64 nm >= S)
+    int64_t frames;
     const int32_t* frame_off;    // [n + 1]
     const int32_t* lab_off;      // [n + 1]
     const int32_t* labels;       // concatenated labels
-    const int64_t* a_off;        // [n] first double of each example's alpha table
+    const int32_t* occ;          // per label: next occurrence of its class in the example | first-occurrence bit 30
     const float* logits;         // [frames][K]
-    double* lp;                  // workspace [frames][K]
-    double* alpha;               // workspace
+    double* y;                   // workspace [frames][K]: softmax
+    double* am;                  // workspace [frames][64 nm]: forward variables, mantissas
+    int32_t* ae;                 //   and exponents
+    double* bm;                  // workspace [frames][64 nm]: backward variables, mantissas
+    int32_t* be;                 //   and exponents
     float* losses;               // [n]
     float* dlogits;              // [frames][K]
 };
@@ -173,7 +177,7 @@ int head_dw_chunk_frames();
 size_t head_fwd_lds(int H, int K);
 size_t head_bwd_lds(int H, int K);
 size_t head_dw_lds(int H, int K);
-size_t ctc_lds(int max_labels, int K);
+int ctc_states_per_lane(int max_labels);
 hipError_t launch_head_fwd(const HeadArgs& a, hipStream_t s);
 hipError_t launch_ctc(const CtcArgs& a, hipStream_t s);
 // zeroes the dy canvas (canvas_floats floats), then writes the rectangles

@@ -752,12 +752,12 @@ mdlstm_status check_head_desc(const mdlstm_head_desc* d) {
 }
 
 // Workspace sections. The first part (tiles .. weight-gradient partials)
-// serves the layer's forward and backward; the second (labels .. alpha) the
-// CTC loss.
+// serves the layer's forward and backward; the second (label tables .. the
+// backward variables) the CTC loss.
 struct HeadPlan {
-    int64_t frames = 0, alpha_doubles = 0;
-    int32_t n_tiles = 0, chunks = 0, labels = 0, max_label = 0;
-    size_t tiles, rects, frame_off, S, part, part1_end, lab_off, lab, a_off, lp, alpha, total;
+    int64_t frames = 0;
+    int32_t n_tiles = 0, chunks = 0, labels = 0, max_label = 0, nm = 1;
+    size_t tiles, rects, frame_off, S, part, part1_end, lab_off, lab, occ, lp, alpha, beta, total;
 };
 
 HeadPlan head_plan(const mdlstm_head_desc* d, int32_t n, const mdlstm_rect* rects, const int32_t* label_lens) {
@@ -769,7 +769,6 @@ HeadPlan head_plan(const mdlstm_head_desc* d, int32_t n, const mdlstm_rect* rect
         if (label_lens) {
             p.labels += label_lens[i];
             p.max_label = std::max(p.max_label, label_lens[i]);
-            p.alpha_doubles += (int64_t)rects[i].w * (2 * label_lens[i] + 1);
         }
     }
     const int dwf = mdl::head_dw_chunk_frames();
@@ -791,12 +790,18 @@ HeadPlan head_plan(const mdlstm_head_desc* d, int32_t n, const mdlstm_rect* rect
     off += align_up((nn + 1) * 4);
     p.lab = off;
     off += align_up((size_t)std::max(p.labels, 1) * 4);
-    p.a_off = off;
-    off += align_up(nn * 8);
+    p.occ = off;
+    off += align_up((size_t)std::max(p.labels, 1) * 4);
     p.lp = off;
     off += align_up((size_t)std::max<int64_t>(p.frames, 1) * d->classes * 8);
+    // rows of 64 nm states per frame for the CTC scans: mantissas (double)
+    // and exponents (int32) of the forward, then the backward variables
+    p.nm = mdl::ctc_states_per_lane(p.max_label);
+    const size_t rows = (size_t)std::max<int64_t>(p.frames, 1) * 64 * p.nm;
     p.alpha = off;
-    off += align_up((size_t)std::max<int64_t>(p.alpha_doubles, 1) * 8);
+    off += align_up(rows * 8) + align_up(rows * 4);
+    p.beta = off;
+    off += align_up(rows * 8) + align_up(rows * 4);
     p.total = off;
     return p;
 }
@@ -936,7 +941,7 @@ mdlstm_status mdlstm_ctc_loss(const mdlstm_head_desc* desc, int32_t n, const mdl
     if (n == 0) return MDLSTM_OK;
     hipStream_t s = as_stream(stream);
     char* ws = static_cast<char*>(d_workspace);
-    if (poison_requested() && (st = poison(ws, p.lp, p.total, s)) != MDLSTM_OK) return st;  // log-probabilities, alpha
+    if (poison_requested() && (st = poison(ws, p.lp, p.total, s)) != MDLSTM_OK) return st;  // softmax, scan variables
     // frame offsets (first part) and the label tables (second part)
     std::vector<int32_t> fo((size_t)n + 1);
     int32_t f = 0;
@@ -947,30 +952,50 @@ mdlstm_status mdlstm_ctc_loss(const mdlstm_head_desc* desc, int32_t n, const mdl
     fo[n] = f;
     std::vector<unsigned char> host(p.lp - p.lab_off, 0);
     int32_t* lo = reinterpret_cast<int32_t*>(host.data());
-    int64_t* ao = reinterpret_cast<int64_t*>(host.data() + (p.a_off - p.lab_off));
+    int32_t* occ = reinterpret_cast<int32_t*>(host.data() + (p.occ - p.lab_off));
     int32_t l = 0;
-    int64_t a = 0;
     for (int32_t i = 0; i < n; ++i) {
         lo[i] = l;
         l += label_lens[i];
-        ao[i] = a;
-        a += (int64_t)rects[i].w * (2 * label_lens[i] + 1);
     }
     lo[n] = l;
     if (total > 0) std::memcpy(host.data() + (p.lab - p.lab_off), labels, (size_t)total * 4);
+    // per label: the next occurrence of its class in the example (all ones
+    // when none) and, in bit 30, whether it is the class's first occurrence
+    {
+        std::vector<int32_t> last((size_t)desc->classes, -1);
+        for (int32_t i = 0; i < n; ++i) {
+            const int32_t* lb = labels + lo[i];
+            for (int32_t j = label_lens[i] - 1; j >= 0; --j) {
+                occ[lo[i] + j] = last[lb[j]] >= 0 ? last[lb[j]] : 0x3fffffff;
+                last[lb[j]] = j;
+            }
+            for (int32_t j = 0; j < label_lens[i]; ++j) {
+                if (last[lb[j]] == j) occ[lo[i] + j] |= 1 << 30;  // after the loop above: the first occurrence
+                last[lb[j]] = -1;
+            }
+        }
+    }
     HIP_OR_FAIL(hipMemcpyAsync(ws + p.frame_off, fo.data(), fo.size() * 4, hipMemcpyHostToDevice, s));
     HIP_OR_FAIL(hipMemcpyAsync(ws + p.lab_off, host.data(), host.size(), hipMemcpyHostToDevice, s));
     mdl::CtcArgs c{};
     c.n = n;
     c.K = desc->classes;
-    c.max_labels = p.max_label;
+    c.nm = p.nm;
+    c.frames = p.frames;
     c.frame_off = reinterpret_cast<const int32_t*>(ws + p.frame_off);
     c.lab_off = reinterpret_cast<const int32_t*>(ws + p.lab_off);
     c.labels = reinterpret_cast<const int32_t*>(ws + p.lab);
-    c.a_off = reinterpret_cast<const int64_t*>(ws + p.a_off);
+    c.occ = reinterpret_cast<const int32_t*>(ws + p.occ);
     c.logits = d_logits;
-    c.lp = reinterpret_cast<double*>(ws + p.lp);
-    c.alpha = reinterpret_cast<double*>(ws + p.alpha);
+    c.y = reinterpret_cast<double*>(ws + p.lp);
+    {
+        const size_t rows = (size_t)std::max<int64_t>(p.frames, 1) * 64 * p.nm;
+        c.am = reinterpret_cast<double*>(ws + p.alpha);
+        c.ae = reinterpret_cast<int32_t*>(ws + p.alpha + align_up(rows * 8));
+        c.bm = reinterpret_cast<double*>(ws + p.beta);
+        c.be = reinterpret_cast<int32_t*>(ws + p.beta + align_up(rows * 8));
+    }
     c.losses = d_losses;
     c.dlogits = d_dlogits;
     HIP_OR_FAIL(mdl::launch_ctc(c, s));

@@ -139,3 +139,34 @@ def test_head_is_deterministic():
         outs.append([t.clone() for t in (l, g, dy, dw, db)])
     for a, c in zip(*outs):
         assert torch.equal(a, c)
+
+
+@pytest.mark.parametrize("L", [40, 128, 250, 500])
+def test_ctc_long_labels(L):
+    """Label lengths that select each width of the CTC scan (states per lane
+    1 to 16), with alignments tight enough that the forward variables span
+    far more than the double range within a frame (500 labels in 1010
+    frames): losses and gradients against the log-space oracle."""
+    from oracle import head as ohead
+    from paper_1902_11208_amd import api
+
+    rng = np.random.default_rng(L)
+    H, K = 8, 80
+    T = 2 * L + 10
+    hs, ws = [2, 3], [T, T // 2 + L]
+    labels = [rng.integers(1, K, L).astype(np.int32), rng.integers(1, K, L // 2).astype(np.int32)]
+    rects, ch, _ = api.pack_layout(hs, ws, max(ws))
+    Y = (rng.standard_normal((ch, max(ws), 4 * H)) * 0.3).astype(np.float32)
+    W = rng.uniform(-0.3, 0.3, (K, H)).astype(np.float32)
+    b = rng.uniform(-0.3, 0.3, K).astype(np.float32)
+    print(f"case: CTC with {L} and {L // 2} labels over {ws} frames", flush=True)
+    hd = api.Head(torch.from_numpy(W).cuda(), torch.from_numpy(b).cuda(), rects, (ch, max(ws)), labels)
+    lg = hd.forward(torch.from_numpy(Y).cuda()).cpu().numpy().astype(np.float64)
+    losses, dl = hd.ctc()
+    torch.cuda.synchronize()
+    losses, dl = losses.cpu().numpy().astype(np.float64), dl.cpu().numpy().astype(np.float64)
+    off = np.concatenate([[0], np.cumsum(ws)])
+    for k in range(2):
+        loss, g = ohead.ctc_loss(lg[off[k]:off[k + 1]], labels[k])
+        assert abs(losses[k] - loss) <= TOL * abs(loss), (k, losses[k], loss)
+        _check(f"dlogits[{k}]", dl[off[k]:off[k + 1]], g)
