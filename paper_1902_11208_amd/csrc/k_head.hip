@@ -458,15 +458,29 @@ k_head_bwd_dw(int H, int K, int frames, const float* __restrict__ dlogits, const
     }
 }
 
-__global__ void k_head_dw_reduce(int H, int K, int chunks, const float* __restrict__ part, float* __restrict__ dW,
-                                 float* __restrict__ db) {
-    const int NJ = H + 1;
-    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < K * NJ; e += gridDim.x * blockDim.x) {
-        float s = 0.0f;
-        for (int c = 0; c < chunks; ++c) s += part[(int64_t)c * K * NJ + e];
+// Fixed-order sum of the chunk partials: a workgroup owns 64 consecutive
+// outputs (one per lane); its four waves sum four consecutive ranges of the
+// chunks (loads of 64 outputs per chunk are contiguous), and the ranges are
+// added in order.
+__global__ void __launch_bounds__(256)
+k_head_dw_reduce(int H, int K, int chunks, const float* __restrict__ part, float* __restrict__ dW,
+                 float* __restrict__ db) {
+    __shared__ float acc[4][64];
+    const int NJ = H + 1, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int e = blockIdx.x * 64 + lane;
+    const int q = (chunks + 3) / 4, c0 = wave * q, c1 = min(chunks, c0 + q);
+    float s = 0.0f;
+    if (e < K * NJ) {
+#pragma unroll 8
+        for (int c = c0; c < c1; ++c) s += part[(int64_t)c * K * NJ + e];
+    }
+    acc[wave][lane] = s;
+    __syncthreads();
+    if (wave == 0 && e < K * NJ) {
+        const float t = ((acc[0][lane] + acc[1][lane]) + acc[2][lane]) + acc[3][lane];
         const int k = e / NJ, j = e - k * NJ;
-        if (j < H) dW[k * H + j] = s;
-        else db[k] = s;
+        if (j < H) dW[k * H + j] = t;
+        else db[k] = t;
     }
 }
 
@@ -540,7 +554,7 @@ hipError_t launch_head_bwd(const HeadArgs& a, int64_t canvas_floats, hipStream_t
                            a.dlogits, a.S, a.part);
     const int nj = a.K * (a.H + 1);
     if (chunks > 0) {
-        hipLaunchKernelGGL(k_head_dw_reduce, dim3((nj + 255) / 256), dim3(256), 0, s, a.H, a.K, chunks, a.part, a.dw,
+        hipLaunchKernelGGL(k_head_dw_reduce, dim3((nj + 63) / 64), dim3(256), 0, s, a.H, a.K, chunks, a.part, a.dw,
                            a.db);
     } else {  // no frames: zero gradients
         hipLaunchKernelGGL(k_zero_f, dim3((a.K * a.H + 255) / 256), dim3(256), 0, s, a.dw, a.K * a.H);
