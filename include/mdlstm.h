@@ -67,9 +67,18 @@ typedef struct {
     int32_t y0, x0, h, w;
 } mdlstm_rect;
 
-/* One MDLSTM layer. Supported: F32 with hidden in {4, 8, 16, 32, 64};
- * BF16 with hidden in {32, 64, 128}; c_in a multiple of 4 (F32) or 8 (BF16),
- * 4 <= c_in <= 256.
+/* One MDLSTM layer. Supported: F32 with 1 <= hidden <= 64, BF16 with
+ * 1 <= hidden <= 128, and 1 <= c_in <= 256 (UNSUPPORTED beyond). The kernels
+ * are built for F32 hidden in {4, 8, 16, 32, 64}, BF16 hidden in {32, 64,
+ * 128}, and c_in a multiple of 4 (F32) or 8 (BF16). Other sizes (the paper's
+ * 2, 10 and 50 hidden units, a single input channel) run on the next built
+ * shape: the call copies the weights and, when those sizes differ, x, y and
+ * dy into zero-padded copies in the workspace and copies y, dx and the
+ * weight gradients back. A padded unit has zero weights, so its gates stay at
+ * 1/2, its cell candidate, state and output at 0 and its gradients at 0; a
+ * padded input channel is 0. The results are those of the layer's own sizes
+ * (bit for bit those of the built shape on zero-padded operands); the copies
+ * cost workspace and a few extra passes over x and y.
  *
  * memory_states = 1 adds the memory-state matrices of Appendix A (three per
  * predecessor memory state S1 = c_L and S2 = c_T, next to the five per
@@ -78,8 +87,9 @@ typedef struct {
  *     a = Wx_d x + b_d + U_d [h_L ; h_T] + [V_d [c_L ; c_T] ; 0 ; 0]
  * The recurrent weight argument then holds U [4][5H][2H] immediately followed
  * by V [4][3H][2H] (one buffer), and the backward writes dU followed by dV the
- * same way. Built for F32 with hidden 16 or 32 (UNSUPPORTED otherwise); the
- * per-diagonal schedule (mdlstm_forward_stepwise) is not built for it.
+ * same way. Built for F32 with hidden 16 or 32 (hidden 1 to 15 and 17 to 31
+ * padded as above; UNSUPPORTED for BF16 and above 32); the per-diagonal
+ * schedule (mdlstm_forward_stepwise) is not built for it.
  * 0 (or a descriptor initialised with its first three fields) is the plain
  * cell. */
 typedef struct {
@@ -177,8 +187,9 @@ mdlstm_status mdlstm_unpack_data(int32_t n, void* const* d_examples, const mdlst
                                  const void* d_canvas, void* d_workspace, size_t workspace_bytes,
                                  void* stream);
 
-/* Device workspace needed by mdlstm_forward followed by mdlstm_backward; 0
- * when the descriptor is invalid or not built, or the canvas or the number of
+/* Device workspace needed by mdlstm_forward followed by mdlstm_backward
+ * (with the zero-padded copies of a shape between the built ones); 0 when the
+ * descriptor is invalid or unsupported, or the canvas or the number of
  * rectangles is out of range (mdlstm_last_error says which). */
 size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
                               int32_t n_rects);

@@ -19,7 +19,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["mdlstm_api.cpp", "k_pack.hip", "k_proj.hip", "k_wave.hip", "k_bwd_big.hip", "k_bwd_strip.hip",
-           "k_stack.hip", "k_head.hip", "k_wave_mem.hip"]
+           "k_stack.hip", "k_head.hip", "k_wave_mem.hip", "k_pad.hip"]
 
 FLAGS = [
     f"--offload-arch={ARCH}",

@@ -39,6 +39,11 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
 // Count the non-finite values of n elements (dtype 0 fp32, 1 bf16) into
 // *d_count (added to; the caller zeroes it).
 hipError_t launch_fill_u32(void* d, int64_t n_words, uint32_t v, hipStream_t s);
+// Block remap between a layer's own sizes and its padded built sizes (k_pad.hip):
+// dst[o][rb*rd + j][cb*cd + k] = src[o][rb*rs + j][cb*cs + k] where j < min(rs, rd) and
+// k < min(cs, cd), else 0; es = element bytes (2 or 4).
+hipError_t launch_remap(const void* src, void* dst, int es, int64_t outer, int rblocks, int rs, int rd, int cblocks,
+                        int cs, int cd, hipStream_t s);
 hipError_t launch_count_nonfinite(const void* d, int64_t n_cells, int row, const uint8_t* d_mask, int dtype,
                                   unsigned long long* d_count, hipStream_t s);
 // Zero the rows of a [n_cells][width] tensor (storage dtype) whose cell is invalid.

@@ -83,7 +83,8 @@ mdlstm_status poison(char* ws, size_t from, size_t to, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // Layer descriptor and workspace plan.
 // ---------------------------------------------------------------------------
-mdlstm_status check_desc(const mdlstm_layer_desc* d) {
+// A shape the kernels are built for.
+mdlstm_status check_built(const mdlstm_layer_desc* d) {
     if (!d) return fail(MDLSTM_ERR_INVALID_ARG, "desc is NULL");
     if (d->dtype != MDLSTM_F32 && d->dtype != MDLSTM_BF16)
         return fail(MDLSTM_ERR_INVALID_ARG, "dtype %d is not MDLSTM_F32 or MDLSTM_BF16", d->dtype);
@@ -106,6 +107,35 @@ mdlstm_status check_desc(const mdlstm_layer_desc* d) {
             return fail(MDLSTM_ERR_UNSUPPORTED, "bf16 c_in %d must be a multiple of 8 in [8, 256]", d->c_in);
     }
     return MDLSTM_OK;
+}
+
+// The kernels' shape for a layer: the hidden size padded to the next built
+// size (fp32 4, 8, 16, 32, 64; bf16 32, 64, 128; with memory-state matrices at
+// least 16), c_in to a multiple of the MFMA K step (4 fp32, 8 bf16). Padded
+// hidden units and input channels carry zero weights, which leaves the
+// layer's results unchanged (k_pad.hip).
+mdlstm_status inner_desc(const mdlstm_layer_desc* d, mdlstm_layer_desc* in) {
+    if (!d) return fail(MDLSTM_ERR_INVALID_ARG, "desc is NULL");
+    if (d->dtype != MDLSTM_F32 && d->dtype != MDLSTM_BF16)
+        return fail(MDLSTM_ERR_INVALID_ARG, "dtype %d is not MDLSTM_F32 or MDLSTM_BF16", d->dtype);
+    if (d->c_in < 1 || d->hidden < 1) return fail(MDLSTM_ERR_INVALID_ARG, "c_in and hidden must be positive");
+    if (d->memory_states != 0 && d->memory_states != 1)
+        return fail(MDLSTM_ERR_INVALID_ARG, "memory_states %d is not 0 or 1", d->memory_states);
+    const bool f32 = d->dtype == MDLSTM_F32;
+    const int hmax = f32 ? 64 : 128;
+    if (d->hidden > hmax) return fail(MDLSTM_ERR_UNSUPPORTED, "%s hidden size %d: at most %d", f32 ? "fp32" : "bf16",
+                                      d->hidden, hmax);
+    if (d->c_in > 256) return fail(MDLSTM_ERR_UNSUPPORTED, "c_in %d: at most 256", d->c_in);
+    int hp = f32 ? 4 : 32;
+    while (hp < d->hidden) hp *= 2;
+    if (d->memory_states && f32) hp = std::max(hp, 16);
+    const int kq = f32 ? 4 : 8;
+    *in = mdlstm_layer_desc{(d->c_in + kq - 1) / kq * kq, hp, d->dtype, d->memory_states};
+    return check_built(in);
+}
+
+bool same_shape(const mdlstm_layer_desc* a, const mdlstm_layer_desc& b) {
+    return a->c_in == b.c_in && a->hidden == b.hidden;
 }
 
 struct Plan {
@@ -154,6 +184,48 @@ Plan plan(const mdlstm_layer_desc* d, int32_t ch, int32_t cw, int32_t nr) {
     off += align_up(8);
     p.total = off;
     return p;
+}
+
+// Sections of the padded copies at the front of the workspace (the kernels'
+// plan follows them); none when the layer is a built shape. x and dx are
+// copied only when c_in is padded, y and dy only when the hidden size is.
+struct PadPlan {
+    bool active = false, pad_c = false, pad_h = false;
+    size_t wx = 0, u = 0, b = 0, x = 0, y = 0, dy = 0, dx = 0, dwx = 0, du = 0, db = 0, total = 0;
+};
+
+PadPlan pad_plan(const mdlstm_layer_desc* d, const mdlstm_layer_desc& in, int32_t ch, int32_t cw) {
+    PadPlan q;
+    if (same_shape(d, in)) return q;
+    q.active = true;
+    q.pad_c = in.c_in != d->c_in;
+    q.pad_h = in.hidden != d->hidden;
+    const size_t es = d->dtype == MDLSTM_BF16 ? 2 : 4, cells = (size_t)ch * (size_t)cw;
+    const size_t H = (size_t)in.hidden, C = (size_t)in.c_in;
+    const size_t nu = 4 * 5 * H * 2 * H + (d->memory_states ? 4 * 3 * H * 2 * H : 0);
+    size_t off = 0;
+    q.wx = off;
+    off += align_up(4 * 5 * H * C * es);
+    q.u = off;
+    off += align_up(nu * es);
+    q.b = off;
+    off += align_up(4 * 5 * H * es);
+    q.x = off;
+    off += q.pad_c ? align_up(cells * C * es) : 0;
+    q.dx = off;
+    off += q.pad_c ? align_up(cells * C * es) : 0;
+    q.y = off;
+    off += q.pad_h ? align_up(cells * 4 * H * es) : 0;
+    q.dy = off;
+    off += q.pad_h ? align_up(cells * 4 * H * es) : 0;
+    q.dwx = off;
+    off += align_up(4 * 5 * H * C * 4);
+    q.du = off;
+    off += align_up(nu * 4);
+    q.db = off;
+    off += align_up(4 * 5 * H * 4);
+    q.total = off;
+    return q;
 }
 
 // ---------------------------------------------------------------------------
@@ -218,7 +290,7 @@ struct Common {
 mdlstm_status prepare(const mdlstm_layer_desc* desc, int32_t ch, int32_t cw, const void* d_x, const uint8_t* d_mask,
                       int32_t n_rects, const mdlstm_rect* rects, const void* d_wx, const void* d_u,
                       const void* d_b, void* d_workspace, size_t ws_bytes, Common* out) {
-    mdlstm_status st = check_desc(desc);
+    mdlstm_status st = check_built(desc);
     if (st != MDLSTM_OK) return st;
     if (ch < 0 || cw < 0 || ch > kMaxDim || cw > kMaxDim)
         return fail(MDLSTM_ERR_INVALID_ARG, "canvas %dx%d out of range", ch, cw);
@@ -540,18 +612,20 @@ mdlstm_status mdlstm_unpack_data(int32_t n, void* const* d_examples, const mdlst
 }
 
 size_t mdlstm_workspace_bytes(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, int32_t n_rects) {
-    if (check_desc(desc) != MDLSTM_OK) return 0;
+    mdlstm_layer_desc in;
+    if (inner_desc(desc, &in) != MDLSTM_OK) return 0;
     if (canvas_h < 0 || canvas_w < 0 || canvas_h > kMaxDim || canvas_w > kMaxDim || n_rects < 0 ||
         n_rects > kMaxRects) {
         fail(MDLSTM_ERR_INVALID_ARG, "canvas %dx%d or %d rectangles out of range", canvas_h, canvas_w, n_rects);
         return 0;
     }
-    return plan(desc, canvas_h, canvas_w, n_rects).total;
+    return pad_plan(desc, in, canvas_h, canvas_w).total + plan(&in, canvas_h, canvas_w, n_rects).total;
 }
 
 int32_t mdlstm_gradients_fused(const mdlstm_layer_desc* desc) {
-    if (check_desc(desc) != MDLSTM_OK) return -1;
-    return mdl::strip_supported(geom(desc, 1, 1)) ? 1 : 0;
+    mdlstm_layer_desc in;
+    if (inner_desc(desc, &in) != MDLSTM_OK) return -1;
+    return mdl::strip_supported(geom(&in, 1, 1)) ? 1 : 0;
 }
 
 namespace {
@@ -644,29 +718,11 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
     return MDLSTM_OK;
 }
 
-}  // namespace
-
-mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
-                             const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
-                             const void* d_u, const void* d_b, void* d_y, void* d_workspace, size_t workspace_bytes,
-                             void* stream) {
-    return forward_impl(false, desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_y,
-                        d_workspace, workspace_bytes, stream);
-}
-
-mdlstm_status mdlstm_forward_stepwise(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
-                                      const void* d_x, const uint8_t* d_mask, int32_t n_rects,
-                                      const mdlstm_rect* rects, const void* d_wx, const void* d_u, const void* d_b,
-                                      void* d_y, void* d_workspace, size_t workspace_bytes, void* stream) {
-    return forward_impl(true, desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_y,
-                        d_workspace, workspace_bytes, stream);
-}
-
-mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
-                              const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
-                              const void* d_u, const void* d_b, const void* d_y, const void* d_dy, void* d_dx,
-                              float* d_dwx, float* d_du, float* d_db, void* d_workspace, size_t workspace_bytes,
-                              void* stream) {
+mdlstm_status backward_impl(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
+                            const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
+                            const void* d_u, const void* d_b, const void* d_y, const void* d_dy, void* d_dx,
+                            float* d_dwx, float* d_du, float* d_db, void* d_workspace, size_t workspace_bytes,
+                            void* stream) {
     Common c;
     mdlstm_status st = prepare(desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_workspace,
                                workspace_bytes, &c);
@@ -732,6 +788,160 @@ mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, i
     }
     HIP_OR_FAIL(mark(7, s));
     return MDLSTM_OK;
+}
+
+// Arguments of a layer call at its own sizes, checked before the padded
+// copies are written.
+mdlstm_status check_padded_call(const PadPlan& q, const mdlstm_layer_desc& in, int32_t ch, int32_t cw,
+                                const void* d_x, const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects,
+                                const void* d_wx, const void* d_u, const void* d_b, void* d_workspace,
+                                size_t ws_bytes) {
+    if (ch < 0 || cw < 0 || ch > kMaxDim || cw > kMaxDim)
+        return fail(MDLSTM_ERR_INVALID_ARG, "canvas %dx%d out of range", ch, cw);
+    int32_t max_h = 0;
+    mdlstm_status st = check_rects(n_rects, rects, ch, cw, &max_h);
+    if (st != MDLSTM_OK) return st;
+    if ((int64_t)ch * cw > 0 && (!d_x || !d_mask)) return fail(MDLSTM_ERR_INVALID_ARG, "x or mask is NULL");
+    if (!d_wx || !d_u || !d_b) return fail(MDLSTM_ERR_INVALID_ARG, "a weight pointer is NULL");
+    if (!d_workspace) return fail(MDLSTM_ERR_INVALID_ARG, "workspace is NULL");
+    if (misaligned(d_x) || misaligned(d_wx) || misaligned(d_u) || misaligned(d_b) || misaligned(d_workspace))
+        return fail(MDLSTM_ERR_INVALID_ARG, "x, weights and workspace must be 16-byte aligned");
+    const size_t need = q.total + plan(&in, ch, cw, n_rects).total;
+    if (ws_bytes < need) return fail(MDLSTM_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+    return MDLSTM_OK;
+}
+
+// Weights at the layer's sizes into the padded sections: Wx [4][5H][C],
+// U [4][5H][2H] (+ V [4][3H][2H]) and b [4][5H], each gate block and each
+// predecessor block padded on its own.
+mdlstm_status pad_weights(const mdlstm_layer_desc* d, const mdlstm_layer_desc& in, const PadPlan& q,
+                          const void* d_wx, const void* d_u, const void* d_b, char* ws, hipStream_t s) {
+    const int es = d->dtype == MDLSTM_BF16 ? 2 : 4, H = d->hidden, Hp = in.hidden;
+    HIP_OR_FAIL(mdl::launch_remap(d_wx, ws + q.wx, es, 4, 5, H, Hp, 1, d->c_in, in.c_in, s));
+    HIP_OR_FAIL(mdl::launch_remap(d_u, ws + q.u, es, 4, 5, H, Hp, 2, H, Hp, s));
+    if (d->memory_states)
+        HIP_OR_FAIL(mdl::launch_remap(static_cast<const char*>(d_u) + (size_t)4 * 5 * H * 2 * H * es,
+                                      ws + q.u + (size_t)4 * 5 * Hp * 2 * Hp * es, es, 4, 3, H, Hp, 2, H, Hp, s));
+    HIP_OR_FAIL(mdl::launch_remap(d_b, ws + q.b, es, 4, 5, H, Hp, 1, 1, 1, s));
+    return MDLSTM_OK;
+}
+
+mdlstm_status padded_forward(bool stepwise, const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
+                             const void* d_x, const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects,
+                             const void* d_wx, const void* d_u, const void* d_b, void* d_y, void* d_workspace,
+                             size_t workspace_bytes, void* stream) {
+    mdlstm_layer_desc in;
+    mdlstm_status st = inner_desc(desc, &in);
+    if (st != MDLSTM_OK) return st;
+    if (same_shape(desc, in))
+        return forward_impl(stepwise, desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_y,
+                            d_workspace, workspace_bytes, stream);
+    if (in.memory_states && stepwise)
+        return fail(MDLSTM_ERR_UNSUPPORTED, "the per-diagonal schedule is not built with memory-state matrices");
+    const PadPlan q = pad_plan(desc, in, canvas_h, canvas_w);
+    st = check_padded_call(q, in, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_workspace,
+                           workspace_bytes);
+    if (st != MDLSTM_OK) return st;
+    const int64_t cells = (int64_t)canvas_h * canvas_w;
+    if (cells > 0 && !d_y) return fail(MDLSTM_ERR_INVALID_ARG, "y is NULL");
+    if (misaligned(d_y)) return fail(MDLSTM_ERR_INVALID_ARG, "y must be 16-byte aligned");
+    if (cells == 0) return MDLSTM_OK;
+    hipStream_t s = as_stream(stream);
+    char* ws = static_cast<char*>(d_workspace);
+    const int es = desc->dtype == MDLSTM_BF16 ? 2 : 4;
+    if ((st = pad_weights(desc, in, q, d_wx, d_u, d_b, ws, s)) != MDLSTM_OK) return st;
+    const void* x = d_x;
+    if (q.pad_c) {
+        HIP_OR_FAIL(mdl::launch_remap(d_x, ws + q.x, es, cells, 1, 1, 1, 1, desc->c_in, in.c_in, s));
+        x = ws + q.x;
+    }
+    void* y = q.pad_h ? static_cast<void*>(ws + q.y) : d_y;
+    st = forward_impl(stepwise, &in, canvas_h, canvas_w, x, d_mask, n_rects, rects, ws + q.wx, ws + q.u, ws + q.b, y,
+                      ws + q.total, workspace_bytes - q.total, stream);
+    if (st != MDLSTM_OK) return st;
+    if (q.pad_h) HIP_OR_FAIL(mdl::launch_remap(y, d_y, es, cells, 1, 1, 1, 4, in.hidden, desc->hidden, s));
+    return MDLSTM_OK;
+}
+
+mdlstm_status padded_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
+                              const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
+                              const void* d_u, const void* d_b, const void* d_y, const void* d_dy, void* d_dx,
+                              float* d_dwx, float* d_du, float* d_db, void* d_workspace, size_t workspace_bytes,
+                              void* stream) {
+    mdlstm_layer_desc in;
+    mdlstm_status st = inner_desc(desc, &in);
+    if (st != MDLSTM_OK) return st;
+    if (same_shape(desc, in))
+        return backward_impl(desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_y, d_dy, d_dx,
+                             d_dwx, d_du, d_db, d_workspace, workspace_bytes, stream);
+    const PadPlan q = pad_plan(desc, in, canvas_h, canvas_w);
+    st = check_padded_call(q, in, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_workspace,
+                           workspace_bytes);
+    if (st != MDLSTM_OK) return st;
+    const int64_t cells = (int64_t)canvas_h * canvas_w;
+    if (!d_dwx || !d_du || !d_db) return fail(MDLSTM_ERR_INVALID_ARG, "a weight-gradient pointer is NULL");
+    if (cells > 0 && (!d_y || !d_dy || !d_dx)) return fail(MDLSTM_ERR_INVALID_ARG, "y, dy or dx is NULL");
+    if (misaligned(d_y) || misaligned(d_dy) || misaligned(d_dx) || misaligned(d_dwx) || misaligned(d_du) ||
+        misaligned(d_db))
+        return fail(MDLSTM_ERR_INVALID_ARG, "y, dy, dx and the weight gradients must be 16-byte aligned");
+    hipStream_t s = as_stream(stream);
+    char* ws = static_cast<char*>(d_workspace);
+    const int es = desc->dtype == MDLSTM_BF16 ? 2 : 4, H = desc->hidden, Hp = in.hidden;
+    if ((st = pad_weights(desc, in, q, d_wx, d_u, d_b, ws, s)) != MDLSTM_OK) return st;
+    const void *x = d_x, *y = d_y, *dy = d_dy;
+    void* dx = d_dx;
+    if (q.pad_c && cells > 0) {
+        HIP_OR_FAIL(mdl::launch_remap(d_x, ws + q.x, es, cells, 1, 1, 1, 1, desc->c_in, in.c_in, s));
+        x = ws + q.x;
+        dx = ws + q.dx;
+    }
+    if (q.pad_h && cells > 0) {
+        HIP_OR_FAIL(mdl::launch_remap(d_y, ws + q.y, es, cells, 1, 1, 1, 4, H, Hp, s));
+        HIP_OR_FAIL(mdl::launch_remap(d_dy, ws + q.dy, es, cells, 1, 1, 1, 4, H, Hp, s));
+        y = ws + q.y;
+        dy = ws + q.dy;
+    }
+    float* dwx = reinterpret_cast<float*>(ws + q.dwx);
+    float* du = reinterpret_cast<float*>(ws + q.du);
+    float* db = reinterpret_cast<float*>(ws + q.db);
+    st = backward_impl(&in, canvas_h, canvas_w, x, d_mask, n_rects, rects, ws + q.wx, ws + q.u, ws + q.b, y, dy, dx,
+                       dwx, du, db, ws + q.total, workspace_bytes - q.total, stream);
+    if (st != MDLSTM_OK) return st;
+    if (q.pad_c && cells > 0) HIP_OR_FAIL(mdl::launch_remap(dx, d_dx, es, cells, 1, 1, 1, 1, in.c_in, desc->c_in, s));
+    HIP_OR_FAIL(mdl::launch_remap(dwx, d_dwx, 4, 4, 5, Hp, H, 1, in.c_in, desc->c_in, s));
+    HIP_OR_FAIL(mdl::launch_remap(du, d_du, 4, 4, 5, Hp, H, 2, Hp, H, s));
+    if (desc->memory_states)
+        HIP_OR_FAIL(mdl::launch_remap(du + (size_t)4 * 5 * Hp * 2 * Hp, d_du + (size_t)4 * 5 * H * 2 * H, 4, 4, 3, Hp,
+                                      H, 2, Hp, H, s));
+    HIP_OR_FAIL(mdl::launch_remap(db, d_db, 4, 4, 5, Hp, H, 1, 1, 1, s));
+    return MDLSTM_OK;
+}
+
+}  // namespace
+
+mdlstm_status mdlstm_forward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
+                             const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
+                             const void* d_u, const void* d_b, void* d_y, void* d_workspace, size_t workspace_bytes,
+                             void* stream) {
+    return padded_forward(false, desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_y,
+                          d_workspace, workspace_bytes, stream);
+}
+
+mdlstm_status mdlstm_forward_stepwise(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w,
+                                      const void* d_x, const uint8_t* d_mask, int32_t n_rects,
+                                      const mdlstm_rect* rects, const void* d_wx, const void* d_u, const void* d_b,
+                                      void* d_y, void* d_workspace, size_t workspace_bytes, void* stream) {
+    return padded_forward(true, desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_y,
+                          d_workspace, workspace_bytes, stream);
+}
+
+mdlstm_status mdlstm_backward(const mdlstm_layer_desc* desc, int32_t canvas_h, int32_t canvas_w, const void* d_x,
+                              const uint8_t* d_mask, int32_t n_rects, const mdlstm_rect* rects, const void* d_wx,
+                              const void* d_u, const void* d_b, const void* d_y, const void* d_dy, void* d_dx,
+                              float* d_dwx, float* d_du, float* d_db, void* d_workspace, size_t workspace_bytes,
+                              void* stream) {
+    return padded_backward(desc, canvas_h, canvas_w, d_x, d_mask, n_rects, rects, d_wx, d_u, d_b, d_y, d_dy, d_dx,
+                           d_dwx, d_du, d_db, d_workspace, workspace_bytes, stream);
 }
 
 // ---------------------------------------------------------------------------

@@ -75,11 +75,36 @@ def _fwd(desc, ch, cw, rects, ws_bytes=None):
 
 
 @pytest.mark.parametrize("c_in,hidden,dtype,code", [
-    (16, 12, 0, 5), (16, 128, 0, 5), (6, 16, 0, 5), (16, 16, 7, 1), (16, 16, 1, 5), (12, 32, 1, 5), (0, 16, 0, 1),
+    (16, 65, 0, 5), (16, 128, 0, 5), (16, 129, 1, 5), (260, 16, 0, 5), (16, 16, 7, 1), (0, 16, 0, 1),
+    (16, 0, 0, 1), (16, 40, 0, 5),  # memory-state matrices not built above hidden 32 (set below)
 ])
 def test_forward_rejects_descriptor(built_lib, c_in, hidden, dtype, code):
-    d = _lib().LayerDesc(c_in, hidden, dtype)
+    d = _lib().LayerDesc(c_in, hidden, dtype, 1 if hidden == 40 else 0)
     assert _fwd(d, 10, 10, [(0, 0, 2, 2)]) == code
+
+
+def test_padded_shapes_are_sized_and_checked(built_lib):
+    """A hidden size or c_in between the built ones is padded inside the
+    call: its workspace holds the padded copies on top of the built shape's,
+    and its arguments are checked at the layer's own sizes before any HIP
+    call."""
+    L = _lib()
+    ws = L.lib().mdlstm_workspace_bytes
+    built = ws(ctypes.byref(L.LayerDesc(16, 16, 0)), 10, 10, 1)
+    for c_in, hidden, dtype in ((16, 12, 0), (6, 16, 0), (1, 2, 0), (30, 50, 0), (12, 100, 1), (3, 32, 1)):
+        assert ws(ctypes.byref(L.LayerDesc(c_in, hidden, dtype)), 10, 10, 1) > 0, (c_in, hidden, dtype)
+    assert ws(ctypes.byref(L.LayerDesc(16, 12, 0)), 10, 10, 1) > built
+    assert ws(ctypes.byref(L.LayerDesc(16, 10, 0, 1)), 10, 10, 1) > ws(ctypes.byref(L.LayerDesc(16, 16, 0, 1)), 10,
+                                                                        10, 1)
+    for d in (L.LayerDesc(16, 12, 0), L.LayerDesc(6, 16, 0), L.LayerDesc(5, 20, 1)):
+        assert _fwd(d, 10, 10, [(0, 0, 3, 3), (2, 2, 3, 3)]) == 3      # overlap
+        assert _fwd(d, 100, 10, [(0, 0, 65, 3)]) == 5                  # too tall
+        need = ws(ctypes.byref(d), 10, 10, 1)
+        assert _fwd(d, 10, 10, [(0, 0, 3, 3)], ws_bytes=need - 1) == 4  # the padded copies need room too
+        assert _bwd(d, 10, 10, [(0, 0, 3, 3)], ws_bytes=need - 1) == 4
+        for nm in ("dwx", "dy", "dx"):
+            assert _bwd(d, 10, 10, [(0, 0, 3, 3)], **{nm: None}) == 1, nm
+        assert _bwd(d, 10, 10, [(0, 0, 3, 3)], dx=FAKE + 4) == 1
 
 
 def test_forward_rejects_layouts(built_lib):
@@ -105,7 +130,7 @@ def test_workspace_bytes_scale():
     # an empty canvas still has a (small) workspace; unsupported shapes and
     # out-of-range canvases report 0 instead of a size
     assert L.lib().mdlstm_workspace_bytes(ctypes.byref(L.LayerDesc(64, 128, 1)), 0, 0, 0) > 0
-    assert L.lib().mdlstm_workspace_bytes(ctypes.byref(L.LayerDesc(16, 12, 0)), 10, 10, 1) == 0
+    assert L.lib().mdlstm_workspace_bytes(ctypes.byref(L.LayerDesc(16, 65, 0)), 10, 10, 1) == 0
     assert L.lib().mdlstm_workspace_bytes(ctypes.byref(L.LayerDesc(16, 1 << 20, 0)), 10, 10, 1) == 0
     assert L.lib().mdlstm_workspace_bytes(ctypes.byref(d), 1 << 22, 10, 1) == 0
     assert L.lib().mdlstm_workspace_bytes(ctypes.byref(d), 10, 10, (1 << 24) + 1) == 0
@@ -202,7 +227,7 @@ def test_backward_rejects_bad_arguments(built_lib):
     before any HIP call."""
     L = _lib()
     ok = L.LayerDesc(16, 16, 0)
-    assert _bwd(L.LayerDesc(16, 12, 0), 10, 10, [(0, 0, 2, 2)]) == 5          # hidden not built
+    assert _bwd(L.LayerDesc(16, 65, 0), 10, 10, [(0, 0, 2, 2)]) == 5          # hidden above the largest built
     assert _bwd(L.LayerDesc(16, 16, 9), 10, 10, [(0, 0, 2, 2)]) == 1          # dtype
     assert _bwd(ok, 10, 10, [(0, 0, 3, 3), (2, 2, 3, 3)]) == 3                # overlap
     assert _bwd(ok, 10, 10, [(0, 8, 3, 3)]) == 3                              # leaves the canvas
@@ -242,7 +267,8 @@ def test_gradients_fused_query(built_lib):
     f = L.lib().mdlstm_gradients_fused
     assert f(ctypes.byref(L.LayerDesc(32, 32, 0))) == 1    # lines: one kernel
     assert f(ctypes.byref(L.LayerDesc(64, 128, 1))) == 0   # bf16 H 128: two kernels
-    assert f(ctypes.byref(L.LayerDesc(16, 12, 0))) == -1   # not built
+    assert f(ctypes.byref(L.LayerDesc(16, 12, 0))) == f(ctypes.byref(L.LayerDesc(16, 16, 0)))  # padded to H 16
+    assert f(ctypes.byref(L.LayerDesc(16, 65, 0))) == -1   # above the largest built
     assert f(None) == -1
 
 
