@@ -14,11 +14,14 @@
 //
 // dX: A = Wx_all^T (rows = channels, from a transposed copy), B = dZ rows
 // (cells), K = 20H; a wave owns 64 cells x 64 channels.
-// dW: per direction, a workgroup owns a 128 x 128 block of [5H] x [c_in + 2H]
-// for one chunk of cells; each step stages 32 cells of dZ and of the column
-// operand in LDS transposed (cells contiguous), so that an MFMA operand is
-// one 16-byte LDS read; the next step's loads are in flight meanwhile. The
-// chunks' partial products are summed in a fixed order.
+// dW: per direction, a workgroup owns a 320 x 160 block of [5H] x [c_in + 2H]
+// for one chunk of cells. fp32 (k_dw_big): each step stages 32 cells of dZ
+// and of the column operand in LDS transposed (cells contiguous) through
+// registers, so that an MFMA operand is one 16-byte LDS read; the next
+// step's loads are in flight meanwhile. bf16 (k_dw_tr): the steps are copied
+// to LDS directly, cell-major as in memory, and the MFMA operands are read
+// with the LDS transpose read. The chunks' partial products are summed in a
+// fixed order.
 #include <algorithm>
 #include <type_traits>
 
@@ -401,6 +404,246 @@ k_dw_big(int64_t n_cells, int canvas_w, int C, int H, BigDw q, const T* __restri
     }
 }
 
+// --- dW, bf16: direct-to-LDS staging and transposed LDS reads ------------------
+// The same blocks, chunks, partial layout and XCD placement as k_dw_big, for
+// bf16 storage. Each step's 32 cells of dZ rows [r0, r0 + 320) and of the
+// column operand [c0, c0 + 160) are copied by direct global-to-LDS loads
+// (no registers, no VALU work per element) in the cell-major layout they have
+// in memory, two steps ahead into a ring of three buffers. The MFMA operands,
+// which hold eight consecutive cells of one row, come from the LDS transpose
+// read (ds_read_b64_tr_b16: within each sixteen lanes, lane 4 j + i/4 reads
+// four consecutive values at its address and lane i receives value i % 4 of
+// the reads of lanes i/4, 4 + i/4, 8 + i/4, 12 + i/4), two reads per
+// operand. The 16-byte chunks of a staged row are permuted (chunk j of cell k
+// at j ^ s(k)) so that the sixteen rows one transpose read touches fall on
+// distinct banks. Invalid cells get their dZ row zeroed once staged, and
+// predecessors outside the cell's rectangle or masked their part of the
+// column operand; the bias gradient is one more MFMA per gate-row tile with a
+// column of ones.
+namespace {
+constexpr int TR_KC = 32;                      // cells per step
+constexpr int TR_AG = BW_RB / 8, TR_BG = BW_CB / 8;  // 16-byte chunks per staged row: dZ, columns
+constexpr int TR_AI = TR_KC * TR_AG / 64;      // wave load instructions per step: dZ
+constexpr int TR_BI = TR_KC * TR_BG / 64;      //   columns
+constexpr int TR_SLOTS = 4;                    // load instructions per wave and step (the last one of the
+                                               // workgroup loads the flags, into a spare slot)
+constexpr int TR_NBUF = 3;
+static_assert(TR_AI + TR_BI + 1 <= 8 * TR_SLOTS && TR_AI + TR_BI + 1 > 8 * (TR_SLOTS - 1), "slot count");
+static_assert(TR_AG % 8 == 0 && TR_BG % 4 == 0, "chunk permutation groups");
+
+__device__ __forceinline__ int tr_sa(int k) { return 2 * (((k >> 1) & 1) | ((k >> 2) & 2)); }  // within 8 chunks
+__device__ __forceinline__ int tr_sb(int k) { return 2 * ((k >> 3) & 1); }                  // within 4 chunks
+
+typedef short tr_s4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 tr_read(const bf16_t* p) {
+    const tr_s4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) tr_s4*)(p));
+    uint2 r;
+    __builtin_memcpy(&r, &v, 8);
+    return r;
+}
+__device__ __forceinline__ bf16x8 tr_pair(uint2 lo, uint2 hi) { return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)); }
+// LDS-only barrier: no fence, so pending direct-to-LDS loads into other
+// buffers are not waited for
+__device__ __forceinline__ void tr_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+}  // namespace
+
+__global__ void __launch_bounds__(BW_THREADS)
+k_dw_tr(int64_t n_cells, int canvas_w, int C, int H, BigDw q, const bf16_t* __restrict__ dZ,
+        const bf16_t* __restrict__ X, const bf16_t* __restrict__ Y, const uint8_t* __restrict__ flags,
+        float* __restrict__ part) {
+    __shared__ __attribute__((aligned(16))) bf16_t sA[TR_NBUF][TR_KC * BW_RB];
+    __shared__ __attribute__((aligned(16))) bf16_t sB[TR_NBUF][TR_KC * BW_CB];
+    __shared__ __attribute__((aligned(16))) uint32_t sF[TR_NBUF][64];
+    __shared__ __attribute__((aligned(16))) uint32_t sink[256];
+
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int g = lane >> 4, i16 = lane & 15;
+    const int wr = wave >> 1, wc = wave & 1;
+    const int M = q.rblocks * q.cblocks, L = blockIdx.x;
+    int gi, mem;
+    if ((4 * q.chunks) % 8 == 0) {
+        const int slot = L >> 3;
+        gi = (slot / M) * 8 + (L & 7);
+        mem = slot % M;
+    } else {
+        gi = L / M;
+        mem = L % M;
+    }
+    const int rb = mem % q.rblocks, cb = mem / q.rblocks, d = gi & 3, chunk = gi >> 2;
+    const int G = q.G, N = 20 * H;
+    const int r0 = rb * BW_RB, c0 = cb * BW_CB;
+    const int64_t k_begin = (int64_t)chunk * q.chunk_cells;
+    const int64_t k_end = min(n_cells, k_begin + q.chunk_cells);
+    const int lstep = (d & 1) ? 1 : -1;
+    const int64_t tstep = (d & 2) ? canvas_w : -(int64_t)canvas_w;
+    const uint32_t lbit = (d & 1) ? 4 : 2, tbit = (d & 2) ? 16 : 8;
+    const int64_t nsteps = (k_end - k_begin + TR_KC - 1) / TR_KC;
+    const int64_t kb_last = k_begin + max(nsteps - 1, (int64_t)0) * TR_KC;  // the last step's first cell
+
+    // The lane's part of every step's loads, slot by slot: the source row
+    // base, the bytes per cell of that source, the cell shift (the left or top
+    // predecessor for the column operand's Y parts), the cell within the step,
+    // the byte offset within the source row and the LDS destination of the
+    // wave instruction. Slots 0 .. TR_AI - 1 load dZ, the next TR_BI the
+    // column operand (X, left Y, top Y by lane), then one loads the flags of
+    // the step's cells and the spare one repeats it into a sink.
+    const char* kbase[TR_SLOTS];
+    int kstride[TR_SLOTS], kshift[TR_SLOTS], kcell[TR_SLOTS], koff[TR_SLOTS];
+    char* kdst[TR_SLOTS];
+#pragma unroll
+    for (int j = 0; j < TR_SLOTS; ++j) {
+        const int sl = wave * TR_SLOTS + j;
+        kshift[j] = 0;
+        if (sl < TR_AI) {
+            const int P = sl * 64 + lane, k = P / TR_AG, pos = P - k * TR_AG, ch = pos ^ tr_sa(k);
+            kbase[j] = reinterpret_cast<const char*>(dZ);
+            kstride[j] = 2 * N;
+            kcell[j] = k;
+            koff[j] = 2 * (d * G + min(r0 + 8 * ch, G - 8));  // rows past the direction's end: any valid row
+            kdst[j] = reinterpret_cast<char*>(&sA[0][sl * 512]);
+        } else if (sl < TR_AI + TR_BI) {
+            const int P = (sl - TR_AI) * 64 + lane, k = P / TR_BG, pos = P - k * TR_BG, ch = pos ^ tr_sb(k);
+            const int col = c0 + 8 * ch;
+            kcell[j] = k;
+            kdst[j] = reinterpret_cast<char*>(&sB[0][(sl - TR_AI) * 512]);
+            if (col < C || col >= C + 2 * H) {  // X; columns past the end: any valid chunk
+                kbase[j] = reinterpret_cast<const char*>(X);
+                kstride[j] = 2 * C;
+                koff[j] = col < C ? 2 * col : 0;
+            } else {
+                const bool left = col < C + H;
+                kbase[j] = reinterpret_cast<const char*>(Y);
+                kstride[j] = 8 * H;
+                kshift[j] = left ? lstep : (int)tstep;
+                koff[j] = 2 * (d * H + col - C - (left ? 0 : H));
+            }
+        } else {
+            kbase[j] = reinterpret_cast<const char*>(flags);
+            kstride[j] = 1;
+            kcell[j] = sl == TR_AI + TR_BI ? 4 * min(lane, 7) : 0;  // flags of cells 4 l .. 4 l + 3
+            koff[j] = 0;
+            kdst[j] = sl == TR_AI + TR_BI ? reinterpret_cast<char*>(&sF[0][0]) : reinterpret_cast<char*>(&sink[0]);
+        }
+    }
+    constexpr int ABUF = TR_KC * BW_RB * 2, BBUF = TR_KC * BW_CB * 2, FBUF = 64 * 4;  // bytes per buffer
+    // loads of the step at cell kb into buffer b; cells past the chunk's end
+    // re-read its last cell (their flags read as invalid below); predecessors
+    // off the canvas read its first or last cell (masked by the flags)
+    auto issue = [&](int64_t kb, int b) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < TR_SLOTS; ++j) {
+            const int sl = wave * TR_SLOTS + j;
+            if (sl < TR_AI + TR_BI) {
+                const int64_t cell = min(kb + kcell[j], k_end - 1);
+                const int64_t src = min(max(cell + kshift[j], (int64_t)0), n_cells - 1);
+                __builtin_amdgcn_global_load_lds(kbase[j] + src * kstride[j] + koff[j],
+                                                 kdst[j] + b * (sl < TR_AI ? ABUF : BBUF), 16, 0, 0);
+            } else {
+                // the flags array is padded past the last cell, so the four
+                // bytes at any cell of a step are readable; steps past the
+                // chunk's end re-read the last step's
+                __builtin_amdgcn_global_load_lds(kbase[j] + min(kb, kb_last) + kcell[j],
+                                                 kdst[j] + (sl == TR_AI + TR_BI ? b * FBUF : 0), 4, 0, 0);
+            }
+        }
+    };
+
+    floatx4 acc[5][5], accb[5];
+#pragma unroll
+    for (int m = 0; m < 5; ++m) {
+        accb[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int n = 0; n < 5; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    // bias: waves of column block 0 and wave column 0, B = a column of ones
+    const bool do_bias = cb == 0 && wc == 0;
+    const bf16x8 ones = as_bf16x8(i16 == 0 ? make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u)
+                                           : make_uint4(0u, 0u, 0u, 0u));
+    // transposed-read addresses (elements within a buffer) of the lane: row
+    // (cell) 8 g + 4 h + (i16 >> 2), chunk of its sixteen rows or columns,
+    // half (i16 & 1) of the chunk
+    int aoff[2][5], boff[2][5];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int k = 8 * g + 4 * h + (i16 >> 2);
+#pragma unroll
+        for (int m = 0; m < 5; ++m) {
+            const int ca = (80 * wr + 16 * m) / 8 + ((i16 & 3) >> 1);
+            aoff[h][m] = k * BW_RB + 8 * (ca ^ tr_sa(k)) + 4 * (i16 & 1);
+            const int cbk = (80 * wc + 16 * m) / 8 + ((i16 & 3) >> 1);
+            boff[h][m] = k * BW_CB + 8 * (cbk ^ tr_sb(k)) + 4 * (i16 & 1);
+        }
+    }
+    // the vmcnt immediate: one step's loads of a wave stay in flight
+    constexpr int VM_ONE_STEP = 0x0f70 | TR_SLOTS;
+
+    if (nsteps > 0) {
+        issue(k_begin, 0);
+        issue(k_begin + TR_KC, 1);
+    }
+    for (int64_t st = 0; st < nsteps; ++st) {
+        const int b = (int)(st % TR_NBUF);
+        const int64_t kb = k_begin + st * TR_KC;
+        __builtin_amdgcn_s_waitcnt(VM_ONE_STEP);  // this wave's loads of step st have landed
+        tr_barrier();
+        // validity: zero the dZ rows of invalid cells (and of cells past the
+        // chunk's end), and the predecessor columns a valid cell must not see
+        {
+            const int k = tid >> 4, sub = tid & 15;
+            const uint32_t f = kb + k < k_end ? (sF[b][k >> 2] >> (8 * (k & 3))) & 0xffu : 0u;
+            const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+            if (!(f & 1)) {
+#pragma unroll
+                for (int c = sub; c < TR_AG; c += 16) *reinterpret_cast<uint4*>(&sA[b][k * BW_RB + 8 * c]) = z;
+            } else if (!(f & lbit) || !(f & tbit)) {
+#pragma unroll
+                for (int c = sub; c < TR_BG; c += 16) {
+                    const int col = c0 + 8 * (c ^ tr_sb(k));
+                    const bool hl = col >= C && col < C + H, ht = col >= C + H && col < C + 2 * H;
+                    if ((hl && !(f & lbit)) || (ht && !(f & tbit)))
+                        *reinterpret_cast<uint4*>(&sB[b][k * BW_CB + 8 * c]) = z;
+                }
+            }
+        }
+        tr_barrier();
+        issue(kb + 2 * TR_KC, (int)((st + 2) % TR_NBUF));  // past the end: re-reads the last cell, never used
+        const bf16_t* A = sA[b];
+        const bf16_t* Bm = sB[b];
+        bf16x8 bop[5];
+#pragma unroll
+        for (int n = 0; n < 5; ++n) bop[n] = tr_pair(tr_read(Bm + boff[0][n]), tr_read(Bm + boff[1][n]));
+#pragma unroll
+        for (int m = 0; m < 5; ++m) {
+            const bf16x8 aop = tr_pair(tr_read(A + aoff[0][m]), tr_read(A + aoff[1][m]));
+#pragma unroll
+            for (int n = 0; n < 5; ++n) acc[m][n] = mfma_bf16(aop, bop[n], acc[m][n]);
+            if (do_bias) accb[m] = mfma_bf16(aop, ones, accb[m]);
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // the loads issued past the last step
+
+    // partial [chunk][d][G][PP]: columns then the bias; lane (g, i16) holds
+    // rows 4 g + r of tile (m, n)
+    float* out = part + ((int64_t)chunk * 4 + d) * (int64_t)G * q.PP;
+#pragma unroll
+    for (int m = 0; m < 5; ++m) {
+#pragma unroll
+        for (int n = 0; n < 5; ++n)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = r0 + 80 * wr + 16 * m + 4 * g + r, col = c0 + 80 * wc + 16 * n + i16;
+                if (row < G && col < q.NB) out[(int64_t)row * q.PP + col] = acc[m][n][r];
+            }
+        if (do_bias && i16 == 0) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = r0 + 80 * wr + 16 * m + 4 * g + r;
+                if (row < G) out[(int64_t)row * q.PP + q.NB] = accb[m][r];
+            }
+        }
+    }
+}
+
 // Fixed-order sum of the chunk partials into dWx, dU, db.
 __global__ void k_dw_big_reduce(int C, int H, BigDw q, const float* __restrict__ part, float* __restrict__ dwx,
                                 float* __restrict__ du, float* __restrict__ db) {
@@ -421,7 +664,9 @@ __global__ void k_dw_big_reduce(int C, int H, BigDw q, const float* __restrict__
 }
 
 // --- host --------------------------------------------------------------------------
-size_t big_flags_bytes(const LayerGeom& g) { return (size_t)(g.n_cells > 0 ? g.n_cells : 1); }
+// the flags, padded past the last cell (the bf16 weight-gradient kernel reads
+// four bytes at a time)
+size_t big_flags_bytes(const LayerGeom& g) { return (size_t)(g.n_cells > 0 ? g.n_cells : 1) + 64; }
 size_t big_wxt_bytes(const LayerGeom& g) {
     return (size_t)g.c_in * 20 * g.hidden * (g.dtype == 0 ? 4 : 2);
 }
@@ -470,11 +715,9 @@ hipError_t launch_bwd_big_dw(const LayerGeom& g, const void* d_dz, const void* d
                            static_cast<const T*>(d_dz), static_cast<const T*>(d_x), static_cast<const T*>(d_y),
                            d_flags, d_part);
     } else {
-        using T = bf16_t;
-        constexpr int PD = 2;
-        hipLaunchKernelGGL((k_dw_big<T, PD>), gw, dim3(BW_THREADS), 0, s, g.n_cells, g.canvas_w, g.c_in, g.hidden, q,
-                           static_cast<const T*>(d_dz), static_cast<const T*>(d_x), static_cast<const T*>(d_y),
-                           d_flags, d_part);
+        hipLaunchKernelGGL(k_dw_tr, gw, dim3(BW_THREADS), 0, s, g.n_cells, g.canvas_w, g.c_in, g.hidden, q,
+                           static_cast<const bf16_t*>(d_dz), static_cast<const bf16_t*>(d_x),
+                           static_cast<const bf16_t*>(d_y), d_flags, d_part);
     }
     hipLaunchKernelGGL(k_dw_big_reduce, dim3(rbk), dim3(256), 0, s, g.c_in, g.hidden, q, d_part, d_dwx, d_du, d_db);
     return hipGetLastError();
