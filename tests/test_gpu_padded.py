@@ -57,6 +57,9 @@ CASES = [
     ("H3_C5", [6, 2, 11], [9, 14, 3], 24, 5, 3, "f32"),
     ("bf16_H100_C12", [20, 9], [30, 41], 80, 12, 100, "bf16"),
     ("bf16_H40_C3", [16, 5, 1], [22, 30, 2], 64, 3, 40, "bf16"),
+    # H 24 -> 32 with C 5 -> 8: the tiled gradient path with fewer gate rows
+    # (160) than a weight-gradient block holds (320)
+    ("bf16_H24_C5", [20, 9, 33], [37, 16, 8], 64, 5, 24, "bf16"),
 ]
 
 
