@@ -196,7 +196,8 @@ static BigDw big_dw(const LayerGeom& g) {
 // operand in LDS transposed (cells contiguous; a thread writes the values of
 // two adjacent cells together), so that an MFMA operand is one 16-byte LDS
 // read; the loads of the next PD steps are in flight meanwhile. The bias
-// gradient is summed from the staged dZ values in registers.
+// gradient is summed from the staged dZ values in registers. Launched for
+// fp32 storage (bf16 takes k_dw_tr below); the kernel itself handles both.
 template <typename T, int PD>
 __global__ void __launch_bounds__(BW_THREADS)
 k_dw_big(int64_t n_cells, int canvas_w, int C, int H, BigDw q, const T* __restrict__ dZ, const T* __restrict__ X,
