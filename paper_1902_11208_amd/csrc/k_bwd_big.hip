@@ -159,6 +159,214 @@ k_dx_big(int64_t n_cells, int C, int N, const T* __restrict__ dZ, const T* __res
     }
 }
 
+// --- dX, bf16: direct-to-LDS staging --------------------------------------------
+// A workgroup of four waves takes blocks of 64 cells in turn; each wave owns
+// 16 of them (one N tile) and every channel tile. The reduction over the 20H
+// gate rows runs in stages of KC (256 values, fewer for wide inputs): the
+// stage's dZ rows of the block's cells (512 contiguous bytes of each, which
+// HBM serves far better than 64- or 128-byte pieces of many rows) and the
+// WxT rows (channels, padded to a multiple of 64 with re-read rows) are
+// copied by direct global-to-LDS loads, the next stage's copy in flight
+// during the current one's MFMAs (one stream across blocks). A staged row's
+// 16-byte chunk j sits at j ^ (r & 15) within aligned groups of sixteen (of
+// eight at KC = 64), so the sixteen rows one operand read touches fall on
+// distinct banks. The dX rows of invalid cells are written as zero.
+namespace {
+constexpr int DX_CELLS = 64;
+// LDS-only barrier without a fence, so that the direct-to-LDS loads of the
+// next stage (into the other buffers) are not waited for
+__device__ __forceinline__ void dx_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// The operands of one reduction step, 1 + MT 16-byte LDS reads, issued and
+// waited for in one asm statement (MT <= 4): the compiler does not know
+// which buffer the direct loads in flight fill, and before its own LDS reads
+// it would wait for the next stage's loads as well. The values are complete
+// when the statement ends.
+template <int MT>
+__device__ __forceinline__ void dx_read_ops(uint32_t pb, const uint32_t (&pa)[MT], uint4& b, uint4 (&a)[MT]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    static_assert(MT >= 1 && MT <= 4, "batched reads up to four channel tiles");
+    if constexpr (MT == 1)
+        asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3\n\ts_waitcnt lgkmcnt(0)"
+                     : "=&v"(b), "=&v"(a[0]) : "v"(pb), "v"(pa[0]) : "memory");
+    else if constexpr (MT == 2)
+        asm volatile("ds_read_b128 %0, %3\n\tds_read_b128 %1, %4\n\tds_read_b128 %2, %5\n\ts_waitcnt lgkmcnt(0)"
+                     : "=&v"(b), "=&v"(a[0]), "=&v"(a[1]) : "v"(pb), "v"(pa[0]), "v"(pa[1]) : "memory");
+    else if constexpr (MT == 3)
+        asm volatile(
+            "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\tds_read_b128 %3, %7\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(b), "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]) : "v"(pb), "v"(pa[0]), "v"(pa[1]), "v"(pa[2])
+            : "memory");
+    else
+        asm volatile(
+            "ds_read_b128 %0, %5\n\tds_read_b128 %1, %6\n\tds_read_b128 %2, %7\n\tds_read_b128 %3, %8\n\t"
+            "ds_read_b128 %4, %9\n\ts_waitcnt lgkmcnt(0)"
+            : "=&v"(b), "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]), "=&v"(a[3])
+            : "v"(pb), "v"(pa[0]), "v"(pa[1]), "v"(pa[2]), "v"(pa[3])
+            : "memory");
+#else
+    (void)pb;
+    (void)pa;
+    b = make_uint4(0u, 0u, 0u, 0u);
+    for (int m = 0; m < MT; ++m) a[m] = b;
+#endif
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+template <int KC>
+__device__ __forceinline__ int dx_chunk(int r, int j) {
+    return j ^ (r & (KC / 8 >= 16 ? 15 : 7));
+}
+template <int MT>
+struct DxCfg {
+    static constexpr int WI = (MT * 16 + 63) / 64;           // 64-row groups of staged WxT
+    static constexpr int KC = MT <= 4 ? 256 : (MT <= 8 ? 128 : 64);
+    static constexpr int SZ = DX_CELLS * KC, SW = 64 * WI * KC;  // staged elements per buffer
+    static constexpr int ZI = SZ / 8 / 64 / 4, WLI = SW / 8 / 64 / 4;  // load instructions per wave and stage
+    static_assert(SZ % (8 * 64 * 4) == 0 && SW % (8 * 64 * 4) == 0, "whole instructions on every wave");
+};
+}  // namespace
+
+template <int MT>
+__global__ void __launch_bounds__(256)
+k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restrict__ dZ,
+        const bf16_t* __restrict__ WxT, const uint8_t* __restrict__ flags, bf16_t* __restrict__ dX) {
+    using Cf = DxCfg<MT>;
+    constexpr int KC = Cf::KC, SZ = Cf::SZ, SW = Cf::SW, ZI = Cf::ZI, WLI = Cf::WLI;
+    constexpr int RG = KC / 8;  // 16-byte chunks per staged row
+    // two buffer sets, as separate arrays so that reads of one are not
+    // ordered behind the direct loads into the other
+    __shared__ __attribute__((aligned(16))) bf16_t szA[SZ], szB[SZ];
+    __shared__ __attribute__((aligned(16))) bf16_t swA[SW], swB[SW];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int g = lane >> 4, i16 = lane & 15;
+    const int nk = N / KC;
+
+    // the lane's chunk of every stage: instruction j of the wave fills chunks
+    // (wave + 4 j) * 64 + lane of the buffer
+    int zrow[ZI], zoff[ZI], wrow[WLI], woff[WLI];
+#pragma unroll
+    for (int j = 0; j < ZI; ++j) {
+        const int P = (wave + 4 * j) * 64 + lane, r = P / RG, pos = P - r * RG;
+        zrow[j] = r;
+        zoff[j] = 8 * dx_chunk<KC>(r, pos);
+    }
+#pragma unroll
+    for (int j = 0; j < WLI; ++j) {
+        const int P = (wave + 4 * j) * 64 + lane, r = P / RG, pos = P - r * RG;
+        wrow[j] = min(r, C - 1);  // padded channels re-read the last one (results not stored)
+        woff[j] = 8 * dx_chunk<KC>(r, pos);
+    }
+    auto issue = [&](int64_t blk, int kc, bf16_t* zb, bf16_t* wb) __attribute__((always_inline)) {
+        const int64_t cell0 = blk * DX_CELLS;
+        const int k0 = kc * KC;
+#pragma unroll
+        for (int j = 0; j < ZI; ++j) {
+            const int64_t cell = min(cell0 + zrow[j], n_cells - 1);
+            __builtin_amdgcn_global_load_lds(static_cast<const void*>(dZ + cell * N + k0 + zoff[j]),
+                                             static_cast<void*>(zb + (wave + 4 * j) * 512), 16, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < WLI; ++j)
+            __builtin_amdgcn_global_load_lds(static_cast<const void*>(WxT + (int64_t)wrow[j] * N + k0 + woff[j]),
+                                             static_cast<void*>(wb + (wave + 4 * j) * 512), 16, 0, 0);
+    };
+    floatx4 acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    int64_t blk = blockIdx.x;
+    int kc = 0;
+    // one stage from buffers (zb, wb), the next one's loads into (zn, wn);
+    // false once the last stage is done
+    auto stage = [&](const bf16_t* zb, const bf16_t* wb, bf16_t* zn, bf16_t* wn) __attribute__((always_inline)) {
+        int64_t nblk = blk;
+        int nkc = kc + 1;
+        if (nkc == nk) {
+            nkc = 0;
+            nblk += gridDim.x;
+        }
+        if (nblk < n_blocks) {
+            issue(nblk, nkc, zn, wn);
+            // the next stage's loads stay in flight (vmcnt: bits 3:0 and 15:14)
+            constexpr int n = ZI + WLI;
+            static_assert(n < 64, "vmcnt range");
+            __builtin_amdgcn_s_waitcnt(0x0f70 | (n & 15) | ((n >> 4) << 14));
+        } else {
+            __builtin_amdgcn_s_waitcnt(0x0f70);
+        }
+        dx_barrier();
+        const int rz = 16 * wave + i16;
+#pragma unroll 4
+        for (int ks = 0; ks < KC / 32; ++ks) {
+            if constexpr (MT <= 4) {
+                uint32_t pa[MT];
+                uint4 bo, ao[MT];
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const int r = 16 * m + i16;
+                    pa[m] = lds_addr(&wb[r * KC + 8 * dx_chunk<KC>(r, 4 * ks + g)]);
+                }
+                dx_read_ops<MT>(lds_addr(&zb[rz * KC + 8 * dx_chunk<KC>(rz, 4 * ks + g)]), pa, bo, ao);
+#pragma unroll
+                for (int m = 0; m < MT; ++m) acc[m] = mfma_bf16(as_bf16x8(ao[m]), as_bf16x8(bo), acc[m]);
+            } else {
+                const bf16x8 bo =
+                    as_bf16x8(*reinterpret_cast<const uint4*>(&zb[rz * KC + 8 * dx_chunk<KC>(rz, 4 * ks + g)]));
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const int r = 16 * m + i16;
+                    const bf16x8 ao =
+                        as_bf16x8(*reinterpret_cast<const uint4*>(&wb[r * KC + 8 * dx_chunk<KC>(r, 4 * ks + g)]));
+                    acc[m] = mfma_bf16(ao, bo, acc[m]);
+                }
+            }
+        }
+        dx_barrier();  // every wave is done with these buffers before the next stage's issue refills them
+        if (kc == nk - 1) {
+            // lane (g, i16) holds channels 16 m + 4 g .. + 3 of cell 16 wave + i16
+            const int64_t cell = blk * DX_CELLS + 16 * wave + i16;
+            if (cell < n_cells) {
+                const bool ok = flags[cell] & 1;
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const int ch = 16 * m + 4 * g;
+                    if (ch < C) St<bf16_t>::st4(dX + cell * C + ch, ok ? acc[m] : floatx4{0.f, 0.f, 0.f, 0.f});
+                }
+            }
+#pragma unroll
+            for (int m = 0; m < MT; ++m) acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+        blk = nblk;
+        kc = nkc;
+        return blk < n_blocks;
+    };
+    if (blk < n_blocks) {
+        issue(blk, 0, szA, swA);
+        while (stage(szA, swA, szB, swB) && stage(szB, swB, szA, swA)) {
+        }
+    }
+}
+
+// false when the stage length does not divide 20H (H = 32 with c_in up to
+// 64): the caller takes k_dx_big
+template <int MT>
+static bool launch_dx_tr(const LayerGeom& g, const bf16_t* dz, const bf16_t* wxt, const uint8_t* flags, bf16_t* dx,
+                         hipStream_t s) {
+    using Cf = DxCfg<MT>;
+    if ((20 * g.hidden) % Cf::KC != 0) return false;
+    constexpr size_t lds = 2 * ((size_t)Cf::SZ + Cf::SW) * sizeof(bf16_t);
+    static_assert(lds <= 160 * 1024, "LDS of a CU");
+    const int64_t n_blocks = (g.n_cells + DX_CELLS - 1) / DX_CELLS;
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        cus = 256;
+    const int per_cu = (int)std::max<size_t>(1, (160 * 1024) / lds);
+    const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(n_blocks, (int64_t)per_cu * cus));
+    hipLaunchKernelGGL(k_dx_tr<MT>, dim3(grid), dim3(256), 0, s, g.n_cells, g.c_in, 20 * g.hidden, n_blocks, dz, wxt,
+                       flags, dx);
+    return true;
+}
+
 // --- dW --------------------------------------------------------------------------
 constexpr int BW_KC = 32;         // cells per step
 constexpr int BW_RB = 320;        // gate rows per workgroup
@@ -695,8 +903,21 @@ hipError_t launch_bwd_big_dx(const LayerGeom& g, const void* d_dz, const void* d
         using T = bf16_t;
         hipLaunchKernelGGL(k_transpose<T>, dim3(tb), dim3(256), 0, s, N, g.c_in, static_cast<const T*>(d_wx),
                            static_cast<T*>(d_wxt));
-        hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, static_cast<const T*>(d_dz),
-                           static_cast<const T*>(d_wxt), d_flags, static_cast<T*>(d_dx));
+        const T* dz = static_cast<const T*>(d_dz);
+        const T* wxt = static_cast<const T*>(d_wxt);
+        T* dx = static_cast<T*>(d_dx);
+        bool done = false;
+        switch ((g.c_in + 15) / 16) {  // channel tiles (c_in is a multiple of 8, at most 256)
+#define MDL_DX_TR(mt) \
+    case mt: done = launch_dx_tr<mt>(g, dz, wxt, d_flags, dx, s); break;
+            MDL_DX_TR(1) MDL_DX_TR(2) MDL_DX_TR(3) MDL_DX_TR(4) MDL_DX_TR(5) MDL_DX_TR(6) MDL_DX_TR(7) MDL_DX_TR(8)
+            MDL_DX_TR(9) MDL_DX_TR(10) MDL_DX_TR(11) MDL_DX_TR(12) MDL_DX_TR(13) MDL_DX_TR(14) MDL_DX_TR(15)
+            MDL_DX_TR(16)
+#undef MDL_DX_TR
+            default: return hipErrorInvalidValue;
+        }
+        if (!done)
+            hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, dz, wxt, d_flags, dx);
     }
     return hipGetLastError();
 }
