@@ -212,6 +212,17 @@ __device__ __forceinline__ void dx_read_ops(uint32_t pb, const uint32_t (&pa)[MT
 #endif
 }
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+// one dword LDS read, complete when the statement ends (as above)
+__device__ __forceinline__ uint32_t dx_read_u32(uint32_t p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    uint32_t v;
+    asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=&v"(v) : "v"(p) : "memory");
+    return v;
+#else
+    (void)p;
+    return 0u;
+#endif
+}
 template <int KC>
 __device__ __forceinline__ int dx_chunk(int r, int j) {
     return j ^ (r & (KC / 8 >= 16 ? 15 : 7));
@@ -237,6 +248,8 @@ k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restric
     // ordered behind the direct loads into the other
     __shared__ __attribute__((aligned(16))) bf16_t szA[SZ], szB[SZ];
     __shared__ __attribute__((aligned(16))) bf16_t swA[SW], swB[SW];
+    // per wave: the flag bytes of its sixteen cells in the first four dwords
+    __shared__ __attribute__((aligned(16))) uint32_t sfA[4 * 64], sfB[4 * 64];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int g = lane >> 4, i16 = lane & 15;
     const int nk = N / KC;
@@ -256,9 +269,14 @@ k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restric
         wrow[j] = min(r, C - 1);  // padded channels re-read the last one (results not stored)
         woff[j] = 8 * dx_chunk<KC>(r, pos);
     }
-    auto issue = [&](int64_t blk, int kc, bf16_t* zb, bf16_t* wb) __attribute__((always_inline)) {
+    auto issue = [&](int64_t blk, int kc, bf16_t* zb, bf16_t* wb, uint32_t* fb) __attribute__((always_inline)) {
         const int64_t cell0 = blk * DX_CELLS;
         const int k0 = kc * KC;
+        // flags of the wave's cells, four per lane in lanes 0-3 (the array is
+        // padded past the last cell; every stage loads them, so that every
+        // stage has the same loads)
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(flags + cell0 + 16 * wave + 4 * min(lane, 3)),
+                                         static_cast<void*>(fb + wave * 64), 4, 0, 0);
 #pragma unroll
         for (int j = 0; j < ZI; ++j) {
             const int64_t cell = min(cell0 + zrow[j], n_cells - 1);
@@ -278,7 +296,8 @@ k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restric
     int kc = 0;
     // one stage from buffers (zb, wb), the next one's loads into (zn, wn);
     // false once the last stage is done
-    auto stage = [&](const bf16_t* zb, const bf16_t* wb, bf16_t* zn, bf16_t* wn) __attribute__((always_inline)) {
+    auto stage = [&](const bf16_t* zb, const bf16_t* wb, const uint32_t* fb, bf16_t* zn, bf16_t* wn, uint32_t* fn)
+                     __attribute__((always_inline)) {
         int64_t nblk = blk;
         int nkc = kc + 1;
         if (nkc == nk) {
@@ -286,9 +305,9 @@ k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restric
             nblk += gridDim.x;
         }
         if (nblk < n_blocks) {
-            issue(nblk, nkc, zn, wn);
+            issue(nblk, nkc, zn, wn, fn);
             // the next stage's loads stay in flight (vmcnt: bits 3:0 and 15:14)
-            constexpr int n = ZI + WLI;
+            constexpr int n = ZI + WLI + 1;
             static_assert(n < 64, "vmcnt range");
             __builtin_amdgcn_s_waitcnt(0x0f70 | (n & 15) | ((n >> 4) << 14));
         } else {
@@ -323,10 +342,12 @@ k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restric
         }
         dx_barrier();  // every wave is done with these buffers before the next stage's issue refills them
         if (kc == nk - 1) {
-            // lane (g, i16) holds channels 16 m + 4 g .. + 3 of cell 16 wave + i16
+            // lane (g, i16) holds channels 16 m + 4 g .. + 3 of cell 16 wave + i16;
+            // the wave's sixteen flag bytes were staged with the stage's loads
             const int64_t cell = blk * DX_CELLS + 16 * wave + i16;
+            const uint32_t fw = dx_read_u32(lds_addr(&fb[wave * 64 + (i16 >> 2)]));
             if (cell < n_cells) {
-                const bool ok = flags[cell] & 1;
+                const bool ok = (fw >> (8 * (i16 & 3))) & 1;
 #pragma unroll
                 for (int m = 0; m < MT; ++m) {
                     const int ch = 16 * m + 4 * g;
@@ -341,8 +362,8 @@ k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restric
         return blk < n_blocks;
     };
     if (blk < n_blocks) {
-        issue(blk, 0, szA, swA);
-        while (stage(szA, swA, szB, swB) && stage(szB, swB, szA, swA)) {
+        issue(blk, 0, szA, swA, sfA);
+        while (stage(szA, swA, sfA, szB, swB, sfB) && stage(szB, swB, sfB, szA, swA, sfA)) {
         }
     }
 }
