@@ -160,11 +160,12 @@ k_dx_big(int64_t n_cells, int C, int N, const T* __restrict__ dZ, const T* __res
 }
 
 // --- dX, bf16: direct-to-LDS staging --------------------------------------------
-// A workgroup of four waves takes blocks of 64 cells in turn; each wave owns
-// 16 of them (one N tile) and every channel tile. The reduction over the 20H
-// gate rows runs in stages of KC (256 values, fewer for wide inputs): the
-// stage's dZ rows of the block's cells (512 contiguous bytes of each, which
-// HBM serves far better than 64- or 128-byte pieces of many rows) and the
+// A workgroup of eight waves takes blocks of 128 cells in turn; each wave
+// owns 16 of them (one N tile) and every channel tile, so that one staged
+// copy of the WxT rows serves 128 cells. The reduction over the 20H gate rows
+// runs in stages of KC (128 values, 64 for inputs wider than 128): the
+// stage's dZ rows of the block's cells (256 contiguous bytes of each; HBM
+// serves such runs far better than 64-byte pieces of many rows) and the
 // WxT rows (channels, padded to a multiple of 64 with re-read rows) are
 // copied by direct global-to-LDS loads, the next stage's copy in flight
 // during the current one's MFMAs (one stream across blocks). A staged row's
@@ -172,7 +173,8 @@ k_dx_big(int64_t n_cells, int C, int N, const T* __restrict__ dZ, const T* __res
 // eight at KC = 64), so the sixteen rows one operand read touches fall on
 // distinct banks. The dX rows of invalid cells are written as zero.
 namespace {
-constexpr int DX_CELLS = 64;
+constexpr int DX_CELLS = 128;
+constexpr int NWV = DX_CELLS / 16;
 // LDS-only barrier without a fence, so that the direct-to-LDS loads of the
 // next stage (into the other buffers) are not waited for
 __device__ __forceinline__ void dx_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
@@ -230,15 +232,15 @@ __device__ __forceinline__ int dx_chunk(int r, int j) {
 template <int MT>
 struct DxCfg {
     static constexpr int WI = (MT * 16 + 63) / 64;           // 64-row groups of staged WxT
-    static constexpr int KC = MT <= 4 ? 256 : (MT <= 8 ? 128 : 64);
+    static constexpr int KC = MT <= 8 ? 128 : 64;
     static constexpr int SZ = DX_CELLS * KC, SW = 64 * WI * KC;  // staged elements per buffer
-    static constexpr int ZI = SZ / 8 / 64 / 4, WLI = SW / 8 / 64 / 4;  // load instructions per wave and stage
-    static_assert(SZ % (8 * 64 * 4) == 0 && SW % (8 * 64 * 4) == 0, "whole instructions on every wave");
+    static constexpr int ZI = SZ / 8 / 64 / NWV, WLI = SW / 8 / 64 / NWV;  // load instructions per wave and stage
+    static_assert(SZ % (8 * 64 * NWV) == 0 && SW % (8 * 64 * NWV) == 0, "whole instructions on every wave");
 };
 }  // namespace
 
 template <int MT>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(64 * NWV)
 k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restrict__ dZ,
         const bf16_t* __restrict__ WxT, const uint8_t* __restrict__ flags, bf16_t* __restrict__ dX) {
     using Cf = DxCfg<MT>;
@@ -249,7 +251,7 @@ k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restric
     __shared__ __attribute__((aligned(16))) bf16_t szA[SZ], szB[SZ];
     __shared__ __attribute__((aligned(16))) bf16_t swA[SW], swB[SW];
     // per wave: the flag bytes of its sixteen cells in the first four dwords
-    __shared__ __attribute__((aligned(16))) uint32_t sfA[4 * 64], sfB[4 * 64];
+    __shared__ __attribute__((aligned(16))) uint32_t sfA[NWV * 64], sfB[NWV * 64];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int g = lane >> 4, i16 = lane & 15;
     const int nk = N / KC;
@@ -259,13 +261,13 @@ k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restric
     int zrow[ZI], zoff[ZI], wrow[WLI], woff[WLI];
 #pragma unroll
     for (int j = 0; j < ZI; ++j) {
-        const int P = (wave + 4 * j) * 64 + lane, r = P / RG, pos = P - r * RG;
+        const int P = (wave + NWV * j) * 64 + lane, r = P / RG, pos = P - r * RG;
         zrow[j] = r;
         zoff[j] = 8 * dx_chunk<KC>(r, pos);
     }
 #pragma unroll
     for (int j = 0; j < WLI; ++j) {
-        const int P = (wave + 4 * j) * 64 + lane, r = P / RG, pos = P - r * RG;
+        const int P = (wave + NWV * j) * 64 + lane, r = P / RG, pos = P - r * RG;
         wrow[j] = min(r, C - 1);  // padded channels re-read the last one (results not stored)
         woff[j] = 8 * dx_chunk<KC>(r, pos);
     }
@@ -281,12 +283,12 @@ k_dx_tr(int64_t n_cells, int C, int N, int64_t n_blocks, const bf16_t* __restric
         for (int j = 0; j < ZI; ++j) {
             const int64_t cell = min(cell0 + zrow[j], n_cells - 1);
             __builtin_amdgcn_global_load_lds(static_cast<const void*>(dZ + cell * N + k0 + zoff[j]),
-                                             static_cast<void*>(zb + (wave + 4 * j) * 512), 16, 0, 0);
+                                             static_cast<void*>(zb + (wave + NWV * j) * 512), 16, 0, 0);
         }
 #pragma unroll
         for (int j = 0; j < WLI; ++j)
             __builtin_amdgcn_global_load_lds(static_cast<const void*>(WxT + (int64_t)wrow[j] * N + k0 + woff[j]),
-                                             static_cast<void*>(wb + (wave + 4 * j) * 512), 16, 0, 0);
+                                             static_cast<void*>(wb + (wave + NWV * j) * 512), 16, 0, 0);
     };
     floatx4 acc[MT];
 #pragma unroll
@@ -383,7 +385,7 @@ static bool launch_dx_tr(const LayerGeom& g, const bf16_t* dz, const bf16_t* wxt
         cus = 256;
     const int per_cu = (int)std::max<size_t>(1, (160 * 1024) / lds);
     const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(n_blocks, (int64_t)per_cu * cus));
-    hipLaunchKernelGGL(k_dx_tr<MT>, dim3(grid), dim3(256), 0, s, g.n_cells, g.c_in, 20 * g.hidden, n_blocks, dz, wxt,
+    hipLaunchKernelGGL(k_dx_tr<MT>, dim3(grid), dim3(64 * NWV), 0, s, g.n_cells, g.c_in, 20 * g.hidden, n_blocks, dz, wxt,
                        flags, dx);
     return true;
 }
@@ -894,9 +896,12 @@ __global__ void k_dw_big_reduce(int C, int H, BigDw q, const float* __restrict__
 }
 
 // --- host --------------------------------------------------------------------------
-// the flags, padded past the last cell (the bf16 weight-gradient kernel reads
-// four bytes at a time)
-size_t big_flags_bytes(const LayerGeom& g) { return (size_t)(g.n_cells > 0 ? g.n_cells : 1) + 64; }
+// the flags, padded past the last cell: the bf16 input-gradient kernel loads
+// the flags of a whole block of DX_CELLS cells from the block's first cell
+// (last block: up to n_cells - 1 + DX_CELLS), the bf16 weight-gradient
+// kernel those of TR_KC cells from any step's first cell
+static_assert(DX_CELLS >= TR_KC, "flag padding covers both kernels");
+size_t big_flags_bytes(const LayerGeom& g) { return (size_t)(g.n_cells > 0 ? g.n_cells : 1) + DX_CELLS; }
 size_t big_wxt_bytes(const LayerGeom& g) {
     return (size_t)g.c_in * 20 * g.hidden * (g.dtype == 0 ? 4 : 2);
 }
