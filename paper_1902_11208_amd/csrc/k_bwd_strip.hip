@@ -482,11 +482,13 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
     constexpr int TC = Dc::TC, HW = Dc::HW, N = Dc::N, G = Dc::G, NW = Dc::NW, NTH = Dc::THREADS;
     constexpr int RTW = Cf::RTW, WPD = Cf::WPD, CT = Cf::CT, CXT = Cf::CXT, XP = Cf::XP;
     static_assert(TC == Cf::TC && NTH == Cf::THREADS, "same strips and waves as the staged kernel");
-    static_assert(4 * TC * XP <= 3 * HW * 4 * H, "dX partials fit in a buffer's Y rows");
     __shared__ __attribute__((aligned(16))) float zA[TC * N], zB[TC * N];
     __shared__ __attribute__((aligned(16))) float yA[3 * HW * 4 * H], yB[3 * HW * 4 * H];
     __shared__ __attribute__((aligned(16))) float xA[TC * C], xB[TC * C];
     __shared__ __attribute__((aligned(16))) int32_t vA[64], vB[64];
+    // the four directions' dX partials of a strip, summed at the next strip's
+    // first barrier (so a strip needs two barriers)
+    __shared__ __attribute__((aligned(16))) float sdx[4][TC][XP];
     static_assert(3 * HW <= 64, "the halo's ids fill one 256-byte load instruction");
 
     const int tid = threadIdx.x;
@@ -556,13 +558,34 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
         }
     };
 
-    auto process = [&](int strip, float* zb, float* yb, float* xb, int32_t* vb, float* zn, float* yn, float* xn,
-                       int32_t* vn) __attribute__((always_inline)) {
+    // dX of a strip: the sum of its four direction partials, in a fixed order
+    auto dx_sum = [&](int strip) __attribute__((always_inline)) {
+        int cy, cx0, len;
+        int64_t p0;
+        strip_pos(strip, cy, cx0, len, p0);
+        constexpr int NXS = TC * C / 4, PXS = (NXS + NTH - 1) / NTH;
+#pragma unroll
+        for (int k = 0; k < PXS; ++k) {
+            const int e = min(tid + k * NTH, NXS - 1);
+            const int c = min(e / (C / 4), len - 1), k4 = 4 * (e - (e / (C / 4)) * (C / 4));
+            const float4 a0 = *reinterpret_cast<const float4*>(&sdx[0][c][k4]);
+            const float4 a1 = *reinterpret_cast<const float4*>(&sdx[1][c][k4]);
+            const float4 a2 = *reinterpret_cast<const float4*>(&sdx[2][c][k4]);
+            const float4 a3 = *reinterpret_cast<const float4*>(&sdx[3][c][k4]);
+            *reinterpret_cast<float4*>(dX + (p0 + c) * C + k4) =
+                make_float4(((a0.x + a1.x) + a2.x) + a3.x, ((a0.y + a1.y) + a2.y) + a3.y,
+                            ((a0.z + a1.z) + a2.z) + a3.z, ((a0.w + a1.w) + a2.w) + a3.w);
+        }
+    };
+
+    auto process = [&](int strip, int prev, float* zb, float* yb, float* xb, int32_t* vb, float* zn, float* yn,
+                       float* xn, int32_t* vn) __attribute__((always_inline)) {
         int cy, cx0, len;
         int64_t p0;
         strip_pos(strip, cy, cx0, len, p0);
         __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's copies into zb, yb, xb, vb have landed
-        lds_barrier();
+        lds_barrier();  // also: every wave's dX partials of the previous strip are in sdx
+        if (prev >= 0) dx_sum(prev);  // before the next barrier, after which this strip's partials overwrite sdx
         // validity folded into the staged data (as in the staged kernel): a
         // cell is valid with a nonnegative id, a predecessor counts when it is
         // on the canvas and has the cell's id
@@ -645,8 +668,8 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
             }
             axs[cc] = ax;
         }
-        lds_barrier();  // every wave is done reading this buffer's Y rows
-        auto sdx = reinterpret_cast<float(*)[TC][XP]>(yb);
+        // every wave read the previous strip's partials before the second
+        // barrier above
 #pragma unroll
         for (int cc = 0; cc < CXW; ++cc) {
             const int ct = rslice + cc * WPD;
@@ -655,30 +678,22 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
                 for (int r = 0; r < 4; ++r) sdx[d][i16][ct * 16 + 4 * g + r] = axs[cc][r];
             }
         }
-        lds_barrier();
-        constexpr int NXS = TC * C / 4, PXS = (NXS + NTH - 1) / NTH;
-#pragma unroll
-        for (int k = 0; k < PXS; ++k) {
-            const int e = min(tid + k * NTH, NXS - 1);
-            const int c = min(e / (C / 4), len - 1), k4 = 4 * (e - (e / (C / 4)) * (C / 4));
-            const float4 a0 = *reinterpret_cast<const float4*>(&sdx[0][c][k4]);
-            const float4 a1 = *reinterpret_cast<const float4*>(&sdx[1][c][k4]);
-            const float4 a2 = *reinterpret_cast<const float4*>(&sdx[2][c][k4]);
-            const float4 a3 = *reinterpret_cast<const float4*>(&sdx[3][c][k4]);
-            *reinterpret_cast<float4*>(dX + (p0 + c) * C + k4) =
-                make_float4(((a0.x + a1.x) + a2.x) + a3.x, ((a0.y + a1.y) + a2.y) + a3.y,
-                            ((a0.z + a1.z) + a2.z) + a3.z, ((a0.w + a1.w) + a2.w) + a3.w);
-        }
     };
 
-    int strip = blockIdx.x;
+    int strip = blockIdx.x, prev = -1;
     if (strip < n_strips) copy_in(strip, zA, yA, xA, vA);
     while (strip < n_strips) {
-        process(strip, zA, yA, xA, vA, zB, yB, xB, vB);
+        process(strip, prev, zA, yA, xA, vA, zB, yB, xB, vB);
+        prev = strip;
         strip += gridDim.x;
         if (strip >= n_strips) break;
-        process(strip, zB, yB, xB, vB, zA, yA, xA, vA);
+        process(strip, prev, zB, yB, xB, vB, zA, yA, xA, vA);
+        prev = strip;
         strip += gridDim.x;
+    }
+    if (prev >= 0) {
+        lds_barrier();
+        dx_sum(prev);
     }
 
     float* out = part + ((int64_t)blockIdx.x * 4 + d) * (Cf::RT * 16) * Cf::PP;
