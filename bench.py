@@ -239,23 +239,28 @@ class Run:
 
         Recording an event costs the stream a few microseconds, so the timed
         region records only the step boundaries and the two boundaries of the
-        dominant kernel (chosen from the last warm-up step, which records all
-        eight); the full phase breakdown comes from a second pass of the same
-        number of steps after it. The dominant kernel's duration in the
-        returned phases is the one measured in the timed region.
+        dominant kernel (chosen from the mean phase times of the last warm-up
+        steps, up to three, which record all eight); the full phase breakdown
+        comes from a second pass of the same number of steps after it. The
+        dominant kernel's duration in the returned phases is the one measured
+        in the timed region.
         """
         torch = self.torch
         from paper_1902_11208_amd import _lib
 
         L = _lib.lib()
-        for _ in range(max(warmup - 1, 0)):
+        n_rec = max(1, min(warmup, 3))
+        for _ in range(max(warmup - n_rec, 0)):
             self.step()
-        last_warm = _events(torch, 8)
-        torch.cuda.synchronize()
-        _lib.check(L.mdlstm_set_phase_events(8, _handles(last_warm)))
-        self.step()
-        torch.cuda.synchronize()
-        warm = {n: last_warm[a].elapsed_time(last_warm[b]) for n, a, b in self.phases}
+        warm = {n: 0.0 for n, _, _ in self.phases}
+        for _ in range(n_rec):
+            ev = _events(torch, 8)
+            torch.cuda.synchronize()
+            _lib.check(L.mdlstm_set_phase_events(8, _handles(ev)))
+            self.step()
+            torch.cuda.synchronize()
+            for n, a, b in self.phases:
+                warm[n] += ev[a].elapsed_time(ev[b]) / n_rec
         dom = max(warm, key=lambda k: warm[k])
         da, db = next((a, b) for n, a, b in self.phases if n == dom)
 
