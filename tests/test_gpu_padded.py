@@ -60,6 +60,14 @@ CASES = [
     # H 24 -> 32 with C 5 -> 8: the tiled gradient path with fewer gate rows
     # (160) than a weight-gradient block holds (320)
     ("bf16_H24_C5", [20, 9, 33], [37, 16, 8], 64, 5, 24, "bf16"),
+    # wide inputs: the input-gradient kernel with more than four channel tiles
+    # (two or four 64-row groups of WxT, stages of 128 and 64 gate rows) and
+    # weight-gradient blocks over three and four column blocks
+    ("bf16_H64_C96", [17, 6], [23, 40], 64, 96, 64, "bf16"),
+    ("bf16_H30_C200", [9, 14, 3], [26, 11, 30], 64, 200, 30, "bf16"),
+    ("bf16_H128_C256", [12, 5], [19, 24], 48, 256, 128, "bf16"),
+    ("H16_C150", [10, 17], [25, 12], 48, 150, 16, "f32"),
+    ("H64_C256", [9, 4], [14, 22], 32, 256, 64, "f32"),
 ]
 
 
