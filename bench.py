@@ -239,29 +239,28 @@ class Run:
 
         Recording an event costs the stream a few microseconds, so the timed
         region records only the step boundaries and the two boundaries of the
-        dominant kernel (chosen from the mean phase times of the last warm-up
-        steps, up to three, which record all eight); the full phase breakdown
-        comes from a second pass of the same number of steps after it. The
-        dominant kernel's duration in the returned phases is the one measured
-        in the timed region.
+        dominant kernel. A phase pass of the same number of steps before it
+        records all eight boundaries: it gives the per-phase breakdown and
+        picks the dominant kernel (the longest mean phase). The dominant
+        kernel's duration in the returned phases is the one measured in the
+        timed region.
         """
         torch = self.torch
         from paper_1902_11208_amd import _lib
 
         L = _lib.lib()
-        n_rec = max(1, min(warmup, 3))
-        for _ in range(max(warmup - n_rec, 0)):
+        for _ in range(warmup):
             self.step()
-        warm = {n: 0.0 for n, _, _ in self.phases}
-        for _ in range(n_rec):
-            ev = _events(torch, 8)
-            torch.cuda.synchronize()
-            _lib.check(L.mdlstm_set_phase_events(8, _handles(ev)))
+
+        evs = [_events(torch, 8) for _ in range(steps)]
+        torch.cuda.synchronize()
+        for k in range(steps):
+            _lib.check(L.mdlstm_set_phase_events(8, _handles(evs[k])))
             self.step()
-            torch.cuda.synchronize()
-            for n, a, b in self.phases:
-                warm[n] += ev[a].elapsed_time(ev[b]) / n_rec
-        dom = max(warm, key=lambda k: warm[k])
+        torch.cuda.synchronize()
+        phase = {n: float(np.mean([evs[k][a].elapsed_time(evs[k][b]) for k in range(steps)]))
+                 for n, a, b in self.phases}
+        dom = max(phase, key=lambda k: phase[k])
         da, db = next((a, b) for n, a, b in self.phases if n == dom)
 
         marks = _events(torch, steps + 1)
@@ -275,20 +274,10 @@ class Run:
         marks[steps].record()
         torch.cuda.synchronize()
         wall_ms = (time.perf_counter() - t0) * 1e3
+        _lib.check(L.mdlstm_set_phase_events(0, None))
         ev_ms = marks[0].elapsed_time(marks[steps])
         per_step = [marks[k].elapsed_time(marks[k + 1]) for k in range(steps)]
-        dom_ms = float(np.mean([dev[k][da].elapsed_time(dev[k][db]) for k in range(steps)]))
-
-        evs = [_events(torch, 8) for _ in range(steps)]
-        torch.cuda.synchronize()
-        for k in range(steps):
-            _lib.check(L.mdlstm_set_phase_events(8, _handles(evs[k])))
-            self.step()
-        torch.cuda.synchronize()
-        _lib.check(L.mdlstm_set_phase_events(0, None))
-        phase = {n: float(np.mean([evs[k][a].elapsed_time(evs[k][b]) for k in range(steps)]))
-                 for n, a, b in self.phases}
-        phase[dom] = dom_ms
+        phase[dom] = float(np.mean([dev[k][da].elapsed_time(dev[k][db]) for k in range(steps)]))
         return ev_ms / steps, wall_ms / steps, phase, per_step, dom
 
     def time_stepwise_forward(self, steps: int, warmup: int) -> float:
