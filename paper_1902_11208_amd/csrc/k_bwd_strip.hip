@@ -474,9 +474,10 @@ __device__ __forceinline__ int zswz(int cell, int f) {  // LDS float index of dZ
 
 template <int H, int C>
 __global__ void __launch_bounds__((DmaCfg<H, C>::THREADS))
-k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float* __restrict__ dZ,
-                const float* __restrict__ X, const float* __restrict__ Y, const float* __restrict__ Wx,
-                const int32_t* __restrict__ vid, float* __restrict__ dX, float* __restrict__ part) {
+k_bwd_strip_dma(int canvas_h, int canvas_w, int segs, const int32_t* list,
+                const float* __restrict__ dZ, const float* __restrict__ X, const float* __restrict__ Y,
+                const float* __restrict__ Wx, const int32_t* __restrict__ vid, float* __restrict__ dX,
+                float* __restrict__ part) {
     using Cf = StripCfg<H, C>;
     using Dc = DmaCfg<H, C>;
     constexpr int TC = Dc::TC, HW = Dc::HW, N = Dc::N, G = Dc::G, NW = Dc::NW, NTH = Dc::THREADS;
@@ -578,8 +579,26 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
         }
     };
 
-    auto process = [&](int strip, int prev, float* zb, float* yb, float* xb, int32_t* vb, float* zn, float* yn,
-                       float* xn, int32_t* vn) __attribute__((always_inline)) {
+    // The strips with a valid cell, in increasing order after their count
+    // (the others hold none: their dX rows were zeroed with the ids); this
+    // workgroup takes every gridDim.x-th of them. Entries are read one strip
+    // ahead with vector loads, and made uniform only after the next strip's
+    // wait (a read right after the load would wait for the copies issued
+    // before it).
+    auto ld = [&](int64_t k) { return __hip_atomic_load(list + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+    auto uni = [](int v) { return __builtin_amdgcn_readfirstlane(v); };
+    const int n_live = uni(ld(0)), wg = (int)blockIdx.x, nwg = (int)gridDim.x;
+    const int n_my = n_live > wg ? (n_live - wg + nwg - 1) / nwg : 0;
+    auto entry_raw = [&](int k) { return ld(1 + wg + (int64_t)(k - 1) * nwg); };  // k = 1 .. n_my
+
+    // strip: the strip to compute (its copies in zb, yb, xb, vb); next_raw:
+    // the loaded entry of the strip whose copies start here into the other
+    // buffers (-1: none), returned uniform in next; prev: the strip before,
+    // whose dX partials are summed here; ahead: the list position read here
+    // (the strip after next), its raw entry returned in after_next
+    auto process = [&](int strip, int next_raw, int& next, int prev, int ahead, int& after_next, float* zb,
+                       float* yb, float* xb, int32_t* vb, float* zn, float* yn, float* xn,
+                       int32_t* vn) __attribute__((always_inline)) {
         int cy, cx0, len;
         int64_t p0;
         strip_pos(strip, cy, cx0, len, p0);
@@ -612,9 +631,10 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
                     st_f4(&yb[(row * HW + k) * (4 * H) + dd * H + j], make_float4(0.f, 0.f, 0.f, 0.f));
             }
         }
-        const int next = strip + (int)gridDim.x;
         lds_barrier();
-        if (next < n_strips) copy_in(next, zn, yn, xn, vn);  // the other buffers: free since the last barrier
+        next = uni(next_raw);
+        if (next >= 0) copy_in(next, zn, yn, xn, vn);  // the other buffers: free since the last barrier
+        after_next = ahead <= n_my ? entry_raw(ahead) : -1;  // waited for with the next strip's copies
 
         // dW (K = the strip's cells, four per MFMA step, slot g = cell 16 (ks / 4) + 4 g + ks % 4);
         // a strip without a valid cell (separator rows, row slack) adds
@@ -680,16 +700,22 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int n_strips, int segs, const float*
         }
     };
 
-    int strip = blockIdx.x, prev = -1;
-    if (strip < n_strips) copy_in(strip, zA, yA, xA, vA);
-    while (strip < n_strips) {
-        process(strip, prev, zA, yA, xA, vA, zB, yB, xB, vB);
+    // list position k + 1 holds the k-th strip
+    int strip = n_my > 0 ? uni(entry_raw(1)) : -1, next_raw = n_my > 1 ? entry_raw(2) : -1, prev = -1, k = 0;
+    if (strip >= 0) copy_in(strip, zA, yA, xA, vA);
+    while (strip >= 0) {
+        int next = -1, an = -1;
+        process(strip, next_raw, next, prev, k + 3, an, zA, yA, xA, vA, zB, yB, xB, vB);
         prev = strip;
-        strip += gridDim.x;
-        if (strip >= n_strips) break;
-        process(strip, prev, zB, yB, xB, vB, zA, yA, xA, vA);
+        strip = next;
+        next_raw = an;
+        ++k;
+        if (strip < 0) break;
+        process(strip, next_raw, next, prev, k + 3, an, zB, yB, xB, vB, zA, yA, xA, vA);
         prev = strip;
-        strip += gridDim.x;
+        strip = next;
+        next_raw = an;
+        ++k;
     }
     if (prev >= 0) {
         lds_barrier();
@@ -796,12 +822,65 @@ size_t strip_partial_bytes(const LayerGeom& g) {
     return (size_t)strip_wgs(g) * 4 * RT * 16 * strip_pp(g) * sizeof(float);
 }
 
-// Validity id of every canvas cell: its rectangle id where the cell is
-// inside a rectangle and unmasked, else -1.
-__global__ void k_valid_ids(int64_t n_cells, const uint8_t* __restrict__ mask, const int32_t* __restrict__ rid,
-                            int32_t* __restrict__ vid) {
-    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n_cells; p += (int64_t)gridDim.x * blockDim.x)
-        vid[p] = (mask[p] && rid[p] >= 0) ? rid[p] : -1;
+// Validity id of every canvas cell (its rectangle id where the cell is inside
+// a rectangle and unmasked, else -1), a thread per (strip of TC cells, cell),
+// plus a byte
+// per strip that says whether it holds a valid cell; the dX rows of the
+// strips without one are zeroed here (the strip kernel skips them).
+template <int TC>
+__global__ void k_valid_ids_strips(int canvas_h, int canvas_w, int segs, int C, const uint8_t* __restrict__ mask,
+                                   const int32_t* __restrict__ rid, int32_t* __restrict__ vid,
+                                   uint8_t* __restrict__ live, float* __restrict__ dX) {
+    static_assert(64 % TC == 0, "strips within a wave");
+    const int64_t n_strips = (int64_t)canvas_h * segs;
+    const int64_t total = (n_strips * TC + 63) / 64 * 64;  // whole waves: every lane takes part in the ballot
+    const int lane = threadIdx.x & 63;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t strip = i / TC;
+        const int j = (int)(i - strip * TC);
+        const int cy = (int)(strip / segs), x = (int)(strip - (int64_t)cy * segs) * TC + j;
+        const bool in = strip < n_strips && x < canvas_w;
+        const int64_t p = (int64_t)cy * canvas_w + x;
+        int32_t v = -1;
+        if (in) {
+            v = (mask[p] && rid[p] >= 0) ? rid[p] : -1;
+            vid[p] = v;
+        }
+        const uint64_t b = __ballot(v >= 0);
+        const bool any = ((b >> (lane & ~(TC - 1))) & ((1ull << TC) - 1)) != 0;
+        if (in && j == 0) live[strip] = any ? 1 : 0;
+        if (in && !any)
+            for (int c = 0; c < C; c += 4) *reinterpret_cast<float4*>(dX + p * C + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+}
+
+// The list of strips with a valid cell, in increasing order: a count per
+// chunk of STRIP_CHUNKS equal chunks (one wave each), then each chunk writes
+// its strips after the counts of the chunks before it; list[0] is the total.
+constexpr int STRIP_CHUNKS = 256;
+__global__ void k_strip_counts(int64_t n_strips, const uint8_t* __restrict__ live, int32_t* __restrict__ counts) {
+    const int c = blockIdx.x, lane = threadIdx.x & 63;
+    const int64_t per = (n_strips + STRIP_CHUNKS - 1) / STRIP_CHUNKS, b0 = c * per, b1 = min(n_strips, b0 + per);
+    int n = 0;
+    for (int64_t k = b0 + lane; k < b1; k += 64) n += live[k] ? 1 : 0;
+    for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o);
+    if (lane == 0) counts[c] = n;
+}
+__global__ void k_strip_compact(int64_t n_strips, const uint8_t* __restrict__ live,
+                                const int32_t* __restrict__ counts, int32_t* __restrict__ list) {
+    const int c = blockIdx.x, lane = threadIdx.x & 63;
+    const int64_t per = (n_strips + STRIP_CHUNKS - 1) / STRIP_CHUNKS, b0 = c * per, b1 = min(n_strips, b0 + per);
+    int off = 0;
+    for (int k = lane; k < c; k += 64) off += counts[k];
+    for (int o = 32; o > 0; o >>= 1) off += __shfl_xor(off, o);
+    if (c == STRIP_CHUNKS - 1 && lane == 0) list[0] = off + counts[c];
+    for (int64_t k0 = b0; k0 < b1; k0 += 64) {
+        const int64_t k = k0 + lane;
+        const bool lv = k < b1 && live[k];
+        const uint64_t b = __ballot(lv);
+        if (lv) list[1 + off + __popcll(b & ((1ull << lane) - 1))] = (int32_t)k;
+        off += __popcll(b);
+    }
 }
 
 // fp32 storage at H = 32 takes the direct-to-LDS kernel, the other shapes
@@ -811,12 +890,19 @@ static void launch_strip_shape(const LayerGeom& g, int nwg, int n_strips, int se
                                const void* d_y, const void* d_wx, const uint8_t* d_mask, const int32_t* d_rid,
                                int32_t* d_vid, void* d_dx, float* d_part, hipStream_t s) {
     if constexpr (std::is_same<T, float>::value && H == 32) {
-        const int vb = (int)std::min<int64_t>((g.n_cells + 255) / 256, 4096);
-        hipLaunchKernelGGL(k_valid_ids, dim3(vb), dim3(256), 0, s, g.n_cells, d_mask, d_rid, d_vid);
+        constexpr int TC = DmaCfg<H, C>::TC;
+        uint8_t* live = reinterpret_cast<uint8_t*>(d_vid + g.n_cells);
+        int32_t* counts = reinterpret_cast<int32_t*>(live + (n_strips + 3) / 4 * 4);
+        int32_t* list = counts + STRIP_CHUNKS;
+        const int vb = (int)std::min<int64_t>(((int64_t)n_strips * TC + 255) / 256, 4096);
+        hipLaunchKernelGGL(k_valid_ids_strips<TC>, dim3(vb), dim3(256), 0, s, g.canvas_h, g.canvas_w, segs, C, d_mask,
+                           d_rid, d_vid, live, static_cast<float*>(d_dx));
+        hipLaunchKernelGGL(k_strip_counts, dim3(STRIP_CHUNKS), dim3(64), 0, s, (int64_t)n_strips, live, counts);
+        hipLaunchKernelGGL(k_strip_compact, dim3(STRIP_CHUNKS), dim3(64), 0, s, (int64_t)n_strips, live, counts, list);
         hipLaunchKernelGGL((k_bwd_strip_dma<H, C>), dim3(nwg), dim3(DmaCfg<H, C>::THREADS), 0, s, g.canvas_h,
-                           g.canvas_w, n_strips, segs, static_cast<const float*>(d_dz), static_cast<const float*>(d_x),
-                           static_cast<const float*>(d_y), static_cast<const float*>(d_wx), d_vid,
-                           static_cast<float*>(d_dx), d_part);
+                           g.canvas_w, segs, list, static_cast<const float*>(d_dz),
+                           static_cast<const float*>(d_x), static_cast<const float*>(d_y),
+                           static_cast<const float*>(d_wx), d_vid, static_cast<float*>(d_dx), d_part);
     } else {
         hipLaunchKernelGGL((k_bwd_strip<T, H, C>), dim3(nwg), dim3(StripCfg<H, C>::THREADS), 0, s, g.canvas_h,
                            g.canvas_w, n_strips, segs, static_cast<const T*>(d_dz), static_cast<const T*>(d_x),
@@ -825,7 +911,14 @@ static void launch_strip_shape(const LayerGeom& g, int nwg, int n_strips, int se
     }
 }
 
-size_t strip_vid_bytes(const LayerGeom& g) { return (size_t)(g.n_cells > 0 ? g.n_cells : 1) * 4; }
+// validity ids (int32 per cell), then the list of strips with a valid cell:
+// a byte per strip (padded to 4), the chunk counts, the count and the strips
+size_t strip_vid_bytes(const LayerGeom& g) {
+    const int tc = strip_tc(g);
+    const int64_t n_strips = (int64_t)g.canvas_h * ((g.canvas_w + tc - 1) / tc);
+    return (size_t)(g.n_cells > 0 ? g.n_cells : 1) * 4 + (size_t)(n_strips + 3) / 4 * 4 +
+           (size_t)(STRIP_CHUNKS + 1 + n_strips) * 4;
+}
 
 hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y, const void* d_wx,
                             const uint8_t* d_mask, const int32_t* d_rid, int32_t* d_vid, void* d_dx, float* d_part,
