@@ -474,7 +474,7 @@ __device__ __forceinline__ int zswz(int cell, int f) {  // LDS float index of dZ
 
 template <int H, int C>
 __global__ void __launch_bounds__((DmaCfg<H, C>::THREADS))
-k_bwd_strip_dma(int canvas_h, int canvas_w, int segs, const int32_t* list,
+k_bwd_strip_dma(int canvas_h, int canvas_w, int segs, int ngroups, int list_pitch, const int32_t* lists,
                 const float* __restrict__ dZ, const float* __restrict__ X, const float* __restrict__ Y,
                 const float* __restrict__ Wx, const int32_t* __restrict__ vid, float* __restrict__ dX,
                 float* __restrict__ part) {
@@ -579,17 +579,22 @@ k_bwd_strip_dma(int canvas_h, int canvas_w, int segs, const int32_t* list,
         }
     };
 
-    // The strips with a valid cell, in increasing order after their count
-    // (the others hold none: their dX rows were zeroed with the ids); this
-    // workgroup takes every gridDim.x-th of them. Entries are read one strip
-    // ahead with vector loads, and made uniform only after the next strip's
-    // wait (a read right after the load would wait for the copies issued
-    // before it).
+    // The strips with a valid cell of this workgroup's group (the strips
+    // whose column segment is the group's modulo ngroups; workgroups are
+    // dealt to the XCDs in turn, so a group's strips, which share halo rows
+    // from one row to the next, stay in one L2), after their count (the
+    // others hold no valid cell: their dX rows were zeroed with the ids).
+    // The group's workgroups take every (gridDim.x / ngroups)-th of them.
+    // Entries are read one strip ahead with vector loads, and made uniform
+    // only after the next strip's wait (a read right after the load would
+    // wait for the copies issued before it).
+    const int wg = (int)blockIdx.x, grp = wg % ngroups, gi = wg / ngroups, gn = (int)gridDim.x / ngroups;
+    const int32_t* list = lists + (int64_t)grp * list_pitch;
     auto ld = [&](int64_t k) { return __hip_atomic_load(list + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
     auto uni = [](int v) { return __builtin_amdgcn_readfirstlane(v); };
-    const int n_live = uni(ld(0)), wg = (int)blockIdx.x, nwg = (int)gridDim.x;
-    const int n_my = n_live > wg ? (n_live - wg + nwg - 1) / nwg : 0;
-    auto entry_raw = [&](int k) { return ld(1 + wg + (int64_t)(k - 1) * nwg); };  // k = 1 .. n_my
+    const int n_live = uni(ld(0));
+    const int n_my = n_live > gi ? (n_live - gi + gn - 1) / gn : 0;
+    auto entry_raw = [&](int k) { return ld(1 + gi + (int64_t)(k - 1) * gn); };  // k = 1 .. n_my
 
     // strip: the strip to compute (its copies in zb, yb, xb, vb); next_raw:
     // the loaded entry of the strip whose copies start here into the other
@@ -815,6 +820,15 @@ static int strip_wgs(const LayerGeom& g) {
     return (int)std::max<int64_t>(1, std::min<int64_t>(wgs, strips));
 }
 
+// strip groups of the direct-to-LDS kernel: one per XCD (workgroups are dealt
+// to the eight XCDs in turn) when the workgroups and column segments split
+// evenly, else one
+constexpr int STRIP_GROUPS_MAX = 8;
+static int strip_groups(int nwg, int segs) { return (nwg % 8 == 0 && segs >= 8) ? 8 : 1; }
+// int32 entries per group list: its count, then at most every strip of the
+// largest group (ceil(segs / ng) segments of every row)
+static int64_t strip_list_pitch(int canvas_h, int segs, int ng) { return (int64_t)canvas_h * ((segs + ng - 1) / ng) + 1; }
+
 static int strip_pp(const LayerGeom& g) { return (g.c_in + 2 * g.hidden + 15) / 16 * 16 + 4; }
 
 size_t strip_partial_bytes(const LayerGeom& g) {
@@ -854,34 +868,54 @@ __global__ void k_valid_ids_strips(int canvas_h, int canvas_w, int segs, int C, 
     }
 }
 
-// The list of strips with a valid cell, in increasing order: a count per
-// chunk of STRIP_CHUNKS equal chunks (one wave each), then each chunk writes
-// its strips after the counts of the chunks before it; list[0] is the total.
-constexpr int STRIP_CHUNKS = 256;
-__global__ void k_strip_counts(int64_t n_strips, const uint8_t* __restrict__ live, int32_t* __restrict__ counts) {
-    const int c = blockIdx.x, lane = threadIdx.x & 63;
-    const int64_t per = (n_strips + STRIP_CHUNKS - 1) / STRIP_CHUNKS, b0 = c * per, b1 = min(n_strips, b0 + per);
+// Per group of strips (column segment modulo ngroups; row-major within a
+// group), the list of its strips with a valid cell in that order: a count per
+// chunk of STRIP_CHUNKS equal chunks of the group's strips (one wave each),
+// then each chunk writes its strips after the counts of the chunks before it;
+// entry 0 of a group's list is its total.
+constexpr int STRIP_CHUNKS = 32;
+struct StripGroup {  // the group's k-th strip: row k / per_row, segment grp + ngroups (k % per_row)
+    int64_t total;
+    int per_row;
+    __device__ StripGroup(int canvas_h, int segs, int ngroups, int grp) {
+        per_row = (segs - grp + ngroups - 1) / ngroups;
+        total = (int64_t)canvas_h * per_row;
+    }
+    __device__ int64_t strip(int64_t k, int segs, int ngroups, int grp) const {
+        const int64_t r = k / per_row;
+        return r * segs + grp + (k - r * per_row) * ngroups;
+    }
+};
+__global__ void k_strip_counts(int canvas_h, int segs, int ngroups, const uint8_t* __restrict__ live,
+                               int32_t* __restrict__ counts) {
+    const int grp = blockIdx.x / STRIP_CHUNKS, c = blockIdx.x % STRIP_CHUNKS, lane = threadIdx.x & 63;
+    const StripGroup sg(canvas_h, segs, ngroups, grp);
+    const int64_t per = (sg.total + STRIP_CHUNKS - 1) / STRIP_CHUNKS, b0 = c * per, b1 = min(sg.total, b0 + per);
     int n = 0;
-    for (int64_t k = b0 + lane; k < b1; k += 64) n += live[k] ? 1 : 0;
+    for (int64_t k = b0 + lane; k < b1; k += 64) n += live[sg.strip(k, segs, ngroups, grp)] ? 1 : 0;
     for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o);
-    if (lane == 0) counts[c] = n;
+    if (lane == 0) counts[blockIdx.x] = n;
 }
-__global__ void k_strip_compact(int64_t n_strips, const uint8_t* __restrict__ live,
-                                const int32_t* __restrict__ counts, int32_t* __restrict__ list) {
-    const int c = blockIdx.x, lane = threadIdx.x & 63;
-    const int64_t per = (n_strips + STRIP_CHUNKS - 1) / STRIP_CHUNKS, b0 = c * per, b1 = min(n_strips, b0 + per);
-    int off = 0;
-    for (int k = lane; k < c; k += 64) off += counts[k];
+__global__ void k_strip_compact(int canvas_h, int segs, int ngroups, int list_pitch, const uint8_t* __restrict__ live,
+                                const int32_t* __restrict__ counts, int32_t* __restrict__ lists) {
+    const int grp = blockIdx.x / STRIP_CHUNKS, c = blockIdx.x % STRIP_CHUNKS, lane = threadIdx.x & 63;
+    const StripGroup sg(canvas_h, segs, ngroups, grp);
+    const int64_t per = (sg.total + STRIP_CHUNKS - 1) / STRIP_CHUNKS, b0 = c * per, b1 = min(sg.total, b0 + per);
+    const int32_t* cnt = counts + grp * STRIP_CHUNKS;
+    int32_t* list = lists + (int64_t)grp * list_pitch;
+    int off = lane < c ? cnt[lane] : 0;  // STRIP_CHUNKS <= 64
     for (int o = 32; o > 0; o >>= 1) off += __shfl_xor(off, o);
-    if (c == STRIP_CHUNKS - 1 && lane == 0) list[0] = off + counts[c];
+    if (c == STRIP_CHUNKS - 1 && lane == 0) list[0] = off + cnt[c];
     for (int64_t k0 = b0; k0 < b1; k0 += 64) {
         const int64_t k = k0 + lane;
-        const bool lv = k < b1 && live[k];
+        const int64_t st = k < b1 ? sg.strip(k, segs, ngroups, grp) : 0;
+        const bool lv = k < b1 && live[st];
         const uint64_t b = __ballot(lv);
-        if (lv) list[1 + off + __popcll(b & ((1ull << lane) - 1))] = (int32_t)k;
+        if (lv) list[1 + off + __popcll(b & ((1ull << lane) - 1))] = (int32_t)st;
         off += __popcll(b);
     }
 }
+static_assert(STRIP_CHUNKS <= 64, "one wave sums the chunk counts");
 
 // fp32 storage at H = 32 takes the direct-to-LDS kernel, the other shapes
 // the register-staged one.
@@ -891,16 +925,19 @@ static void launch_strip_shape(const LayerGeom& g, int nwg, int n_strips, int se
                                int32_t* d_vid, void* d_dx, float* d_part, hipStream_t s) {
     if constexpr (std::is_same<T, float>::value && H == 32) {
         constexpr int TC = DmaCfg<H, C>::TC;
+        const int ng = strip_groups(nwg, segs);
         uint8_t* live = reinterpret_cast<uint8_t*>(d_vid + g.n_cells);
         int32_t* counts = reinterpret_cast<int32_t*>(live + (n_strips + 3) / 4 * 4);
-        int32_t* list = counts + STRIP_CHUNKS;
+        int32_t* lists = counts + STRIP_GROUPS_MAX * STRIP_CHUNKS;
+        const int pitch = (int)strip_list_pitch(g.canvas_h, segs, ng);
         const int vb = (int)std::min<int64_t>(((int64_t)n_strips * TC + 255) / 256, 4096);
         hipLaunchKernelGGL(k_valid_ids_strips<TC>, dim3(vb), dim3(256), 0, s, g.canvas_h, g.canvas_w, segs, C, d_mask,
                            d_rid, d_vid, live, static_cast<float*>(d_dx));
-        hipLaunchKernelGGL(k_strip_counts, dim3(STRIP_CHUNKS), dim3(64), 0, s, (int64_t)n_strips, live, counts);
-        hipLaunchKernelGGL(k_strip_compact, dim3(STRIP_CHUNKS), dim3(64), 0, s, (int64_t)n_strips, live, counts, list);
+        hipLaunchKernelGGL(k_strip_counts, dim3(ng * STRIP_CHUNKS), dim3(64), 0, s, g.canvas_h, segs, ng, live, counts);
+        hipLaunchKernelGGL(k_strip_compact, dim3(ng * STRIP_CHUNKS), dim3(64), 0, s, g.canvas_h, segs, ng, pitch, live,
+                           counts, lists);
         hipLaunchKernelGGL((k_bwd_strip_dma<H, C>), dim3(nwg), dim3(DmaCfg<H, C>::THREADS), 0, s, g.canvas_h,
-                           g.canvas_w, segs, list, static_cast<const float*>(d_dz),
+                           g.canvas_w, segs, ng, pitch, lists, static_cast<const float*>(d_dz),
                            static_cast<const float*>(d_x), static_cast<const float*>(d_y),
                            static_cast<const float*>(d_wx), d_vid, static_cast<float*>(d_dx), d_part);
     } else {
@@ -911,13 +948,16 @@ static void launch_strip_shape(const LayerGeom& g, int nwg, int n_strips, int se
     }
 }
 
-// validity ids (int32 per cell), then the list of strips with a valid cell:
-// a byte per strip (padded to 4), the chunk counts, the count and the strips
+// validity ids (int32 per cell), then the lists of strips with a valid cell:
+// a byte per strip (padded to 4), the chunk counts, and per group its count
+// and strips
 size_t strip_vid_bytes(const LayerGeom& g) {
     const int tc = strip_tc(g);
-    const int64_t n_strips = (int64_t)g.canvas_h * ((g.canvas_w + tc - 1) / tc);
+    const int segs = (g.canvas_w + tc - 1) / tc;
+    const int64_t n_strips = (int64_t)g.canvas_h * segs;
+    const int ng = strip_groups(strip_wgs(g), segs);
     return (size_t)(g.n_cells > 0 ? g.n_cells : 1) * 4 + (size_t)(n_strips + 3) / 4 * 4 +
-           (size_t)(STRIP_CHUNKS + 1 + n_strips) * 4;
+           (size_t)STRIP_GROUPS_MAX * STRIP_CHUNKS * 4 + (size_t)ng * strip_list_pitch(g.canvas_h, segs, ng) * 4;
 }
 
 hipError_t launch_bwd_strip(const LayerGeom& g, const void* d_dz, const void* d_x, const void* d_y, const void* d_wx,
