@@ -863,8 +863,11 @@ __global__ void k_valid_ids_strips(int canvas_h, int canvas_w, int segs, int C, 
         const uint64_t b = __ballot(v >= 0);
         const bool any = ((b >> (lane & ~(TC - 1))) & ((1ull << TC) - 1)) != 0;
         if (in && j == 0) live[strip] = any ? 1 : 0;
-        if (in && !any)
-            for (int c = 0; c < C; c += 4) *reinterpret_cast<float4*>(dX + p * C + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (strip < n_strips && !any) {  // the strip's dX rows, contiguous: lane j takes every TC-th 16 bytes
+            const int len = min(TC, canvas_w - (x - j));
+            float4* row = reinterpret_cast<float4*>(dX + (p - j) * C);
+            for (int e = j; e < len * C / 4; e += TC) row[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
     }
 }
 
