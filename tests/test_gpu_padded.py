@@ -181,20 +181,47 @@ def test_padded_stepwise_forward():
         assert rel_err(g, r) <= 1e-5 and rel_max(g, r) <= 1e-5, k
 
 
-def test_padded_empty_layout():
-    """No rectangles: Y and dX are zero and the weight gradients are zero."""
+@pytest.mark.parametrize("shape", [(3, 10), (32, 32)], ids=["C3_H10", "C32_H32"])
+def test_padded_empty_layout(shape):
+    """No rectangles: Y and dX are zero and the weight gradients are zero (C 32,
+    H 32 takes the direct-to-LDS strip kernel, whose strip lists are empty)."""
     from paper_1902_11208_amd import api
 
-    _say("case padded empty layout: C=3 H=10, 12x20 canvas, no rectangles")
+    C, H = shape
+    _say(f"case padded empty layout: C={C} H={H}, 12x40 canvas, no rectangles")
     dev = "cuda"
     g = torch.Generator().manual_seed(5)
-    wx = torch.randn(4, 50, 3, generator=g).to(dev)
-    u = torch.randn(4, 50, 20, generator=g).to(dev)
-    b = torch.randn(4, 50, generator=g).to(dev)
-    mask = torch.zeros(12, 20, dtype=torch.uint8, device=dev)
-    layer = api.MDLSTMLayer(wx, u, b, 12, 20, np.zeros((0, 4), np.int32), mask)
-    y = layer.forward(torch.randn(12, 20, 3, generator=g).to(dev))
-    dx, dwx, du, db = layer.backward(torch.randn(12, 20, 40, generator=g).to(dev))
+    wx = torch.randn(4, 5 * H, C, generator=g).to(dev)
+    u = torch.randn(4, 5 * H, 2 * H, generator=g).to(dev)
+    b = torch.randn(4, 5 * H, generator=g).to(dev)
+    mask = torch.zeros(12, 40, dtype=torch.uint8, device=dev)
+    layer = api.MDLSTMLayer(wx, u, b, 12, 40, np.zeros((0, 4), np.int32), mask)
+    y = layer.forward(torch.randn(12, 40, C, generator=g).to(dev))
+    dx, dwx, du, db = layer.backward(torch.randn(12, 40, 4 * H, generator=g).to(dev))
     torch.cuda.synchronize()
     for t in (y, dx, dwx, du, db):
         assert not torch.any(t != 0)
+
+
+def test_strip_lists_with_empty_rows_and_slack():
+    """C 32, H 32 (the direct-to-LDS strip kernel): rectangles that leave whole
+    canvas rows, row ends and a column band empty, so most strips are skipped
+    and the others are spread unevenly over the groups; against the oracle,
+    and dX exactly zero on every cell outside the rectangles."""
+    import gpu_run
+    import oracle_run
+    from synth.configs import custom_workload
+
+    hs, ws, cw = [3, 17, 5], [70, 9, 33], 160
+    _say(f"case strip lists: heights={hs} widths={ws} W={cw} C=32 H=32 f32")
+    wl = custom_workload(360, hs, ws, cw, 32, 32)
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    gpu = gpu_run.run_layer(xs, params, dys, hs, ws, cw, dtype="f32")
+    ref = oracle_run.run_layer(xs, params, dys)
+    _cmp(gpu, ref, "f32", "strip lists")
+    dxc = gpu_run.to_np(gpu["dx_canvas"])
+    mask = gpu["mask"]
+    mask = mask.cpu().numpy() if hasattr(mask, "cpu") else np.asarray(mask)
+    _say(f"  canvas {dxc.shape[0]}x{dxc.shape[1]}, {int((mask != 0).sum())} cells in rectangles")
+    assert not np.any(dxc[mask == 0]), "dX outside the rectangles"
