@@ -113,9 +113,10 @@ __device__ __forceinline__ void st_f4(float* p, float4 v) { *reinterpret_cast<fl
 
 template <typename T, int H, int C>
 __global__ void __launch_bounds__((StripCfg<H, C>::THREADS))
-k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restrict__ dZ, const T* __restrict__ X,
-            const T* __restrict__ Y, const T* __restrict__ Wx, const uint8_t* __restrict__ mask,
-            const int32_t* __restrict__ rid, T* __restrict__ dX, float* __restrict__ part) {
+k_bwd_strip(int canvas_h, int canvas_w, int segs, int ngroups, int list_pitch, const int32_t* lists,
+            const T* __restrict__ dZ, const T* __restrict__ X, const T* __restrict__ Y, const T* __restrict__ Wx,
+            const uint8_t* __restrict__ mask, const int32_t* __restrict__ rid, T* __restrict__ dX,
+            float* __restrict__ part) {
     using Cf = StripCfg<H, C>;
     using L4 = V4<T>;
     constexpr int TC = Cf::TC, RTW = Cf::RTW, WPD = Cf::WPD, CT = Cf::CT, CXT = Cf::CXT, HW = Cf::HW;
@@ -265,9 +266,23 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
     // compute; shapes whose dW tiles fill the register file load each strip
     // just before staging it, one tensor at a time.
     constexpr bool PREFETCH = Cf::PREFETCH;
-    int strip = blockIdx.x;
-    if constexpr (PREFETCH) issue(strip, 15);
-    for (; strip < n_strips; strip += gridDim.x) {
+    // The strips with a valid cell of this workgroup's group, as in the
+    // direct-to-LDS kernel below (the others were skipped, their dX rows
+    // zeroed with the strip flags). An entry is loaded two strips ahead, before
+    // the next strip's loads, so that it has landed when those are waited for.
+    const int wg = (int)blockIdx.x, grp = wg % ngroups, gi = wg / ngroups, gn = (int)gridDim.x / ngroups;
+    const int32_t* list = lists + (int64_t)grp * list_pitch;
+    auto ld = [&](int64_t k) { return __hip_atomic_load(list + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+    auto uni = [](int v) { return __builtin_amdgcn_readfirstlane(v); };
+    const int n_live = uni(ld(0));
+    const int n_my = n_live > gi ? (n_live - gi + gn - 1) / gn : 0;
+    auto entry_raw = [&](int k) { return ld(1 + gi + (int64_t)(k - 1) * gn); };  // k = 1 .. n_my
+    int strip = n_my > 0 ? uni(entry_raw(1)) : -1;
+    int next_raw = n_my > 1 ? entry_raw(2) : -1;
+    if constexpr (PREFETCH) {
+        if (strip >= 0) issue(strip, 15);
+    }
+    for (int kpos = 1; strip >= 0; ++kpos) {
         int cy, cx0, len;
         int64_t p0;
         strip_pos(strip, cy, cx0, len, p0);
@@ -311,7 +326,9 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
             }
         }
         // the next strip's loads (the last strip re-reads itself) stay in flight
-        if constexpr (PREFETCH) issue(min(strip + (int)gridDim.x, n_strips - 1), 15);
+        const int next = uni(next_raw);
+        next_raw = kpos + 2 <= n_my ? entry_raw(kpos + 2) : -1;
+        if constexpr (PREFETCH) issue(next >= 0 ? next : strip, 15);
         lds_barrier();
 
         // --- dW: K = cells of the strip, 4 per MFMA step; in step ks, K slot g
@@ -418,6 +435,7 @@ k_bwd_strip(int canvas_h, int canvas_w, int n_strips, int segs, const T* __restr
             }
         }
         lds_barrier();
+        strip = next;
     }
 
     // partial of this workgroup: [wg][4][RT*16][PP], bias in column CT*16
@@ -837,14 +855,14 @@ size_t strip_partial_bytes(const LayerGeom& g) {
 }
 
 // Validity id of every canvas cell (its rectangle id where the cell is inside
-// a rectangle and unmasked, else -1), a thread per (strip of TC cells, cell),
-// plus a byte
+// a rectangle and unmasked, else -1; written where vid is given), a thread per
+// (strip of TC cells, cell), plus a byte
 // per strip that says whether it holds a valid cell; the dX rows of the
 // strips without one are zeroed here (the strip kernel skips them).
-template <int TC>
+template <int TC, typename T>
 __global__ void k_valid_ids_strips(int canvas_h, int canvas_w, int segs, int C, const uint8_t* __restrict__ mask,
                                    const int32_t* __restrict__ rid, int32_t* __restrict__ vid,
-                                   uint8_t* __restrict__ live, float* __restrict__ dX) {
+                                   uint8_t* __restrict__ live, T* __restrict__ dX) {
     static_assert(64 % TC == 0, "strips within a wave");
     const int64_t n_strips = (int64_t)canvas_h * segs;
     const int64_t total = (n_strips * TC + 63) / 64 * 64;  // whole waves: every lane takes part in the ballot
@@ -858,15 +876,16 @@ __global__ void k_valid_ids_strips(int canvas_h, int canvas_w, int segs, int C, 
         int32_t v = -1;
         if (in) {
             v = (mask[p] && rid[p] >= 0) ? rid[p] : -1;
-            vid[p] = v;
+            if (vid) vid[p] = v;
         }
         const uint64_t b = __ballot(v >= 0);
         const bool any = ((b >> (lane & ~(TC - 1))) & ((1ull << TC) - 1)) != 0;
         if (in && j == 0) live[strip] = any ? 1 : 0;
         if (strip < n_strips && !any) {  // the strip's dX rows, contiguous: lane j takes every TC-th 16 bytes
             const int len = min(TC, canvas_w - (x - j));
-            float4* row = reinterpret_cast<float4*>(dX + (p - j) * C);
-            for (int e = j; e < len * C / 4; e += TC) row[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+            uint4* row = reinterpret_cast<uint4*>(dX + (p - j) * C);
+            const int n16 = len * C * (int)sizeof(T) / 16;
+            for (int e = j; e < n16; e += TC) row[e] = make_uint4(0u, 0u, 0u, 0u);
         }
     }
 }
@@ -926,26 +945,29 @@ template <typename T, int H, int C>
 static void launch_strip_shape(const LayerGeom& g, int nwg, int n_strips, int segs, const void* d_dz, const void* d_x,
                                const void* d_y, const void* d_wx, const uint8_t* d_mask, const int32_t* d_rid,
                                int32_t* d_vid, void* d_dx, float* d_part, hipStream_t s) {
-    if constexpr (std::is_same<T, float>::value && H == 32) {
-        constexpr int TC = DmaCfg<H, C>::TC;
-        const int ng = strip_groups(nwg, segs);
-        uint8_t* live = reinterpret_cast<uint8_t*>(d_vid + g.n_cells);
-        int32_t* counts = reinterpret_cast<int32_t*>(live + (n_strips + 3) / 4 * 4);
-        int32_t* lists = counts + STRIP_GROUPS_MAX * STRIP_CHUNKS;
-        const int pitch = (int)strip_list_pitch(g.canvas_h, segs, ng);
-        const int vb = (int)std::min<int64_t>(((int64_t)n_strips * TC + 255) / 256, 4096);
-        hipLaunchKernelGGL(k_valid_ids_strips<TC>, dim3(vb), dim3(256), 0, s, g.canvas_h, g.canvas_w, segs, C, d_mask,
-                           d_rid, d_vid, live, static_cast<float*>(d_dx));
-        hipLaunchKernelGGL(k_strip_counts, dim3(ng * STRIP_CHUNKS), dim3(64), 0, s, g.canvas_h, segs, ng, live, counts);
-        hipLaunchKernelGGL(k_strip_compact, dim3(ng * STRIP_CHUNKS), dim3(64), 0, s, g.canvas_h, segs, ng, pitch, live,
-                           counts, lists);
+    constexpr bool DMA = std::is_same<T, float>::value && H == 32;
+    constexpr int TC = StripCfg<H, C>::TC;
+    // the strip lists: validity (ids for the direct-to-LDS kernel), a flag per
+    // strip and the dX rows of the strips without a valid cell, then the lists
+    const int ng = strip_groups(nwg, segs);
+    uint8_t* live = reinterpret_cast<uint8_t*>(d_vid + g.n_cells);
+    int32_t* counts = reinterpret_cast<int32_t*>(live + (n_strips + 3) / 4 * 4);
+    int32_t* lists = counts + STRIP_GROUPS_MAX * STRIP_CHUNKS;
+    const int pitch = (int)strip_list_pitch(g.canvas_h, segs, ng);
+    const int vb = (int)std::min<int64_t>(((int64_t)n_strips * TC + 255) / 256, 4096);
+    hipLaunchKernelGGL((k_valid_ids_strips<TC, T>), dim3(vb), dim3(256), 0, s, g.canvas_h, g.canvas_w, segs, C,
+                       d_mask, d_rid, DMA ? d_vid : nullptr, live, static_cast<T*>(d_dx));
+    hipLaunchKernelGGL(k_strip_counts, dim3(ng * STRIP_CHUNKS), dim3(64), 0, s, g.canvas_h, segs, ng, live, counts);
+    hipLaunchKernelGGL(k_strip_compact, dim3(ng * STRIP_CHUNKS), dim3(64), 0, s, g.canvas_h, segs, ng, pitch, live,
+                       counts, lists);
+    if constexpr (DMA) {
         hipLaunchKernelGGL((k_bwd_strip_dma<H, C>), dim3(nwg), dim3(DmaCfg<H, C>::THREADS), 0, s, g.canvas_h,
                            g.canvas_w, segs, ng, pitch, lists, static_cast<const float*>(d_dz),
                            static_cast<const float*>(d_x), static_cast<const float*>(d_y),
                            static_cast<const float*>(d_wx), d_vid, static_cast<float*>(d_dx), d_part);
     } else {
         hipLaunchKernelGGL((k_bwd_strip<T, H, C>), dim3(nwg), dim3(StripCfg<H, C>::THREADS), 0, s, g.canvas_h,
-                           g.canvas_w, n_strips, segs, static_cast<const T*>(d_dz), static_cast<const T*>(d_x),
+                           g.canvas_w, segs, ng, pitch, lists, static_cast<const T*>(d_dz), static_cast<const T*>(d_x),
                            static_cast<const T*>(d_y), static_cast<const T*>(d_wx), d_mask, d_rid,
                            static_cast<T*>(d_dx), d_part);
     }
