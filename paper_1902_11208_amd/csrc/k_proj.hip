@@ -64,7 +64,8 @@ struct PK<bf16_t> {  // 16x16x32 bf16: K step ks, slot g holds k = 32 ks + 8 g +
 template <typename T, int KS>
 __global__ void __launch_bounds__(256)
 k_projection(int64_t n_cells, int64_t n_blocks, int C, int N, int nch, const T* __restrict__ X,
-             const T* __restrict__ Wx, const T* __restrict__ bias, T* __restrict__ Z) {
+             const T* __restrict__ Wx, const T* __restrict__ bias, const int32_t* __restrict__ rid,
+             T* __restrict__ Z) {
     using K = PK<T>;
     using Op = typename K::Op;
     constexpr int RW = K::PERK * KS;  // staged k values per row
@@ -86,8 +87,13 @@ k_projection(int64_t n_cells, int64_t n_blocks, int C, int N, int nch, const T* 
     // B operands of a block's 64 cells of this wave (rows past the canvas
     // re-read its last cell; their results are not stored)
     Op b[4][KS];
+    // rectangle id of the lane's cell of the block: a wave whose 64 cells all
+    // lie outside the rectangles (row slack, separators) skips the block; no
+    // later step reads their pre-activations
+    int32_t rv = 0;
     auto load_b = [&](int64_t blk) {
         const int64_t cell0 = (blk * 4 + wave) * PCELLS;
+        rv = rid ? rid[min(cell0 + lane, n_cells - 1)] : 0;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const T* row = X + min(cell0 + 16 * t + n16, n_cells - 1) * C;
@@ -98,6 +104,10 @@ k_projection(int64_t n_cells, int64_t n_blocks, int C, int N, int nch, const T* 
     load_b(blockIdx.x);
     for (int64_t blk = blockIdx.x; blk < n_blocks; blk += gridDim.x) {
         const int64_t cell0 = (blk * 4 + wave) * PCELLS;
+        if (__ballot(rv >= 0 && cell0 + lane < n_cells) == 0) {
+            load_b(min(blk + (int64_t)gridDim.x, n_blocks - 1));
+            continue;
+        }
         for (int mg = 0; mg * 4 < ntiles; ++mg) {
             const int mc = min(4, ntiles - 4 * mg);  // column tiles in this group
             floatx4 acc[4][4];
@@ -143,7 +153,8 @@ k_projection(int64_t n_cells, int64_t n_blocks, int C, int N, int nch, const T* 
 }
 
 template <typename T, int KS>
-static hipError_t launch_proj(const LayerGeom& g, const T* X, const T* W, const T* B, T* Z, hipStream_t s) {
+static hipError_t launch_proj(const LayerGeom& g, const T* X, const T* W, const T* B, const int32_t* rid, T* Z,
+                              hipStream_t s) {
     constexpr int RW = PK<T>::PERK * KS, P = RW + PK<T>::PAD;
     const int N = 20 * g.hidden;
     // columns per workgroup: as many as the LDS budget holds (a multiple of 16,
@@ -166,12 +177,12 @@ static hipError_t launch_proj(const LayerGeom& g, const T* X, const T* W, const 
     const int64_t want = std::max<int64_t>(1, (int64_t)per_cu * std::max(cus, 1) / nchunks_col);
     const dim3 grid((unsigned)std::min<int64_t>(blocks, want), (unsigned)nchunks_col), block(256);
     hipLaunchKernelGGL((k_projection<T, KS>), grid, block, (size_t)nch * P * sizeof(T), s, g.n_cells, blocks, g.c_in,
-                       N, nch, X, W, B, Z);
+                       N, nch, X, W, B, rid, Z);
     return hipGetLastError();
 }
 
-hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_wx, const void* d_b, void* d_z,
-                             hipStream_t s) {
+hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_wx, const void* d_b,
+                             const int32_t* d_rid, void* d_z, hipStream_t s) {
     if (g.n_cells == 0) return hipSuccess;
     if (g.dtype == 0) {
         const int ks = (g.c_in + 3) / 4;
@@ -179,13 +190,13 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
         auto W = static_cast<const float*>(d_wx);
         auto B = static_cast<const float*>(d_b);
         auto Z = static_cast<float*>(d_z);
-        if (ks <= 1) return launch_proj<float, 1>(g, X, W, B, Z, s);
-        if (ks <= 2) return launch_proj<float, 2>(g, X, W, B, Z, s);
-        if (ks <= 4) return launch_proj<float, 4>(g, X, W, B, Z, s);
-        if (ks <= 8) return launch_proj<float, 8>(g, X, W, B, Z, s);
-        if (ks <= 16) return launch_proj<float, 16>(g, X, W, B, Z, s);
-        if (ks <= 32) return launch_proj<float, 32>(g, X, W, B, Z, s);
-        if (ks <= 64) return launch_proj<float, 64>(g, X, W, B, Z, s);
+        if (ks <= 1) return launch_proj<float, 1>(g, X, W, B, d_rid, Z, s);
+        if (ks <= 2) return launch_proj<float, 2>(g, X, W, B, d_rid, Z, s);
+        if (ks <= 4) return launch_proj<float, 4>(g, X, W, B, d_rid, Z, s);
+        if (ks <= 8) return launch_proj<float, 8>(g, X, W, B, d_rid, Z, s);
+        if (ks <= 16) return launch_proj<float, 16>(g, X, W, B, d_rid, Z, s);
+        if (ks <= 32) return launch_proj<float, 32>(g, X, W, B, d_rid, Z, s);
+        if (ks <= 64) return launch_proj<float, 64>(g, X, W, B, d_rid, Z, s);
         return hipErrorInvalidValue;
     }
     const int ks = (g.c_in + 31) / 32;
@@ -193,10 +204,10 @@ hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_
     auto W = static_cast<const bf16_t*>(d_wx);
     auto B = static_cast<const bf16_t*>(d_b);
     auto Z = static_cast<bf16_t*>(d_z);
-    if (ks <= 1) return launch_proj<bf16_t, 1>(g, X, W, B, Z, s);
-    if (ks <= 2) return launch_proj<bf16_t, 2>(g, X, W, B, Z, s);
-    if (ks <= 4) return launch_proj<bf16_t, 4>(g, X, W, B, Z, s);
-    if (ks <= 8) return launch_proj<bf16_t, 8>(g, X, W, B, Z, s);
+    if (ks <= 1) return launch_proj<bf16_t, 1>(g, X, W, B, d_rid, Z, s);
+    if (ks <= 2) return launch_proj<bf16_t, 2>(g, X, W, B, d_rid, Z, s);
+    if (ks <= 4) return launch_proj<bf16_t, 4>(g, X, W, B, d_rid, Z, s);
+    if (ks <= 8) return launch_proj<bf16_t, 8>(g, X, W, B, d_rid, Z, s);
     return hipErrorInvalidValue;
 }
 

@@ -33,9 +33,11 @@ hipError_t launch_gather(int n, void* const* d_ptrs, const int32_t* d_rects, int
                          int esize, const void* d_canvas, int max_h, hipStream_t s);
 
 // --- forward ---------------------------------------------------------------
-// Z[p][20H] = Wx_all[20H][C] x[p] + b_all.
+// Z[p][20H] = Wx_all[20H][C] x[p] + b_all, for the cells of every 64-cell
+// chunk that holds a cell of a rectangle (d_rid: rectangle id per cell, -1
+// outside; NULL: every chunk).
 hipError_t launch_projection(const LayerGeom& g, const void* d_x, const void* d_wx, const void* d_b,
-                             void* d_z, hipStream_t s);
+                             const int32_t* d_rid, void* d_z, hipStream_t s);
 // Count the non-finite values of n elements (dtype 0 fp32, 1 bf16) into
 // *d_count (added to; the caller zeroes it).
 hipError_t launch_fill_u32(void* d, int64_t n_words, uint32_t v, hipStream_t s);

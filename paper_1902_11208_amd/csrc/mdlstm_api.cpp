@@ -665,7 +665,7 @@ mdlstm_status forward_impl(bool stepwise, const mdlstm_layer_desc* desc, int32_t
     if (desc->memory_states && stepwise)
         return fail(MDLSTM_ERR_UNSUPPORTED, "the per-diagonal schedule is not built with memory-state matrices");
     HIP_OR_FAIL(mark(0, s));
-    HIP_OR_FAIL(mdl::launch_projection(c.g, d_x, d_wx, d_b, c.ws + c.p.z, s));
+    HIP_OR_FAIL(mdl::launch_projection(c.g, d_x, d_wx, d_b, rid, c.ws + c.p.z, s));
     HIP_OR_FAIL(mark(1, s));
     if (stepwise || n_rects == 0 || desc->memory_states)
         HIP_OR_FAIL(mdl::launch_zero_invalid(c.g, 4 * c.g.hidden, d_mask, rid, d_y, s));
