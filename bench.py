@@ -104,7 +104,8 @@ def algorithmic(H: int, C: int, s: int, useful_cells: int):
 
 def design_bytes(H: int, C: int, s: int, useful_cells: int, canvas_cells: int, unit_cells: int):
     """HBM bytes the kernels move beyond the cost model, by design: the
-    projection over separator and padding cells, the activated gates the
+    projection over separator and padding cells (an upper bound: its waves
+    skip 64-cell chunks without a rectangle cell), the activated gates the
     forward writes back for the backward, and the zero output rows."""
     cd = 4 * useful_cells
     return {
