@@ -352,6 +352,28 @@ def test_placement_invariance_and_determinism():
         assert np.array_equal(r1[nm], r3[nm])
 
 
+@pytest.mark.parametrize("shape", [(32, 32, "f32"), (64, 128, "bf16")], ids=["C32_H32", "bf16_C64_H128"])
+def test_gradients_are_deterministic(shape):
+    """Repeated backward passes give bitwise identical gradients on the
+    direct-to-LDS strip kernel (fp32 H 32, strips from the per-XCD lists)
+    and on the bf16 tiled kernels (their chunk partials summed in a fixed
+    order)."""
+    import gpu_run
+    from synth.configs import custom_workload
+
+    C, H, dt = shape
+    wl = custom_workload(11, [20, 9, 33, 5], [57, 120, 14, 80], 160, C, H, dt)
+    xs, params = wl.examples(), wl.params()
+    dys = [wl.dy(k) for k in range(wl.n)]
+    _say(f"case determinism: C={C} H={H} {dt}")
+    r1 = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w, dtype=dt)
+    r2 = gpu_run.run_layer(xs, params, dys, wl.heights, wl.widths, wl.canvas_w, dtype=dt)
+    for nm in ("dWx", "dU", "db"):
+        assert np.array_equal(r1[nm], r2[nm]), nm
+    for k in range(wl.n):
+        assert np.array_equal(r1["dX"][k], r2["dX"][k]), k
+
+
 def test_exploding_state_regime():
     """Forget-gate biases U(-0.1, 0.1): the forget gates sum to about 1 and the
     state grows to |c| ~ 1e5 over these lines (Section III). The bounds come
