@@ -39,20 +39,6 @@ struct BlockPos {
     int64_t out;   // canvas index of the output pixel
 };
 
-// Position of block b: example k, block (by, bx) of its output rectangle.
-__device__ __forceinline__ BlockPos block_pos(const int32_t* __restrict__ blk_off, int n, int b,
-                                              const int32_t* __restrict__ in_rects, int in_w,
-                                              const int32_t* __restrict__ out_rects, int out_w, int bh, int bw) {
-    const int k = find_example(blk_off, n, b);
-    const int local = b - blk_off[k];
-    const int ow = out_rects[4 * k + 3];
-    const int by = local / ow, bx = local - by * ow;
-    BlockPos r;
-    r.out = (int64_t)(out_rects[4 * k] + by) * out_w + out_rects[4 * k + 1] + bx;
-    r.in0 = (int64_t)(in_rects[4 * k] + by * bh) * in_w + in_rects[4 * k + 1] + bx * bw;
-    return r;
-}
-
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -79,163 +65,279 @@ __global__ void k_pack_blocks(const float* const* __restrict__ imgs, const int32
 }
 
 // ---------------------------------------------------------------------------
-// Forward: one thread per (block, group d); og outputs, K = bh*bw*H inputs.
-// W of all groups sits in LDS.
+// The convolution kernels take the blocks in steps of consecutive blocks
+// (grid-stride over steps). A step mostly lies in one block row of one
+// rectangle, where block t's pixels sit t * bw columns right of the first
+// block's and its output pixel t to the right: only the first block's
+// position needs the search over the examples.
 // ---------------------------------------------------------------------------
-template <int H, int OG>
-__global__ void __launch_bounds__(256)
-k_conv_fwd(const float* __restrict__ y, const float* __restrict__ W, const float* __restrict__ bias,
-           const int32_t* __restrict__ blk_off, int n, const int32_t* __restrict__ in_rects, int in_w,
-           const int32_t* __restrict__ out_rects, int out_w, float* __restrict__ out) {
-    constexpr int bh = CBH, bw = CBW, K = bh * bw * H;
-    __shared__ float sw[4 * OG * K];
-    for (int i = threadIdx.x; i < 4 * OG * K; i += blockDim.x) sw[i] = W[i];
-    __syncthreads();
-    const int nb = blk_off[n];
-    const int gid = blockIdx.x * blockDim.x + threadIdx.x;
-    if (gid >= 4 * nb) return;
-    const int b = gid >> 2, d = gid & 3;
-    const BlockPos P = block_pos(blk_off, n, b, in_rects, in_w, out_rects, out_w, CBH, CBW);
-    float acc[OG];
-#pragma unroll
-    for (int o = 0; o < OG; ++o) acc[o] = bias[d * OG + o];
-    const float* wd = sw + d * OG * K;
-    for (int dy = 0; dy < bh; ++dy)
-        for (int dx = 0; dx < bw; ++dx) {
-            const float* yp = y + (P.in0 + (int64_t)dy * in_w + dx) * (4 * H) + d * H;
-            const int k0 = (dy * bw + dx) * H;
-#pragma unroll
-            for (int j = 0; j < H; j += 4) {
-                const float4 v = *reinterpret_cast<const float4*>(yp + j);
-#pragma unroll
-                for (int o = 0; o < OG; ++o) {
-                    const float* wr = wd + o * K + k0 + j;
-                    acc[o] += wr[0] * v.x + wr[1] * v.y + wr[2] * v.z + wr[3] * v.w;
-                }
-            }
-        }
-    float* op = out + P.out * (4 * OG) + d * OG;
-#pragma unroll
-    for (int o = 0; o < OG; o += 4)
-        *reinterpret_cast<float4*>(op + o) = make_float4(tanhf(acc[o]), tanhf(acc[o + 1]), tanhf(acc[o + 2]),
-                                                         tanhf(acc[o + 3]));
+struct ConvGeo {
+    const int32_t* blk_off;
+    int n;
+    const int32_t* in_rects;
+    int in_w;
+    const int32_t* out_rects;
+    int out_w;
+};
+
+struct RowPos {
+    int64_t in0, out;
+    int rem;  // blocks from this one to the end of its block row
+};
+
+__device__ __forceinline__ RowPos row_pos(const ConvGeo& g, int b) {
+    const int k = find_example(g.blk_off, g.n, b);
+    const int local = b - g.blk_off[k];
+    const int ow = g.out_rects[4 * k + 3];
+    const int by = local / ow, bx = local - by * ow;
+    RowPos r;
+    r.out = (int64_t)(g.out_rects[4 * k] + by) * g.out_w + g.out_rects[4 * k + 1] + bx;
+    r.in0 = (int64_t)(g.in_rects[4 * k] + by * CBH) * g.in_w + g.in_rects[4 * k + 1] + bx * CBW;
+    r.rem = ow - bx;
+    return r;
 }
 
-// ---------------------------------------------------------------------------
-// Backward, input gradient: one thread per (block, group d):
-//   g[o] = dout[o] (1 - out[o]^2),  dy[pixel][d*H + j] = sum_o g[o] W[d][o][(dy*bw+dx)*H + j].
-// ---------------------------------------------------------------------------
+// Block s0 + t, given block s0's position r0.
+__device__ __forceinline__ BlockPos stage_pos(const ConvGeo& g, const RowPos& r0, int s0, int t) {
+    if (t < r0.rem) return BlockPos{r0.in0 + (int64_t)t * CBW, r0.out + t};
+    const RowPos r = row_pos(g, s0 + t);
+    return BlockPos{r.in0, r.out};
+}
+
+// Every kernel runs a wave per (group d, step of NG = 64 / OG consecutive
+// blocks), no LDS and no barriers. Lane l holds inputs k = l, l + 64, ... of
+// the K = bh * bw * H inputs of each block of the step (pixel k / H, channel
+// d*H + k % H) with their OG weights, or weight-gradient sums, in registers;
+// the step's data loads one step ahead.
+template <int H, int OG>
+struct ConvCfg {
+    static constexpr int K = CBH * CBW * H, KL = (K + 63) / 64, NG = 64 / OG;
+    static_assert(64 % OG == 0, "outputs per group");
+};
+
+// Canvas float index of input k of group d of the block at in0.
+template <int H>
+__device__ __forceinline__ int64_t in_index(int64_t in0, int in_w, int d, int k) {
+    const int pix = k / H, j = k - pix * H, dyy = pix / CBW, dx = pix - dyy * CBW;
+    return (in0 + (int64_t)dyy * in_w + dx) * (4 * H) + d * H + j;
+}
+
+// The step's inputs of group d: x[t][i] = input lane + 64 i of block s0 + t
+// (zero past the last block or past K).
+template <int H, int OG>
+__device__ __forceinline__ void load_step(const ConvGeo& g, const float* __restrict__ y, int d, int lane, int s0,
+                                          int lim, RowPos& r0,
+                                          float (&x)[ConvCfg<H, OG>::NG][ConvCfg<H, OG>::KL]) {
+    using Cg = ConvCfg<H, OG>;
+    r0 = row_pos(g, s0);
+#pragma unroll
+    for (int t = 0; t < Cg::NG; ++t) {
+        const bool live = s0 + t < lim;
+        const BlockPos P = live ? stage_pos(g, r0, s0, t) : BlockPos{0, 0};
+#pragma unroll
+        for (int i = 0; i < Cg::KL; ++i) {
+            const int k = lane + 64 * i;
+            x[t][i] = live && k < Cg::K ? y[in_index<H>(P.in0, g.in_w, d, k)] : 0.0f;
+        }
+    }
+}
+
+// Sums a[v] over the 64 lanes of the wave and leaves the sum for v = lane in
+// a[0]: each halving step keeps the half of the values selected by one lane
+// bit and adds the partner lane's copy of that half (fixed order).
+template <int C>
+__device__ __forceinline__ void reduce_scatter_step(float (&a)[64], int lane) {
+    constexpr int HALF = C / 2;
+    const bool up = (lane & HALF) != 0;
+#pragma unroll
+    for (int j = 0; j < HALF; ++j) {
+        const float mine = up ? a[HALF + j] : a[j], other = up ? a[j] : a[HALF + j];
+        a[j] = mine + __shfl_xor(other, HALF);
+    }
+}
+
+__device__ __forceinline__ float reduce_scatter64(float (&a)[64], int lane) {
+    reduce_scatter_step<64>(a, lane);
+    reduce_scatter_step<32>(a, lane);
+    reduce_scatter_step<16>(a, lane);
+    reduce_scatter_step<8>(a, lane);
+    reduce_scatter_step<4>(a, lane);
+    reduce_scatter_step<2>(a, lane);
+    return a[0];
+}
+
+// Forward: out[d*OG + o] = tanh(b[d][o] + sum_k W[d][o][k] in_d[k]). A lane's
+// partial sums for the step's NG x OG outputs are summed over the wave by a
+// reduce-scatter that leaves output (t, o) = (lane / OG, lane % OG) in lane l.
+template <int H, int OG>
+__global__ void __launch_bounds__(256)
+k_conv_fwd(const float* __restrict__ y, const float* __restrict__ W, const float* __restrict__ bias, ConvGeo geo,
+           float* __restrict__ out) {
+    using Cg = ConvCfg<H, OG>;
+    constexpr int K = Cg::K, KL = Cg::KL, NG = Cg::NG;
+    const int d = threadIdx.x >> 6, lane = threadIdx.x & 63, to = lane / OG, oo = lane % OG;
+    float w[KL][OG];
+#pragma unroll
+    for (int i = 0; i < KL; ++i) {
+        const int k = lane + 64 * i;
+#pragma unroll
+        for (int o = 0; o < OG; ++o) w[i][o] = k < K ? W[((int64_t)d * OG + o) * K + k] : 0.0f;
+    }
+    const float bo = bias[d * OG + oo];
+    const int nb = geo.blk_off[geo.n], nst = (nb + NG - 1) / NG;
+    float x[NG][KL];
+    RowPos r0;
+    int st = blockIdx.x;
+    if (st < nst) load_step<H, OG>(geo, y, d, lane, st * NG, nb, r0, x);
+    for (; st < nst; st += gridDim.x) {
+        float a[64];
+#pragma unroll
+        for (int t = 0; t < NG; ++t)
+#pragma unroll
+            for (int o = 0; o < OG; ++o) {
+                float acc = 0.0f;
+#pragma unroll
+                for (int i = 0; i < KL; ++i) acc += w[i][o] * x[t][i];
+                a[t * OG + o] = acc;
+            }
+        const RowPos rc = r0;
+        const int s0 = st * NG;
+        if (st + (int)gridDim.x < nst) load_step<H, OG>(geo, y, d, lane, (st + gridDim.x) * NG, nb, r0, x);
+        const float v = reduce_scatter64(a, lane);
+        if (s0 + to < nb) {
+            const BlockPos P = stage_pos(geo, rc, s0, to);
+            out[P.out * (4 * OG) + d * OG + oo] = tanhf(v + bo);
+        }
+    }
+}
+
+// Backward, input gradient: g[o] = dout[o] (1 - out[o]^2),
+// dy[pixel][d*H + j] = sum_o g[o] W[d][o][(dy*bw+dx)*H + j]. Lane (t, o)
+// loads block t's g[o] (one step ahead); the g values reach every lane as
+// scalars.
 template <int H, int OG>
 __global__ void __launch_bounds__(256)
 k_conv_bwd_dy(const float* __restrict__ out, const float* __restrict__ dout, const float* __restrict__ W,
-              const int32_t* __restrict__ blk_off, int n, const int32_t* __restrict__ in_rects, int in_w,
-              const int32_t* __restrict__ out_rects, int out_w, float* __restrict__ dy) {
-    constexpr int bh = CBH, bw = CBW, K = bh * bw * H;
-    __shared__ float sw[4 * OG * K];
-    for (int i = threadIdx.x; i < 4 * OG * K; i += blockDim.x) sw[i] = W[i];
-    __syncthreads();
-    const int nb = blk_off[n];
-    const int gid = blockIdx.x * blockDim.x + threadIdx.x;
-    if (gid >= 4 * nb) return;
-    const int b = gid >> 2, d = gid & 3;
-    const BlockPos P = block_pos(blk_off, n, b, in_rects, in_w, out_rects, out_w, CBH, CBW);
-    float g[OG];
+              ConvGeo geo, float* __restrict__ dy) {
+    using Cg = ConvCfg<H, OG>;
+    constexpr int K = Cg::K, KL = Cg::KL, NG = Cg::NG;
+    const int d = threadIdx.x >> 6, lane = threadIdx.x & 63, tb = lane / OG, ob = lane % OG;
+    float w[KL][OG];
 #pragma unroll
-    for (int o = 0; o < OG; o += 4) {
-        const float4 ov = *reinterpret_cast<const float4*>(out + P.out * (4 * OG) + d * OG + o);
-        const float4 gv = *reinterpret_cast<const float4*>(dout + P.out * (4 * OG) + d * OG + o);
-        g[o] = gv.x * (1.0f - ov.x * ov.x);
-        g[o + 1] = gv.y * (1.0f - ov.y * ov.y);
-        g[o + 2] = gv.z * (1.0f - ov.z * ov.z);
-        g[o + 3] = gv.w * (1.0f - ov.w * ov.w);
+    for (int i = 0; i < KL; ++i) {
+        const int k = min(lane + 64 * i, K - 1);
+#pragma unroll
+        for (int o = 0; o < OG; ++o) w[i][o] = W[((int64_t)d * OG + o) * K + k];
     }
-    const float* wd = sw + d * OG * K;
-    for (int dyy = 0; dyy < bh; ++dyy)
-        for (int dx = 0; dx < bw; ++dx) {
-            float* dp = dy + (P.in0 + (int64_t)dyy * in_w + dx) * (4 * H) + d * H;
-            const int k0 = (dyy * bw + dx) * H;
+    const int nb = geo.blk_off[geo.n], nst = (nb + NG - 1) / NG;
+    RowPos r0;
+    float ov = 0.0f, gv = 0.0f;
+    auto fetch = [&](int st) {
+        const int s0 = st * NG;
+        r0 = row_pos(geo, s0);
+        ov = gv = 0.0f;
+        if (s0 + tb < nb) {
+            const BlockPos P = stage_pos(geo, r0, s0, tb);
+            ov = out[P.out * (4 * OG) + d * OG + ob];
+            gv = dout[P.out * (4 * OG) + d * OG + ob];
+        }
+    };
+    int st = blockIdx.x;
+    if (st < nst) fetch(st);
+    for (; st < nst; st += gridDim.x) {
+        const float gl = gv * (1.0f - ov * ov);
+        const RowPos rc = r0;
+        const int s0 = st * NG, cnt = min(NG, nb - s0);
+        if (st + (int)gridDim.x < nst) fetch(st + gridDim.x);
 #pragma unroll
-            for (int j = 0; j < H; j += 4) {
-                float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int t = 0; t < NG; ++t) {
+            if (t < cnt) {
+                float g[OG];
 #pragma unroll
-                for (int o = 0; o < OG; ++o) {
-                    const float* wr = wd + o * K + k0 + j;
-                    a.x += g[o] * wr[0];
-                    a.y += g[o] * wr[1];
-                    a.z += g[o] * wr[2];
-                    a.w += g[o] * wr[3];
+                for (int o = 0; o < OG; ++o)
+                    g[o] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gl), t * OG + o));
+                const BlockPos P = stage_pos(geo, rc, s0, t);
+#pragma unroll
+                for (int i = 0; i < KL; ++i) {
+                    const int k = lane + 64 * i;
+                    if (k < K) {
+                        float a = 0.0f;
+#pragma unroll
+                        for (int o = 0; o < OG; ++o) a += g[o] * w[i][o];
+                        dy[in_index<H>(P.in0, geo.in_w, d, k)] = a;
+                    }
                 }
-                *reinterpret_cast<float4*>(dp + j) = a;
             }
         }
+    }
 }
 
 // ---------------------------------------------------------------------------
 // Backward, weight and bias gradients. Workgroup c sums blocks
-// [c*per, (c+1)*per) in order into partial[c][4*OG*K + 4*OG]; BPP blocks per
-// pass are staged in LDS (their g values and input pixels), each thread owns
-// fixed (d, o, k) entries. A second kernel adds the partials in chunk order,
-// so the result does not depend on scheduling.
+// [c*per, (c+1)*per) in order into partial[c][4*OG*K + 4*OG] (entry
+// (d, o, k) at (d*OG + o)*K + k, then the biases): lane l of wave d
+// accumulates g[o] in_d[k] for its inputs k and every o, and lane (t, o) the
+// g[o] of the step's block t, added over t at the end. A second kernel adds
+// the partials in chunk order, so the result does not depend on scheduling.
 // ---------------------------------------------------------------------------
 template <int H, int OG>
 __global__ void __launch_bounds__(256)
 k_conv_bwd_dw(const float* __restrict__ y, const float* __restrict__ out, const float* __restrict__ dout,
-              const int32_t* __restrict__ blk_off, int n, const int32_t* __restrict__ in_rects, int in_w,
-              const int32_t* __restrict__ out_rects, int out_w, int per, float* __restrict__ partial) {
-    constexpr int bh = CBH, bw = CBW, BPP = 8;
-    constexpr int K = bh * bw * H, CB = bh * bw;  // inputs per group, pixels per block
-    constexpr int M = 4 * OG * K;
-    constexpr int MAXE = (M + 255) / 256;          // (d, o, k) entries per thread
-    __shared__ __attribute__((aligned(16))) float sg[BPP * 4 * OG];     // g of the staged blocks
-    __shared__ __attribute__((aligned(16))) float sy[BPP * CB * 4 * H];  // their input pixels
-    const int nb = blk_off[n];
+              ConvGeo geo, int per, float* __restrict__ partial) {
+    using Cg = ConvCfg<H, OG>;
+    constexpr int K = Cg::K, KL = Cg::KL, NG = Cg::NG, M = 4 * OG * K;
+    const int d = threadIdx.x >> 6, lane = threadIdx.x & 63, tb = lane / OG, ob = lane % OG;
+    const int nb = geo.blk_off[geo.n];
     const int b0 = blockIdx.x * per, b1 = min(nb, b0 + per);
-    float acc[MAXE];
+    float acc[KL][OG];
+#pragma unroll
+    for (int i = 0; i < KL; ++i)
+#pragma unroll
+        for (int o = 0; o < OG; ++o) acc[i][o] = 0.0f;
     float accb = 0.0f;
-#pragma unroll
-    for (int e = 0; e < MAXE; ++e) acc[e] = 0.0f;
-    for (int bb = b0; bb < b1; bb += BPP) {
-        const int nblk = min(BPP, b1 - bb);
-        // stage g = dout (1 - out^2) and the input pixels of nblk blocks
-        for (int i = threadIdx.x; i < nblk * 4 * OG; i += blockDim.x) {
-            const int lb = i / (4 * OG), ch = i - lb * (4 * OG);
-            const BlockPos P = block_pos(blk_off, n, bb + lb, in_rects, in_w, out_rects, out_w, CBH, CBW);
-            const float ov = out[P.out * (4 * OG) + ch];
-            sg[i] = dout[P.out * (4 * OG) + ch] * (1.0f - ov * ov);
+    float x[NG][KL];
+    float ov = 0.0f, gv = 0.0f;
+    auto fetch = [&](int s0) {
+        RowPos r0;
+        load_step<H, OG>(geo, y, d, lane, s0, b1, r0, x);
+        ov = gv = 0.0f;
+        if (s0 + tb < b1) {
+            const BlockPos P = stage_pos(geo, r0, s0, tb);
+            ov = out[P.out * (4 * OG) + d * OG + ob];
+            gv = dout[P.out * (4 * OG) + d * OG + ob];
         }
-        for (int i = threadIdx.x; i < nblk * CB * H; i += blockDim.x) {  // float4 units of [lb][pix][4H]
-            const int lb = i / (CB * H), rem = i - lb * (CB * H);
-            const int pix = rem / H, c4 = rem - pix * H;
-            const int dyy = pix / bw, dx = pix - dyy * bw;
-            const BlockPos P = block_pos(blk_off, n, bb + lb, in_rects, in_w, out_rects, out_w, CBH, CBW);
-            reinterpret_cast<float4*>(sy)[i] =
-                *reinterpret_cast<const float4*>(y + (P.in0 + (int64_t)dyy * in_w + dx) * (4 * H) + 4 * c4);
-        }
-        __syncthreads();
-        for (int lb = 0; lb < nblk; ++lb) {
-            const float* gb = sg + lb * 4 * OG;
-            const float* yb = sy + lb * CB * 4 * H;
+    };
+    if (b0 < b1) fetch(b0);
+    for (int s0 = b0; s0 < b1; s0 += NG) {
+        const float gl = gv * (1.0f - ov * ov);  // zero past b1, as are the inputs
+        float xc[NG][KL];
 #pragma unroll
-            for (int e = 0; e < MAXE; ++e) {
-                const int idx = e * 256 + (int)threadIdx.x;  // entry (d, o, k) = ((d*OG + o)*K + k)
-                if (idx < M) {
-                    const int dk = idx / K, kk = idx - dk * K;  // dk = d*OG + o
-                    const int d = dk / OG;
-                    const int pix = kk / H, j = kk - pix * H;
-                    acc[e] += gb[dk] * yb[pix * 4 * H + d * H + j];
-                }
+        for (int t = 0; t < NG; ++t)
+#pragma unroll
+            for (int i = 0; i < KL; ++i) xc[t][i] = x[t][i];
+        if (s0 + NG < b1) fetch(s0 + NG);
+        accb += gl;
+#pragma unroll
+        for (int t = 0; t < NG; ++t)
+#pragma unroll
+            for (int o = 0; o < OG; ++o) {
+                const float g = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gl), t * OG + o));
+#pragma unroll
+                for (int i = 0; i < KL; ++i) acc[i][o] += g * xc[t][i];
             }
-            if ((int)threadIdx.x < 4 * OG) accb += gb[threadIdx.x];
-        }
-        __syncthreads();
     }
+#pragma unroll
+    for (int m = OG; m < 64; m <<= 1) accb += __shfl_xor(accb, m);
     float* pc = partial + (size_t)blockIdx.x * (M + 4 * OG);
 #pragma unroll
-    for (int e = 0; e < MAXE; ++e) {
-        const int idx = e * 256 + (int)threadIdx.x;
-        if (idx < M) pc[idx] = acc[e];
+    for (int i = 0; i < KL; ++i) {
+        const int k = lane + 64 * i;
+        if (k < K) {
+#pragma unroll
+            for (int o = 0; o < OG; ++o) pc[((int64_t)d * OG + o) * K + k] = acc[i][o];
+        }
     }
-    if ((int)threadIdx.x < 4 * OG) pc[M + threadIdx.x] = accb;
+    if (tb == 0) pc[M + d * OG + ob] = accb;
 }
 
 // Fixed-order sum of the chunk partials: a block takes 64 consecutive
@@ -312,18 +414,20 @@ static hipError_t conv_launch(bool fwd, const ConvArgs& a, hipStream_t s) {
         return hipErrorInvalidValue;  // rejected by conv_supported
     } else {
         constexpr int K = CBH * CBW * H;
-        const unsigned grid = (unsigned)((4 * a.total_blocks + 255) / 256);
+        const ConvGeo geo{a.blk_off, a.n, a.in_rects, a.in_w, a.out_rects, a.out_w};
+        // enough workgroups to fill the CUs several times over, each loading
+        // its weights once
+        constexpr int NG = ConvCfg<H, OG>::NG;
+        const unsigned grid = (unsigned)std::min((a.total_blocks + NG - 1) / NG, 2048);
         if (fwd) {
-            hipLaunchKernelGGL((k_conv_fwd<H, OG>), dim3(grid), dim3(256), 0, s, a.y, a.w, a.b, a.blk_off, a.n,
-                               a.in_rects, a.in_w, a.out_rects, a.out_w, a.out);
+            hipLaunchKernelGGL((k_conv_fwd<H, OG>), dim3(grid), dim3(256), 0, s, a.y, a.w, a.b, geo, a.out);
             return hipGetLastError();
         }
-        hipLaunchKernelGGL((k_conv_bwd_dy<H, OG>), dim3(grid), dim3(256), 0, s, a.out, a.dout, a.w, a.blk_off, a.n,
-                           a.in_rects, a.in_w, a.out_rects, a.out_w, a.dy);
+        hipLaunchKernelGGL((k_conv_bwd_dy<H, OG>), dim3(grid), dim3(256), 0, s, a.out, a.dout, a.w, geo, a.dy);
         const int chunks = conv_chunks(a.total_blocks);
         const int per = (a.total_blocks + chunks - 1) / chunks;
-        hipLaunchKernelGGL((k_conv_bwd_dw<H, OG>), dim3(chunks), dim3(256), 0, s, a.y, a.out, a.dout, a.blk_off,
-                           a.n, a.in_rects, a.in_w, a.out_rects, a.out_w, per, a.partial);
+        hipLaunchKernelGGL((k_conv_bwd_dw<H, OG>), dim3(chunks), dim3(256), 0, s, a.y, a.out, a.dout, geo, per,
+                           a.partial);
         const int m = 4 * OG * K + 4 * OG;
         hipLaunchKernelGGL(k_sum_partials, dim3((m + 63) / 64), dim3(256), 0, s, a.partial, chunks, m, a.dw,
                            a.db, 4 * OG * K);
