@@ -98,25 +98,28 @@ __global__ void k_transpose(int rows, int cols, const T* __restrict__ src, T* __
 // --- dX ------------------------------------------------------------------------
 // Wave: 64 cells (four N tiles) x up to 64 channels (four M tiles) of one
 // channel group (blockIdx.y). Lane (g, i16) reads, per reduction step, the
-// 16 bytes of row k0 + E g of its channel (WxT) and of its cell (dZ).
-template <typename T>
+// 16 bytes of row k0 + E g of its channel (WxT) and of its cell (dZ). When
+// there are too few cells to fill the CUs with such waves (SPLIT), the four
+// waves of a workgroup take 16 cells together, each a quarter of the
+// reduction steps, and their sums are added in LDS in wave order.
+template <typename T, bool SPLIT>
 __global__ void __launch_bounds__(256)
 k_dx_big(int64_t n_cells, int C, int N, const T* __restrict__ dZ, const T* __restrict__ WxT,
          const uint8_t* __restrict__ flags, T* __restrict__ dX) {
     using B = BigT<T>;
-    constexpr int E = B::E, KS = B::KSTEP;
+    constexpr int E = B::E, KS = B::KSTEP, CT = SPLIT ? 1 : 4;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int g = lane >> 4, i16 = lane & 15;
-    const int64_t cell0 = ((int64_t)blockIdx.x * 4 + wave) * 64;
+    const int64_t cell0 = SPLIT ? (int64_t)blockIdx.x * 16 : ((int64_t)blockIdx.x * 4 + wave) * 64;
     if (cell0 >= n_cells) return;
     const int ch0 = blockIdx.y * 64;
     const int nmt = min(4, (C - ch0 + 15) / 16);
     const char* Zb = reinterpret_cast<const char*>(dZ);
     const char* Wb = reinterpret_cast<const char*>(WxT);
-    int64_t cl[4];
-    bool ok[4];
+    int64_t cl[CT];
+    bool ok[CT];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < CT; ++t) {
         const int64_t c = cell0 + 16 * t + i16;
         ok[t] = c < n_cells && (flags[min(c, n_cells - 1)] & 1);
         cl[t] = min(c, n_cells - 1);
@@ -124,27 +127,43 @@ k_dx_big(int64_t n_cells, int C, int N, const T* __restrict__ dZ, const T* __res
     int chl[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) chl[m] = min(ch0 + 16 * m + i16, C - 1);
-    floatx4 acc[4][4];
+    floatx4 acc[4][CT];
 #pragma unroll
     for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < CT; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
     const int64_t rb = (int64_t)N * sizeof(T);
     const int koff = E * g * (int)sizeof(T);
-    for (int k0 = 0; k0 < N; k0 += KS) {
-        u32x4 a[4], b[4];
+    const int nsteps = (N + KS - 1) / KS;
+    const int k_begin = SPLIT ? KS * (nsteps * wave / 4) : 0;
+    const int k_end = SPLIT ? min(N, KS * (nsteps * (wave + 1) / 4)) : N;
+    for (int k0 = k_begin; k0 < k_end; k0 += KS) {
+        u32x4 a[4], b[CT];
 #pragma unroll
         for (int m = 0; m < 4; ++m)
             a[m] = *reinterpret_cast<const u32x4*>(Wb + chl[m] * rb + (int64_t)k0 * sizeof(T) + koff);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < CT; ++t) {
             const u32x4 v = *reinterpret_cast<const u32x4*>(Zb + cl[t] * rb + (int64_t)k0 * sizeof(T) + koff);
             b[t] = ok[t] ? v : zero4();
         }
 #pragma unroll
         for (int m = 0; m < 4; ++m)
 #pragma unroll
-            for (int t = 0; t < 4; ++t) acc[m][t] = mma16<T>(a[m], b[t], acc[m][t]);
+            for (int t = 0; t < CT; ++t) acc[m][t] = mma16<T>(a[m], b[t], acc[m][t]);
+    }
+    if constexpr (SPLIT) {
+        __shared__ floatx4 part[3][4][64];
+        if (wave > 0) {
+#pragma unroll
+            for (int m = 0; m < 4; ++m) part[wave - 1][m][lane] = acc[m][0];
+        }
+        __syncthreads();
+        if (wave > 0) return;
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int w = 0; w < 3; ++w) acc[m][0] += part[w][m][lane];
     }
     // lane (q, n) holds channels 4 q .. 4 q + 3 of cell n of every tile pair
 #pragma unroll
@@ -152,7 +171,7 @@ k_dx_big(int64_t n_cells, int C, int N, const T* __restrict__ dZ, const T* __res
         const int ch = ch0 + 16 * m + 4 * g;
         if (m >= nmt || ch >= C) continue;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < CT; ++t) {
             const int64_t c = cell0 + 16 * t + i16;
             if (c < n_cells) St<T>::st4(dX + c * C + ch, acc[m][t]);
         }
@@ -411,7 +430,7 @@ static BigDw big_dw(const LayerGeom& g) {
     q.PP = q.NB + 1;  // partial row: the columns, then the bias
     const int per_chunk = q.rblocks * q.cblocks * 4;
     int64_t ch = (BW_TARGET + per_chunk - 1) / per_chunk;
-    const int64_t by_size = std::max<int64_t>(1, g.n_cells / (16 * BW_KC));  // at least 16 steps per chunk
+    const int64_t by_size = std::max<int64_t>(1, g.n_cells / (4 * BW_KC));  // at least 4 steps per chunk
     ch = std::max<int64_t>(1, std::min(ch, by_size));
     q.chunk_cells = (g.n_cells + ch - 1) / ch;
     q.chunk_cells = std::max<int64_t>(BW_KC, (q.chunk_cells + BW_KC - 1) / BW_KC * BW_KC);  // an empty canvas: one chunk
@@ -918,13 +937,24 @@ hipError_t launch_bwd_big_dx(const LayerGeom& g, const void* d_dz, const void* d
     hipLaunchKernelGGL(k_cell_flags, dim3(fb), dim3(256), 0, s, g.canvas_h, g.canvas_w, d_mask, d_rid, d_flags);
     const int64_t nw = (int64_t)N * g.c_in;
     const int tb = (int)std::min<int64_t>((nw + 255) / 256, 4096);
-    const dim3 gx((unsigned)(((g.n_cells + 63) / 64 + 3) / 4), (unsigned)((g.c_in + 63) / 64));
+    // 64-cell waves while they fill the CUs four times over, else workgroups
+    // of 16 cells with the reduction split over their waves
+    const int64_t cgroups = (g.c_in + 63) / 64, waves64 = (g.n_cells + 63) / 64 * cgroups;
+    const bool split = waves64 < 4 * 256;
+    const dim3 gx((unsigned)(split ? (g.n_cells + 15) / 16 : ((g.n_cells + 63) / 64 + 3) / 4), (unsigned)cgroups);
+    auto dx_big = [&](auto tag, const auto* dz, const auto* wxt, auto* dx) {
+        using T = decltype(tag);
+        if (split)
+            hipLaunchKernelGGL((k_dx_big<T, true>), gx, dim3(256), 0, s, g.n_cells, g.c_in, N, dz, wxt, d_flags, dx);
+        else
+            hipLaunchKernelGGL((k_dx_big<T, false>), gx, dim3(256), 0, s, g.n_cells, g.c_in, N, dz, wxt, d_flags,
+                               dx);
+    };
     if (g.dtype == 0) {
         using T = float;
         hipLaunchKernelGGL(k_transpose<T>, dim3(tb), dim3(256), 0, s, N, g.c_in, static_cast<const T*>(d_wx),
                            static_cast<T*>(d_wxt));
-        hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, static_cast<const T*>(d_dz),
-                           static_cast<const T*>(d_wxt), d_flags, static_cast<T*>(d_dx));
+        dx_big(T{}, static_cast<const T*>(d_dz), static_cast<const T*>(d_wxt), static_cast<T*>(d_dx));
     } else {
         using T = bf16_t;
         hipLaunchKernelGGL(k_transpose<T>, dim3(tb), dim3(256), 0, s, N, g.c_in, static_cast<const T*>(d_wx),
@@ -943,7 +973,7 @@ hipError_t launch_bwd_big_dx(const LayerGeom& g, const void* d_dz, const void* d
             default: return hipErrorInvalidValue;
         }
         if (!done)
-            hipLaunchKernelGGL(k_dx_big<T>, gx, dim3(256), 0, s, g.n_cells, g.c_in, N, dz, wxt, d_flags, dx);
+            dx_big(T{}, dz, wxt, dx);
     }
     return hipGetLastError();
 }

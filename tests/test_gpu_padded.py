@@ -68,6 +68,9 @@ CASES = [
     ("bf16_H128_C256", [12, 5], [19, 24], 48, 256, 128, "bf16"),
     ("H16_C150", [10, 17], [25, 12], 48, 150, 16, "f32"),
     ("H64_C256", [9, 4], [14, 22], 32, 256, 64, "f32"),
+    # a canvas of 16k cells and more: the fp32 input gradient with 64-cell
+    # waves (smaller canvases take 16-cell ones)
+    ("H64_C256_64x256", [64, 64], [120, 130], 256, 256, 64, "f32"),
 ]
 
 
