@@ -46,8 +46,8 @@ struct StripCfg {
     static constexpr int WPD = H >= 32 ? 2 : 1;       // waves per direction
     static constexpr int RTW = (RT + WPD - 1) / WPD;  // gate-row tiles per wave
     // cells per strip: 16 where the registers need it (H >= 32) or where two
-    // workgroups then fit on a CU (H = 16 with 16 input channels), else 32
-    static constexpr int TC = (H >= 32 || (H == 16 && C >= 16)) ? 16 : 32;
+    // workgroups then fit on a CU (H = 16), else 32
+    static constexpr int TC = H >= 16 ? 16 : 32;
     static constexpr int THREADS = 256 * WPD;
     static constexpr int ZP = N + 4;                  // LDS pitch of dZ rows (4 mod 16: the cells read by one MFMA hit distinct banks)
     static constexpr int YP = 4 * H + 4;              // LDS pitch of Y rows
@@ -57,14 +57,15 @@ struct StripCfg {
     // The next strip's loads are prefetched into registers where the dW tiles
     // leave room (H <= 16). With 32-cell strips at H = 16 that takes over 256
     // registers per lane (one workgroup per CU); the 16-cell strips of H = 16
-    // with 16 input channels and the other shapes run two workgroups per CU.
+    // (dW steps unrolled by two with 8 input channels) and the other shapes
+    // run two workgroups per CU.
     static constexpr bool PREFETCH = H <= 16;
     // workgroups launched: one round of resident workgroups (H = 32 holds
     // one per CU: its registers, and LDS in the direct-to-LDS kernel)
     static constexpr int WGS = (H == 16 && TC == 32) || H >= 32 ? 256 : 512;
     // register budget of the H = 32 shapes: dW steps unrolled by two, dX
     // operands read five blocks at a time
-    static constexpr int DW_UNROLL = H >= 32 ? 2 : TC / 4;
+    static constexpr int DW_UNROLL = H >= 32 || (H == 16 && C < 16) ? 2 : TC / 4;
     static constexpr int DXB = H >= 32 ? 5 : (G + 15) / 16;
 };
 
