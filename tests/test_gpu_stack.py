@@ -109,3 +109,60 @@ def test_stack_weight_gradients_are_deterministic():
     for ga, gb in zip(a["conv_grads"] + a["layer_grads"], b["conv_grads"] + b["layer_grads"]):
         for x, y in zip(ga, gb):
             assert np.array_equal(x, y)
+
+
+# (hidden, og, output rectangles (h, w) in blocks): every lane layout of the
+# convolution kernels (K = 8 H below, at and above 64; 64 / og blocks per wave
+# step from 2 to 16), steps that wrap a block row, and for (4, 32) more steps
+# than one grid-stride round.
+CONV_CASES = [
+    (4, 32, [(3, 5), (1, 7), (40, 120)]),
+    (8, 4, [(2, 9), (5, 3), (1, 1), (4, 13)]),
+    (16, 32, [(3, 11), (2, 2), (6, 7)]),
+    (16, 8, [(4, 17), (1, 5), (3, 3)]),
+    (32, 16, [(2, 6), (5, 9)]),
+    (64, 8, [(3, 7), (2, 10), (1, 3)]),
+]
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[f"H{c[0]}_og{c[1]}" for c in CONV_CASES])
+def test_block_conv_shapes(case):
+    """The grouped block convolution alone through the C ABI, input and output
+    rectangles placed independently on their canvases (the input canvas
+    holds the examples side by side, the output canvas one above the other):
+    every example's output and input gradient and the weight and bias
+    gradients against the oracle, example by example."""
+    from oracle import stack as ostack
+    from paper_1902_11208_amd import api
+
+    H, og, outs = case
+    bh, bw = 2, 4
+    print(f"case: block convolution H={H} og={og} rectangles {outs}", flush=True)
+    rng = np.random.default_rng(1000 + H + og)
+    in_rects, out_rects, x0, y0 = [], [], 1, 0
+    for (h, w) in outs:
+        in_rects.append((1, x0, bh * h, bw * w))
+        out_rects.append((y0, 2, h, w))
+        x0 += bw * w + 3
+        y0 += h + 1
+    in_h, in_w = bh * max(h for h, _ in outs) + 2, x0 + 1
+    out_h, out_w = y0, max(w for _, w in outs) + 3
+    y = rng.standard_normal((in_h, in_w, 4 * H)).astype(np.float32)
+    dout = rng.standard_normal((out_h, out_w, 4 * og)).astype(np.float32)
+    W = (rng.standard_normal((4, og, bh * bw * H)) / np.sqrt(bh * bw * H)).astype(np.float32)
+    b = (0.1 * rng.standard_normal((4, og))).astype(np.float32)
+    conv = api.BlockConv(torch.from_numpy(W).cuda(), torch.from_numpy(b).cuda(), in_rects, (in_h, in_w), out_rects,
+                         (out_h, out_w), bh, bw)
+    out = conv.forward(torch.from_numpy(y).cuda()).cpu().numpy()
+    dy, dW, db = (t.cpu().numpy() for t in conv.backward(torch.from_numpy(dout).cuda()))
+    dW_ref, db_ref = np.zeros(W.shape), np.zeros(b.shape)
+    for (iy, ix, ih, iw), (oy, ox, oh, ow) in zip(in_rects, out_rects):
+        yk = y[iy:iy + ih, ix:ix + iw]
+        ok = ostack.grouped_block_conv(yk, W, b, bh, bw)
+        dyk, dWk, dbk = ostack.grouped_block_conv_backward(yk, W, ok, dout[oy:oy + oh, ox:ox + ow], bh, bw)
+        _check("out", out[oy:oy + oh, ox:ox + ow], ok)
+        _check("dy", dy[iy:iy + ih, ix:ix + iw], dyk)
+        dW_ref += dWk
+        db_ref += dbk
+    _check("dW", dW, dW_ref)
+    _check("db", db, db_ref)
