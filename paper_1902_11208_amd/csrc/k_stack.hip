@@ -98,17 +98,17 @@ __device__ __forceinline__ RowPos row_pos(const ConvGeo& g, int b) {
 }
 
 // Block s0 + t, given block s0's position r0.
-__device__ __forceinline__ BlockPos stage_pos(const ConvGeo& g, const RowPos& r0, int s0, int t) {
+__device__ __forceinline__ BlockPos step_pos(const ConvGeo& g, const RowPos& r0, int s0, int t) {
     if (t < r0.rem) return BlockPos{r0.in0 + (int64_t)t * CBW, r0.out + t};
     const RowPos r = row_pos(g, s0 + t);
     return BlockPos{r.in0, r.out};
 }
 
 // Every kernel runs a wave per (group d, step of NG = 64 / OG consecutive
-// blocks), no LDS and no barriers. Lane l holds inputs k = l, l + 64, ... of
-// the K = bh * bw * H inputs of each block of the step (pixel k / H, channel
-// d*H + k % H) with their OG weights, or weight-gradient sums, in registers;
-// the step's data loads one step ahead.
+// blocks), with no LDS buffer and no barrier. Lane l holds inputs k = l,
+// l + 64, ... of the K = bh * bw * H inputs of each block of the step (pixel
+// k / H, channel d*H + k % H) with their OG weights, or weight-gradient sums,
+// in registers; the step's data loads one step ahead.
 template <int H, int OG>
 struct ConvCfg {
     static constexpr int K = CBH * CBW * H, KL = (K + 63) / 64, NG = 64 / OG;
@@ -133,7 +133,7 @@ __device__ __forceinline__ void load_step(const ConvGeo& g, const float* __restr
 #pragma unroll
     for (int t = 0; t < Cg::NG; ++t) {
         const bool live = s0 + t < lim;
-        const BlockPos P = live ? stage_pos(g, r0, s0, t) : BlockPos{0, 0};
+        const BlockPos P = live ? step_pos(g, r0, s0, t) : BlockPos{0, 0};
 #pragma unroll
         for (int i = 0; i < Cg::KL; ++i) {
             const int k = lane + 64 * i;
@@ -205,7 +205,7 @@ k_conv_fwd(const float* __restrict__ y, const float* __restrict__ W, const float
         if (st + (int)gridDim.x < nst) load_step<H, OG>(geo, y, d, lane, (st + gridDim.x) * NG, nb, r0, x);
         const float v = reduce_scatter64(a, lane);
         if (s0 + to < nb) {
-            const BlockPos P = stage_pos(geo, rc, s0, to);
+            const BlockPos P = step_pos(geo, rc, s0, to);
             out[P.out * (4 * OG) + d * OG + oo] = tanhf(v + bo);
         }
     }
@@ -237,7 +237,7 @@ k_conv_bwd_dy(const float* __restrict__ out, const float* __restrict__ dout, con
         r0 = row_pos(geo, s0);
         ov = gv = 0.0f;
         if (s0 + tb < nb) {
-            const BlockPos P = stage_pos(geo, r0, s0, tb);
+            const BlockPos P = step_pos(geo, r0, s0, tb);
             ov = out[P.out * (4 * OG) + d * OG + ob];
             gv = dout[P.out * (4 * OG) + d * OG + ob];
         }
@@ -256,7 +256,7 @@ k_conv_bwd_dy(const float* __restrict__ out, const float* __restrict__ dout, con
 #pragma unroll
                 for (int o = 0; o < OG; ++o)
                     g[o] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gl), t * OG + o));
-                const BlockPos P = stage_pos(geo, rc, s0, t);
+                const BlockPos P = step_pos(geo, rc, s0, t);
 #pragma unroll
                 for (int i = 0; i < KL; ++i) {
                     const int k = lane + 64 * i;
@@ -302,7 +302,7 @@ k_conv_bwd_dw(const float* __restrict__ y, const float* __restrict__ out, const 
         load_step<H, OG>(geo, y, d, lane, s0, b1, r0, x);
         ov = gv = 0.0f;
         if (s0 + tb < b1) {
-            const BlockPos P = stage_pos(geo, r0, s0, tb);
+            const BlockPos P = step_pos(geo, r0, s0, tb);
             ov = out[P.out * (4 * OG) + d * OG + ob];
             gv = dout[P.out * (4 * OG) + d * OG + ob];
         }
