@@ -408,6 +408,18 @@ size_t conv_partial_bytes(int hidden, int og, int bh, int bw, int total_blocks) 
     return (size_t)conv_chunks(total_blocks) * (4 * og * bh * bw * hidden + 4 * og) * 4;
 }
 
+// Workgroups of 256 threads of `kernel` that the device holds at once (2048
+// if the runtime cannot say).
+template <typename K>
+static int resident_workgroups(K kernel) {
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, 0) != hipSuccess || per_cu < 1 ||
+        hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        return 2048;
+    return per_cu * cus;
+}
+
 template <int H, int OG>
 static hipError_t conv_launch(bool fwd, const ConvArgs& a, hipStream_t s) {
     if constexpr (4 * OG * CBH * CBW * H * 4 > 64 * 1024) {
@@ -415,14 +427,18 @@ static hipError_t conv_launch(bool fwd, const ConvArgs& a, hipStream_t s) {
     } else {
         constexpr int K = CBH * CBW * H;
         const ConvGeo geo{a.blk_off, a.n, a.in_rects, a.in_w, a.out_rects, a.out_w};
-        // enough workgroups to fill the CUs several times over, each loading
-        // its weights once
+        // one round of resident workgroups (each loads its weights once and
+        // then strides over the steps), or one per step if there are fewer
         constexpr int NG = ConvCfg<H, OG>::NG;
-        const unsigned grid = (unsigned)std::min((a.total_blocks + NG - 1) / NG, 2048);
+        const int steps = (a.total_blocks + NG - 1) / NG;
         if (fwd) {
+            static const int resident = resident_workgroups(k_conv_fwd<H, OG>);
+            const unsigned grid = (unsigned)std::min(steps, resident);
             hipLaunchKernelGGL((k_conv_fwd<H, OG>), dim3(grid), dim3(256), 0, s, a.y, a.w, a.b, geo, a.out);
             return hipGetLastError();
         }
+        static const int resident = resident_workgroups(k_conv_bwd_dy<H, OG>);
+        const unsigned grid = (unsigned)std::min(steps, resident);
         hipLaunchKernelGGL((k_conv_bwd_dy<H, OG>), dim3(grid), dim3(256), 0, s, a.out, a.dout, a.w, geo, a.dy);
         const int chunks = conv_chunks(a.total_blocks);
         const int per = (a.total_blocks + chunks - 1) / chunks;
