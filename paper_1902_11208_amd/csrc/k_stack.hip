@@ -342,7 +342,7 @@ k_conv_bwd_dw(const float* __restrict__ y, const float* __restrict__ out, const 
 
 // Fixed-order sum of the chunk partials: a block takes 64 consecutive
 // outputs; its four thread groups sum every fourth chunk each (loads batched
-// eight at a time), and the four sums are added in a fixed order.
+// 32 at a time), and the four sums are added in a fixed order.
 __global__ void __launch_bounds__(256)
 k_sum_partials(const float* __restrict__ partial, int chunks, int m, float* __restrict__ dw,
                float* __restrict__ db, int mw) {
@@ -352,12 +352,12 @@ k_sum_partials(const float* __restrict__ partial, int chunks, int m, float* __re
     float s = 0.0f;
     if (i < m) {
         int c = grp;
-        for (; c + 28 < chunks; c += 32) {
-            float v[8];
+        for (; c + 124 < chunks; c += 128) {
+            float v[32];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) v[k] = partial[(size_t)(c + 4 * k) * m + i];
+            for (int k = 0; k < 32; ++k) v[k] = partial[(size_t)(c + 4 * k) * m + i];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) s += v[k];
+            for (int k = 0; k < 32; ++k) s += v[k];
         }
         for (; c < chunks; c += 4) s += partial[(size_t)c * m + i];
     }
