@@ -409,14 +409,17 @@ size_t conv_partial_bytes(int hidden, int og, int bh, int bw, int total_blocks) 
 }
 
 // Workgroups of 256 threads of `kernel` that the device holds at once (2048
-// if the runtime cannot say).
+// if the runtime cannot say; its error is then cleared, so that it is not
+// reported for the launch that follows).
 template <typename K>
 static int resident_workgroups(K kernel) {
     int per_cu = 0, dev = 0, cus = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, 0) != hipSuccess || per_cu < 1 ||
         hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) {
+        (void)hipGetLastError();
         return 2048;
+    }
     return per_cu * cus;
 }
 
