@@ -400,8 +400,10 @@ static bool launch_dx_tr(const LayerGeom& g, const bf16_t* dz, const bf16_t* wxt
     static_assert(lds <= 160 * 1024, "LDS of a CU");
     const int64_t n_blocks = (g.n_cells + DX_CELLS - 1) / DX_CELLS;
     int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
         cus = 256;
+        (void)hipGetLastError();  // not reported for the launch below
+    }
     const int per_cu = (int)std::max<size_t>(1, (160 * 1024) / lds);
     const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(n_blocks, (int64_t)per_cu * cus));
     hipLaunchKernelGGL(k_dx_tr<MT>, dim3(grid), dim3(64 * NWV), 0, s, g.n_cells, g.c_in, 20 * g.hidden, n_blocks, dz, wxt,

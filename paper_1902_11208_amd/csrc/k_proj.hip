@@ -170,8 +170,10 @@ static hipError_t launch_proj(const LayerGeom& g, const T* X, const T* W, const 
     // workgroups that loop over the cell blocks: as many as fit on the CUs at
     // once (LDS-limited, at most four per CU)
     int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
         cus = 256;
+        (void)hipGetLastError();  // not reported for the launch below
+    }
     const size_t lds = (size_t)nch * P * sizeof(T) + 4 * 16 * (64 + 4) * sizeof(float);
     const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(4, 160 * 1024 / lds));
     const int64_t want = std::max<int64_t>(1, (int64_t)per_cu * std::max(cus, 1) / nchunks_col);
